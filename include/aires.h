@@ -1,0 +1,268 @@
+/*
+ * aires.h -- C-ABI of an MI355X (gfx950) library for the out-of-core sparse
+ * product at the heart of GCN aggregation, after AIRES (Jayakody, Zhao,
+ * Wang, "AIRES: Accelerating Out-of-Core GCNs via Algorithm-System
+ * Co-Design", arXiv 2507.02006).
+ *
+ * The operation (Sec. II-A, Eq. 1 with Eq. 2): X = A_norm * H where A_norm is
+ * the normalised sparse adjacency and H a sparse feature matrix, both in
+ * compressed form.  Here: C = A * B with A (m x K) and B (K x N) in CSR and
+ * C (m x N) returned in CSR with strictly increasing column indices per row.
+ *
+ * The paper pairs a CSR first operand with a CSC second operand and matches
+ * rows against columns (Sec. II-B, Sec. III-B).  This library takes B in CSR
+ * and uses the row-wise (Gustavson) formulation; the set of products and the
+ * result are the same.
+ *
+ * Out-of-core execution follows the paper's row block-wise (RoBW) alignment
+ * (Sec. III-A, Algorithm 1: blocks of whole rows of A whose bytes fit a
+ * device budget, never splitting a row) and its three-phase schedule
+ * (Sec. III-B, Algorithm 2: B resident on the device; A row blocks moved to
+ * the device one at a time and multiplied; C stored, then moved to host).
+ *
+ * Conventions for every entry point
+ *  - No exceptions cross this boundary.  Every call that can fail returns an
+ *    aires_status: 0 on success, a negative code on error.  The text of the
+ *    last error on the calling thread is available from aires_last_error().
+ *  - Input matrices are BORROWED: the caller owns their memory and keeps it
+ *    alive and unmodified until the last call on any plan built from them.
+ *  - A plan is used by one thread at a time.
+ *  - Streams are hipStream_t values passed as void*.  NULL means the
+ *    device's null stream.
+ *  - Device-resident pointers must be device memory of the current HIP
+ *    device; host pointers must be host memory (pinned for streaming).
+ */
+#ifndef AIRES_H
+#define AIRES_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AIRES_ABI_VERSION 1
+
+typedef enum aires_status {
+    AIRES_OK = 0,
+    AIRES_E_INVALID_ARG = -1,  /* NULL pointer, bad enum, bad struct_size  */
+    AIRES_E_INVALID_CSR = -2,  /* input fails the canonical-CSR check      */
+    AIRES_E_DIM = -3,          /* A.ncols != B.nrows, negative sizes       */
+    AIRES_E_BUDGET = -4,       /* device budget cannot hold B plus one row */
+    AIRES_E_OVERFLOW = -5,     /* an index or size exceeds its type        */
+    AIRES_E_OOM = -6,          /* an allocation failed                     */
+    AIRES_E_HIP = -7,          /* a HIP runtime call failed                */
+    AIRES_E_STATE = -8,        /* plan in use / wrong call order           */
+    AIRES_E_UNSUPPORTED = -9,  /* combination not supported                */
+    AIRES_E_CAPACITY = -10     /* caller output buffer too small           */
+} aires_status;
+
+/* Row-pointer width of an input matrix. */
+typedef enum aires_idx { AIRES_IDX_I32 = 0, AIRES_IDX_I64 = 1 } aires_idx;
+
+/* Where an array lives. */
+typedef enum aires_mem {
+    AIRES_MEM_DEVICE = 0,       /* HBM of the current device               */
+    AIRES_MEM_HOST_PINNED = 1,  /* page-locked host memory (streamable)    */
+    AIRES_MEM_HOST = 2          /* pageable host memory (planning only)    */
+} aires_mem;
+
+/*
+ * Input CSR descriptor (borrowed).  Canonical form: row_ptr[0] == 0,
+ * non-decreasing, row_ptr[nrows] == nnz; within a row, columns strictly
+ * increasing in [0, ncols); values finite.  row_ptr has nrows + 1 entries
+ * of the width given by rp_type.  All three arrays live in `mem`.
+ */
+typedef struct aires_csr {
+    int64_t nrows, ncols, nnz;
+    int32_t rp_type;            /* aires_idx                               */
+    int32_t mem;                /* aires_mem                               */
+    const void *row_ptr;
+    const int32_t *col_idx;
+    const float *vals;
+} aires_csr;
+
+/*
+ * Output CSR descriptor.  row_ptr is ALWAYS int64 (nnz(C) can exceed 2^31)
+ * and has nrows + 1 entries.  Arrays are allocated by the library (through
+ * the plan's allocator, or hipMallocAsync / hipHostMalloc by default) and
+ * owned by this struct until aires_csr_out_free().  `mem` says where they
+ * live.  Zero-initialise before passing to aires_spgemm.
+ */
+typedef struct aires_csr_out {
+    int64_t nrows, ncols, nnz;
+    int64_t *row_ptr;
+    int32_t *col_idx;
+    float *vals;
+    int32_t mem;                /* aires_mem of the three arrays           */
+    int32_t _reserved;
+    void *_owner;               /* library bookkeeping; do not touch       */
+} aires_csr_out;
+
+/*
+ * Optional device-memory allocator.  alloc returns device memory usable on
+ * `stream` (a hipStream_t) or NULL on failure; free releases it
+ * stream-ordered on `stream`.  A NULL return makes the call fail with
+ * AIRES_E_OOM after releasing what it had allocated.
+ */
+typedef struct aires_allocator {
+    void *(*alloc)(void *ctx, size_t bytes, void *stream);
+    void (*free)(void *ctx, void *ptr, void *stream);
+    void *ctx;
+} aires_allocator;
+
+/* Upper bound used for the size of C when planning. */
+typedef enum aires_cbound {
+    AIRES_CBOUND_PRODUCTS = 0,  /* u_i = min(N, P_i), P_i = sum nnz(B_k)   */
+    AIRES_CBOUND_DENSE = 1,     /* u_i = N                                 */
+    AIRES_CBOUND_PAPER_EQ5 = 2  /* the paper's Eq. 5 estimate (not a bound;
+                                   for planning experiments only)          */
+} aires_cbound;
+
+typedef struct aires_plan_opts {
+    uint32_t struct_size;       /* = sizeof(aires_plan_opts)               */
+    int32_t validate;           /* 1: canonical-CSR check of host inputs   */
+    int32_t c_placement;        /* AIRES_MEM_DEVICE or AIRES_MEM_HOST_PINNED */
+    int32_t c_bound;            /* aires_cbound                            */
+    int32_t timing;             /* 1: record per-phase HIP events          */
+    int32_t _pad0;
+    int64_t max_tile_rows;      /* 0: no cap                               */
+    int64_t max_tile_bytes;     /* 0: no cap on a tile's A bytes           */
+    int64_t m_a_bytes;          /* > 0: plan exactly as Algorithm 1 with
+                                   calcMem(k,q) = (k+1)*rp_bytes + 8q <=
+                                   m_a_bytes, ignoring the budget split    */
+    const aires_allocator *allocator; /* NULL: hipMallocAsync/hipFreeAsync */
+    int64_t dense_max_cols;     /* 0: default.  Widest dense accumulator
+                                   window (columns) held in LDS            */
+    int64_t hash_max_products;  /* 0: default.  Rows of a wide product with
+                                   at most this many products use the LDS
+                                   hash path                               */
+    int64_t wave_max_products;  /* 0: default.  Rows with at most this many
+                                   products are handled by one wavefront   */
+} aires_plan_opts;
+
+/* Fill *o with defaults (struct_size set, validate 0, C on device). */
+aires_status aires_plan_opts_default(aires_plan_opts *o);
+
+typedef struct aires_plan aires_plan;
+
+/*
+ * aires_tile_plan -- RoBW row-block partition of A (Sec. III-A, Algorithm 1;
+ * budget split after Eqs. 6-7).
+ *
+ * A: m x K, B: K x N.  hbm_budget caps every device byte the library
+ * allocates or uses during aires_spgemm/aires_stream_tiles: resident B
+ * (M_B of Eq. 6: values, column ids, row pointers), A (resident, or two
+ * double-buffered tile slots when A is in host memory), C (resident, or two
+ * tile slots sized by the tile's C bound when C is placed in host memory),
+ * and workspace.  0 means "the device's free memory".  Each tile is a
+ * maximal run of whole rows [r0, r1) whose per-tile bytes fit what the
+ * budget leaves after the resident parts, found greedily from row 0 as in
+ * Algorithm 1.  With opts->m_a_bytes > 0, tiles follow Algorithm 1 exactly
+ * with calcMem(k, q) <= m_a_bytes.
+ *
+ * Planning reads A.row_ptr on the host (copying it from the device when A
+ * is device-resident) and, for a host-resident A with C placed in host
+ * memory, computes P_i on the host for the C bound.  It launches no
+ * kernels.
+ *
+ * Errors: AIRES_E_INVALID_ARG (NULL A/B/out, bad enums), AIRES_E_DIM,
+ * AIRES_E_INVALID_CSR (opts->validate and a host input is not canonical),
+ * AIRES_E_BUDGET (B plus one row plus workspace exceeds the budget; this
+ * includes a single row larger than the tile budget), AIRES_E_OVERFLOW,
+ * AIRES_E_UNSUPPORTED (an input in pageable host memory with no m_a_bytes
+ * planning-only use), AIRES_E_HIP.  *out is untouched on error.
+ */
+aires_status aires_tile_plan(const aires_csr *A, const aires_csr *B, uint64_t hbm_budget,
+                             const aires_plan_opts *opts, aires_plan **out);
+
+typedef struct aires_plan_info {
+    int64_t ntiles;
+    int64_t m, k, n;            /* A is m x k, B is k x n                  */
+    int64_t budget;             /* effective budget in bytes               */
+    int64_t b_bytes;            /* M_B                                     */
+    int64_t a_bytes;            /* bytes of all of A                       */
+    int64_t tile_budget;        /* bytes available to one tile slot        */
+    int64_t peak_bytes;         /* planned peak device bytes               */
+    int64_t c_bound_entries;    /* sum of u_i, or -1 when not computed     */
+    int32_t a_streamed;         /* 1: A moves host->device per tile        */
+    int32_t c_on_host;          /* 1: C tiles move device->host            */
+} aires_plan_info;
+
+typedef struct aires_tile {
+    int64_t r0, r1;             /* rows [r0, r1)                           */
+    int64_t nnz0, nnz1;         /* A.row_ptr[r0], A.row_ptr[r1]            */
+    int64_t a_bytes;            /* (r1-r0+1)*rp_bytes + 8*(nnz1-nnz0)      */
+    int64_t c_bound_entries;    /* sum of u_i over the tile, or -1         */
+    int64_t tile_bytes;         /* planned bytes of one slot of this tile  */
+} aires_tile;
+
+aires_status aires_plan_info_get(const aires_plan *plan, aires_plan_info *info);
+aires_status aires_plan_tile(const aires_plan *plan, int64_t t, aires_tile *tile);
+
+/*
+ * aires_spgemm -- C = A * B over the plan's tiles (Algorithm 2, Phase II
+ * per tile; C = A_norm * H of Eq. 1).
+ *
+ * Device-resident A: every kernel runs on `stream`.  For each tile: row
+ * analysis (intermediate products P_i), binning, symbolic phase (nnz of each
+ * row of C); then one device-wide scan gives C.row_ptr, the library reads
+ * nnz(C) back (the single host synchronisation: the size of C is data
+ * dependent, Sec. I and Sec. III-B), allocates C exactly, and runs the
+ * numeric phase tile by tile.  C is device-resident.
+ *
+ * Host-resident (pinned) A: delegates to aires_stream_tiles with internal
+ * copy streams.
+ *
+ * Returns once all work is enqueued and C's arrays exist; C's contents are
+ * valid when `stream` reaches the end of the enqueued work.  Columns of
+ * every row of C are strictly increasing; entries whose value sums to zero
+ * are kept (the structure is the union of the column sets).
+ * Errors: AIRES_E_INVALID_ARG, AIRES_E_STATE (C not zeroed / plan busy),
+ * AIRES_E_BUDGET (exact C does not fit), AIRES_E_OOM, AIRES_E_HIP,
+ * AIRES_E_OVERFLOW.
+ */
+aires_status aires_spgemm(aires_plan *plan, void *stream, aires_csr_out *C);
+
+/*
+ * aires_stream_tiles -- out-of-core Phase II/III of Algorithm 2 for a
+ * host-resident (pinned) A: B is copied to the device once (Phase I); for
+ * each tile, its contiguous row_ptr/col/val slices are copied on `h2d` into
+ * one of two device slots while the previous tile computes on `compute`;
+ * each finished C tile is copied on `d2h` into pinned host memory at the
+ * running offset (opts->c_placement == AIRES_MEM_HOST_PINNED) or kept on
+ * the device.  The host waits only for each tile's nnz, one tile behind.
+ * Host C arrays are sized by the plan's C bound.  On return all work has
+ * completed and C is valid.
+ * Errors: as aires_spgemm, plus AIRES_E_UNSUPPORTED if A is not pinned.
+ */
+aires_status aires_stream_tiles(aires_plan *plan, void *h2d, void *compute, void *d2h,
+                                aires_csr_out *C);
+
+typedef struct aires_stats {
+    int64_t ntiles;
+    int64_t products;           /* sum of P_i (2 flops each)               */
+    int64_t nnz_c;
+    int64_t h2d_bytes, d2h_bytes;
+    int64_t host_syncs;
+    /* milliseconds from HIP events (opts->timing), summed over tiles      */
+    double analyze_ms, bin_ms, symbolic_ms, scan_ms, numeric_ms;
+    double h2d_ms, d2h_ms, total_ms;
+    int64_t numeric_launches;   /* numeric-phase kernel launches           */
+} aires_stats;
+
+/* Statistics of the last aires_spgemm / aires_stream_tiles on the plan. */
+aires_status aires_plan_stats(const aires_plan *plan, aires_stats *stats);
+
+/* Release C's arrays through the allocator that made them; zeroes *C. */
+void aires_csr_out_free(aires_csr_out *C);
+void aires_plan_destroy(aires_plan *plan);
+const char *aires_status_string(aires_status s);
+const char *aires_last_error(void);
+int aires_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AIRES_H */
