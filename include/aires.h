@@ -135,7 +135,7 @@ typedef struct aires_plan_opts {
     const aires_allocator *allocator; /* NULL: hipMallocAsync/hipFreeAsync */
     int64_t dense_max_cols;     /* 0: default.  Widest dense accumulator
                                    window (columns) held in LDS            */
-    int64_t hash_max_products;  /* 0: default.  Rows of a wide product with
+    int64_t hash_max_products;  /* 0: default, < 0: none.  Rows of a wide product with
                                    at most this many products use the LDS
                                    hash path                               */
     int64_t wave_max_products;  /* 0: default.  Rows with at most this many
@@ -250,6 +250,9 @@ typedef struct aires_stats {
     double analyze_ms, bin_ms, symbolic_ms, scan_ms, numeric_ms;
     double h2d_ms, d2h_ms, total_ms;
     int64_t numeric_launches;   /* numeric-phase kernel launches           */
+    /* milliseconds per kernel kind (index = kind id of the row bins,
+       0 empty .. 5 hash-8192); [0] symbolic phase, [1] numeric phase      */
+    double kind_ms[2][8];
 } aires_stats;
 
 /* Statistics of the last aires_spgemm / aires_stream_tiles on the plan. */

@@ -1,0 +1,217 @@
+"""MI355X (gfx950) out-of-core CSR x CSR product for GCN aggregation, after
+AIRES (arXiv 2507.02006): C = A * B over row block-wise (RoBW) tiles
+(Sec. III-A, Algorithm 1) under a device budget, with B resident and A
+tiles streamed from pinned host memory when they do not fit (Sec. III-B,
+Algorithm 2).
+
+Python names mirror the C-ABI of include/aires.h:
+  tile_plan(A, B, hbm_budget, ...)  -> Plan       (aires_tile_plan)
+  spgemm(plan, stream=None)         -> Output     (aires_spgemm)
+  stream_tiles(plan, ...)           -> Output     (aires_stream_tiles)
+  plan_info / plan_tile / plan_stats
+A and B are (nrows, ncols, row_ptr, col_idx, vals) tuples or objects with
+those attributes (``nrows, ncols, rp, col, val``); arrays are device torch
+tensors, pinned host torch tensors, or numpy arrays (planning only).
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+from . import _binding as B_
+
+__all__ = ["tile_plan", "spgemm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
+           "Plan", "Output", "AiresError", "to_device", "to_pinned"]
+
+AiresError = B_.AiresError
+
+
+def _parts(M):
+    if isinstance(M, tuple):
+        return M
+    return (M.nrows, M.ncols, M.rp, M.col, M.val)
+
+
+class Plan:
+    """An aires_plan plus references keeping its borrowed inputs alive."""
+
+    def __init__(self, handle, A, B, allocator, opts):
+        self.handle = handle
+        self._inputs = (A, B)
+        self.allocator = allocator
+        self.opts = opts
+
+    def close(self):
+        if self.handle:
+            B_.load().aires_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # noqa: BLE001 -- interpreter shutdown
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+
+def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: bool = False,
+              c_bound: int = B_.CBOUND_PRODUCTS, timing: bool = False, max_tile_rows: int = 0,
+              max_tile_bytes: int = 0, m_a_bytes: int = 0, dense_max_cols: int = 0,
+              hash_max_products: int = 0, wave_max_products: int = 0, torch_allocator: bool = True,
+              device: int = 0) -> Plan:
+    lib = B_.load()
+    a = B_.make_csr(*_parts(A))
+    b = B_.make_csr(*_parts(B))
+    o = B_.PlanOpts()
+    B_.check(lib.aires_plan_opts_default(ctypes.byref(o)), "aires_plan_opts_default")
+    o.validate = int(validate)
+    o.c_placement = B_.MEM_HOST_PINNED if c_on_host else B_.MEM_DEVICE
+    o.c_bound = c_bound
+    o.timing = int(timing)
+    o.max_tile_rows = max_tile_rows
+    o.max_tile_bytes = max_tile_bytes
+    o.m_a_bytes = m_a_bytes
+    o.dense_max_cols = dense_max_cols
+    o.hash_max_products = hash_max_products
+    o.wave_max_products = wave_max_products
+    alloc = None
+    if torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
+        alloc = B_.TorchAllocator(device)
+        o.allocator = ctypes.pointer(alloc.struct)
+    h = ctypes.c_void_p()
+    B_.check(lib.aires_tile_plan(ctypes.byref(a), ctypes.byref(b), int(hbm_budget), ctypes.byref(o),
+                                 ctypes.byref(h)), "aires_tile_plan")
+    return Plan(h.value, A, B, alloc, o)
+
+
+@dataclass
+class Info:
+    ntiles: int
+    m: int
+    k: int
+    n: int
+    budget: int
+    b_bytes: int
+    a_bytes: int
+    tile_budget: int
+    peak_bytes: int
+    c_bound_entries: int
+    a_streamed: bool
+    c_on_host: bool
+
+
+def plan_info(plan: Plan) -> Info:
+    i = B_.PlanInfo()
+    B_.check(B_.load().aires_plan_info_get(plan.handle, ctypes.byref(i)), "aires_plan_info_get")
+    return Info(*(getattr(i, f) for f, _ in B_.PlanInfo._fields_))
+
+
+def plan_tile(plan: Plan, t: int) -> dict:
+    x = B_.Tile()
+    B_.check(B_.load().aires_plan_tile(plan.handle, int(t), ctypes.byref(x)), "aires_plan_tile")
+    return {f: getattr(x, f) for f, _ in B_.Tile._fields_}
+
+
+def plan_tiles(plan: Plan) -> list[dict]:
+    return [plan_tile(plan, t) for t in range(plan_info(plan).ntiles)]
+
+
+def plan_stats(plan: Plan) -> dict:
+    s = B_.Stats()
+    B_.check(B_.load().aires_plan_stats(plan.handle, ctypes.byref(s)), "aires_plan_stats")
+    d = {f: getattr(s, f) for f, _ in B_.Stats._fields_ if f != "kind_ms"}
+    d["kind_ms"] = {ph: {B_.KIND_NAMES[k]: s.kind_ms[p][k] for k in range(len(B_.KIND_NAMES))}
+                    for p, ph in enumerate(("symbolic", "numeric"))}
+    return d
+
+
+class Output:
+    """C in CSR.  Device results are torch tensors owned by torch's
+    allocator; host results are numpy views of pinned memory owned by the
+    library until free() (or garbage collection)."""
+
+    def __init__(self, out: B_.CsrOut, allocator):
+        self.nrows, self.ncols, self.nnz = out.nrows, out.ncols, out.nnz
+        self.on_host = out.mem == B_.MEM_HOST_PINNED
+        self._out = out
+        if self.on_host or allocator is None:
+            if self.on_host:
+                import numpy as np
+                self.rp = np.ctypeslib.as_array(ctypes.cast(out.row_ptr, ctypes.POINTER(ctypes.c_int64)),
+                                                (self.nrows + 1,))
+                n = max(self.nnz, 0)
+                if n:
+                    self.col = np.ctypeslib.as_array(ctypes.cast(out.col_idx, ctypes.POINTER(ctypes.c_int32)), (n,))
+                    self.val = np.ctypeslib.as_array(ctypes.cast(out.vals, ctypes.POINTER(ctypes.c_float)), (n,))
+                else:
+                    self.col = np.zeros(0, np.int32)
+                    self.val = np.zeros(0, np.float32)
+            else:
+                raise RuntimeError("device output without the torch allocator is not wrapped")
+        else:
+            import torch
+            self.rp = allocator.take(out.row_ptr, torch.int64, self.nrows + 1)
+            self.col = allocator.take(out.col_idx, torch.int32, self.nnz)
+            self.val = allocator.take(out.vals, torch.float32, self.nnz)
+            B_.load().aires_csr_out_free(ctypes.byref(self._out))  # registry already released
+
+    def free(self):
+        if self._out is not None and self._out._owner:
+            self.rp = self.col = self.val = None
+            B_.load().aires_csr_out_free(ctypes.byref(self._out))
+        self._out = None
+
+    def __del__(self):
+        try:
+            if self.on_host:
+                self.free()
+        except Exception:  # noqa: BLE001
+            pass
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def spgemm(plan: Plan, stream=None) -> Output:
+    """C = A * B (aires_spgemm).  Work is enqueued on ``stream`` (torch's
+    current stream by default); C is valid once that stream reaches it."""
+    out = B_.CsrOut()
+    B_.check(B_.load().aires_spgemm(plan.handle, _stream_handle(stream), ctypes.byref(out)), "aires_spgemm")
+    return Output(out, plan.allocator)
+
+
+def stream_tiles(plan: Plan, h2d=None, compute=None, d2h=None) -> Output:
+    """Out-of-core C = A * B with A in pinned host memory (aires_stream_tiles)."""
+    import torch
+    h2d = h2d or torch.cuda.Stream()
+    d2h = d2h or torch.cuda.Stream()
+    out = B_.CsrOut()
+    B_.check(B_.load().aires_stream_tiles(plan.handle, _stream_handle(h2d), _stream_handle(compute),
+                                          _stream_handle(d2h), ctypes.byref(out)), "aires_stream_tiles")
+    return Output(out, plan.allocator)
+
+
+def to_device(M, device="cuda"):
+    """Copy a numpy CSR (nrows, ncols, rp, col, val) to device torch tensors."""
+    import torch
+    n, k, rp, col, val = _parts(M)
+    return (n, k, torch.from_numpy(rp).to(device), torch.from_numpy(col).to(device),
+            torch.from_numpy(val).to(device))
+
+
+def to_pinned(M):
+    import torch
+    n, k, rp, col, val = _parts(M)
+    return (n, k, torch.from_numpy(rp).pin_memory(), torch.from_numpy(col).pin_memory(),
+            torch.from_numpy(val).pin_memory())

@@ -1,0 +1,1054 @@
+// Host runtime of the library: the C-ABI of aires.h, the RoBW planner
+// (Sec. III-A, Algorithm 1; budget split after Eqs. 5-7), in-core execution
+// over device-resident tiles, and the out-of-core streaming schedule
+// (Sec. III-B, Algorithm 2).
+#include "../../include/aires.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace aires;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+aires_status fail(aires_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                 \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return fail(AIRES_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
+  } while (0)
+
+#define ST_TRY(expr)                       \
+  do {                                     \
+    aires_status s_ = (expr);              \
+    if (s_ != AIRES_OK) return s_;         \
+  } while (0)
+
+constexpr int64_t kDenseWaveMaxN = 2048;     // widest dense row one wavefront holds
+constexpr int64_t kDenseMaxCols = 16384;     // widest dense window of a workgroup
+constexpr int64_t kWaveMaxProducts = 8192;   // rows up to this go to one wavefront
+constexpr int64_t kHashMaxProducts = 4096;   // = 8192-slot table at load <= 1/2
+constexpr int64_t kFixedWorkspace = 4 << 20; // scan partials, counters, slack
+
+int64_t rp_bytes(const aires_csr& M) { return M.rp_type == AIRES_IDX_I64 ? 8 : 4; }
+int64_t csr_bytes(const aires_csr& M) { return (M.nrows + 1) * rp_bytes(M) + 8 * M.nnz; }
+
+int64_t host_rp(const aires_csr& M, int64_t i) {
+  return M.rp_type == AIRES_IDX_I64 ? static_cast<const int64_t*>(M.row_ptr)[i]
+                                    : (int64_t) static_cast<const int32_t*>(M.row_ptr)[i];
+}
+
+// --------------------------------------------------------------- allocator
+
+void* default_alloc(void*, size_t bytes, void* stream) {
+  void* p = nullptr;
+  if (bytes == 0) bytes = 256;
+  if (hipMallocAsync(&p, bytes, (hipStream_t)stream) != hipSuccess) {
+    (void)hipGetLastError();
+    p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+  }
+  return p;
+}
+
+void default_free(void*, void* p, void* stream) {
+  if (!p) return;
+  if (hipFreeAsync(p, (hipStream_t)stream) != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(p);
+  }
+}
+
+const aires_allocator kDefaultAllocator = {default_alloc, default_free, nullptr};
+
+// Device allocations of one call, released together (stream-ordered).
+struct DevPool {
+  aires_allocator a;
+  hipStream_t s;
+  std::vector<void*> live;
+  DevPool(const aires_allocator& al, hipStream_t st) : a(al), s(st) {}
+  ~DevPool() { release(); }
+  aires_status get(size_t bytes, void** out) {
+    void* p = a.alloc(a.ctx, bytes ? bytes : 256, (void*)s);
+    if (!p) return fail(AIRES_E_OOM, "device allocation of %zu bytes failed", bytes);
+    live.push_back(p);
+    *out = p;
+    return AIRES_OK;
+  }
+  template <typename T>
+  aires_status get_n(int64_t n, T** out) {
+    return get((size_t)std::max<int64_t>(n, 1) * sizeof(T), reinterpret_cast<void**>(out));
+  }
+  void release() {
+    for (void* p : live) a.free(a.ctx, p, (void*)s);
+    live.clear();
+  }
+  // hand ownership of p to the caller
+  void detach(void* p) { live.erase(std::remove(live.begin(), live.end(), p), live.end()); }
+};
+
+struct OutOwner {
+  aires_allocator a;
+  hipStream_t s;
+  int host;  // 1: hipHostMalloc'd arrays
+};
+
+}  // namespace
+
+// ------------------------------------------------------------------- plan
+
+struct aires_plan {
+  aires_csr A, B;
+  aires_plan_opts opts;
+  aires_allocator alloc;
+  int64_t budget;
+  std::vector<aires_tile> tiles;
+  aires_plan_info info;
+  aires_stats stats;
+  int busy = 0;
+  // kernel configuration
+  kern::BinThresholds th;
+  int wide = 0;
+  int32_t W = 0, nwin = 1;
+  // host copies needed for streaming
+  std::vector<int64_t> P_host;  // per-row products when computed on the host
+  // timing events of the last call
+  std::vector<hipEvent_t> ev;
+  struct Mark { int kind; int phase; int a, b; };  // elapsed(ev[a], ev[b])
+  std::vector<Mark> marks;
+  ~aires_plan() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  }
+};
+
+namespace {
+
+void bin_plan(aires_plan* p) {
+  const int64_t N = p->B.ncols;
+  const aires_plan_opts& o = p->opts;
+  const int64_t dense_max = o.dense_max_cols > 0 ? std::min<int64_t>(o.dense_max_cols, kDenseMaxCols) : kDenseMaxCols;
+  const int64_t wave_max = o.wave_max_products > 0 ? o.wave_max_products : kWaveMaxProducts;
+  const int64_t hash_max = o.hash_max_products > 0   ? std::min<int64_t>(o.hash_max_products, kHashMaxProducts)
+                           : o.hash_max_products < 0 ? 0  // < 0: no hash bins
+                                                     : kHashMaxProducts;
+  kern::BinThresholds& th = p->th;
+  std::memset(&th, 0, sizeof th);
+  int nb = 0;
+  auto add = [&](int kind, int64_t maxp) { th.kind[nb] = kind; th.max_p[nb] = maxp; ++nb; };
+  add(kern::KIND_EMPTY, 0);
+  if (N <= std::min(kDenseWaveMaxN, dense_max)) {
+    // narrow product: every row fits a dense LDS row
+    add(kern::KIND_DENSE_WAVE, wave_max);
+    add(kern::KIND_DENSE_BLOCK, INT64_MAX);
+    p->wide = 0;
+    p->W = (int32_t)std::max<int64_t>(N, 1);
+    p->nwin = 1;
+  } else {
+    // light rows hash in LDS (load factor <= 1/2: nnz(C_i) <= P_i <= slots/2)
+    if (hash_max > 0) add(kern::KIND_HASH_128, std::min<int64_t>(hash_max, 64));
+    if (hash_max > 64) add(kern::KIND_HASH_1024, std::min<int64_t>(hash_max, 512));
+    if (hash_max > 512) add(kern::KIND_HASH_8192, hash_max);
+    add(kern::KIND_DENSE_BLOCK, INT64_MAX);
+    if (N <= dense_max) {
+      p->wide = 0;
+      p->W = (int32_t)N;
+      p->nwin = 1;
+    } else {
+      p->wide = 1;
+      p->W = (int32_t)dense_max;
+      p->nwin = (int32_t)((N + dense_max - 1) / dense_max);
+    }
+  }
+  th.nb = nb;
+}
+
+aires_status check_csr_desc(const aires_csr* M, const char* name) {
+  if (!M) return fail(AIRES_E_INVALID_ARG, "%s is NULL", name);
+  if (M->nrows < 0 || M->ncols < 0 || M->nnz < 0)
+    return fail(AIRES_E_DIM, "%s has a negative size", name);
+  if (M->rp_type != AIRES_IDX_I32 && M->rp_type != AIRES_IDX_I64)
+    return fail(AIRES_E_INVALID_ARG, "%s.rp_type %d invalid", name, M->rp_type);
+  if (M->mem != AIRES_MEM_DEVICE && M->mem != AIRES_MEM_HOST_PINNED && M->mem != AIRES_MEM_HOST)
+    return fail(AIRES_E_INVALID_ARG, "%s.mem %d invalid", name, M->mem);
+  if (!M->row_ptr) return fail(AIRES_E_INVALID_ARG, "%s.row_ptr is NULL", name);
+  if (M->nnz > 0 && (!M->col_idx || !M->vals)) return fail(AIRES_E_INVALID_ARG, "%s arrays are NULL", name);
+  if (M->ncols > INT32_MAX) return fail(AIRES_E_OVERFLOW, "%s.ncols exceeds int32 column indices", name);
+  if (M->rp_type == AIRES_IDX_I32 && M->nnz > INT32_MAX)
+    return fail(AIRES_E_OVERFLOW, "%s.nnz needs int64 row pointers", name);
+  return AIRES_OK;
+}
+
+aires_status validate_host(const aires_csr& M, const char* name) {
+  if (host_rp(M, 0) != 0) return fail(AIRES_E_INVALID_CSR, "%s.row_ptr[0] != 0", name);
+  if (host_rp(M, M.nrows) != M.nnz) return fail(AIRES_E_INVALID_CSR, "%s.row_ptr[nrows] != nnz", name);
+  for (int64_t i = 0; i < M.nrows; ++i) {
+    const int64_t a = host_rp(M, i), b = host_rp(M, i + 1);
+    if (b < a) return fail(AIRES_E_INVALID_CSR, "%s.row_ptr decreases at row %lld", name, (long long)i);
+    for (int64_t q = a; q < b; ++q) {
+      const int32_t c = M.col_idx[q];
+      if (c < 0 || c >= M.ncols)
+        return fail(AIRES_E_INVALID_CSR, "%s column %d out of range in row %lld", name, c, (long long)i);
+      if (q > a && c <= M.col_idx[q - 1])
+        return fail(AIRES_E_INVALID_CSR, "%s columns not strictly increasing in row %lld", name, (long long)i);
+      if (!std::isfinite(M.vals[q])) return fail(AIRES_E_INVALID_CSR, "%s has a non-finite value", name);
+    }
+  }
+  return AIRES_OK;
+}
+
+// P_i on the host: A and B.rp in host memory; multithreaded over row ranges.
+void host_products(const aires_csr& A, const std::vector<int64_t>& brp, std::vector<int64_t>& P) {
+  const int64_t m = A.nrows;
+  P.assign((size_t)m, 0);
+  unsigned nt = std::max(1u, std::min(32u, std::thread::hardware_concurrency()));
+  if (m < 65536) nt = 1;
+  std::vector<std::thread> th;
+  for (unsigned t = 0; t < nt; ++t) {
+    th.emplace_back([&, t]() {
+      const int64_t r0 = m * t / nt, r1 = m * (t + 1) / nt;
+      for (int64_t i = r0; i < r1; ++i) {
+        int64_t s = 0;
+        for (int64_t q = host_rp(A, i); q < host_rp(A, i + 1); ++q) {
+          const int64_t k = A.col_idx[q];
+          s += brp[(size_t)k + 1] - brp[(size_t)k];
+        }
+        P[(size_t)i] = s;
+      }
+    });
+  }
+  for (auto& x : th) x.join();
+}
+
+aires_status host_row_ptr(const aires_csr& M, std::vector<int64_t>& out) {
+  out.resize((size_t)M.nrows + 1);
+  if (M.mem == AIRES_MEM_DEVICE) {
+    if (M.rp_type == AIRES_IDX_I64) {
+      HIP_TRY(hipMemcpy(out.data(), M.row_ptr, out.size() * 8, hipMemcpyDeviceToHost));
+    } else {
+      std::vector<int32_t> tmp(out.size());
+      HIP_TRY(hipMemcpy(tmp.data(), M.row_ptr, tmp.size() * 4, hipMemcpyDeviceToHost));
+      for (size_t i = 0; i < tmp.size(); ++i) out[i] = tmp[i];
+    }
+  } else {
+    for (int64_t i = 0; i <= M.nrows; ++i) out[(size_t)i] = host_rp(M, i);
+  }
+  return AIRES_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int aires_abi_version(void) { return AIRES_ABI_VERSION; }
+
+const char* aires_last_error(void) { return g_last_error.c_str(); }
+
+const char* aires_status_string(aires_status s) {
+  switch (s) {
+    case AIRES_OK: return "AIRES_OK";
+    case AIRES_E_INVALID_ARG: return "AIRES_E_INVALID_ARG";
+    case AIRES_E_INVALID_CSR: return "AIRES_E_INVALID_CSR";
+    case AIRES_E_DIM: return "AIRES_E_DIM";
+    case AIRES_E_BUDGET: return "AIRES_E_BUDGET";
+    case AIRES_E_OVERFLOW: return "AIRES_E_OVERFLOW";
+    case AIRES_E_OOM: return "AIRES_E_OOM";
+    case AIRES_E_HIP: return "AIRES_E_HIP";
+    case AIRES_E_STATE: return "AIRES_E_STATE";
+    case AIRES_E_UNSUPPORTED: return "AIRES_E_UNSUPPORTED";
+    case AIRES_E_CAPACITY: return "AIRES_E_CAPACITY";
+  }
+  return "AIRES_E_UNKNOWN";
+}
+
+aires_status aires_plan_opts_default(aires_plan_opts* o) {
+  if (!o) return fail(AIRES_E_INVALID_ARG, "opts is NULL");
+  std::memset(o, 0, sizeof *o);
+  o->struct_size = sizeof(aires_plan_opts);
+  o->c_placement = AIRES_MEM_DEVICE;
+  o->c_bound = AIRES_CBOUND_PRODUCTS;
+  return AIRES_OK;
+}
+
+aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hbm_budget,
+                             const aires_plan_opts* opts, aires_plan** out) {
+  if (!out) return fail(AIRES_E_INVALID_ARG, "out is NULL");
+  ST_TRY(check_csr_desc(A, "A"));
+  ST_TRY(check_csr_desc(B, "B"));
+  if (A->ncols != B->nrows)
+    return fail(AIRES_E_DIM, "A.ncols (%lld) != B.nrows (%lld)", (long long)A->ncols, (long long)B->nrows);
+  if (A->nrows > INT32_MAX - 1) return fail(AIRES_E_OVERFLOW, "A.nrows exceeds int32 row ids");
+  aires_plan_opts o;
+  aires_plan_opts_default(&o);
+  if (opts) {
+    if (opts->struct_size != sizeof(aires_plan_opts))
+      return fail(AIRES_E_INVALID_ARG, "opts.struct_size %u != %zu", opts->struct_size, sizeof(aires_plan_opts));
+    o = *opts;
+  }
+  if (o.c_placement != AIRES_MEM_DEVICE && o.c_placement != AIRES_MEM_HOST_PINNED)
+    return fail(AIRES_E_INVALID_ARG, "opts.c_placement %d invalid", o.c_placement);
+  if (o.c_bound < AIRES_CBOUND_PRODUCTS || o.c_bound > AIRES_CBOUND_PAPER_EQ5)
+    return fail(AIRES_E_INVALID_ARG, "opts.c_bound %d invalid", o.c_bound);
+  if (o.max_tile_rows < 0 || o.max_tile_bytes < 0 || o.m_a_bytes < 0)
+    return fail(AIRES_E_INVALID_ARG, "negative tile cap");
+  if (o.validate) {
+    if (A->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*A, "A"));
+    if (B->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*B, "B"));
+  }
+
+  const int a_streamed = A->mem != AIRES_MEM_DEVICE;
+  const int c_on_host = o.c_placement == AIRES_MEM_HOST_PINNED;
+  if (!a_streamed && c_on_host)
+    return fail(AIRES_E_UNSUPPORTED, "C in host memory needs A in host memory (streamed tiles)");
+
+  int64_t budget = (int64_t)hbm_budget;
+  if (budget == 0) {
+    size_t fr = 0, tot = 0;
+    HIP_TRY(hipMemGetInfo(&fr, &tot));
+    budget = (int64_t)fr;
+  }
+
+  auto* p = new aires_plan();
+  p->A = *A;
+  p->B = *B;
+  p->opts = o;
+  p->alloc = o.allocator ? *o.allocator : kDefaultAllocator;
+  p->budget = budget;
+  bin_plan(p);
+  const int64_t m = A->nrows, K = A->ncols, N = B->ncols;
+  const int64_t sA = rp_bytes(*A);
+  std::memset(&p->info, 0, sizeof p->info);
+  p->info.m = m;
+  p->info.k = K;
+  p->info.n = N;
+  p->info.budget = budget;
+  p->info.b_bytes = csr_bytes(*B);
+  p->info.a_bytes = csr_bytes(*A);
+  p->info.a_streamed = a_streamed;
+  p->info.c_on_host = c_on_host;
+  p->info.c_bound_entries = -1;
+
+  const int64_t nwin = p->nwin;
+  const int64_t index_bytes = p->wide ? 4 * (nwin + 1) * K : 0;
+  if (p->wide && B->nnz > INT32_MAX) {
+    delete p;
+    return fail(AIRES_E_UNSUPPORTED, "windowed path needs nnz(B) < 2^31");
+  }
+
+  std::vector<int64_t> arp;
+  aires_status st = host_row_ptr(*A, arp);
+  if (st != AIRES_OK) { delete p; return st; }
+
+  // Per-row and per-tile bytes of one tile slot.
+  // ws per row: P_i (8) + bin list (4) + window counts (4 per window) + C row
+  // pointer of the tile (8, streamed only).
+  std::vector<int64_t> cu;  // C bound per row (entries), streamed + host C
+  int64_t resident = p->info.b_bytes + kFixedWorkspace + index_bytes;
+  int64_t per_row_ws = 8 + 4 + (p->wide ? 4 * nwin : 0);
+  if (!a_streamed) {
+    // A and C.row_ptr resident; bin lists and window counts for all rows
+    resident += p->info.a_bytes + 8 * (m + 1) + (4 + (p->wide ? 4 * nwin : 0)) * m;
+    per_row_ws = 8;
+  } else if (o.m_a_bytes == 0) {
+    // C bound per row for the C slots (or for a device-resident C)
+    if (o.c_bound == AIRES_CBOUND_PRODUCTS) {
+      std::vector<int64_t> brp;
+      st = host_row_ptr(*B, brp);
+      if (st != AIRES_OK) { delete p; return st; }
+      host_products(*A, brp, p->P_host);
+      cu.resize((size_t)m);
+      int64_t tot = 0;
+      for (int64_t i = 0; i < m; ++i) { cu[(size_t)i] = std::min<int64_t>(N, p->P_host[(size_t)i]); tot += cu[(size_t)i]; }
+      p->info.c_bound_entries = tot;
+    } else if (o.c_bound == AIRES_CBOUND_DENSE) {
+      cu.assign((size_t)m, N);
+      p->info.c_bound_entries = m * N;
+    } else {
+      // Eq. 5 with alpha_A read as dense value bytes: M_C = 12 nnzA (1 + N/m + rho_B),
+      // shared out over rows in proportion to their A entries.
+      const double rhoB = (K > 0 && N > 0) ? (double)B->nnz / ((double)K * (double)N) : 0.0;
+      const double mc_entries = 12.0 * (double)A->nnz * (1.0 + (m ? (double)N / (double)m : 0.0) + rhoB) / 8.0;
+      cu.resize((size_t)m);
+      int64_t tot = 0;
+      for (int64_t i = 0; i < m; ++i) {
+        const double share = A->nnz ? mc_entries * (double)(arp[(size_t)i + 1] - arp[(size_t)i]) / (double)A->nnz : 0.0;
+        cu[(size_t)i] = std::min<int64_t>(N, (int64_t)std::ceil(share));
+        tot += cu[(size_t)i];
+      }
+      p->info.c_bound_entries = tot;
+    }
+    if (!c_on_host) resident += 8 * p->info.c_bound_entries + 8 * (m + 1);
+  }
+
+  const int nslots = a_streamed ? 2 : 1;
+  int64_t tile_budget;
+  if (o.m_a_bytes > 0) {
+    tile_budget = o.m_a_bytes;
+  } else {
+    if (resident >= budget) {
+      delete p;
+      return fail(AIRES_E_BUDGET, "budget %lld bytes cannot hold the resident %lld bytes", (long long)budget,
+                  (long long)resident);
+    }
+    tile_budget = (budget - resident) / nslots;
+  }
+  p->info.tile_budget = tile_budget;
+
+  // bytes of a slot holding rows [r0, r1)
+  auto slot_bytes = [&](int64_t r0, int64_t r1) -> int64_t {
+    const int64_t k = r1 - r0, q = arp[(size_t)r1] - arp[(size_t)r0];
+    if (o.m_a_bytes > 0) return (k + 1) * sA + 8 * q;  // calcMem of Algorithm 1
+    int64_t b = k * per_row_ws;
+    if (a_streamed) {
+      b += (k + 1) * sA + 8 * q;
+      if (c_on_host) {
+        int64_t c = 0;
+        for (int64_t i = r0; i < r1; ++i) c += cu[(size_t)i];
+        b += 8 * c + 8 * (k + 1);
+      }
+    }
+    return b;
+  };
+  // Greedy maximal blocks of whole rows (Algorithm 1).  Costs grow with
+  // every added row, so the longest feasible block is found by doubling
+  // and bisection; this yields exactly the linear scan's blocks.
+  std::vector<int64_t> cpre;
+  if (a_streamed && c_on_host && o.m_a_bytes == 0) {
+    cpre.assign((size_t)m + 1, 0);
+    for (int64_t i = 0; i < m; ++i) cpre[(size_t)i + 1] = cpre[(size_t)i] + cu[(size_t)i];
+  }
+  auto slot_bytes_fast = [&](int64_t r0, int64_t r1) -> int64_t {
+    if (cpre.empty()) return slot_bytes(r0, r1);
+    const int64_t k = r1 - r0, q = arp[(size_t)r1] - arp[(size_t)r0];
+    return k * per_row_ws + (k + 1) * sA + 8 * q + 8 * (cpre[(size_t)r1] - cpre[(size_t)r0]) + 8 * (k + 1);
+  };
+  auto fits = [&](int64_t r0, int64_t r1) -> bool {
+    if (o.max_tile_rows > 0 && r1 - r0 > o.max_tile_rows) return false;
+    if (o.max_tile_bytes > 0 && (r1 - r0 + 1) * sA + 8 * (arp[(size_t)r1] - arp[(size_t)r0]) > o.max_tile_bytes)
+      return false;
+    return slot_bytes_fast(r0, r1) <= tile_budget;
+  };
+  int64_t peak_slot = 0;
+  int64_t r0 = 0;
+  while (r0 < m) {
+    if (!fits(r0, r0 + 1)) {
+      const int64_t need = slot_bytes_fast(r0, r0 + 1);
+      delete p;
+      return fail(AIRES_E_BUDGET, "row %lld alone needs %lld bytes; a tile slot has %lld", (long long)r0,
+                  (long long)need, (long long)tile_budget);
+    }
+    int64_t lo = r0 + 1, step = 1;  // fits(r0, lo)
+    int64_t hi = -1;                // first end that does not fit
+    while (true) {
+      const int64_t cand = std::min(m, r0 + step * 2);
+      if (cand == lo) break;
+      if (fits(r0, cand)) {
+        lo = cand;
+        if (cand == m) break;
+        step *= 2;
+      } else {
+        hi = cand;
+        break;
+      }
+    }
+    if (hi > 0) {
+      while (hi - lo > 1) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (fits(r0, mid)) lo = mid; else hi = mid;
+      }
+    }
+    aires_tile t;
+    t.r0 = r0;
+    t.r1 = lo;
+    t.nnz0 = arp[(size_t)r0];
+    t.nnz1 = arp[(size_t)lo];
+    t.a_bytes = (lo - r0 + 1) * sA + 8 * (t.nnz1 - t.nnz0);
+    t.c_bound_entries = cpre.empty() ? -1 : cpre[(size_t)lo] - cpre[(size_t)r0];
+    t.tile_bytes = slot_bytes_fast(r0, lo);
+    peak_slot = std::max(peak_slot, t.tile_bytes);
+    p->tiles.push_back(t);
+    r0 = lo;
+  }
+  p->info.ntiles = (int64_t)p->tiles.size();
+  p->info.peak_bytes = resident + nslots * peak_slot;
+  std::memset(&p->stats, 0, sizeof p->stats);
+  *out = p;
+  return AIRES_OK;
+}
+
+aires_status aires_plan_info_get(const aires_plan* plan, aires_plan_info* info) {
+  if (!plan || !info) return fail(AIRES_E_INVALID_ARG, "NULL argument");
+  *info = plan->info;
+  return AIRES_OK;
+}
+
+aires_status aires_plan_tile(const aires_plan* plan, int64_t t, aires_tile* tile) {
+  if (!plan || !tile) return fail(AIRES_E_INVALID_ARG, "NULL argument");
+  if (t < 0 || t >= (int64_t)plan->tiles.size()) return fail(AIRES_E_INVALID_ARG, "tile %lld out of range", (long long)t);
+  *tile = plan->tiles[(size_t)t];
+  return AIRES_OK;
+}
+
+void aires_plan_destroy(aires_plan* plan) { delete plan; }
+
+}  // extern "C"
+
+// ------------------------------------------------------------- execution
+
+namespace {
+
+struct Timer {
+  aires_plan* p;
+  hipStream_t s;
+  bool on;
+  int record() {
+    if (!on) return -1;
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) { on = false; return -1; }
+    (void)hipEventRecord(e, s);
+    p->ev.push_back(e);
+    return (int)p->ev.size() - 1;
+  }
+  void mark(int kind, int phase, int a, int b) {
+    if (on && a >= 0 && b >= 0) p->marks.push_back({kind, phase, a, b});
+  }
+};
+
+void reset_timing(aires_plan* p) {
+  for (hipEvent_t e : p->ev) (void)hipEventDestroy(e);
+  p->ev.clear();
+  p->marks.clear();
+}
+
+kern::Operands tile_operands(const aires_plan* p, const void* arp, int64_t a_base, const int32_t* acol,
+                             const float* aval, const void* brp, const int32_t* bcol, const float* bval,
+                             const int32_t* bidx) {
+  kern::Operands op;
+  op.arp = arp;
+  op.rpa64 = p->A.rp_type == AIRES_IDX_I64;
+  op.a_base = a_base;
+  op.acol = acol;
+  op.aval = aval;
+  op.brp = brp;
+  op.rpb64 = p->B.rp_type == AIRES_IDX_I64;
+  op.bcol = bcol;
+  op.bval = bval;
+  op.K = p->B.nrows;
+  op.N = p->B.ncols;
+  op.bidx = p->wide ? bidx : nullptr;
+  op.W = p->W;
+  op.nwin = p->nwin;
+  return op;
+}
+
+// Phase markers for the stats: kinds >= 100 are whole phases.
+enum { PH_ANALYZE = 100, PH_BIN, PH_SYMBOLIC, PH_SCAN, PH_NUMERIC, PH_H2D, PH_D2H, PH_TOTAL, PH_INDEX };
+
+// analyze + bin + symbolic + scan of one tile; counts land in crp[1..n] and
+// are scanned in place on top of crp[0].
+aires_status tile_symbolic(aires_plan* p, const kern::Operands& op, int64_t n, int64_t* P, int32_t* list,
+                           int32_t* binoff, int32_t* cntcur, int32_t* wcnt, int64_t* crp, void* scan_ws,
+                           unsigned long long* prod_total, hipStream_t s, Timer& tm) {
+  const int e0 = tm.record();
+  HIP_TRY(kern::analyze(op, n, P, prod_total, s));
+  const int e1 = tm.record();
+  HIP_TRY(hipMemsetAsync(cntcur, 0, sizeof(int32_t) * 2 * kern::MAX_BINS, s));
+  HIP_TRY(kern::bin_rows(P, n, p->th, cntcur, binoff, list, s));
+  HIP_TRY(hipMemsetAsync(crp + 1, 0, sizeof(int64_t) * (size_t)std::max<int64_t>(n, 0), s));
+  const int e2 = tm.record();
+  kern::Outputs out{};
+  out.counts = crp + 1;
+  out.wcnt = wcnt;
+  for (int b = 0; b < p->th.nb; ++b) {
+    const int kind = p->th.kind[b];
+    if (kind == kern::KIND_EMPTY) continue;
+    kern::BinView bv{list, binoff, b};
+    const int ka = tm.record();
+    HIP_TRY(kern::run_bin(kind, 0, op, bv, out, n, s));
+    if (kind == kern::KIND_DENSE_BLOCK && p->wide)
+      HIP_TRY(kern::window_rowsum(bv, p->nwin, wcnt, crp + 1, n, s));
+    tm.mark(kind, 0, ka, tm.record());
+  }
+  const int e3 = tm.record();
+  HIP_TRY(kern::scan_inplace(crp + 1, n, scan_ws, s));
+  const int e4 = tm.record();
+  tm.mark(PH_ANALYZE, 0, e0, e1);
+  tm.mark(PH_BIN, 0, e1, e2);
+  tm.mark(PH_SYMBOLIC, 0, e2, e3);
+  tm.mark(PH_SCAN, 0, e3, e4);
+  return AIRES_OK;
+}
+
+aires_status tile_numeric(aires_plan* p, const kern::Operands& op, int64_t n, const int32_t* list,
+                          const int32_t* binoff, int32_t* wcnt, const int64_t* crp, int32_t* ccol, float* cval,
+                          int64_t c_base, hipStream_t s, Timer& tm) {
+  kern::Outputs out{};
+  out.wcnt = wcnt;
+  out.crp = crp;
+  out.ccol = ccol - c_base;
+  out.cval = cval - c_base;
+  const int e0 = tm.record();
+  for (int b = 0; b < p->th.nb; ++b) {
+    const int kind = p->th.kind[b];
+    if (kind == kern::KIND_EMPTY) continue;
+    kern::BinView bv{list, binoff, b};
+    const int ka = tm.record();
+    HIP_TRY(kern::run_bin(kind, 1, op, bv, out, n, s));
+    tm.mark(kind, 1, ka, tm.record());
+    p->stats.numeric_launches++;
+  }
+  tm.mark(PH_NUMERIC, 1, e0, tm.record());
+  return AIRES_OK;
+}
+
+aires_status begin_call(aires_plan* p, aires_csr_out* C) {
+  if (!p || !C) return fail(AIRES_E_INVALID_ARG, "NULL argument");
+  if (p->busy) return fail(AIRES_E_STATE, "plan is in use");
+  if (C->row_ptr || C->col_idx || C->vals || C->_owner)
+    return fail(AIRES_E_STATE, "output descriptor is not zeroed (free it first)");
+  std::memset(&p->stats, 0, sizeof p->stats);
+  p->stats.ntiles = (int64_t)p->tiles.size();
+  reset_timing(p);
+  return AIRES_OK;
+}
+
+aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
+  const int64_t m = p->A.nrows, K = p->B.nrows, N = p->B.ncols;
+  const int64_t sA = rp_bytes(p->A);
+  Timer tm{p, s, p->opts.timing != 0};
+  const int e_total0 = tm.record();
+  DevPool ws(p->alloc, s);
+  int64_t max_rows = 1;
+  for (const auto& t : p->tiles) max_rows = std::max(max_rows, t.r1 - t.r0);
+  const int64_t nt = (int64_t)p->tiles.size();
+
+  int64_t* crp = nullptr;
+  ST_TRY(ws.get_n(m + 1, &crp));
+  int64_t* P = nullptr;
+  int32_t *list = nullptr, *binoff = nullptr, *cntcur = nullptr, *wcnt = nullptr, *bidx = nullptr;
+  unsigned long long* prod = nullptr;
+  void* scan_ws = nullptr;
+  ST_TRY(ws.get_n(max_rows, &P));
+  ST_TRY(ws.get_n(m, &list));
+  ST_TRY(ws.get_n(nt * (kern::MAX_BINS + 1), &binoff));
+  ST_TRY(ws.get_n(2 * kern::MAX_BINS, &cntcur));
+  ST_TRY(ws.get_n(1, &prod));
+  ST_TRY(ws.get(kern::scan_workspace_bytes(max_rows), &scan_ws));
+  if (p->wide) {
+    ST_TRY(ws.get_n(m * (int64_t)p->nwin, &wcnt));
+    ST_TRY(ws.get_n(((int64_t)p->nwin + 1) * K, &bidx));
+  }
+  HIP_TRY(hipMemsetAsync(crp, 0, sizeof(int64_t), s));
+  HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long), s));
+  if (p->wide) {
+    const int ea = tm.record();
+    HIP_TRY(kern::build_window_index(p->B.row_ptr, p->B.rp_type == AIRES_IDX_I64, p->B.col_idx, K, p->W,
+                                     p->nwin, bidx, s));
+    tm.mark(PH_INDEX, 0, ea, tm.record());
+  }
+
+  // Sweep 1: symbolic phase of every tile; C.row_ptr grows tile by tile.
+  for (int64_t t = 0; t < nt; ++t) {
+    const aires_tile& T = p->tiles[(size_t)t];
+    const int64_t n = T.r1 - T.r0;
+    const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
+    kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, p->A.vals, p->B.row_ptr, p->B.col_idx,
+                                      p->B.vals, bidx);
+    ST_TRY(tile_symbolic(p, op, n, P, list + T.r0, binoff + t * (kern::MAX_BINS + 1), cntcur,
+                         wcnt ? wcnt + T.r0 * p->nwin : nullptr, crp + T.r0, scan_ws, prod, s, tm));
+  }
+  // The one host synchronisation: nnz(C) decides C's allocation.
+  int64_t nnz = 0;
+  unsigned long long products = 0;
+  HIP_TRY(hipMemcpyAsync(&nnz, crp + m, sizeof nnz, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(&products, prod, sizeof products, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  p->stats.host_syncs = 1;
+  p->stats.products = (int64_t)products;
+  p->stats.nnz_c = nnz;
+  const int64_t resident = p->info.b_bytes + p->info.a_bytes + 8 * (m + 1);
+  if (resident + 8 * nnz > p->budget)
+    return fail(AIRES_E_BUDGET, "C needs %lld bytes; budget %lld leaves %lld", (long long)(8 * nnz),
+                (long long)p->budget, (long long)(p->budget - resident));
+  int32_t* ccol = nullptr;
+  float* cval = nullptr;
+  ST_TRY(ws.get_n(nnz, &ccol));
+  ST_TRY(ws.get_n(nnz, &cval));
+
+  // Sweep 2: numeric phase of every tile.
+  for (int64_t t = 0; t < nt; ++t) {
+    const aires_tile& T = p->tiles[(size_t)t];
+    const int64_t n = T.r1 - T.r0;
+    const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
+    kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, p->A.vals, p->B.row_ptr, p->B.col_idx,
+                                      p->B.vals, bidx);
+    ST_TRY(tile_numeric(p, op, n, list + T.r0, binoff + t * (kern::MAX_BINS + 1),
+                        wcnt ? wcnt + T.r0 * p->nwin : nullptr, crp + T.r0, ccol, cval, 0, s, tm));
+  }
+  tm.mark(PH_TOTAL, 0, e_total0, tm.record());
+
+  // hand C to the caller
+  ws.detach(crp);
+  ws.detach(ccol);
+  ws.detach(cval);
+  auto* own = new OutOwner{p->alloc, s, 0};
+  C->nrows = m;
+  C->ncols = N;
+  C->nnz = nnz;
+  C->row_ptr = crp;
+  C->col_idx = ccol;
+  C->vals = cval;
+  C->mem = AIRES_MEM_DEVICE;
+  C->_owner = own;
+  return AIRES_OK;  // ws releases the workspace stream-ordered on s
+}
+
+// Out-of-core schedule (Algorithm 2): B resident (Phase I), A tiles
+// double-buffered host->device (Phase II), C tiles device->host (Phase III).
+aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStream_t sd, aires_csr_out* C) {
+  const aires_csr& A = p->A;
+  const aires_csr& B = p->B;
+  const int64_t m = A.nrows, K = B.nrows, N = B.ncols;
+  const int64_t sA = rp_bytes(A), sB = rp_bytes(B);
+  const int c_on_host = p->opts.c_placement == AIRES_MEM_HOST_PINNED;
+  if (A.mem != AIRES_MEM_HOST_PINNED) return fail(AIRES_E_UNSUPPORTED, "streaming needs A in pinned host memory");
+  if (B.mem == AIRES_MEM_HOST) return fail(AIRES_E_UNSUPPORTED, "B in pageable host memory");
+  if (p->info.c_bound_entries < 0) return fail(AIRES_E_STATE, "plan has no C bound (Algorithm 1 planning mode)");
+  Timer tm{p, sc, p->opts.timing != 0};
+  const int e_total0 = tm.record();
+  DevPool ws(p->alloc, sc);
+  const int64_t nt = (int64_t)p->tiles.size();
+  int64_t max_rows = 1, max_q = 1, max_cb = 1;
+  for (const auto& t : p->tiles) {
+    max_rows = std::max(max_rows, t.r1 - t.r0);
+    max_q = std::max(max_q, t.nnz1 - t.nnz0);
+    max_cb = std::max(max_cb, t.c_bound_entries);
+  }
+  const int64_t cap = p->info.c_bound_entries;
+
+  // output arrays
+  int64_t* C_rp = nullptr;
+  int32_t* C_col = nullptr;
+  float* C_val = nullptr;
+  struct HostBufs {
+    std::vector<void*> v;
+    ~HostBufs() { for (void* x : v) (void)hipHostFree(x); }
+  } hb;
+  // Destroyed first on every exit: no copy or kernel may still touch the
+  // workspace or host buffers when they are released.
+  struct Drain {
+    hipStream_t a, b, c;
+    ~Drain() { (void)hipStreamSynchronize(a); (void)hipStreamSynchronize(b); (void)hipStreamSynchronize(c); }
+  } drain{sh, sc, sd};
+  if (c_on_host) {
+    HIP_TRY(hipHostMalloc((void**)&C_rp, sizeof(int64_t) * (size_t)(m + 1), hipHostMallocDefault));
+    hb.v.push_back(C_rp);
+    HIP_TRY(hipHostMalloc((void**)&C_col, sizeof(int32_t) * (size_t)std::max<int64_t>(cap, 1), hipHostMallocDefault));
+    hb.v.push_back(C_col);
+    HIP_TRY(hipHostMalloc((void**)&C_val, sizeof(float) * (size_t)std::max<int64_t>(cap, 1), hipHostMallocDefault));
+    hb.v.push_back(C_val);
+  } else {
+    ST_TRY(ws.get_n(m + 1, &C_rp));
+    ST_TRY(ws.get_n(cap, &C_col));
+    ST_TRY(ws.get_n(cap, &C_val));
+  }
+
+  // Phase I: B resident on the device
+  const void* brp = B.row_ptr;
+  const int32_t* bcol = B.col_idx;
+  const float* bval = B.vals;
+  void *d_brp = nullptr, *d_bcol = nullptr, *d_bval = nullptr;
+  const int eh0 = tm.record();
+  if (B.mem != AIRES_MEM_DEVICE) {
+    ST_TRY(ws.get((size_t)(K + 1) * sB, &d_brp));
+    ST_TRY(ws.get((size_t)std::max<int64_t>(B.nnz, 1) * 4, &d_bcol));
+    ST_TRY(ws.get((size_t)std::max<int64_t>(B.nnz, 1) * 4, &d_bval));
+    HIP_TRY(hipMemcpyAsync(d_brp, B.row_ptr, (size_t)(K + 1) * sB, hipMemcpyHostToDevice, sh));
+    HIP_TRY(hipMemcpyAsync(d_bcol, B.col_idx, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
+    HIP_TRY(hipMemcpyAsync(d_bval, B.vals, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
+    p->stats.h2d_bytes += (K + 1) * sB + 8 * B.nnz;
+    brp = d_brp;
+    bcol = (const int32_t*)d_bcol;
+    bval = (const float*)d_bval;
+  }
+
+  // two slots of everything a tile needs on the device
+  struct Slot {
+    void* arp; int32_t* acol; float* aval;
+    int64_t* P; int32_t* list; int32_t* binoff; int32_t* cntcur; int32_t* wcnt;
+    int64_t* crp; int32_t* ccol; float* cval; int64_t ccap;
+    void* scan_ws;
+  } slot[2];
+  int32_t* bidx = nullptr;
+  unsigned long long* prod = nullptr;
+  int64_t* running = nullptr;
+  ST_TRY(ws.get_n(1, &prod));
+  ST_TRY(ws.get_n(1, &running));
+  if (p->wide) ST_TRY(ws.get_n(((int64_t)p->nwin + 1) * K, &bidx));
+  for (int s = 0; s < 2; ++s) {
+    Slot& S = slot[s];
+    std::memset(&S, 0, sizeof S);
+    ST_TRY(ws.get((size_t)(max_rows + 1) * sA, &S.arp));
+    ST_TRY(ws.get_n(max_q, &S.acol));
+    ST_TRY(ws.get_n(max_q, &S.aval));
+    ST_TRY(ws.get_n(max_rows, &S.P));
+    ST_TRY(ws.get_n(max_rows, &S.list));
+    ST_TRY(ws.get_n(kern::MAX_BINS + 1, &S.binoff));
+    ST_TRY(ws.get_n(2 * kern::MAX_BINS, &S.cntcur));
+    if (p->wide) ST_TRY(ws.get_n(max_rows * (int64_t)p->nwin, &S.wcnt));
+    ST_TRY(ws.get_n(max_rows + 1, &S.crp));
+    ST_TRY(ws.get(kern::scan_workspace_bytes(max_rows), &S.scan_ws));
+    if (c_on_host) {
+      ST_TRY(ws.get_n(max_cb, &S.ccol));
+      ST_TRY(ws.get_n(max_cb, &S.cval));
+      S.ccap = max_cb;
+    }
+  }
+  int64_t* nnz_host = nullptr;  // pinned per-tile running totals
+  HIP_TRY(hipHostMalloc((void**)&nnz_host, sizeof(int64_t) * (size_t)std::max<int64_t>(nt, 1), hipHostMallocDefault));
+  hb.v.push_back(nnz_host);
+  HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long), sc));
+  HIP_TRY(hipMemsetAsync(running, 0, sizeof(int64_t), sc));
+
+  std::vector<hipEvent_t> evs;
+  struct EvGuard {
+    std::vector<hipEvent_t>& v;
+    ~EvGuard() { for (hipEvent_t e : v) (void)hipEventDestroy(e); }
+  } eg{evs};
+  auto mkev = [&](hipEvent_t* e) -> aires_status {
+    HIP_TRY(hipEventCreateWithFlags(e, hipEventDisableTiming));
+    evs.push_back(*e);
+    return AIRES_OK;
+  };
+  std::vector<hipEvent_t> ev_in(nt), ev_cnt(nt), ev_done(nt);
+  hipEvent_t ev_cfree[2] = {nullptr, nullptr};
+  for (int64_t t = 0; t < nt; ++t) {
+    ST_TRY(mkev(&ev_in[(size_t)t]));
+    ST_TRY(mkev(&ev_cnt[(size_t)t]));
+    ST_TRY(mkev(&ev_done[(size_t)t]));
+  }
+  ST_TRY(mkev(&ev_cfree[0]));
+  ST_TRY(mkev(&ev_cfree[1]));
+  hipEvent_t ev_ws;  // workspace allocations (on sc) complete before h2d uses them
+  ST_TRY(mkev(&ev_ws));
+  HIP_TRY(hipEventRecord(ev_ws, sc));
+  HIP_TRY(hipStreamWaitEvent(sh, ev_ws, 0));
+
+  auto issue_h2d = [&](int64_t t) -> aires_status {
+    const aires_tile& T = p->tiles[(size_t)t];
+    Slot& S = slot[t % 2];
+    if (t >= 2) HIP_TRY(hipStreamWaitEvent(sh, ev_done[(size_t)t - 2], 0));
+    const int64_t k = T.r1 - T.r0, q = T.nnz1 - T.nnz0;
+    HIP_TRY(hipMemcpyAsync(S.arp, static_cast<const char*>(A.row_ptr) + T.r0 * sA, (size_t)(k + 1) * sA,
+                           hipMemcpyHostToDevice, sh));
+    if (q > 0) {
+      HIP_TRY(hipMemcpyAsync(S.acol, A.col_idx + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
+      HIP_TRY(hipMemcpyAsync(S.aval, A.vals + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
+    }
+    HIP_TRY(hipEventRecord(ev_in[(size_t)t], sh));
+    p->stats.h2d_bytes += (k + 1) * sA + 8 * q;
+    return AIRES_OK;
+  };
+
+  if (nt > 0) ST_TRY(issue_h2d(0));
+  if (nt > 1) ST_TRY(issue_h2d(1));
+  const int eh1 = tm.record();
+  tm.mark(PH_H2D, 0, eh0, eh1);
+  if (p->wide) {
+    HIP_TRY(hipStreamWaitEvent(sc, ev_in[0], 0));  // B is resident once tile 0 arrived
+    HIP_TRY(kern::build_window_index(brp, B.rp_type == AIRES_IDX_I64, bcol, K, p->W, p->nwin, bidx, sc));
+  }
+  int64_t base = 0;
+  for (int64_t t = 0; t < nt; ++t) {
+    const aires_tile& T = p->tiles[(size_t)t];
+    Slot& S = slot[t % 2];
+    const int64_t k = T.r1 - T.r0;
+    HIP_TRY(hipStreamWaitEvent(sc, ev_in[(size_t)t], 0));
+    if (t >= 2 && c_on_host) HIP_TRY(hipStreamWaitEvent(sc, ev_cfree[t % 2], 0));
+    kern::Operands op = tile_operands(p, S.arp, T.nnz0, S.acol, S.aval, brp, bcol, bval, bidx);
+    // running base of C.row_ptr for this tile: crp[0] = total so far
+    HIP_TRY(hipMemcpyAsync(S.crp, running, sizeof(int64_t), hipMemcpyDeviceToDevice, sc));
+    ST_TRY(tile_symbolic(p, op, k, S.P, S.list, S.binoff, S.cntcur, S.wcnt, S.crp, S.scan_ws, prod, sc, tm));
+    HIP_TRY(hipMemcpyAsync(running, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToDevice, sc));
+    HIP_TRY(hipMemcpyAsync(nnz_host + t, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
+    HIP_TRY(hipEventRecord(ev_cnt[(size_t)t], sc));
+    HIP_TRY(hipEventSynchronize(ev_cnt[(size_t)t]));
+    p->stats.host_syncs++;
+    const int64_t end = nnz_host[t];
+    const int64_t nnz_t = end - base;
+    if (end > cap)
+      return fail(AIRES_E_CAPACITY, "C needs more than the planned bound of %lld entries (tile %lld)",
+                  (long long)cap, (long long)t);
+    if (c_on_host && nnz_t > S.ccap) {
+      // the bound was an estimate (Eq. 5 mode): grow this slot
+      HIP_TRY(hipStreamWaitEvent(sc, ev_cfree[t % 2], 0));
+      ws.a.free(ws.a.ctx, S.ccol, (void*)sc);
+      ws.detach(S.ccol);
+      ws.a.free(ws.a.ctx, S.cval, (void*)sc);
+      ws.detach(S.cval);
+      ST_TRY(ws.get_n(nnz_t, &S.ccol));
+      ST_TRY(ws.get_n(nnz_t, &S.cval));
+      S.ccap = nnz_t;
+    }
+    if (c_on_host) {
+      ST_TRY(tile_numeric(p, op, k, S.list, S.binoff, S.wcnt, S.crp, S.ccol, S.cval, base, sc, tm));
+    } else {
+      ST_TRY(tile_numeric(p, op, k, S.list, S.binoff, S.wcnt, S.crp, C_col, C_val, 0, sc, tm));
+    }
+    HIP_TRY(hipEventRecord(ev_done[(size_t)t], sc));
+    // Phase III for this tile
+    if (c_on_host) {
+      HIP_TRY(hipStreamWaitEvent(sd, ev_done[(size_t)t], 0));
+      HIP_TRY(hipMemcpyAsync(C_rp + T.r0 + 1, S.crp + 1, sizeof(int64_t) * (size_t)k, hipMemcpyDeviceToHost, sd));
+      if (nnz_t > 0) {
+        HIP_TRY(hipMemcpyAsync(C_col + base, S.ccol, sizeof(int32_t) * (size_t)nnz_t, hipMemcpyDeviceToHost, sd));
+        HIP_TRY(hipMemcpyAsync(C_val + base, S.cval, sizeof(float) * (size_t)nnz_t, hipMemcpyDeviceToHost, sd));
+      }
+      HIP_TRY(hipEventRecord(ev_cfree[t % 2], sd));
+      p->stats.d2h_bytes += 8 * k + 8 * nnz_t;
+    } else {
+      HIP_TRY(hipMemcpyAsync(C_rp + T.r0 + 1, S.crp + 1, sizeof(int64_t) * (size_t)k, hipMemcpyDeviceToDevice, sc));
+    }
+    base = end;
+    if (t + 2 < nt) ST_TRY(issue_h2d(t + 2));
+  }
+  HIP_TRY(hipStreamSynchronize(sd));
+  HIP_TRY(hipStreamSynchronize(sh));
+  tm.mark(PH_TOTAL, 0, e_total0, tm.record());
+  unsigned long long products = 0;
+  HIP_TRY(hipMemcpyAsync(&products, prod, sizeof products, hipMemcpyDeviceToHost, sc));
+  HIP_TRY(hipStreamSynchronize(sc));
+  p->stats.products = (int64_t)products;
+  p->stats.nnz_c = base;
+  if (c_on_host) C_rp[0] = 0;
+  else HIP_TRY(hipMemsetAsync(C_rp, 0, sizeof(int64_t), sc));
+
+  auto* own = new OutOwner{p->alloc, sc, c_on_host};
+  if (c_on_host) {
+    hb.v.erase(std::remove(hb.v.begin(), hb.v.end(), (void*)C_rp), hb.v.end());
+    hb.v.erase(std::remove(hb.v.begin(), hb.v.end(), (void*)C_col), hb.v.end());
+    hb.v.erase(std::remove(hb.v.begin(), hb.v.end(), (void*)C_val), hb.v.end());
+  } else {
+    ws.detach(C_rp);
+    ws.detach(C_col);
+    ws.detach(C_val);
+  }
+  C->nrows = m;
+  C->ncols = N;
+  C->nnz = base;
+  C->row_ptr = C_rp;
+  C->col_idx = C_col;
+  C->vals = C_val;
+  C->mem = c_on_host ? AIRES_MEM_HOST_PINNED : AIRES_MEM_DEVICE;
+  C->_owner = own;
+  HIP_TRY(hipStreamSynchronize(sc));
+  return AIRES_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+aires_status aires_spgemm(aires_plan* plan, void* stream, aires_csr_out* C) {
+  ST_TRY(begin_call(plan, C));
+  if (plan->A.mem != AIRES_MEM_DEVICE) {
+    hipStream_t sh = nullptr, sd = nullptr;
+    HIP_TRY(hipStreamCreateWithFlags(&sh, hipStreamNonBlocking));
+    if (hipStreamCreateWithFlags(&sd, hipStreamNonBlocking) != hipSuccess) {
+      (void)hipStreamDestroy(sh);
+      return fail(AIRES_E_HIP, "hipStreamCreate failed");
+    }
+    plan->busy = 1;
+    aires_status st = stream_impl(plan, sh, (hipStream_t)stream, sd, C);
+    plan->busy = 0;
+    (void)hipStreamSynchronize(sh);
+    (void)hipStreamSynchronize(sd);
+    (void)hipStreamDestroy(sh);
+    (void)hipStreamDestroy(sd);
+    return st;
+  }
+  if (plan->B.mem != AIRES_MEM_DEVICE)
+    return fail(AIRES_E_UNSUPPORTED, "device-resident A needs device-resident B");
+  plan->busy = 1;
+  aires_status st = spgemm_device(plan, (hipStream_t)stream, C);
+  plan->busy = 0;
+  return st;
+}
+
+aires_status aires_stream_tiles(aires_plan* plan, void* h2d, void* compute, void* d2h, aires_csr_out* C) {
+  ST_TRY(begin_call(plan, C));
+  plan->busy = 1;
+  aires_status st = stream_impl(plan, (hipStream_t)h2d, (hipStream_t)compute, (hipStream_t)d2h, C);
+  plan->busy = 0;
+  return st;
+}
+
+aires_status aires_plan_stats(const aires_plan* plan, aires_stats* stats) {
+  if (!plan || !stats) return fail(AIRES_E_INVALID_ARG, "NULL argument");
+  *stats = plan->stats;
+  if (!plan->ev.empty()) {
+    HIP_TRY(hipEventSynchronize(plan->ev.back()));
+    for (const auto& mk : plan->marks) {
+      float ms = 0.f;
+      HIP_TRY(hipEventElapsedTime(&ms, plan->ev[(size_t)mk.a], plan->ev[(size_t)mk.b]));
+      switch (mk.kind) {
+        case PH_ANALYZE: stats->analyze_ms += ms; break;
+        case PH_BIN: stats->bin_ms += ms; break;
+        case PH_SYMBOLIC: stats->symbolic_ms += ms; break;
+        case PH_SCAN: stats->scan_ms += ms; break;
+        case PH_NUMERIC: stats->numeric_ms += ms; break;
+        case PH_H2D: stats->h2d_ms += ms; break;
+        case PH_D2H: stats->d2h_ms += ms; break;
+        case PH_TOTAL: stats->total_ms += ms; break;
+        default:
+          if (mk.kind >= 0 && mk.kind < 8) stats->kind_ms[mk.phase][mk.kind] += ms;
+          break;
+      }
+    }
+  }
+  return AIRES_OK;
+}
+
+void aires_csr_out_free(aires_csr_out* C) {
+  if (!C) return;
+  auto* own = static_cast<OutOwner*>(C->_owner);
+  if (own) {
+    if (own->host) {
+      if (C->row_ptr) (void)hipHostFree(C->row_ptr);
+      if (C->col_idx) (void)hipHostFree(C->col_idx);
+      if (C->vals) (void)hipHostFree(C->vals);
+    } else {
+      if (C->row_ptr) own->a.free(own->a.ctx, C->row_ptr, (void*)own->s);
+      if (C->col_idx) own->a.free(own->a.ctx, C->col_idx, (void*)own->s);
+      if (C->vals) own->a.free(own->a.ctx, C->vals, (void*)own->s);
+    }
+    delete own;
+  }
+  std::memset(C, 0, sizeof *C);
+}
+
+}  // extern "C"

@@ -1,0 +1,308 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle.
+
+Bar: C.row_ptr and C.col_idx bit-exact; values within
+|c - ref| <= 1e-5 * (1 + |ref|) (fp32 accumulation in any order).  Every
+kernel path is forced on its own through the plan options, on seeded
+inputs shaped like the five aggregation workloads (scaled down so the
+oracle finishes in seconds, spanning several tiles/windows and ragged
+tails), plus edge cases and sampled rows at full size."""
+import json
+import os
+import sys
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from workloads import CSR
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    return torch
+
+
+def say(msg):
+    print("[gpu-case] " + msg, flush=True)
+    sys.stdout.flush()
+
+
+def run(torch, A, B, budget=0, **kw):
+    import paper_2507_02006_amd as aires
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    with aires.tile_plan(dA, dB, budget, timing=True, **kw) as plan:
+        C = aires.spgemm(plan)
+        torch.cuda.synchronize()
+        st = aires.plan_stats(plan)
+        ntiles = aires.plan_info(plan).ntiles
+    return C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), st, ntiles
+
+
+def assert_match(rp, col, val, ref, r0=0):
+    assert rp.dtype == np.int64
+    base = rp[0]
+    assert np.array_equal(rp - base, ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    err = np.abs(val.astype(np.float64) - ref.val.astype(np.float64))
+    bad = err > TOL * (1 + np.abs(ref.val.astype(np.float64)))
+    assert not bad.any(), "values differ at %d entries, max err %g" % (bad.sum(), err.max())
+
+
+def check(torch, A, B, name, **kw):
+    say("%s m=%d K=%d N=%d nnzA=%d nnzB=%d opts=%s" % (name, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, kw))
+    ref = oracle.spgemm(A, B)
+    rp, col, val, st, nt = run(torch, A, B, **kw)
+    assert_match(rp, col, val, ref)
+    assert st["products"] == ref.products
+    assert st["nnz_c"] == ref.nnz
+    return st, nt, ref
+
+
+# ------------------------------------------------------------ golden / tiny
+
+def test_hand_4x4(torch_gpu, golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "hand_4x4.json")))
+    mk = lambda d: CSR(d["nrows"], d["ncols"], np.array(d["rp"], np.int32), np.array(d["col"], np.int32),
+                       np.array(d["val"], np.float32))
+    A, B = mk(g["A"]), mk(g["B"])
+    for kw in ({}, {"wave_max_products": 1}):
+        rp, col, val, st, _ = run(torch_gpu, A, B, **kw)
+        assert rp.tolist() == g["C"]["rp"] and col.tolist() == g["C"]["col"]
+        assert val.tolist() == g["C"]["val"]
+
+
+PATHS = {
+    # narrow N (<= 2048): wavefront rows, workgroup rows
+    "dense_wave": dict(),
+    "dense_block": dict(wave_max_products=1),
+    # wide N through forced small windows: LDS hash bins and windowed dense rows
+    "windows_only": dict(dense_max_cols=64, hash_max_products=-1),
+    "hash128_then_windows": dict(dense_max_cols=96, hash_max_products=64),
+    "hash1024_then_windows": dict(dense_max_cols=128, hash_max_products=512),
+    "hash8192_then_windows": dict(dense_max_cols=160, hash_max_products=4096),
+}
+
+
+@pytest.mark.parametrize("path", list(PATHS))
+def test_each_path_integer_values_exact(torch_gpu, path):
+    """Integer values: every product and partial sum is exact in fp32, so
+    values are bit-exact whatever the summation order."""
+    rng = np.random.default_rng(zlib.crc32(path.encode()))
+    A = workloads.random_csr(rng, 700, 300, 0.03, values="int")
+    B = workloads.random_csr(rng, 300, 333, 0.05, values="int")
+    say("int-exact %s" % path)
+    ref = oracle.spgemm(A, B)
+    rp, col, val, st, _ = run(torch_gpu, A, B, **PATHS[path])
+    assert np.array_equal(rp, ref.rp) and np.array_equal(col, ref.col)
+    assert np.array_equal(val, ref.val)
+
+
+@pytest.mark.parametrize("path", list(PATHS))
+def test_each_path_cfg1(torch_gpu, path):
+    A, B = workloads.workload(1)
+    check(torch_gpu, A, B, "cfg1/" + path, **PATHS[path])
+
+
+# --------------------------------------------------- scaled workload shapes
+
+def test_cfg2_scaled(torch_gpu):
+    A, B = workloads.workload(2, n=32768)
+    check(torch_gpu, A, B, "cfg2 n=32768")
+
+
+def test_cfg3_scaled_wide(torch_gpu):
+    """A*A with N = 40000 > 16384: hash bins plus 3 column windows (ragged)."""
+    A, B = workloads.workload(3, n=40000)
+    st, _, _ = check(torch_gpu, A, B, "cfg3 n=40000")
+    assert st["kind_ms"]["numeric"]["dense_block"] > 0
+
+
+def test_cfg3_scaled_narrow_block(torch_gpu):
+    """A*A with 2048 < N <= 16384: hash bins plus single-window workgroup rows."""
+    A, B = workloads.workload(3, n=12000)
+    check(torch_gpu, A, B, "cfg3 n=12000")
+
+
+def test_cfg4_scaled(torch_gpu):
+    A, B = workloads.workload(4, n=65536)
+    check(torch_gpu, A, B, "cfg4 n=65536")
+
+
+def test_cfg5_scaled_int64_rowptr(torch_gpu):
+    A, B = workloads.workload(5, n=50000)
+    assert A.rp.dtype == np.int64
+    check(torch_gpu, A, B, "cfg5 n=50000 (int64 A.row_ptr)")
+
+
+def test_int64_rowptr_B(torch_gpu):
+    A, B = workloads.workload(1, n=3000)
+    B64 = CSR(B.nrows, B.ncols, B.rp.astype(np.int64), B.col, B.val)
+    check(torch_gpu, A, B64, "int64 B.row_ptr")
+
+
+# ----------------------------------------------------------------- tiling
+
+def test_tiled_equals_untiled(torch_gpu):
+    A, B = workloads.workload(2, n=20000)
+    st1, n1, ref = check(torch_gpu, A, B, "cfg2 untiled")
+    st2, n2, _ = check(torch_gpu, A, B, "cfg2 tiled", max_tile_rows=3001)
+    assert n1 == 1 and n2 == 7
+
+
+def test_tiled_wide(torch_gpu):
+    A, B = workloads.workload(3, n=30000)
+    check(torch_gpu, A, B, "cfg3 tiled wide", max_tile_rows=4099)
+
+
+def test_streamed_tiles_host_c(torch_gpu):
+    """A in pinned host memory, double-buffered tiles, C tiles copied to
+    pinned host memory at the running offset (Algorithm 2, Phases I-III)."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(5, n=60000)
+    ref = oracle.spgemm(A, B)
+    pA, pB = aires.to_pinned(A), aires.to_pinned(B)
+    budget = B.nbytes() + (4 << 20) + 2 * 1_500_000
+    say("streamed cfg5 n=60000 budget=%d" % budget)
+    with aires.tile_plan(pA, pB, budget, c_on_host=True, timing=True) as plan:
+        info = aires.plan_info(plan)
+        C = aires.spgemm(plan)
+        st = aires.plan_stats(plan)
+        assert info.ntiles >= 3
+        assert C.on_host
+        assert_match(C.rp, C.col, C.val, ref)
+        assert st["host_syncs"] == info.ntiles
+        # each tile copies its own k+1 row pointers: one shared word per boundary
+        assert st["h2d_bytes"] == A.nbytes() + B.nbytes() + 8 * (info.ntiles - 1)
+        C.free()
+
+
+def test_streamed_tiles_device_c(torch_gpu):
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(4, n=40000)
+    ref = oracle.spgemm(A, B)
+    pA = aires.to_pinned(A)
+    dB = aires.to_device(B)
+    budget = B.nbytes() + (4 << 20) + 8 * 40001 + 8 * int(np.minimum(oracle.products(A, B), 128).sum()) \
+        + 2 * 400_000
+    say("streamed cfg4 n=40000 device C")
+    with aires.tile_plan(pA, dB, budget) as plan:
+        assert aires.plan_info(plan).ntiles >= 2
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
+
+
+def test_streamed_wide(torch_gpu):
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(3, n=20000)
+    ref = oracle.spgemm(A, B)
+    say("streamed wide cfg3 n=20000")
+    with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 34, c_on_host=True, max_tile_rows=5000,
+                         dense_max_cols=4096) as plan:
+        C = aires.spgemm(plan)
+        assert_match(C.rp, C.col, C.val, ref)
+        C.free()
+
+
+# ------------------------------------------------------------- edge cases
+
+def _csr(m, n, rows):
+    rp = np.zeros(m + 1, np.int32)
+    col, val = [], []
+    for i, r in enumerate(rows):
+        for j, v in r:
+            col.append(j)
+            val.append(v)
+        rp[i + 1] = len(col)
+    return CSR(m, n, rp, np.array(col, np.int32), np.array(val, np.float32))
+
+
+def test_edge_empty_operands(torch_gpu):
+    A = _csr(5, 4, [[]] * 5)
+    B = workloads.random_csr(np.random.default_rng(0), 4, 7, 0.5)
+    check(torch_gpu, A, B, "empty A")
+    check(torch_gpu, B, _csr(7, 3, [[]] * 7), "empty B")
+    check(torch_gpu, _csr(0, 4, []), B, "zero rows")
+
+
+def test_edge_single_row_and_column(torch_gpu):
+    rng = np.random.default_rng(2)
+    check(torch_gpu, workloads.random_csr(rng, 1, 50, 0.5), workloads.random_csr(rng, 50, 1, 0.5), "1x50*50x1")
+    check(torch_gpu, workloads.random_csr(rng, 300, 1, 0.5), workloads.random_csr(rng, 1, 900, 0.5), "outer")
+
+
+def test_edge_hub_row(torch_gpu):
+    """One row touching every B row: the heaviest row of the tile."""
+    rng = np.random.default_rng(3)
+    B = workloads.random_csr(rng, 5000, 512, 0.05)
+    A = _csr(3, 5000, [[(k, 1.0) for k in range(5000)], [], [(7, 2.0)]])
+    check(torch_gpu, A, B, "hub row narrow")
+    B2 = workloads.random_csr(rng, 5000, 40000, 0.0005)
+    check(torch_gpu, A, B2, "hub row wide")
+
+
+def test_edge_stored_zeros_kept(torch_gpu):
+    A = _csr(2, 2, [[(0, 1.0), (1, 1.0)], [(0, 0.0)]])
+    B = _csr(2, 3, [[(0, 1.0), (2, 5.0)], [(0, -1.0)]])
+    rp, col, val, _, _ = run(torch_gpu, A, B)
+    assert rp.tolist() == [0, 2, 4] and col.tolist() == [0, 2, 0, 2]
+    assert val.tolist() == [0.0, 5.0, 0.0, 0.0]
+
+
+def test_determinism_of_structure(torch_gpu):
+    A, B = workloads.workload(3, n=20000)
+    r1 = run(torch_gpu, A, B)
+    r2 = run(torch_gpu, A, B)
+    assert np.array_equal(r1[0], r2[0]) and np.array_equal(r1[1], r2[1])
+    assert np.allclose(r1[2], r2[2], rtol=1e-5, atol=1e-6)
+
+
+# ------------------------------------------------------ full-size samples
+
+def sampled_check(torch, A, B, name, rows):
+    import paper_2507_02006_amd as aires
+    say("%s full size" % name)
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    with aires.tile_plan(dA, dB, 0) as plan:
+        C = aires.spgemm(plan)
+        torch.cuda.synchronize()
+        rp = C.rp.cpu().numpy()
+        P = oracle.products(A, B)
+        assert rp[0] == 0 and np.all(np.diff(rp) <= np.minimum(P, B.ncols))
+        assert np.all(np.diff(rp) >= (P > 0))
+        for r in rows:
+            ref = oracle.spgemm(A, B, int(r), int(r) + 1)
+            s, e = int(rp[r]), int(rp[r + 1])
+            assert e - s == ref.nnz, "row %d nnz" % r
+            col = C.col[s:e].cpu().numpy()
+            val = C.val[s:e].cpu().numpy()
+            assert np.array_equal(col, ref.col), "row %d cols" % r
+            assert np.all(np.abs(val - ref.val) <= TOL * (1 + np.abs(ref.val))), "row %d vals" % r
+        del C
+
+
+def _rows(A, B, k=150, heavy=5, seed=0):
+    P = oracle.products(A, B)
+    rng = np.random.default_rng(seed)
+    return np.concatenate([rng.choice(A.nrows, k, replace=False), np.argsort(P)[-heavy:]])
+
+
+def test_cfg2_full_sampled(torch_gpu):
+    A, B = workloads.workload(2)
+    sampled_check(torch_gpu, A, B, "cfg2", _rows(A, B))
+
+
+@pytest.mark.slow
+def test_cfg3_full_sampled(torch_gpu):
+    A, B = workloads.workload(3)
+    sampled_check(torch_gpu, A, B, "cfg3", _rows(A, B, k=60, heavy=2))
