@@ -1,0 +1,203 @@
+"""Benchmark of the out-of-core CSR x CSR product (GCN aggregation, after
+AIRES arXiv 2507.02006) on one MI355X.
+
+A step is one pass of the whole path over the workload with inputs
+resident in HBM: RoBW planning (aires_tile_plan), row analysis, binning,
+symbolic phase, scan, the nnz read-back, C allocation, numeric phase
+(aires_spgemm), until C is ready on the stream.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload 3] [--cpu-seconds S]
+
+value  = whole-job GFLOP/s (2 flops per intermediate product) per step.
+roofline = the dominant kernel (the numeric launch with the largest time):
+  achieved = its algorithmic bytes per launch / its average launch time,
+  from HIP events the library records around that launch on the compute
+  stream during the timed steps.
+cpu_baseline = the CPU oracle (serial) on a bounded random row sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "SpGEMM GFLOP/s and achieved HBM GB/s (% of peak) on 1 MI355X; end-to-end latency"
+
+WORKLOAD_NAMES = {
+    1: "tiny GCN aggregation: symmetric R-MAT(.57,.19,.19,.05) n=4096 deg 16 + self-loops, sym-normalised; "
+       "X 4096x256 10% U(-1,1)",
+    2: "mid GCN aggregation: symmetric R-MAT n=262144 deg 32 + self-loops, sym-normalised; X 262144x512 5% U(-1,1)",
+    3: "two-hop square A*A: symmetric R-MAT n=1048576 deg 16 + self-loops, sym-normalised fp32 CSR",
+    4: "large GCN aggregation: symmetric R-MAT n=8388608 deg 24 + self-loops; X 8388608x128 10% U(-1,1)",
+}
+
+KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192"]
+
+
+def row_kinds(P: np.ndarray, N: int) -> np.ndarray:
+    """The library's default row bins (aires.cpp bin_plan) for the byte model."""
+    k = np.zeros(len(P), dtype=np.int8)
+    if N <= 2048:
+        k[(P > 0) & (P <= 8192)] = 1
+        k[P > 8192] = 2
+    else:
+        k[(P > 0) & (P <= 64)] = 3
+        k[(P > 64) & (P <= 512)] = 4
+        k[(P > 512) & (P <= 4096)] = 5
+        k[P > 4096] = 2
+    return k
+
+
+def row_products(A, B) -> np.ndarray:
+    lenB = np.diff(B.rp.astype(np.int64))
+    rows = np.repeat(np.arange(A.nrows), np.diff(A.rp.astype(np.int64)))
+    return np.bincount(rows, weights=lenB[A.col], minlength=A.nrows).astype(np.int64)
+
+
+def cpu_baseline(A, B, P, seconds: float, seed: int = 7):
+    """Time the serial CPU oracle on random rows whose products add up to
+    about `seconds` of oracle work (rate probed on a first small sample)."""
+    import oracle
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(A.nrows)
+    cum = np.cumsum(P[order])
+
+    def run(nprod):
+        n = int(np.searchsorted(cum, nprod)) + 1
+        rows = np.sort(order[:n])
+        t0 = time.perf_counter()
+        prods = 0
+        for r in rows:
+            prods += oracle.spgemm(A, B, int(r), int(r) + 1).products
+        return prods, time.perf_counter() - t0, n
+
+    p0, t0, _ = run(2_000_000)
+    rate = p0 / max(t0, 1e-9)
+    prods, dt, n = run(rate * seconds)
+    return {
+        "value": round(2 * prods / dt / 1e9, 4),
+        "unit": "GFLOP/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "%d random rows (seed %d), %d intermediate products = %.2f%% of the workload, %.1f s serial"
+                  % (n, seed, prods, 100.0 * prods / max(int(P.sum()), 1), dt),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=3, choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="first run one device copy of this many MiB (a known-size kernel for "
+                         "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU; --gpus %d is not supported "
+              "(the path would shard by row blocks, see DESIGN.md)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads
+    import paper_2507_02006_amd as aires
+
+    torch.cuda.set_device(0)
+    if args.copy_probe_mib:
+        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    t0 = time.perf_counter()
+    A, B = workloads.workload(args.workload)
+    gen_s = time.perf_counter() - t0
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    torch.cuda.synchronize()
+    P = row_products(A, B)
+    total_products = int(P.sum())
+
+    def step(timing):
+        with aires.tile_plan(dA, dB, 0, timing=timing) as plan:
+            C = aires.spgemm(plan)
+            torch.cuda.synchronize()
+            st = aires.plan_stats(plan) if timing else None
+        return C, st
+
+    for _ in range(args.warmup):
+        C, _ = step(True)
+        del C
+    torch.cuda.synchronize()
+    stats = []
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        C, st = step(True)
+        stats.append(st)
+        last = C
+        del C
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = 1e3 * elapsed / args.steps
+    assert all(s["products"] == total_products for s in stats)
+    nnz_c = stats[-1]["nnz_c"]
+
+    # dominant kernel: numeric launch of the kind with the largest time
+    num_ms = {k: np.mean([s["kind_ms"]["numeric"][k] for s in stats]) for k in KIND_NAMES}
+    dom = max(num_ms, key=num_ms.get)
+    kinds = row_kinds(P, B.ncols)
+    sel = kinds == KIND_NAMES.index(dom)
+    crow = np.diff(last.rp.cpu().numpy())
+    alen = np.diff(A.rp.astype(np.int64))
+    sA = A.rp.dtype.itemsize
+    dom_bytes = int((sA + 8 * alen[sel] + 8 + 8 * crow[sel]).sum()) + B.nbytes()
+    dom_gbs = dom_bytes / (num_ms[dom] * 1e-3) / 1e9
+    del last
+
+    phase = {k: round(float(np.mean([s[k] for s in stats])), 4)
+             for k in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "total_ms")}
+    compulsory = A.nbytes() + B.nbytes() + 8 * (A.nrows + 1) + 8 * nnz_c
+    res = {
+        "metric": METRIC,
+        "value": round(2 * total_products / (ms_per_step * 1e-3) / 1e9, 3),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded R-MAT graph and uniform sparse features, generated on the host)",
+        "config": {"workload": "cfg%d %s" % (args.workload, WORKLOAD_NAMES[args.workload]),
+                   "m": A.nrows, "n": B.ncols, "nnz_a": A.nnz, "nnz_b": B.nnz,
+                   "products": total_products, "nnz_c": nnz_c, "tiles": stats[-1]["ntiles"],
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "numeric/%s" % dom, "achieved": round(dom_gbs, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "algorithmic_bytes": dom_bytes,
+                     "avg_launch_ms": round(num_ms[dom], 4)},
+        "phases_ms": phase,
+        "numeric_gflops": round(2 * total_products / (phase["numeric_ms"] * 1e-3) / 1e9, 2),
+        "end_to_end_compulsory_gbs": round(compulsory / (ms_per_step * 1e-3) / 1e9, 2),
+        "numeric_kind_ms": {k: round(float(v), 4) for k, v in num_ms.items() if v > 0},
+        "generation_s": round(gen_s, 2),
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(A, B, P, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
