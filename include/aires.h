@@ -133,13 +133,20 @@ typedef struct aires_plan_opts {
                                    calcMem(k,q) = (k+1)*rp_bytes + 8q <=
                                    m_a_bytes, ignoring the budget split    */
     const aires_allocator *allocator; /* NULL: hipMallocAsync/hipFreeAsync */
-    int64_t dense_max_cols;     /* 0: default.  Widest dense accumulator
-                                   window (columns) held in LDS            */
+    int64_t dense_max_cols;     /* 0: default (16384).  Widest N handled
+                                   as a dense LDS row per output row       */
     int64_t hash_max_products;  /* 0: default, < 0: none.  Rows of a wide product with
                                    at most this many products use the LDS
                                    hash path                               */
     int64_t wave_max_products;  /* 0: default.  Rows with at most this many
                                    products are handled by one wavefront   */
+    /* Wide products (N > dense_max_cols) cut columns into grains and rows
+       into windows of whole grains; 0 = default for each.                 */
+    int64_t window_grain_cols;  /* grain width, multiple of 32 (8192)      */
+    int64_t window_max_grains;  /* grains one window may span (16)         */
+    int64_t window_max_entries; /* C entries one window may hold, in
+                                   [grain, 65535] (8192)                   */
+    int64_t count_grains;       /* grains one symbolic item covers (32)    */
 } aires_plan_opts;
 
 /* Fill *o with defaults (struct_size set, validate 0, C on device). */
@@ -250,8 +257,9 @@ typedef struct aires_stats {
     double analyze_ms, bin_ms, symbolic_ms, scan_ms, numeric_ms;
     double h2d_ms, d2h_ms, total_ms;
     int64_t numeric_launches;   /* numeric-phase kernel launches           */
-    /* milliseconds per kernel kind (index = kind id of the row bins,
-       0 empty .. 5 hash-8192); [0] symbolic phase, [1] numeric phase      */
+    /* milliseconds per kernel kind (index = kind id of the row bins:
+       0 empty, 1 dense-wave, 2 dense-block, 3 hash-128, 4 hash-1024,
+       5 hash-8192, 6 column windows); [0] symbolic, [1] numeric phase     */
     double kind_ms[2][8];
 } aires_stats;
 

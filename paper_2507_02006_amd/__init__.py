@@ -62,8 +62,9 @@ class Plan:
 def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: bool = False,
               c_bound: int = B_.CBOUND_PRODUCTS, timing: bool = False, max_tile_rows: int = 0,
               max_tile_bytes: int = 0, m_a_bytes: int = 0, dense_max_cols: int = 0,
-              hash_max_products: int = 0, wave_max_products: int = 0, torch_allocator: bool = True,
-              device: int = 0) -> Plan:
+              hash_max_products: int = 0, wave_max_products: int = 0, window_grain_cols: int = 0,
+              window_max_grains: int = 0, window_max_entries: int = 0, count_grains: int = 0,
+              torch_allocator: bool = True, device: int = 0) -> Plan:
     lib = B_.load()
     a = B_.make_csr(*_parts(A))
     b = B_.make_csr(*_parts(B))
@@ -79,6 +80,10 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
     o.dense_max_cols = dense_max_cols
     o.hash_max_products = hash_max_products
     o.wave_max_products = wave_max_products
+    o.window_grain_cols = window_grain_cols
+    o.window_max_grains = window_max_grains
+    o.window_max_entries = window_max_entries
+    o.count_grains = count_grains
     alloc = None
     if torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
         alloc = B_.TorchAllocator(device)

@@ -47,7 +47,11 @@ aires_status fail(aires_status s, const char* fmt, ...) {
   } while (0)
 
 constexpr int64_t kDenseWaveMaxN = 2048;     // widest dense row one wavefront holds
-constexpr int64_t kDenseMaxCols = 16384;     // widest dense window of a workgroup
+constexpr int64_t kDenseMaxCols = 16384;     // widest dense row a workgroup holds
+constexpr int64_t kGrainCols = 8192;         // column grain of wide products
+constexpr int64_t kWindowMaxGrains = 16;     // grains one window may span
+constexpr int64_t kWindowMaxEntries = 8192;  // C entries one window may hold
+constexpr int64_t kCountGrains = 32;         // grains one symbolic item covers
 constexpr int64_t kWaveMaxProducts = 8192;   // rows up to this go to one wavefront
 constexpr int64_t kHashMaxProducts = 4096;   // = 8192-slot table at load <= 1/2
 constexpr int64_t kFixedWorkspace = 4 << 20; // scan partials, counters, slack
@@ -134,7 +138,8 @@ struct aires_plan {
   // kernel configuration
   kern::BinThresholds th;
   int wide = 0;
-  int32_t W = 0, nwin = 1;
+  int32_t G = 0, nG = 0;           // column grains (wide products)
+  int32_t win_grains = 0, win_entries = 0, count_grains = 0;
   // host copies needed for streaming
   std::vector<int64_t> P_host;  // per-row products when computed on the host
   // timing events of the last call
@@ -161,27 +166,29 @@ void bin_plan(aires_plan* p) {
   int nb = 0;
   auto add = [&](int kind, int64_t maxp) { th.kind[nb] = kind; th.max_p[nb] = maxp; ++nb; };
   add(kern::KIND_EMPTY, 0);
+  p->wide = 0;
   if (N <= std::min(kDenseWaveMaxN, dense_max)) {
     // narrow product: every row fits a dense LDS row
     add(kern::KIND_DENSE_WAVE, wave_max);
     add(kern::KIND_DENSE_BLOCK, INT64_MAX);
-    p->wide = 0;
-    p->W = (int32_t)std::max<int64_t>(N, 1);
-    p->nwin = 1;
   } else {
     // light rows hash in LDS (load factor <= 1/2: nnz(C_i) <= P_i <= slots/2)
     if (hash_max > 0) add(kern::KIND_HASH_128, std::min<int64_t>(hash_max, 64));
     if (hash_max > 64) add(kern::KIND_HASH_1024, std::min<int64_t>(hash_max, 512));
     if (hash_max > 512) add(kern::KIND_HASH_8192, hash_max);
-    add(kern::KIND_DENSE_BLOCK, INT64_MAX);
     if (N <= dense_max) {
-      p->wide = 0;
-      p->W = (int32_t)N;
-      p->nwin = 1;
+      add(kern::KIND_DENSE_BLOCK, INT64_MAX);
     } else {
+      // two window bins, the heavy rows last in the list (processed first)
+      add(kern::KIND_WINDOWS, std::max<int64_t>(hash_max, 1) << 8);
+      add(kern::KIND_WINDOWS, INT64_MAX);
       p->wide = 1;
-      p->W = (int32_t)dense_max;
-      p->nwin = (int32_t)((N + dense_max - 1) / dense_max);
+      p->G = (int32_t)(o.window_grain_cols > 0 ? o.window_grain_cols : kGrainCols);
+      p->nG = (int32_t)((N + p->G - 1) / p->G);
+      p->win_grains = (int32_t)(o.window_max_grains > 0 ? o.window_max_grains : kWindowMaxGrains);
+      p->win_entries = (int32_t)(o.window_max_entries > 0 ? o.window_max_entries
+                                                          : std::max<int64_t>(kWindowMaxEntries, p->G));
+      p->count_grains = (int32_t)(o.count_grains > 0 ? o.count_grains : kCountGrains);
     }
   }
   th.nb = nb;
@@ -352,12 +359,25 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   p->info.c_on_host = c_on_host;
   p->info.c_bound_entries = -1;
 
-  const int64_t nwin = p->nwin;
-  const int64_t index_bytes = p->wide ? 4 * (nwin + 1) * K : 0;
-  if (p->wide && B->nnz > INT32_MAX) {
-    delete p;
-    return fail(AIRES_E_UNSUPPORTED, "windowed path needs nnz(B) < 2^31");
+  if (p->wide) {
+    if (p->G < 32 || p->G % 32 || p->G > (1 << 20) || p->win_entries < p->G || p->win_entries > 65535 ||
+        p->win_grains < 1 || p->count_grains < 1 ||
+        kern::window_numeric_lds(p->win_grains, p->win_entries, p->G) > kern::kMaxLds ||
+        kern::grain_count_lds(p->count_grains, p->G) > kern::kMaxLds || p->nG > 65535) {
+      aires_status st = fail(AIRES_E_INVALID_ARG,
+                             "window options out of range (grain %d, windows of %d grains / %d entries, "
+                             "%d grains per count item, %d grains)",
+                             p->G, p->win_grains, p->win_entries, p->count_grains, p->nG);
+      delete p;
+      return st;
+    }
+    if (B->nnz > INT32_MAX) {
+      delete p;
+      return fail(AIRES_E_UNSUPPORTED, "column windows need nnz(B) < 2^31");
+    }
   }
+  const int64_t nG = p->wide ? p->nG : 0;
+  const int64_t index_bytes = p->wide ? 4 * (nG + 1) * K : 0;
 
   std::vector<int64_t> arp;
   aires_status st = host_row_ptr(*A, arp);
@@ -368,10 +388,11 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   // pointer of the tile (8, streamed only).
   std::vector<int64_t> cu;  // C bound per row (entries), streamed + host C
   int64_t resident = p->info.b_bytes + kFixedWorkspace + index_bytes;
-  int64_t per_row_ws = 8 + 4 + (p->wide ? 4 * nwin : 0);
+  // (+ per-grain counts and per-row window counts of wide products)
+  int64_t per_row_ws = 8 + 4 + (p->wide ? 4 * nG + 8 : 0);
   if (!a_streamed) {
-    // A and C.row_ptr resident; bin lists and window counts for all rows
-    resident += p->info.a_bytes + 8 * (m + 1) + (4 + (p->wide ? 4 * nwin : 0)) * m;
+    // A and C.row_ptr resident; bin lists and window bookkeeping for all rows
+    resident += p->info.a_bytes + 8 * (m + 1) + (4 + (p->wide ? 4 * nG + 8 : 0)) * m;
     per_row_ws = 8;
   } else if (o.m_a_bytes == 0) {
     // C bound per row for the C slots (or for a device-resident C)
@@ -560,41 +581,89 @@ kern::Operands tile_operands(const aires_plan* p, const void* arp, int64_t a_bas
   op.K = p->B.nrows;
   op.N = p->B.ncols;
   op.bidx = p->wide ? bidx : nullptr;
-  op.W = p->W;
-  op.nwin = p->nwin;
+  op.G = p->G;
+  op.nG = p->nG;
   return op;
 }
 
 // Phase markers for the stats: kinds >= 100 are whole phases.
 enum { PH_ANALYZE = 100, PH_BIN, PH_SYMBOLIC, PH_SCAN, PH_NUMERIC, PH_H2D, PH_D2H, PH_TOTAL, PH_INDEX };
 
+// Device workspace of one tile (tile-local rows).
+struct TileWs {
+  int64_t* P = nullptr;          // [n] intermediate products per row
+  int32_t* list = nullptr;       // [n] rows grouped by bin (long-row list during analysis)
+  int32_t* binoff = nullptr;     // [MAX_BINS + 1]
+  int32_t* cntcur = nullptr;     // [2 * MAX_BINS + 1] bin counts, cursors, long-row count
+  int32_t* gcnt = nullptr;       // [n * nG] entries per (row, grain)     (wide)
+  int64_t* icount = nullptr;     // [n + 1] windows per bin row, scanned  (wide)
+  kern::WinItem* items = nullptr;
+  int64_t nitems = 0;            // host copy of icount[n]
+  int32_t* wcounter = nullptr;   // row counter of the window kernel
+  void* scan_ws = nullptr;
+};
+
+aires_status alloc_tile_ws(aires_plan* p, DevPool& ws, int64_t n, bool with_list_gcnt, TileWs& w) {
+  ST_TRY(ws.get_n(n, &w.P));
+  if (with_list_gcnt) {
+    ST_TRY(ws.get_n(n, &w.list));
+    if (p->wide) {
+      ST_TRY(ws.get_n(n * (int64_t)p->nG, &w.gcnt));
+      ST_TRY(ws.get_n(n + 1, &w.icount));
+    }
+    ST_TRY(ws.get_n(kern::MAX_BINS + 1, &w.binoff));
+  }
+  ST_TRY(ws.get_n(2 * kern::MAX_BINS + 1, &w.cntcur));
+  ST_TRY(ws.get_n(1, &w.wcounter));
+  ST_TRY(ws.get(kern::scan_workspace_bytes(n), &w.scan_ws));
+  return AIRES_OK;
+}
+
+kern::WindowParams window_params(const aires_plan* p, const TileWs& w) {
+  kern::WindowParams wp;
+  wp.gcnt = w.gcnt;
+  wp.grains_per_count_item = p->count_grains;
+  wp.max_grains = p->win_grains;
+  wp.max_entries = p->win_entries;
+  wp.item_count = w.icount;
+  wp.items = w.items;
+  wp.row_counter = w.wcounter;
+  return wp;
+}
+
 // analyze + bin + symbolic + scan of one tile; counts land in crp[1..n] and
-// are scanned in place on top of crp[0].
-aires_status tile_symbolic(aires_plan* p, const kern::Operands& op, int64_t n, int64_t* P, int32_t* list,
-                           int32_t* binoff, int32_t* cntcur, int32_t* wcnt, int64_t* crp, void* scan_ws,
+// are scanned in place on top of crp[0].  Wide rows also get their window
+// counts scanned into w.icount.
+aires_status tile_symbolic(aires_plan* p, const kern::Operands& op, int64_t n, TileWs& w, int64_t* crp,
                            unsigned long long* prod_total, hipStream_t s, Timer& tm) {
   const int e0 = tm.record();
-  HIP_TRY(kern::analyze(op, n, P, prod_total, s));
+  HIP_TRY(hipMemsetAsync(w.cntcur, 0, sizeof(int32_t) * (2 * kern::MAX_BINS + 1), s));
+  HIP_TRY(kern::analyze(op, n, w.P, prod_total, w.cntcur + 2 * kern::MAX_BINS, w.list, s));
   const int e1 = tm.record();
-  HIP_TRY(hipMemsetAsync(cntcur, 0, sizeof(int32_t) * 2 * kern::MAX_BINS, s));
-  HIP_TRY(kern::bin_rows(P, n, p->th, cntcur, binoff, list, s));
+  HIP_TRY(kern::bin_rows(w.P, n, p->th, w.cntcur, w.binoff, w.list, s));
   HIP_TRY(hipMemsetAsync(crp + 1, 0, sizeof(int64_t) * (size_t)std::max<int64_t>(n, 0), s));
+  if (p->wide) HIP_TRY(hipMemsetAsync(w.icount, 0, sizeof(int64_t) * (size_t)(n + 1), s));
   const int e2 = tm.record();
   kern::Outputs out{};
   out.counts = crp + 1;
-  out.wcnt = wcnt;
   for (int b = 0; b < p->th.nb; ++b) {
     const int kind = p->th.kind[b];
     if (kind == kern::KIND_EMPTY) continue;
-    kern::BinView bv{list, binoff, b};
+    kern::BinView bv{w.list, w.binoff, b};
     const int ka = tm.record();
-    HIP_TRY(kern::run_bin(kind, 0, op, bv, out, n, s));
-    if (kind == kern::KIND_DENSE_BLOCK && p->wide)
-      HIP_TRY(kern::window_rowsum(bv, p->nwin, wcnt, crp + 1, n, s));
+    if (kind == kern::KIND_WINDOWS) {
+      // all window bins (consecutive) as one range
+      while (bv.last() + 1 < p->th.nb && p->th.kind[bv.last() + 1] == kern::KIND_WINDOWS) bv.bin_last = bv.last() + 1;
+      HIP_TRY(kern::windows_symbolic(op, bv, window_params(p, w), out, n, s));
+      b = bv.last();
+    } else {
+      HIP_TRY(kern::run_bin(kind, 0, op, bv, out, n, s));
+    }
     tm.mark(kind, 0, ka, tm.record());
   }
   const int e3 = tm.record();
-  HIP_TRY(kern::scan_inplace(crp + 1, n, scan_ws, s));
+  HIP_TRY(kern::scan_inplace(crp + 1, n, w.scan_ws, s));
+  if (p->wide) HIP_TRY(kern::scan_inplace(w.icount + 1, n, w.scan_ws, s));
   const int e4 = tm.record();
   tm.mark(PH_ANALYZE, 0, e0, e1);
   tm.mark(PH_BIN, 0, e1, e2);
@@ -603,11 +672,9 @@ aires_status tile_symbolic(aires_plan* p, const kern::Operands& op, int64_t n, i
   return AIRES_OK;
 }
 
-aires_status tile_numeric(aires_plan* p, const kern::Operands& op, int64_t n, const int32_t* list,
-                          const int32_t* binoff, int32_t* wcnt, const int64_t* crp, int32_t* ccol, float* cval,
-                          int64_t c_base, hipStream_t s, Timer& tm) {
+aires_status tile_numeric(aires_plan* p, const kern::Operands& op, int64_t n, const TileWs& w, const int64_t* crp,
+                          int32_t* ccol, float* cval, int64_t c_base, hipStream_t s, Timer& tm) {
   kern::Outputs out{};
-  out.wcnt = wcnt;
   out.crp = crp;
   out.ccol = ccol - c_base;
   out.cval = cval - c_base;
@@ -615,9 +682,15 @@ aires_status tile_numeric(aires_plan* p, const kern::Operands& op, int64_t n, co
   for (int b = 0; b < p->th.nb; ++b) {
     const int kind = p->th.kind[b];
     if (kind == kern::KIND_EMPTY) continue;
-    kern::BinView bv{list, binoff, b};
+    kern::BinView bv{w.list, w.binoff, b};
     const int ka = tm.record();
-    HIP_TRY(kern::run_bin(kind, 1, op, bv, out, n, s));
+    if (kind == kern::KIND_WINDOWS) {
+      while (bv.last() + 1 < p->th.nb && p->th.kind[bv.last() + 1] == kern::KIND_WINDOWS) bv.bin_last = bv.last() + 1;
+      HIP_TRY(kern::windows_numeric(op, bv, window_params(p, w), out, n, w.nitems, s));
+      b = bv.last();
+    } else {
+      HIP_TRY(kern::run_bin(kind, 1, op, bv, out, n, s));
+    }
     tm.mark(kind, 1, ka, tm.record());
     p->stats.numeric_launches++;
   }
@@ -646,49 +719,68 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   for (const auto& t : p->tiles) max_rows = std::max(max_rows, t.r1 - t.r0);
   const int64_t nt = (int64_t)p->tiles.size();
 
+  // Workspace: P, counters and scan partials are reused by every tile; row
+  // lists, bin offsets and window bookkeeping persist from the symbolic
+  // sweep to the numeric sweep (tile regions of whole-matrix arrays).
   int64_t* crp = nullptr;
   ST_TRY(ws.get_n(m + 1, &crp));
-  int64_t* P = nullptr;
-  int32_t *list = nullptr, *binoff = nullptr, *cntcur = nullptr, *wcnt = nullptr, *bidx = nullptr;
+  TileWs shared;
+  ST_TRY(alloc_tile_ws(p, ws, max_rows, false, shared));
+  int32_t *list = nullptr, *binoff = nullptr, *gcnt = nullptr, *bidx = nullptr;
+  int64_t* icount = nullptr;
   unsigned long long* prod = nullptr;
-  void* scan_ws = nullptr;
-  ST_TRY(ws.get_n(max_rows, &P));
   ST_TRY(ws.get_n(m, &list));
   ST_TRY(ws.get_n(nt * (kern::MAX_BINS + 1), &binoff));
-  ST_TRY(ws.get_n(2 * kern::MAX_BINS, &cntcur));
   ST_TRY(ws.get_n(1, &prod));
-  ST_TRY(ws.get(kern::scan_workspace_bytes(max_rows), &scan_ws));
   if (p->wide) {
-    ST_TRY(ws.get_n(m * (int64_t)p->nwin, &wcnt));
-    ST_TRY(ws.get_n(((int64_t)p->nwin + 1) * K, &bidx));
+    ST_TRY(ws.get_n(m * (int64_t)p->nG, &gcnt));
+    ST_TRY(ws.get_n(m + nt, &icount));
+    ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
   }
+  auto tile_ws = [&](int64_t t) {
+    const aires_tile& T = p->tiles[(size_t)t];
+    TileWs w = shared;
+    w.list = list + T.r0;
+    w.binoff = binoff + t * (kern::MAX_BINS + 1);
+    if (p->wide) {
+      w.gcnt = gcnt + T.r0 * (int64_t)p->nG;
+      w.icount = icount + T.r0 + t;
+    }
+    return w;
+  };
   HIP_TRY(hipMemsetAsync(crp, 0, sizeof(int64_t), s));
   HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long), s));
   if (p->wide) {
     const int ea = tm.record();
-    HIP_TRY(kern::build_window_index(p->B.row_ptr, p->B.rp_type == AIRES_IDX_I64, p->B.col_idx, K, p->W,
-                                     p->nwin, bidx, s));
+    HIP_TRY(kern::build_window_index(p->B.row_ptr, p->B.rp_type == AIRES_IDX_I64, p->B.col_idx, K, p->G, p->nG,
+                                     bidx, s));
     tm.mark(PH_INDEX, 0, ea, tm.record());
   }
 
   // Sweep 1: symbolic phase of every tile; C.row_ptr grows tile by tile.
   for (int64_t t = 0; t < nt; ++t) {
     const aires_tile& T = p->tiles[(size_t)t];
-    const int64_t n = T.r1 - T.r0;
+    TileWs w = tile_ws(t);
     const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
     kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, p->A.vals, p->B.row_ptr, p->B.col_idx,
                                       p->B.vals, bidx);
-    ST_TRY(tile_symbolic(p, op, n, P, list + T.r0, binoff + t * (kern::MAX_BINS + 1), cntcur,
-                         wcnt ? wcnt + T.r0 * p->nwin : nullptr, crp + T.r0, scan_ws, prod, s, tm));
+    ST_TRY(tile_symbolic(p, op, T.r1 - T.r0, w, crp + T.r0, prod, s, tm));
   }
-  // The one host synchronisation: nnz(C) decides C's allocation.
-  int64_t nnz = 0;
-  unsigned long long products = 0;
-  HIP_TRY(hipMemcpyAsync(&nnz, crp + m, sizeof nnz, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipMemcpyAsync(&products, prod, sizeof products, hipMemcpyDeviceToHost, s));
+  // The one host synchronisation: nnz(C) (and the window count of every
+  // tile) decide the allocations.
+  std::vector<int64_t> hostbuf(3 + (size_t)nt);
+  int64_t* hb = hostbuf.data();
+  HIP_TRY(hipMemcpyAsync(hb, crp + m, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(hb + 1, prod, sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+  if (p->wide)
+    for (int64_t t = 0; t < nt; ++t) {
+      const aires_tile& T = p->tiles[(size_t)t];
+      HIP_TRY(hipMemcpyAsync(hb + 2 + t, icount + T.r0 + t + (T.r1 - T.r0), sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    }
   HIP_TRY(hipStreamSynchronize(s));
+  const int64_t nnz = hb[0];
   p->stats.host_syncs = 1;
-  p->stats.products = (int64_t)products;
+  p->stats.products = hb[1];
   p->stats.nnz_c = nnz;
   const int64_t resident = p->info.b_bytes + p->info.a_bytes + 8 * (m + 1);
   if (resident + 8 * nnz > p->budget)
@@ -698,16 +790,25 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   float* cval = nullptr;
   ST_TRY(ws.get_n(nnz, &ccol));
   ST_TRY(ws.get_n(nnz, &cval));
+  kern::WinItem* items = nullptr;
+  std::vector<int64_t> item_base((size_t)nt + 1, 0);
+  if (p->wide) {
+    for (int64_t t = 0; t < nt; ++t) item_base[(size_t)t + 1] = item_base[(size_t)t] + hb[2 + t];
+    ST_TRY(ws.get_n(item_base[(size_t)nt], &items));
+  }
 
   // Sweep 2: numeric phase of every tile.
   for (int64_t t = 0; t < nt; ++t) {
     const aires_tile& T = p->tiles[(size_t)t];
-    const int64_t n = T.r1 - T.r0;
+    TileWs w = tile_ws(t);
+    if (p->wide) {
+      w.items = items + item_base[(size_t)t];
+      w.nitems = hb[2 + t];
+    }
     const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
     kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, p->A.vals, p->B.row_ptr, p->B.col_idx,
                                       p->B.vals, bidx);
-    ST_TRY(tile_numeric(p, op, n, list + T.r0, binoff + t * (kern::MAX_BINS + 1),
-                        wcnt ? wcnt + T.r0 * p->nwin : nullptr, crp + T.r0, ccol, cval, 0, s, tm));
+    ST_TRY(tile_numeric(p, op, T.r1 - T.r0, w, crp + T.r0, ccol, cval, 0, s, tm));
   }
   tm.mark(PH_TOTAL, 0, e_total0, tm.record());
 
@@ -787,50 +888,38 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     ST_TRY(ws.get((size_t)(K + 1) * sB, &d_brp));
     ST_TRY(ws.get((size_t)std::max<int64_t>(B.nnz, 1) * 4, &d_bcol));
     ST_TRY(ws.get((size_t)std::max<int64_t>(B.nnz, 1) * 4, &d_bval));
-    HIP_TRY(hipMemcpyAsync(d_brp, B.row_ptr, (size_t)(K + 1) * sB, hipMemcpyHostToDevice, sh));
-    HIP_TRY(hipMemcpyAsync(d_bcol, B.col_idx, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
-    HIP_TRY(hipMemcpyAsync(d_bval, B.vals, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
-    p->stats.h2d_bytes += (K + 1) * sB + 8 * B.nnz;
-    brp = d_brp;
-    bcol = (const int32_t*)d_bcol;
-    bval = (const float*)d_bval;
   }
 
   // two slots of everything a tile needs on the device
   struct Slot {
     void* arp; int32_t* acol; float* aval;
-    int64_t* P; int32_t* list; int32_t* binoff; int32_t* cntcur; int32_t* wcnt;
+    TileWs w;
     int64_t* crp; int32_t* ccol; float* cval; int64_t ccap;
-    void* scan_ws;
+    int64_t icap;
   } slot[2];
   int32_t* bidx = nullptr;
   unsigned long long* prod = nullptr;
   int64_t* running = nullptr;
   ST_TRY(ws.get_n(1, &prod));
   ST_TRY(ws.get_n(1, &running));
-  if (p->wide) ST_TRY(ws.get_n(((int64_t)p->nwin + 1) * K, &bidx));
+  if (p->wide) ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
   for (int s = 0; s < 2; ++s) {
     Slot& S = slot[s];
-    std::memset(&S, 0, sizeof S);
+    S = Slot{};
     ST_TRY(ws.get((size_t)(max_rows + 1) * sA, &S.arp));
     ST_TRY(ws.get_n(max_q, &S.acol));
     ST_TRY(ws.get_n(max_q, &S.aval));
-    ST_TRY(ws.get_n(max_rows, &S.P));
-    ST_TRY(ws.get_n(max_rows, &S.list));
-    ST_TRY(ws.get_n(kern::MAX_BINS + 1, &S.binoff));
-    ST_TRY(ws.get_n(2 * kern::MAX_BINS, &S.cntcur));
-    if (p->wide) ST_TRY(ws.get_n(max_rows * (int64_t)p->nwin, &S.wcnt));
+    ST_TRY(alloc_tile_ws(p, ws, max_rows, true, S.w));
     ST_TRY(ws.get_n(max_rows + 1, &S.crp));
-    ST_TRY(ws.get(kern::scan_workspace_bytes(max_rows), &S.scan_ws));
     if (c_on_host) {
       ST_TRY(ws.get_n(max_cb, &S.ccol));
       ST_TRY(ws.get_n(max_cb, &S.cval));
       S.ccap = max_cb;
     }
   }
-  int64_t* nnz_host = nullptr;  // pinned per-tile running totals
-  HIP_TRY(hipHostMalloc((void**)&nnz_host, sizeof(int64_t) * (size_t)std::max<int64_t>(nt, 1), hipHostMallocDefault));
-  hb.v.push_back(nnz_host);
+  int64_t* cnt_host = nullptr;  // pinned per-tile (running nnz, windows)
+  HIP_TRY(hipHostMalloc((void**)&cnt_host, sizeof(int64_t) * 2 * (size_t)std::max<int64_t>(nt, 1), hipHostMallocDefault));
+  hb.v.push_back(cnt_host);
   HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long), sc));
   HIP_TRY(hipMemsetAsync(running, 0, sizeof(int64_t), sc));
 
@@ -857,6 +946,15 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   ST_TRY(mkev(&ev_ws));
   HIP_TRY(hipEventRecord(ev_ws, sc));
   HIP_TRY(hipStreamWaitEvent(sh, ev_ws, 0));
+  if (B.mem != AIRES_MEM_DEVICE) {
+    HIP_TRY(hipMemcpyAsync(d_brp, B.row_ptr, (size_t)(K + 1) * sB, hipMemcpyHostToDevice, sh));
+    HIP_TRY(hipMemcpyAsync(d_bcol, B.col_idx, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
+    HIP_TRY(hipMemcpyAsync(d_bval, B.vals, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
+    p->stats.h2d_bytes += (K + 1) * sB + 8 * B.nnz;
+    brp = d_brp;
+    bcol = (const int32_t*)d_bcol;
+    bval = (const float*)d_bval;
+  }
 
   auto issue_h2d = [&](int64_t t) -> aires_status {
     const aires_tile& T = p->tiles[(size_t)t];
@@ -878,9 +976,9 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   if (nt > 1) ST_TRY(issue_h2d(1));
   const int eh1 = tm.record();
   tm.mark(PH_H2D, 0, eh0, eh1);
-  if (p->wide) {
+  if (p->wide && nt > 0) {
     HIP_TRY(hipStreamWaitEvent(sc, ev_in[0], 0));  // B is resident once tile 0 arrived
-    HIP_TRY(kern::build_window_index(brp, B.rp_type == AIRES_IDX_I64, bcol, K, p->W, p->nwin, bidx, sc));
+    HIP_TRY(kern::build_window_index(brp, B.rp_type == AIRES_IDX_I64, bcol, K, p->G, p->nG, bidx, sc));
   }
   int64_t base = 0;
   for (int64_t t = 0; t < nt; ++t) {
@@ -892,13 +990,15 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     kern::Operands op = tile_operands(p, S.arp, T.nnz0, S.acol, S.aval, brp, bcol, bval, bidx);
     // running base of C.row_ptr for this tile: crp[0] = total so far
     HIP_TRY(hipMemcpyAsync(S.crp, running, sizeof(int64_t), hipMemcpyDeviceToDevice, sc));
-    ST_TRY(tile_symbolic(p, op, k, S.P, S.list, S.binoff, S.cntcur, S.wcnt, S.crp, S.scan_ws, prod, sc, tm));
+    ST_TRY(tile_symbolic(p, op, k, S.w, S.crp, prod, sc, tm));
     HIP_TRY(hipMemcpyAsync(running, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToDevice, sc));
-    HIP_TRY(hipMemcpyAsync(nnz_host + t, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
+    HIP_TRY(hipMemcpyAsync(cnt_host + 2 * t, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
+    if (p->wide)
+      HIP_TRY(hipMemcpyAsync(cnt_host + 2 * t + 1, S.w.icount + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
     HIP_TRY(hipEventRecord(ev_cnt[(size_t)t], sc));
     HIP_TRY(hipEventSynchronize(ev_cnt[(size_t)t]));
     p->stats.host_syncs++;
-    const int64_t end = nnz_host[t];
+    const int64_t end = cnt_host[2 * t];
     const int64_t nnz_t = end - base;
     if (end > cap)
       return fail(AIRES_E_CAPACITY, "C needs more than the planned bound of %lld entries (tile %lld)",
@@ -914,10 +1014,21 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
       ST_TRY(ws.get_n(nnz_t, &S.cval));
       S.ccap = nnz_t;
     }
+    if (p->wide) {
+      S.w.nitems = cnt_host[2 * t + 1];
+      if (S.w.nitems > S.icap) {
+        if (S.w.items) {
+          ws.a.free(ws.a.ctx, S.w.items, (void*)sc);
+          ws.detach(S.w.items);
+        }
+        S.icap = std::max<int64_t>(S.w.nitems, 2 * S.icap);
+        ST_TRY(ws.get_n(S.icap, &S.w.items));
+      }
+    }
     if (c_on_host) {
-      ST_TRY(tile_numeric(p, op, k, S.list, S.binoff, S.wcnt, S.crp, S.ccol, S.cval, base, sc, tm));
+      ST_TRY(tile_numeric(p, op, k, S.w, S.crp, S.ccol, S.cval, base, sc, tm));
     } else {
-      ST_TRY(tile_numeric(p, op, k, S.list, S.binoff, S.wcnt, S.crp, C_col, C_val, 0, sc, tm));
+      ST_TRY(tile_numeric(p, op, k, S.w, S.crp, C_col, C_val, 0, sc, tm));
     }
     HIP_TRY(hipEventRecord(ev_done[(size_t)t], sc));
     // Phase III for this tile

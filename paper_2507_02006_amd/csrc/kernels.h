@@ -14,12 +14,14 @@ constexpr int MAX_BINS = 8;
 // Kinds of per-row work (see bin_plan in the runtime).
 enum Kind : int {
   KIND_EMPTY = 0,       // P_i == 0: empty C row, no launch
-  KIND_DENSE_WAVE = 1,  // one wavefront per row, dense LDS window = N (N <= 2048)
-  KIND_DENSE_BLOCK = 2, // one workgroup per (row, column window), window <= 16384
+  KIND_DENSE_WAVE = 1,  // one wavefront per row, dense LDS row of N slots (N <= 2048)
+  KIND_DENSE_BLOCK = 2, // one workgroup per row, dense LDS row of N slots (N <= 16384)
   KIND_HASH_128 = 3,    // one wavefront per row, LDS hash of 128 slots
   KIND_HASH_1024 = 4,   // one wavefront per row, LDS hash of 1024 slots
   KIND_HASH_8192 = 5,   // one workgroup per row, LDS hash of 8192 slots
+  KIND_WINDOWS = 6,     // wide rows: per-grain counts, then bitmap-rank column windows
 };
+constexpr int NUM_KINDS = 7;
 
 struct BinThresholds {
   int32_t nb;                    // number of bins
@@ -31,43 +33,71 @@ struct Operands {
   const void* arp; int rpa64; int64_t a_base; const int32_t* acol; const float* aval;
   const void* brp; int rpb64; const int32_t* bcol; const float* bval;
   int64_t K, N;
-  // column windows (wide products): bidx[w*K + k] = first position of B_k with
-  // column >= w*W, for w in [0, nwin]; nullptr for a single window.
-  const int32_t* bidx; int32_t W; int32_t nwin;
+  // Column grains of a wide product: bidx[g*K + k] = first position of B_k
+  // with column >= g*G, for g in [0, nG]; nullptr when N is narrow.
+  const int32_t* bidx; int32_t G; int32_t nG;
 };
 
 struct BinView {
   const int32_t* list;     // tile-local row ids grouped by bin
   const int32_t* binoff;   // [nb+1] offsets into list (device)
-  int32_t bin;
+  int32_t bin;             // first bin of the view
+  int32_t bin_last = -1;   // last bin of the view (-1: same as bin)
+  __host__ __device__ int32_t last() const { return bin_last < 0 ? bin : bin_last; }
 };
 
 struct Outputs {
   int64_t* counts;         // symbolic: nnz of tile row (tile-local index)
-  int32_t* wcnt;           // windowed rows: [row*nwin + w] counts, later offsets
   const int64_t* crp;      // numeric: C row pointers, tile-local index
-  int32_t* ccol;
+  int32_t* ccol;           // numeric: C arrays, indexed by (crp value - c_base)
   float* cval;
 };
 
-hipError_t analyze(const Operands& op, int64_t nrows, int64_t* P,
-                   unsigned long long* total, hipStream_t s);
+// One column window of one wide row: grains [g0, g1), n entries of C,
+// written at C position crp[row] + roff.
+struct WinItem {
+  int32_t row;
+  uint16_t g0, g1;
+  int32_t n;
+  int32_t roff;
+};
+
+struct WindowParams {
+  int32_t* gcnt;           // [row * nG + g] entries of C in grain g (per tile)
+  int32_t grains_per_count_item;  // grains one symbolic item covers
+  int32_t max_grains;      // grains one window may span
+  int32_t max_entries;     // entries one window may hold (>= G)
+  int64_t* item_count;     // [1 + d]: windows of the d-th row of the bins; scanned into offsets
+  WinItem* items;          // filled in the numeric sweep
+  int32_t* row_counter;    // zeroed before the numeric launch (dynamic row scheduling)
+};
+
+// P_i per tile row and their total; rows longer than `long_row` entries are
+// collected in long_list (count in *long_cnt) and summed by a workgroup each.
+hipError_t analyze(const Operands& op, int64_t nrows, int64_t* P, unsigned long long* total,
+                   int32_t* long_cnt, int32_t* long_list, hipStream_t s);
 hipError_t bin_rows(const int64_t* P, int64_t nrows, const BinThresholds& th,
                     int32_t* cnt_cursor /*2*MAX_BINS zeroed*/, int32_t* binoff,
                     int32_t* list, hipStream_t s);
 // phase: 0 symbolic, 1 numeric.  ub_rows: host upper bound on the bin size.
 hipError_t run_bin(int kind, int phase, const Operands& op, const BinView& bv,
                    const Outputs& out, int64_t ub_rows, hipStream_t s);
-hipError_t window_rowsum(const BinView& bv, int32_t nwin, int32_t* wcnt, int64_t* counts,
-                         int64_t ub_rows, hipStream_t s);
+// wide rows: symbolic grain counts + window plan (counts[row], item_count[1+d])
+hipError_t windows_symbolic(const Operands& op, const BinView& bv, const WindowParams& wp,
+                            const Outputs& out, int64_t ub_rows, hipStream_t s);
+// wide rows: fill the window list (item_count scanned into offsets), then numeric
+hipError_t windows_numeric(const Operands& op, const BinView& bv, const WindowParams& wp,
+                           const Outputs& out, int64_t ub_rows, int64_t nitems, hipStream_t s);
 hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, int64_t K,
-                              int32_t W, int32_t nwin, int32_t* bidx, hipStream_t s);
+                              int32_t G, int32_t nG, int32_t* bidx, hipStream_t s);
 // In-place inclusive scan of x[0..n) plus x[-1] (the base): x[i] = x[-1] + sum_{j<=i} x[j].
 size_t scan_workspace_bytes(int64_t n);
 hipError_t scan_inplace(int64_t* x, int64_t n, void* ws, hipStream_t s);
 
-// LDS bytes one block of a kind needs (0 if unknown)
 size_t lds_bytes(int kind, int phase, int32_t W);
+size_t grain_count_lds(int sg, int G);
+size_t window_numeric_lds(int max_grains, int max_entries, int G);
+constexpr size_t kMaxLds = 160 * 1024;  // LDS of one gfx950 workgroup
 int group_size(int kind);
 
 }  // namespace kern

@@ -107,26 +107,74 @@ __device__ __forceinline__ int64_t ld_rp(const void* rp, int64_t i) {
 
 // ---------------------------------------------------------------- analyze
 
-// P_i for every tile row, 16 lanes per row.
+constexpr int64_t kLongRow = 2048;  // longer A rows are summed by a whole workgroup
+
+// P_i for every tile row, 16 lanes per row; rows longer than kLongRow are
+// appended to long_list for k_analyze_long.
 template <typename RA, typename RB>
 __global__ __launch_bounds__(256) void k_analyze(const Operands op, int64_t nrows, int64_t* P,
-                                                 unsigned long long* total) {
+                                                 unsigned long long* total, int32_t* long_cnt,
+                                                 int32_t* long_list) {
   const int sub = threadIdx.x & 15;
   const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
   int64_t s = 0;
+  bool is_long = false;
   if (row < nrows) {
+    const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
     const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
-    for (int64_t p = ld_rp<RA>(op.arp, row) - op.a_base + sub; p < p1; p += 16) {
-      const int64_t k = op.acol[p];
-      s += ld_rp<RB>(op.brp, k + 1) - ld_rp<RB>(op.brp, k);
+    if (p1 - p0 > kLongRow) {
+      is_long = true;
+      if (sub == 0) long_list[atomicAdd(long_cnt, 1)] = (int32_t)row;
+    } else {
+      for (int64_t p = p0 + sub; p < p1; p += 64) {
+        int64_t k[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) k[u] = (p + 16 * u < p1) ? (int64_t)op.acol[p + 16 * u] : -1;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (k[u] >= 0) s += ld_rp<RB>(op.brp, k[u] + 1) - ld_rp<RB>(op.brp, k[u]);
+      }
     }
   }
 #pragma unroll
   for (int d = 8; d > 0; d >>= 1) s += __shfl_xor(s, d, 16);
-  if (row < nrows && sub == 0) P[row] = s;
+  if (row < nrows && sub == 0 && !is_long) P[row] = s;
   int64_t w = (sub == 0) ? s : 0;
   w = wave_sum(w);
   if (lane_id() == 0 && w) atomicAdd(total, (unsigned long long)w);
+}
+
+template <typename RA, typename RB>
+__global__ __launch_bounds__(1024) void k_analyze_long(const Operands op, int64_t* P,
+                                                       unsigned long long* total,
+                                                       const int32_t* long_cnt,
+                                                       const int32_t* long_list) {
+  __shared__ int64_t red[1024 / WAVE];
+  const int n = *long_cnt;
+  for (int it = blockIdx.x; it < n; it += gridDim.x) {
+    const int64_t row = long_list[it];
+    const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
+    const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
+    int64_t s = 0;
+    for (int64_t p = p0 + threadIdx.x; p < p1; p += 4 * 1024) {
+      int64_t k[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) k[u] = (p + 1024 * u < p1) ? (int64_t)op.acol[p + 1024 * u] : -1;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (k[u] >= 0) s += ld_rp<RB>(op.brp, k[u] + 1) - ld_rp<RB>(op.brp, k[u]);
+    }
+    s = wave_sum(s);
+    if (lane_id() == 0) red[threadIdx.x / WAVE] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int64_t t = 0;
+      for (int i = 0; i < 1024 / WAVE; ++i) t += red[i];
+      P[row] = t;
+      if (t) atomicAdd(total, (unsigned long long)t);
+    }
+    __syncthreads();
+  }
 }
 
 // ----------------------------------------------------------------- binning
@@ -176,19 +224,89 @@ __global__ __launch_bounds__(256) void k_bin_scatter(const int64_t* P, int64_t n
 
 // ---------------------------------------------------- flattened product loop
 
-// Per-group LDS for one chunk of A_i: inclusive term counts, the B position
-// of term 0 of each segment (shifted so pos = s_shift[c] + q), and a_ik.
-template <int GROUP>
+// Per-group LDS for one chunk of A_i: the B position
+// of term 0 of each segment (shifted so pos = shift[c] + q), a_ik, and a
+// segment map for a run of SEG_PER_THREAD * GROUP consecutive terms.  A
+// chunk holds fewer than 2^31 terms: segments are at most one window or one
+// B row wide and a chunk has at most GROUP of them.
+#ifndef AIRES_SEG_PER_THREAD
+#define AIRES_SEG_PER_THREAD 16
+#endif
+constexpr int SEG_PER_THREAD = AIRES_SEG_PER_THREAD;
+
+template <int GROUP, typename S>
 struct Chunk {
-  int64_t incl[GROUP];
-  int64_t shift[GROUP];
-  float av[GROUP];
+  using shift_t = S;  // B positions fit B's row-pointer type
+  struct Rec {
+    S shift;
+    float av;
+  };
+  Rec rec[GROUP];
+  uint16_t seg[GROUP * SEG_PER_THREAD];
 };
 
-// Calls f(pos, a_ik) for every term of row `row` restricted to window w.
-template <typename RA, typename RB, int GROUP, int BLOCK, bool NUM, bool WIDE, typename F>
+// Where the terms of a k come from: the whole B row ...
+template <typename RB>
+struct FullRows {
+  const void* brp;
+  __device__ __forceinline__ void operator()(int64_t k, int64_t& lo, int64_t& len) const {
+    lo = ld_rp<RB>(brp, k);
+    len = ld_rp<RB>(brp, k + 1) - lo;
+  }
+};
+// ... or the part of it in a run of column grains (two slabs of the index).
+struct GrainRange {
+  const int32_t* lo_slab;
+  const int32_t* hi_slab;
+  __device__ __forceinline__ void operator()(int64_t k, int64_t& lo, int64_t& len) const {
+    lo = lo_slab[k];
+    len = (int64_t)hi_slab[k] - lo;
+  }
+};
+
+#ifndef AIRES_UNROLL
+#define AIRES_UNROLL 4
+#endif
+constexpr int UNROLL = AIRES_UNROLL;  // independent B loads each thread keeps in flight
+
+template <int GROUP, int BLOCK>
+__device__ __forceinline__ int group_excl_max_scan(int v, const Group<GROUP, BLOCK>& g) {
+  // exclusive max over the threads before t (-1 for the first)
+  int x = v;
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    const int u = __shfl_up(x, d, WAVE);
+    if (lane_id() >= d) x = max(x, u);
+  }
+  int before = __shfl_up(x, 1, WAVE);
+  if (lane_id() == 0) before = -1;
+  if constexpr (GROUP == WAVE) {
+    return before;
+  } else {
+    const int w = threadIdx.x / WAVE;
+    int32_t* red = reinterpret_cast<int32_t*>(g.red);
+    if (lane_id() == WAVE - 1) red[w] = x;
+    __syncthreads();
+    int pre = -1;
+#pragma unroll
+    for (int i = 0; i < GROUP / WAVE; ++i)
+      if (i < w) pre = max(pre, red[i]);
+    __syncthreads();
+    return max(before, pre);
+  }
+}
+
+// Calls f(column, a_ik * b_kj) (NUM) or f(column, 0) for every term of a row.
+// Terms are numbered q = 0..total-1 over the chunk's segments; thread t
+// takes q = t, t + GROUP, ... so consecutive lanes read consecutive entries
+// of a B row.  The segment of each term comes from a map built per run of
+// GROUP * SEG_PER_THREAD terms: each segment's owner writes its id at its
+// first term, and a group max-scan carries ids forward.
+template <typename RA, int GROUP, int BLOCK, bool NUM, typename CH, typename SEG, typename F>
 __device__ __forceinline__ void for_each_term(const Operands& op, const Group<GROUP, BLOCK>& g,
-                                              Chunk<GROUP>& ch, int64_t row, int64_t w, F&& f) {
+                                              CH& ch, int64_t row, const SEG& seg, F&& f) {
+  using S = typename CH::shift_t;
+  constexpr int RUN = GROUP * SEG_PER_THREAD;
   const int t = g.t();
   const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
   const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
@@ -199,83 +317,112 @@ __device__ __forceinline__ void for_each_term(const Operands& op, const Group<GR
     if (p < p1) {
       const int64_t k = op.acol[p];
       if constexpr (NUM) av = op.aval[p];
-      if constexpr (WIDE) {
-        lo = op.bidx[w * op.K + k];
-        len = (int64_t)op.bidx[(w + 1) * op.K + k] - lo;
-      } else {
-        lo = ld_rp<RB>(op.brp, k);
-        len = ld_rp<RB>(op.brp, k + 1) - lo;
-      }
+      seg(k, lo, len);
     }
     int64_t total;
     const int64_t incl = g.incl_scan(len, &total);
-    ch.incl[t] = incl;
-    ch.shift[t] = lo - (incl - len);
-    if constexpr (NUM) ch.av[t] = av;
-    g.sync();
-    const int nseg = (int)((p1 - cb) < GROUP ? (p1 - cb) : GROUP);
-    for (int64_t q = t; q < total; q += GROUP) {
-      int a = 0, b = nseg - 1;
-      while (a < b) {
-        const int mid = (a + b) >> 1;
-        if (ch.incl[mid] > q) b = mid; else a = mid + 1;
+    const int64_t excl = incl - len;
+    ch.rec[t].shift = (S)(lo - excl);
+    ch.rec[t].av = av;
+    for (int64_t r0 = 0; r0 < total; r0 += RUN) {
+      const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
+      // segment map of terms [r0, r0 + rn)
+#pragma unroll
+      for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[i * GROUP + t] = 0;
+      g.sync();
+      if (len > 0 && incl > r0 && excl < r0 + rn) ch.seg[(excl > r0 ? excl : r0) - r0] = (uint16_t)t;
+      g.sync();
+      int run[SEG_PER_THREAD];
+      int m = -1;
+#pragma unroll
+      for (int i = 0; i < SEG_PER_THREAD; ++i) {
+        const int v = ch.seg[t * SEG_PER_THREAD + i];
+        m = max(m, v);
+        run[i] = m;
       }
-      f(ch.shift[a] + q, NUM ? ch.av[a] : 0.f);
+      const int before = group_excl_max_scan(m, g);
+#pragma unroll
+      for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[t * SEG_PER_THREAD + i] = (uint16_t)max(before, run[i]);
+      g.sync();
+      for (int q0 = t; q0 < rn; q0 += GROUP * UNROLL) {
+        int64_t pos[UNROLL];
+        float am[UNROLL];
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+          const int q = q0 + u * GROUP;
+          pos[u] = -1;
+          am[u] = 0.f;
+          if (q < rn) {
+            const typename CH::Rec rc = ch.rec[ch.seg[q]];
+            pos[u] = (int64_t)rc.shift + r0 + q;
+            am[u] = rc.av;
+          }
+        }
+        int j[UNROLL];
+        float bv[UNROLL];
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+          j[u] = 0;
+          bv[u] = 0.f;
+          if (pos[u] >= 0) {
+            j[u] = op.bcol[pos[u]];
+            if constexpr (NUM) bv[u] = op.bval[pos[u]];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u)
+          if (pos[u] >= 0) f(j[u], am[u] * bv[u]);
+      }
+      g.sync();
     }
-    g.sync();
   }
 }
 
-// -------------------------------------------------------- dense window path
+// -------------------------------------------------- dense path (narrow N)
 
-// LDS layout of one group: [bitmap W/32 words][acc W floats if NUM][Chunk][red]
+// LDS layout of one group: [bitmap N/32 words][acc N floats if NUM][Chunk][red]
 __host__ __device__ constexpr size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
 
-template <int GROUP, bool NUM>
+template <int GROUP, bool NUM, typename S>
 __host__ __device__ constexpr size_t dense_group_bytes(int W) {
   return align16(((size_t)W + 31) / 32 * 4) + (NUM ? align16((size_t)W * 4) : 0) +
-         align16(sizeof(Chunk<GROUP>)) + 64;
+         align16(sizeof(Chunk<GROUP, S>)) + 64;
 }
 
-template <typename RA, typename RB, int GROUP, int BLOCK, bool NUM, bool WIDE>
+// Narrow products (N <= 16384): a dense fp32 row of N slots plus a presence
+// bitmap in LDS per group; compaction walks the bitmap words with a group
+// scan of their popcounts, so the row is written with increasing columns.
+template <typename RA, typename RB, int GROUP, int BLOCK, bool NUM>
 __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinView bv,
                                                  const Outputs out) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NG = BLOCK / GROUP;
-  const int W = WIDE ? op.W : (int)op.N;
-  const size_t per = dense_group_bytes<GROUP, NUM>(W);
+  const int W = (int)op.N;
+  const size_t per = dense_group_bytes<GROUP, NUM, RB>(W);
   const int gi = threadIdx.x / GROUP;
   unsigned char* base = smem + gi * per;
   uint32_t* bm = reinterpret_cast<uint32_t*>(base);
   float* acc = reinterpret_cast<float*>(base + align16(((size_t)W + 31) / 32 * 4));
-  Chunk<GROUP>& ch = *reinterpret_cast<Chunk<GROUP>*>(
-      base + align16(((size_t)W + 31) / 32 * 4) + (NUM ? align16((size_t)W * 4) : 0));
+  using CH = Chunk<GROUP, RB>;
+  CH& ch = *reinterpret_cast<CH*>(base + align16(((size_t)W + 31) / 32 * 4) + (NUM ? align16((size_t)W * 4) : 0));
   Group<GROUP, BLOCK> g;
-  g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(Chunk<GROUP>)));
+  g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
   const int t = g.t();
-  const int nwd_full = (W + 31) / 32;
-  for (int i = t; i < nwd_full; i += GROUP) bm[i] = 0u;
+  const int nwd = (W + 31) / 32;
+  for (int i = t; i < nwd; i += GROUP) bm[i] = 0u;
   if constexpr (NUM)
     for (int i = t; i < W; i += GROUP) acc[i] = 0.f;
   g.sync();
 
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.bin + 1] - bv.binoff[bv.bin];
-  const int64_t nwin = WIDE ? op.nwin : 1;
-  const int64_t nitems = cnt * nwin;
-  for (int64_t it = (int64_t)blockIdx.x * NG + gi; it < nitems; it += (int64_t)gridDim.x * NG) {
-    const int64_t w = it / cnt;          // window-major: one B column slab at a time
-    const int64_t row = list[it - w * cnt];
-    const int64_t c0 = w * W;
-    const int Wn = (int)((op.N - c0) < W ? (op.N - c0) : W);
-
-    for_each_term<RA, RB, GROUP, BLOCK, NUM, WIDE>(op, g, ch, row, w, [&](int64_t pos, float a) {
-      const int j = op.bcol[pos] - (int)c0;
+  const FullRows<RB> seg{op.brp};
+  for (int64_t it = (int64_t)blockIdx.x * NG + gi; it < cnt; it += (int64_t)gridDim.x * NG) {
+    const int64_t row = list[it];
+    for_each_term<RA, GROUP, BLOCK, NUM>(op, g, ch, row, seg, [&](int j, float v) {
       atomicOr(&bm[j >> 5], 1u << (j & 31));
-      if constexpr (NUM) atomicAdd(&acc[j], a * op.bval[pos]);
+      if constexpr (NUM) atomicAdd(&acc[j], v);
     });
-
-    const int nwd = (Wn + 31) / 32;
     if constexpr (!NUM) {
       int64_t c = 0;
       for (int i = t; i < nwd; i += GROUP) {
@@ -283,31 +430,31 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
         bm[i] = 0u;
       }
       c = g.sum(c);
-      if (t == 0) {
-        if constexpr (WIDE) out.wcnt[row * nwin + w] = (int32_t)c;
-        else out.counts[row] = c;
-      }
+      if (t == 0) out.counts[row] = c;
     } else {
+      // one column per thread per round: present columns get consecutive
+      // output slots, so both C arrays are written with coalesced stores
       int64_t o0 = out.crp[row];
-      if constexpr (WIDE) o0 += out.wcnt[row * nwin + w];
-      for (int i0 = 0; i0 < nwd; i0 += GROUP) {
-        const int i = i0 + t;
-        uint32_t bits = (i < nwd) ? bm[i] : 0u;
-        int64_t tot;
-        const int64_t c = __popc(bits);
-        int64_t o = o0 + g.incl_scan(c, &tot) - c;
-        while (bits) {
-          const int b = __ffs(bits) - 1;
-          bits &= bits - 1;
-          const int j = i * 32 + b;
-          out.ccol[o] = j + (int)c0;
-          out.cval[o] = acc[j];
-          acc[j] = 0.f;
-          ++o;
+      for (int j0 = 0; j0 < W; j0 += GROUP) {
+        const int j = j0 + t;
+        const bool present = j < W && ((bm[j >> 5] >> (j & 31)) & 1u);
+        int64_t before, tot;
+        if constexpr (GROUP == WAVE) {
+          const uint64_t mask = __ballot(present);
+          before = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+          tot = __popcll(mask);
+        } else {
+          before = g.incl_scan(present ? 1 : 0, &tot) - (present ? 1 : 0);
         }
-        if (i < nwd) bm[i] = 0u;
+        if (present) {
+          out.ccol[o0 + before] = j;
+          out.cval[o0 + before] = acc[j];
+          acc[j] = 0.f;
+        }
         o0 += tot;
       }
+      g.sync();
+      for (int i = t; i < nwd; i += GROUP) bm[i] = 0u;
     }
     g.sync();
   }
@@ -315,11 +462,11 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
 
 // -------------------------------------------------------------- hash path
 
-template <int TABLE, int GROUP>
+template <int TABLE, int GROUP, bool NUM, typename S>
 struct HashLds {
   int32_t key[TABLE];
-  float val[TABLE];
-  Chunk<GROUP> ch;
+  float val[NUM ? TABLE : 1];
+  Chunk<GROUP, S> ch;
   int64_t red[GROUP / WAVE + 1];
 };
 
@@ -329,15 +476,18 @@ __device__ __forceinline__ uint32_t hslot(int j) {
   return ((uint32_t)j * 2654435761u) >> (32 - LOG2);
 }
 
+// Light rows of wide products: open addressing keyed by column (linear
+// probing, load <= 1/2 since nnz(C_i) <= P_i <= TABLE/2), then the occupied
+// slots are compacted and bitonic-sorted in LDS.
 template <typename RA, typename RB, int TABLE, int GROUP, int BLOCK, bool NUM>
 __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView bv,
                                                 const Outputs out) {
   constexpr int NG = BLOCK / GROUP;
   constexpr int SPT = TABLE / GROUP;   // table slots per thread
   static_assert(TABLE % GROUP == 0, "table divides over the group");
-  __shared__ HashLds<TABLE, GROUP> lds[NG];
+  __shared__ HashLds<TABLE, GROUP, NUM, RB> lds[NG];
   const int gi = threadIdx.x / GROUP;
-  HashLds<TABLE, GROUP>& L = lds[gi];
+  HashLds<TABLE, GROUP, NUM, RB>& L = lds[gi];
   Group<GROUP, BLOCK> g;
   g.red = L.red;
   const int t = g.t();
@@ -349,16 +499,16 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.bin + 1] - bv.binoff[bv.bin];
+  const FullRows<RB> seg{op.brp};
   for (int64_t it = (int64_t)blockIdx.x * NG + gi; it < cnt; it += (int64_t)gridDim.x * NG) {
     const int64_t row = list[it];
     int64_t mine = 0;
-    for_each_term<RA, RB, GROUP, BLOCK, NUM, false>(op, g, L.ch, row, 0, [&](int64_t pos, float a) {
-      const int j = op.bcol[pos];
+    for_each_term<RA, GROUP, BLOCK, NUM>(op, g, L.ch, row, seg, [&](int j, float v) {
       uint32_t h = hslot<TABLE>(j);
       for (;;) {
         const int old = atomicCAS(&L.key[h], -1, j);
         if (old == -1 || old == j) {
-          if constexpr (NUM) atomicAdd(&L.val[h], a * op.bval[pos]);
+          if constexpr (NUM) atomicAdd(&L.val[h], v);
           else mine += (old == -1);
           break;
         }
@@ -424,32 +574,384 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
   }
 }
 
-// ------------------------------------------------------- windowed row sums
+// ------------------------------------------------- wide rows: column windows
+//
+// Wide products (N above the densest LDS row) split the columns into grains
+// of G columns.  Symbolic: a workgroup sets a presence bitmap for a run of
+// grains of one row and writes each grain's popcount.  A plan kernel then
+// cuts every row into windows of whole grains holding at most max_entries
+// entries and spanning at most max_grains grains.  Numeric, per window:
+// pass 1 sets the window's presence bitmap, a workgroup scan turns word
+// popcounts into ranks, pass 2 adds each term into a compact fp32 array at
+// the rank of its column, and the array and the bitmap's columns are written
+// out in column order.  LDS grows with the window's entries, not its width.
 
-// For each row of a windowed bin: exclusive scan of its window counts in
-// place (they become offsets inside the row) and the row total.
-__global__ __launch_bounds__(256) void k_window_rowsum(const BinView bv, int32_t nwin,
-                                                       int32_t* wcnt, int64_t* counts) {
+constexpr int WIN_BLOCK = 512;
+
+template <typename S>
+__host__ __device__ constexpr size_t count_lds_bytes(int sg, int G) {
+  return align16((size_t)sg * (G / 32) * 4) + align16((size_t)sg * 4) + align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128;
+}
+
+template <typename RA, typename RB>
+__global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op, const BinView bv,
+                                                           const WindowParams wp) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int SG = wp.grains_per_count_item;
+  const int WPG = op.G / 32;  // bitmap words per grain
+  uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
+  int32_t* gc = reinterpret_cast<int32_t*>(smem + align16((size_t)SG * WPG * 4));
+  using CH = Chunk<WIN_BLOCK, RB>;
+  CH& ch = *reinterpret_cast<CH*>(smem + align16((size_t)SG * WPG * 4) + align16((size_t)SG * 4));
+  Group<WIN_BLOCK, WIN_BLOCK> g;
+  g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
+  const int t = threadIdx.x;
+  for (int i = t; i < SG * WPG; i += WIN_BLOCK) bm[i] = 0u;
+  for (int i = t; i < SG; i += WIN_BLOCK) gc[i] = 0;
+  __syncthreads();
+
   const int32_t* list = bv.list + bv.binoff[bv.bin];
-  const int64_t cnt = bv.binoff[bv.bin + 1] - bv.binoff[bv.bin];
-  for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt;
-       d += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t row = list[d];
-    int32_t* c = wcnt + row * nwin;
-    int64_t s = 0;
-    for (int w = 0; w < nwin; ++w) {
-      const int32_t v = c[w];
-      c[w] = (int32_t)s;
-      s += v;
+  const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
+  const int64_t ngg = (op.nG + SG - 1) / SG;
+  for (int64_t it = blockIdx.x; it < cnt * ngg; it += gridDim.x) {
+    const int64_t gg = it / cnt;  // grain-group major: one column slab of B at a time
+    const int64_t row = list[it - gg * cnt];
+    const int g0 = (int)(gg * SG);
+    const int g1 = min((int)op.nG, g0 + SG);
+    const int c0 = g0 * op.G;
+    const GrainRange seg{op.bidx + (int64_t)g0 * op.K, op.bidx + (int64_t)g1 * op.K};
+    for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg, [&](int j, float) {
+      j -= c0;
+      atomicOr(&bm[j >> 5], 1u << (j & 31));
+    });
+    // per-grain popcounts (a wavefront's 64 words lie in one grain when
+    // grains are a multiple of 64 words; otherwise each lane adds its own)
+    const int nw = (g1 - g0) * WPG;
+    const bool wave_grains = (WPG % WAVE) == 0;
+    for (int w0 = 0; w0 < nw; w0 += WIN_BLOCK) {
+      const int w = w0 + t;
+      int c = 0;
+      if (w < nw) {
+        c = __popc(bm[w]);
+        bm[w] = 0u;
+      }
+      if (wave_grains) {
+        c = wave_sum(c);
+        if (lane_id() == 0 && w < nw && c) atomicAdd(&gc[w / WPG], c);
+      } else if (w < nw && c) {
+        atomicAdd(&gc[w / WPG], c);
+      }
     }
-    counts[row] = s;
+    __syncthreads();
+    for (int k = t; k < g1 - g0; k += WIN_BLOCK) {
+      wp.gcnt[row * op.nG + g0 + k] = gc[k];
+      gc[k] = 0;
+    }
+    __syncthreads();
+  }
+}
+
+// Greedy windows of whole grains (at most max_grains grains and max_entries
+// entries); empty windows are skipped.  Calls f(g0, g1, n, roff).
+template <typename F>
+__device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, int max_grains, int max_entries,
+                                                F&& f) {
+  int64_t roff = 0;
+  int g0 = 0;
+  while (g0 < nG) {
+    int n = gc[g0];
+    int g1 = g0 + 1;
+    while (g1 < nG && g1 - g0 < max_grains && n + gc[g1] <= max_entries) n += gc[g1++];
+    if (n > 0) f(g0, g1, n, roff);
+    roff += n;
+    g0 = g1;
+  }
+  return roff;
+}
+
+__global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, const WindowParams wp,
+                                                  int64_t* counts) {
+  const int32_t* list = bv.list + bv.binoff[bv.bin];
+  const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
+  for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = list[d];
+    int64_t nwin = 0;
+    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries,
+                               [&](int, int, int, int64_t) { ++nwin; });
+    wp.item_count[1 + d] = nwin;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, const WindowParams wp) {
+  const int32_t* list = bv.list + bv.binoff[bv.bin];
+  const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
+  for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = list[d];
+    int64_t o = wp.item_count[d];  // scanned: windows of the rows before d
+    plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries,
+                 [&](int g0, int g1, int n, int64_t roff) {
+                   WinItem w;
+                   w.row = (int32_t)row;
+                   w.g0 = (uint16_t)g0;
+                   w.g1 = (uint16_t)g1;
+                   w.n = n;
+                   w.roff = (int32_t)roff;
+                   wp.items[o++] = w;
+                 });
+  }
+}
+
+// A window's LDS: its presence bitmap and the rank of each word's first set
+// bit, both with one pad word after every `wpt` words (wpt = words a thread
+// owns in the rank scan) so the per-thread runs fall in distinct banks; the
+// window's fp32 values (reused to stage its column ids); the chunk.
+__host__ __device__ constexpr int window_wpt_log2(int maxw) {
+  int l = 0;
+  while ((1 << l) * WIN_BLOCK < maxw) ++l;
+  return l;
+}
+__host__ __device__ constexpr int window_words_padded(int maxw) {
+  return maxw + (maxw >> window_wpt_log2(maxw)) + 1;
+}
+
+template <typename S>
+__host__ __device__ constexpr size_t window_lds_bytes(int max_grains, int max_entries, int G) {
+  return align16((size_t)window_words_padded(max_grains * (G / 32)) * 4) +
+         align16((size_t)window_words_padded(max_grains * (G / 32)) * 2) + align16((size_t)max_entries * 4) +
+         align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128 + 16;  // + the static row slot
+}
+
+// Numeric phase of wide rows.  Workgroups take rows from a shared counter
+// (the heaviest bin first) and walk each row's windows in column order.
+// For a row with at most WIN_BLOCK entries each thread keeps one (k, a_ik)
+// of the row in registers with the position where B_k's segment for the
+// current window starts; consecutive windows share a grain boundary, so a
+// window needs one index lookup per k (its end), issued while the previous
+// window is processed.  A window with at most WIN_BLOCK * SEG_PER_THREAD
+// terms loads each term once into registers; larger windows make two
+// passes over the B segments, keeping the row's state in LDS.
+template <typename RA, typename RB>
+__global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, const BinView bv,
+                                                           const WindowParams wp, const Outputs out) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int64_t s_row;
+  const int WPG = op.G / 32;
+  const int maxw = wp.max_grains * WPG;
+  const int lw = window_wpt_log2(maxw);
+  const int wpt = 1 << lw;
+  const int npad = window_words_padded(maxw);
+  uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
+  uint16_t* pre = reinterpret_cast<uint16_t*>(smem + align16((size_t)npad * 4));
+  float* vals = reinterpret_cast<float*>(smem + align16((size_t)npad * 4) + align16((size_t)npad * 2));
+  int32_t* stage = reinterpret_cast<int32_t*>(vals);  // column ids, once the values are out
+  using CH = Chunk<WIN_BLOCK, RB>;
+  CH& ch = *reinterpret_cast<CH*>(reinterpret_cast<unsigned char*>(vals) + align16((size_t)wp.max_entries * 4));
+  Group<WIN_BLOCK, WIN_BLOCK> g;
+  g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
+  const int t = threadIdx.x;
+  for (int i = t; i < npad; i += WIN_BLOCK) bm[i] = 0u;
+  for (int i = t; i < wp.max_entries; i += WIN_BLOCK) vals[i] = 0.f;
+  auto pidx = [&](int w) { return w + (w >> lw); };
+  constexpr int RUN = WIN_BLOCK * SEG_PER_THREAD;
+  const int32_t* list = bv.list + bv.binoff[bv.bin];
+  const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
+
+  for (;;) {
+    __syncthreads();
+    if (t == 0) s_row = atomicAdd(wp.row_counter, 1);
+    __syncthreads();
+    const int64_t dd = s_row;
+    if (dd >= cnt) break;
+    const int64_t d = cnt - 1 - dd;  // the heavy bin sits at the end of the list
+    const int64_t row = list[d];
+    const int64_t i0 = wp.item_count[d], i1 = wp.item_count[d + 1];
+    const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
+    const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
+    const int64_t rbase = out.crp[row];
+    const bool short_row = (p1 - p0) <= WIN_BLOCK;
+    int64_t k = -1;
+    float a = 0.f;
+    if (short_row && p0 + t < p1) {
+      k = op.acol[p0 + t];
+      a = op.aval[p0 + t];
+    }
+    int64_t cur = 0, nxt_hi = 0;
+    int prev_g1 = -1;
+    WinItem nextI{};
+    if (i0 < i1) {
+      nextI = wp.items[i0];
+      if (k >= 0) nxt_hi = op.bidx[(int64_t)nextI.g1 * op.K + k];
+    }
+    for (int64_t it = i0; it < i1; ++it) {
+      const WinItem I = nextI;
+      const int64_t hi = nxt_hi;
+      if (it + 1 < i1) {  // next window's header and segment ends, in flight meanwhile
+        nextI = wp.items[it + 1];
+        if (k >= 0) nxt_hi = op.bidx[(int64_t)nextI.g1 * op.K + k];
+      }
+      const int g0 = I.g0, g1 = I.g1, n = I.n;
+      const int c0 = g0 * op.G;
+      const int nw = (g1 - g0) * WPG;
+      const int64_t base = rbase + I.roff;
+      auto set_bit = [&](int j) { atomicOr(&bm[pidx(j >> 5)], 1u << (j & 31)); };
+      auto add_at_rank = [&](int j, float v) {
+        const int pw = pidx(j >> 5);
+        const int rk = (int)pre[pw] + __popc(bm[pw] & ((1u << (j & 31)) - 1u));
+        if (rk < n) atomicAdd(&vals[rk], v);
+      };
+      // exclusive popcount prefix over the window's words: each thread owns
+      // a run of wpt consecutive words
+      auto word_ranks = [&]() {
+        const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
+        int64_t sw = 0;
+        for (int w = w0; w < w1; ++w) sw += __popc(bm[pidx(w)]);
+        int64_t tot;
+        int64_t r = g.incl_scan(sw, &tot) - sw;
+        for (int w = w0; w < w1; ++w) {
+          const int pw = pidx(w);
+          pre[pw] = (uint16_t)r;
+          r += __popc(bm[pw]);
+        }
+        __syncthreads();
+      };
+      if (short_row) {
+        if (k >= 0 && g0 != prev_g1) cur = op.bidx[(int64_t)g0 * op.K + k];
+        const int64_t len = (k >= 0) ? hi - cur : 0;
+        int64_t total;
+        const int64_t incl = g.incl_scan(len, &total);
+        const int64_t excl = incl - len;
+        ch.rec[t].shift = (RB)(cur - excl);
+        ch.rec[t].av = a;
+        // segment map of terms [r0, r0 + rn)
+        auto seg_map = [&](int64_t r0, int rn) {
+#pragma unroll
+          for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[i * WIN_BLOCK + t] = 0;
+          __syncthreads();
+          if (len > 0 && incl > r0 && excl < r0 + rn) ch.seg[(excl > r0 ? excl : r0) - r0] = (uint16_t)t;
+          __syncthreads();
+          int runv[SEG_PER_THREAD];
+          int m = -1;
+#pragma unroll
+          for (int i = 0; i < SEG_PER_THREAD; ++i) {
+            m = max(m, (int)ch.seg[t * SEG_PER_THREAD + i]);
+            runv[i] = m;
+          }
+          const int before = group_excl_max_scan(m, g);
+#pragma unroll
+          for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[t * SEG_PER_THREAD + i] = (uint16_t)max(before, runv[i]);
+          __syncthreads();
+        };
+        if (total <= RUN) {
+          seg_map(0, (int)total);
+          int jj[SEG_PER_THREAD];
+          float vv[SEG_PER_THREAD];
+#pragma unroll
+          for (int i = 0; i < SEG_PER_THREAD; ++i) {
+            const int q = t + i * WIN_BLOCK;
+            jj[i] = -1;
+            vv[i] = 0.f;
+            if (q < total) {
+              const typename CH::Rec rc = ch.rec[ch.seg[q]];
+              const int64_t pos = (int64_t)rc.shift + q;
+              jj[i] = op.bcol[pos] - c0;
+              vv[i] = rc.av * op.bval[pos];
+            }
+          }
+#pragma unroll
+          for (int i = 0; i < SEG_PER_THREAD; ++i)
+            if (jj[i] >= 0) set_bit(jj[i]);
+          __syncthreads();
+          word_ranks();
+#pragma unroll
+          for (int i = 0; i < SEG_PER_THREAD; ++i)
+            if (jj[i] >= 0) add_at_rank(jj[i], vv[i]);
+        } else {
+          // two passes over runs of the window's terms; the row's state stays
+          for (int pass = 0; pass < 2; ++pass) {
+            for (int64_t r0 = 0; r0 < total; r0 += RUN) {
+              const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
+              seg_map(r0, rn);
+              for (int q0 = t; q0 < rn; q0 += WIN_BLOCK * UNROLL) {
+                int64_t pos[UNROLL];
+                float am[UNROLL];
+#pragma unroll
+                for (int u = 0; u < UNROLL; ++u) {
+                  const int q = q0 + u * WIN_BLOCK;
+                  pos[u] = -1;
+                  am[u] = 0.f;
+                  if (q < rn) {
+                    const typename CH::Rec rc = ch.rec[ch.seg[q]];
+                    pos[u] = (int64_t)rc.shift + r0 + q;
+                    am[u] = rc.av;
+                  }
+                }
+                int jv[UNROLL];
+                float bv2[UNROLL];
+#pragma unroll
+                for (int u = 0; u < UNROLL; ++u) {
+                  jv[u] = 0;
+                  bv2[u] = 0.f;
+                  if (pos[u] >= 0) {
+                    jv[u] = op.bcol[pos[u]] - c0;
+                    if (pass) bv2[u] = op.bval[pos[u]];
+                  }
+                }
+#pragma unroll
+                for (int u = 0; u < UNROLL; ++u) {
+                  if (pos[u] < 0) continue;
+                  if (pass) add_at_rank(jv[u], am[u] * bv2[u]);
+                  else set_bit(jv[u]);
+                }
+              }
+              __syncthreads();
+            }
+            if (pass == 0) word_ranks();
+          }
+        }
+        cur = hi;
+        prev_g1 = g1;
+      } else {
+        // long row: pass 1 presence bitmap, pass 2 add at the ranks
+        const GrainRange seg{op.bidx + (int64_t)g0 * op.K, op.bidx + (int64_t)g1 * op.K};
+        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg,
+                                                       [&](int j, float) { set_bit(j - c0); });
+        word_ranks();
+        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true>(op, g, ch, row, seg,
+                                                      [&](int j, float v) { add_at_rank(j - c0, v); });
+      }
+      __syncthreads();
+      // values out (coalesced), then the column ids staged in the same LDS
+      // array in rank order and written out coalesced as well
+      for (int kk = t; kk < n; kk += WIN_BLOCK) out.cval[base + kk] = vals[kk];
+      __syncthreads();
+      {
+        const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
+        for (int w = w0; w < w1; ++w) {
+          const int pw = pidx(w);
+          uint32_t bits = bm[pw];
+          int kk = (int)pre[pw];
+          while (bits) {
+            const int b = __ffs(bits) - 1;
+            bits &= bits - 1;
+            if (kk < n) stage[kk] = c0 + w * 32 + b;
+            ++kk;
+          }
+          bm[pw] = 0u;
+        }
+      }
+      __syncthreads();
+      for (int kk = t; kk < n; kk += WIN_BLOCK) {
+        out.ccol[base + kk] = stage[kk];
+        vals[kk] = 0.f;
+      }
+    }
   }
 }
 
 // ------------------------------------------------------------ window index
 
-// bidx[w*K + k] = first position p of B_k with bcol[p] >= w*W (or the row
-// end), for w in [0, nwin].  One wavefront per B row.
+// bidx[g*K + k] = first position p of B_k with bcol[p] >= g*W (or the row
+// end), for grains g in [0, nwin]; W is the grain width.  One wavefront per B row.
 template <typename RB>
 __global__ __launch_bounds__(256) void k_window_index(const void* brp, const int32_t* bcol,
                                                       int64_t K, int32_t W, int32_t nwin,
@@ -568,18 +1070,16 @@ int64_t grid_for(K kernel, int block, size_t lds, int64_t items_per_block, int64
   return need < cap ? need : cap;
 }
 
-template <typename RA, typename RB, int GROUP, int BLOCK, bool NUM, bool WIDE>
+template <typename RA, typename RB, int GROUP, int BLOCK, bool NUM>
 hipError_t launch_dense(const Operands& op, const BinView& bv, const Outputs& out, int64_t ub_rows,
                         hipStream_t s) {
-  auto kern = k_dense<RA, RB, GROUP, BLOCK, NUM, WIDE>;
-  const int W = WIDE ? op.W : (int)op.N;
-  const size_t lds = (BLOCK / GROUP) * dense_group_bytes<GROUP, NUM>(W);
+  auto kern = k_dense<RA, RB, GROUP, BLOCK, NUM>;
+  const size_t lds = (BLOCK / GROUP) * dense_group_bytes<GROUP, NUM, RB>((int)op.N);
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  const int64_t ub = ub_rows * (WIDE ? op.nwin : 1);
-  const int64_t grid = grid_for(kern, BLOCK, lds, BLOCK / GROUP, ub);
+  const int64_t grid = grid_for(kern, BLOCK, lds, BLOCK / GROUP, ub_rows);
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(BLOCK), lds, s, op, bv, out);
   return hipGetLastError();
 }
@@ -598,10 +1098,9 @@ hipError_t run_bin_t(int kind, const Operands& op, const BinView& bv, const Outp
                      int64_t ub_rows, hipStream_t s) {
   switch (kind) {
     case KIND_DENSE_WAVE:
-      return launch_dense<RA, RB, 64, 256, NUM, false>(op, bv, out, ub_rows, s);
+      return launch_dense<RA, RB, 64, 256, NUM>(op, bv, out, ub_rows, s);
     case KIND_DENSE_BLOCK:
-      if (op.bidx) return launch_dense<RA, RB, 512, 512, NUM, true>(op, bv, out, ub_rows, s);
-      return launch_dense<RA, RB, 512, 512, NUM, false>(op, bv, out, ub_rows, s);
+      return launch_dense<RA, RB, 512, 512, NUM>(op, bv, out, ub_rows, s);
     case KIND_HASH_128:
       return launch_hash<RA, RB, 128, 64, 256, NUM>(op, bv, out, ub_rows, s);
     case KIND_HASH_1024:
@@ -620,22 +1119,69 @@ hipError_t run_bin_rp(int kind, int phase, const Operands& op, const BinView& bv
                : run_bin_t<RA, RB, false>(kind, op, bv, out, ub_rows, s);
 }
 
+template <typename RA, typename RB>
+hipError_t win_symbolic_t(const Operands& op, const BinView& bv, const WindowParams& wp,
+                          const Outputs& out, int64_t ub_rows, hipStream_t s) {
+  auto kern = k_grain_count<RA, RB>;
+  const size_t lds = count_lds_bytes<RB>(wp.grains_per_count_item, op.G);
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t ngg = (op.nG + wp.grains_per_count_item - 1) / wp.grains_per_count_item;
+  const int64_t grid = grid_for(kern, WIN_BLOCK, lds, 1, ub_rows * ngg);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WIN_BLOCK), lds, s, op, bv, wp);
+  int64_t pg = (ub_rows + 255) / 256;
+  if (pg > 8192) pg = 8192;
+  hipLaunchKernelGGL(k_win_plan, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, wp, out.counts);
+  return hipGetLastError();
+}
+
+template <typename RA, typename RB>
+hipError_t win_numeric_t(const Operands& op, const BinView& bv, const WindowParams& wp,
+                         const Outputs& out, int64_t ub_rows, int64_t nitems, hipStream_t s) {
+  int64_t pg = (ub_rows + 255) / 256;
+  if (pg > 8192) pg = 8192;
+  hipLaunchKernelGGL(k_win_fill, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, wp);
+  if (nitems <= 0) return hipGetLastError();
+  hipError_t ez = hipMemsetAsync(wp.row_counter, 0, sizeof(int32_t), s);
+  if (ez != hipSuccess) return ez;
+  auto kern = k_win_rows<RA, RB>;
+  const size_t lds = window_lds_bytes<RB>(wp.max_grains, wp.max_entries, op.G);
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t grid = grid_for(kern, WIN_BLOCK, lds, 1, ub_rows);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WIN_BLOCK), lds, s, op, bv, wp, out);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 // ------------------------------------------------------------- host entry
 
-hipError_t analyze(const Operands& op, int64_t nrows, int64_t* P, unsigned long long* total,
-                   hipStream_t s) {
-  if (nrows <= 0) return hipSuccess;
+#define AIRES_DISPATCH_RP(op, FN, ...)                                                      \
+  ((op).rpa64 ? ((op).rpb64 ? FN<int64_t, int64_t>(__VA_ARGS__) : FN<int64_t, int32_t>(__VA_ARGS__)) \
+              : ((op).rpb64 ? FN<int32_t, int64_t>(__VA_ARGS__) : FN<int32_t, int32_t>(__VA_ARGS__)))
+
+template <typename RA, typename RB>
+static hipError_t analyze_t(const Operands& op, int64_t nrows, int64_t* P, unsigned long long* total,
+                            int32_t* long_cnt, int32_t* long_list, hipStream_t s) {
   const int64_t grid = (nrows * 16 + 255) / 256;
-  if (op.rpa64) {
-    if (op.rpb64) hipLaunchKernelGGL((k_analyze<int64_t, int64_t>), dim3((unsigned)grid), dim3(256), 0, s, op, nrows, P, total);
-    else hipLaunchKernelGGL((k_analyze<int64_t, int32_t>), dim3((unsigned)grid), dim3(256), 0, s, op, nrows, P, total);
-  } else {
-    if (op.rpb64) hipLaunchKernelGGL((k_analyze<int32_t, int64_t>), dim3((unsigned)grid), dim3(256), 0, s, op, nrows, P, total);
-    else hipLaunchKernelGGL((k_analyze<int32_t, int32_t>), dim3((unsigned)grid), dim3(256), 0, s, op, nrows, P, total);
-  }
+  hipLaunchKernelGGL((k_analyze<RA, RB>), dim3((unsigned)grid), dim3(256), 0, s, op, nrows, P, total, long_cnt,
+                     long_list);
+  int64_t lg = nrows / 64 + 1;
+  if (lg > 2048) lg = 2048;
+  hipLaunchKernelGGL((k_analyze_long<RA, RB>), dim3((unsigned)lg), dim3(1024), 0, s, op, P, total, long_cnt,
+                     long_list);
   return hipGetLastError();
+}
+
+hipError_t analyze(const Operands& op, int64_t nrows, int64_t* P, unsigned long long* total,
+                   int32_t* long_cnt, int32_t* long_list, hipStream_t s) {
+  if (nrows <= 0) return hipSuccess;
+  return AIRES_DISPATCH_RP(op, analyze_t, op, nrows, P, total, long_cnt, long_list, s);
 }
 
 hipError_t bin_rows(const int64_t* P, int64_t nrows, const BinThresholds& th, int32_t* cnt_cursor,
@@ -650,32 +1196,30 @@ hipError_t bin_rows(const int64_t* P, int64_t nrows, const BinThresholds& th, in
 hipError_t run_bin(int kind, int phase, const Operands& op, const BinView& bv, const Outputs& out,
                    int64_t ub_rows, hipStream_t s) {
   if (ub_rows <= 0) return hipSuccess;
-  if (op.rpa64) {
-    return op.rpb64 ? run_bin_rp<int64_t, int64_t>(kind, phase, op, bv, out, ub_rows, s)
-                    : run_bin_rp<int64_t, int32_t>(kind, phase, op, bv, out, ub_rows, s);
-  }
-  return op.rpb64 ? run_bin_rp<int32_t, int64_t>(kind, phase, op, bv, out, ub_rows, s)
-                  : run_bin_rp<int32_t, int32_t>(kind, phase, op, bv, out, ub_rows, s);
+  return AIRES_DISPATCH_RP(op, run_bin_rp, kind, phase, op, bv, out, ub_rows, s);
 }
 
-hipError_t window_rowsum(const BinView& bv, int32_t nwin, int32_t* wcnt, int64_t* counts,
-                         int64_t ub_rows, hipStream_t s) {
+hipError_t windows_symbolic(const Operands& op, const BinView& bv, const WindowParams& wp, const Outputs& out,
+                            int64_t ub_rows, hipStream_t s) {
   if (ub_rows <= 0) return hipSuccess;
-  int64_t grid = (ub_rows + 255) / 256;
-  if (grid > 4096) grid = 4096;
-  hipLaunchKernelGGL(k_window_rowsum, dim3((unsigned)grid), dim3(256), 0, s, bv, nwin, wcnt, counts);
-  return hipGetLastError();
+  return AIRES_DISPATCH_RP(op, win_symbolic_t, op, bv, wp, out, ub_rows, s);
 }
 
-hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, int64_t K, int32_t W,
-                              int32_t nwin, int32_t* bidx, hipStream_t s) {
+hipError_t windows_numeric(const Operands& op, const BinView& bv, const WindowParams& wp, const Outputs& out,
+                           int64_t ub_rows, int64_t nitems, hipStream_t s) {
+  if (ub_rows <= 0) return hipSuccess;
+  return AIRES_DISPATCH_RP(op, win_numeric_t, op, bv, wp, out, ub_rows, nitems, s);
+}
+
+hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, int64_t K, int32_t G,
+                              int32_t nG, int32_t* bidx, hipStream_t s) {
   if (K <= 0) return hipSuccess;
   int64_t grid = (K + 3) / 4;
   if (grid > 65536) grid = 65536;
   if (rpb64)
-    hipLaunchKernelGGL((k_window_index<int64_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, K, W, nwin, bidx);
+    hipLaunchKernelGGL((k_window_index<int64_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, K, G, nG, bidx);
   else
-    hipLaunchKernelGGL((k_window_index<int32_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, K, W, nwin, bidx);
+    hipLaunchKernelGGL((k_window_index<int32_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, K, G, nG, bidx);
   return hipGetLastError();
 }
 
@@ -697,20 +1241,26 @@ hipError_t scan_inplace(int64_t* x, int64_t n, void* ws, hipStream_t s) {
 size_t lds_bytes(int kind, int phase, int32_t W) {
   switch (kind) {
     case KIND_DENSE_WAVE:
-      return 4 * (phase ? dense_group_bytes<64, true>(W) : dense_group_bytes<64, false>(W));
+      return 4 * (phase ? dense_group_bytes<64, true, int64_t>(W) : dense_group_bytes<64, false, int64_t>(W));
     case KIND_DENSE_BLOCK:
-      return phase ? dense_group_bytes<512, true>(W) : dense_group_bytes<512, false>(W);
-    case KIND_HASH_128: return 4 * sizeof(HashLds<128, 64>);
-    case KIND_HASH_1024: return 4 * sizeof(HashLds<1024, 64>);
-    case KIND_HASH_8192: return sizeof(HashLds<8192, 256>);
+      return phase ? dense_group_bytes<512, true, int64_t>(W) : dense_group_bytes<512, false, int64_t>(W);
+    case KIND_HASH_128: return 4 * sizeof(HashLds<128, 64, true, int64_t>);
+    case KIND_HASH_1024: return 4 * sizeof(HashLds<1024, 64, true, int64_t>);
+    case KIND_HASH_8192: return sizeof(HashLds<8192, 256, true, int64_t>);
     default: return 0;
   }
+}
+
+size_t grain_count_lds(int sg, int G) { return count_lds_bytes<int64_t>(sg, G); }
+size_t window_numeric_lds(int max_grains, int max_entries, int G) {
+  return window_lds_bytes<int64_t>(max_grains, max_entries, G);
 }
 
 int group_size(int kind) {
   switch (kind) {
     case KIND_DENSE_BLOCK: return 512;
     case KIND_HASH_8192: return 256;
+    case KIND_WINDOWS: return WIN_BLOCK;
     default: return 64;
   }
 }

@@ -85,11 +85,18 @@ PATHS = {
     # narrow N (<= 2048): wavefront rows, workgroup rows
     "dense_wave": dict(),
     "dense_block": dict(wave_max_products=1),
-    # wide N through forced small windows: LDS hash bins and windowed dense rows
-    "windows_only": dict(dense_max_cols=64, hash_max_products=-1),
-    "hash128_then_windows": dict(dense_max_cols=96, hash_max_products=64),
-    "hash1024_then_windows": dict(dense_max_cols=128, hash_max_products=512),
-    "hash8192_then_windows": dict(dense_max_cols=160, hash_max_products=4096),
+    # wide N forced through tiny column grains: grain counts, windows of whole
+    # grains (several grains, ragged last grain), per-lane grain popcounts
+    "windows_only": dict(dense_max_cols=64, hash_max_products=-1, window_grain_cols=64,
+                         window_max_grains=2, window_max_entries=64, count_grains=3),
+    "hash128_then_windows": dict(dense_max_cols=96, hash_max_products=64, window_grain_cols=32,
+                                 window_max_grains=3, window_max_entries=40, count_grains=2),
+    "hash1024_then_windows": dict(dense_max_cols=128, hash_max_products=512, window_grain_cols=128,
+                                  window_max_grains=1, window_max_entries=128, count_grains=1),
+    "hash8192_then_windows": dict(dense_max_cols=160, hash_max_products=4096, window_grain_cols=96,
+                                  window_max_grains=4, window_max_entries=200, count_grains=5),
+    # 2048 < N <= 16384 handled as narrow: hash bins then workgroup dense rows
+    "narrow_block_hash": dict(dense_max_cols=200, hash_max_products=512),
 }
 
 
@@ -124,7 +131,17 @@ def test_cfg3_scaled_wide(torch_gpu):
     """A*A with N = 40000 > 16384: hash bins plus 3 column windows (ragged)."""
     A, B = workloads.workload(3, n=40000)
     st, _, _ = check(torch_gpu, A, B, "cfg3 n=40000")
-    assert st["kind_ms"]["numeric"]["dense_block"] > 0
+    assert st["kind_ms"]["numeric"]["windows"] > 0
+
+
+def test_cfg3_scaled_small_windows(torch_gpu):
+    """Many windows per row: 1024-column grains, windows of <= 4 grains and
+    <= 1024 entries, 8 grains per symbolic item (64-word grains: wave sums)."""
+    A, B = workloads.workload(3, n=40000)
+    check(torch_gpu, A, B, "cfg3 n=40000 small windows", window_grain_cols=2048, window_max_grains=4,
+          window_max_entries=2048, count_grains=8)
+    check(torch_gpu, A, B, "cfg3 n=40000 1024-col grains", window_grain_cols=1024, window_max_grains=3,
+          window_max_entries=1024, count_grains=5)
 
 
 def test_cfg3_scaled_narrow_block(torch_gpu):
@@ -208,7 +225,7 @@ def test_streamed_wide(torch_gpu):
     ref = oracle.spgemm(A, B)
     say("streamed wide cfg3 n=20000")
     with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 34, c_on_host=True, max_tile_rows=5000,
-                         dense_max_cols=4096) as plan:
+                         dense_max_cols=4096, window_grain_cols=4096) as plan:
         C = aires.spgemm(plan)
         assert_match(C.rp, C.col, C.val, ref)
         C.free()
