@@ -253,7 +253,10 @@ typedef struct aires_stats {
     int64_t nnz_c;
     int64_t h2d_bytes, d2h_bytes;
     int64_t host_syncs;
-    /* milliseconds from HIP events (opts->timing), summed over tiles      */
+    /* milliseconds from HIP events (opts->timing), summed over tiles.
+       h2d_ms / d2h_ms: busy time of the copy streams (events around each
+       tile's copies, after its waits).  total_ms: the whole call on the
+       compute stream, output allocation included.                        */
     double analyze_ms, bin_ms, symbolic_ms, scan_ms, numeric_ms;
     double h2d_ms, d2h_ms, total_ms;
     int64_t numeric_launches;   /* numeric-phase kernel launches           */
@@ -261,6 +264,9 @@ typedef struct aires_stats {
        0 empty, 1 dense-wave, 2 dense-block, 3 hash-128, 4 hash-1024,
        5 hash-8192, 6 column windows); [0] symbolic, [1] numeric phase     */
     double kind_ms[2][8];
+    /* streamed calls: from the first copy of Phase I to the last copy of
+       Phase III (the tile pipeline, without the output allocation)       */
+    double pipeline_ms;
 } aires_stats;
 
 /* Statistics of the last aires_spgemm / aires_stream_tiles on the plan. */

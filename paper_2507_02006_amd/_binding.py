@@ -70,7 +70,7 @@ class Stats(ctypes.Structure):
     _fields_ = [(n, c_i64) for n in ("ntiles", "products", "nnz_c", "h2d_bytes", "d2h_bytes", "host_syncs")] + \
                [(n, c_dbl) for n in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "h2d_ms",
                                      "d2h_ms", "total_ms")] + \
-               [("numeric_launches", c_i64), ("kind_ms", (c_dbl * 8) * 2)]
+               [("numeric_launches", c_i64), ("kind_ms", (c_dbl * 8) * 2), ("pipeline_ms", c_dbl)]
 
 
 _lib = None

@@ -587,7 +587,8 @@ kern::Operands tile_operands(const aires_plan* p, const void* arp, int64_t a_bas
 }
 
 // Phase markers for the stats: kinds >= 100 are whole phases.
-enum { PH_ANALYZE = 100, PH_BIN, PH_SYMBOLIC, PH_SCAN, PH_NUMERIC, PH_H2D, PH_D2H, PH_TOTAL, PH_INDEX };
+enum { PH_ANALYZE = 100, PH_BIN, PH_SYMBOLIC, PH_SCAN, PH_NUMERIC, PH_H2D, PH_D2H, PH_TOTAL, PH_INDEX,
+       PH_PIPELINE };
 
 // Device workspace of one tile (tile-local rows).
 struct TileWs {
@@ -883,7 +884,6 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   const int32_t* bcol = B.col_idx;
   const float* bval = B.vals;
   void *d_brp = nullptr, *d_bcol = nullptr, *d_bval = nullptr;
-  const int eh0 = tm.record();
   if (B.mem != AIRES_MEM_DEVICE) {
     ST_TRY(ws.get((size_t)(K + 1) * sB, &d_brp));
     ST_TRY(ws.get((size_t)std::max<int64_t>(B.nnz, 1) * 4, &d_bcol));
@@ -946,10 +946,14 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   ST_TRY(mkev(&ev_ws));
   HIP_TRY(hipEventRecord(ev_ws, sc));
   HIP_TRY(hipStreamWaitEvent(sh, ev_ws, 0));
+  Timer th{p, sh, tm.on}, td{p, sd, tm.on};  // copy-stream busy time
+  const int e_pipe0 = th.record();
   if (B.mem != AIRES_MEM_DEVICE) {
+    const int eb0 = th.record();
     HIP_TRY(hipMemcpyAsync(d_brp, B.row_ptr, (size_t)(K + 1) * sB, hipMemcpyHostToDevice, sh));
     HIP_TRY(hipMemcpyAsync(d_bcol, B.col_idx, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
     HIP_TRY(hipMemcpyAsync(d_bval, B.vals, (size_t)B.nnz * 4, hipMemcpyHostToDevice, sh));
+    th.mark(PH_H2D, 0, eb0, th.record());
     p->stats.h2d_bytes += (K + 1) * sB + 8 * B.nnz;
     brp = d_brp;
     bcol = (const int32_t*)d_bcol;
@@ -960,6 +964,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     const aires_tile& T = p->tiles[(size_t)t];
     Slot& S = slot[t % 2];
     if (t >= 2) HIP_TRY(hipStreamWaitEvent(sh, ev_done[(size_t)t - 2], 0));
+    const int ea = th.record();
     const int64_t k = T.r1 - T.r0, q = T.nnz1 - T.nnz0;
     HIP_TRY(hipMemcpyAsync(S.arp, static_cast<const char*>(A.row_ptr) + T.r0 * sA, (size_t)(k + 1) * sA,
                            hipMemcpyHostToDevice, sh));
@@ -968,14 +973,13 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
       HIP_TRY(hipMemcpyAsync(S.aval, A.vals + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
     }
     HIP_TRY(hipEventRecord(ev_in[(size_t)t], sh));
+    th.mark(PH_H2D, 0, ea, th.record());
     p->stats.h2d_bytes += (k + 1) * sA + 8 * q;
     return AIRES_OK;
   };
 
   if (nt > 0) ST_TRY(issue_h2d(0));
   if (nt > 1) ST_TRY(issue_h2d(1));
-  const int eh1 = tm.record();
-  tm.mark(PH_H2D, 0, eh0, eh1);
   if (p->wide && nt > 0) {
     HIP_TRY(hipStreamWaitEvent(sc, ev_in[0], 0));  // B is resident once tile 0 arrived
     HIP_TRY(kern::build_window_index(brp, B.rp_type == AIRES_IDX_I64, bcol, K, p->G, p->nG, bidx, sc));
@@ -1034,12 +1038,14 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     // Phase III for this tile
     if (c_on_host) {
       HIP_TRY(hipStreamWaitEvent(sd, ev_done[(size_t)t], 0));
+      const int ea = td.record();
       HIP_TRY(hipMemcpyAsync(C_rp + T.r0 + 1, S.crp + 1, sizeof(int64_t) * (size_t)k, hipMemcpyDeviceToHost, sd));
       if (nnz_t > 0) {
         HIP_TRY(hipMemcpyAsync(C_col + base, S.ccol, sizeof(int32_t) * (size_t)nnz_t, hipMemcpyDeviceToHost, sd));
         HIP_TRY(hipMemcpyAsync(C_val + base, S.cval, sizeof(float) * (size_t)nnz_t, hipMemcpyDeviceToHost, sd));
       }
       HIP_TRY(hipEventRecord(ev_cfree[t % 2], sd));
+      td.mark(PH_D2H, 0, ea, td.record());
       p->stats.d2h_bytes += 8 * k + 8 * nnz_t;
     } else {
       HIP_TRY(hipMemcpyAsync(C_rp + T.r0 + 1, S.crp + 1, sizeof(int64_t) * (size_t)k, hipMemcpyDeviceToDevice, sc));
@@ -1047,9 +1053,21 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     base = end;
     if (t + 2 < nt) ST_TRY(issue_h2d(t + 2));
   }
+  // the pipeline ends with the last copy: join the copy streams into sc
+  hipEvent_t ev_end[2];
+  ST_TRY(mkev(&ev_end[0]));
+  ST_TRY(mkev(&ev_end[1]));
+  HIP_TRY(hipEventRecord(ev_end[0], sh));
+  HIP_TRY(hipEventRecord(ev_end[1], sd));
+  HIP_TRY(hipStreamWaitEvent(sc, ev_end[0], 0));
+  HIP_TRY(hipStreamWaitEvent(sc, ev_end[1], 0));
+  {
+    const int e_end = tm.record();
+    tm.mark(PH_PIPELINE, 0, e_pipe0, e_end);
+    tm.mark(PH_TOTAL, 0, e_total0, e_end);
+  }
   HIP_TRY(hipStreamSynchronize(sd));
   HIP_TRY(hipStreamSynchronize(sh));
-  tm.mark(PH_TOTAL, 0, e_total0, tm.record());
   unsigned long long products = 0;
   HIP_TRY(hipMemcpyAsync(&products, prod, sizeof products, hipMemcpyDeviceToHost, sc));
   HIP_TRY(hipStreamSynchronize(sc));
@@ -1135,6 +1153,7 @@ aires_status aires_plan_stats(const aires_plan* plan, aires_stats* stats) {
         case PH_H2D: stats->h2d_ms += ms; break;
         case PH_D2H: stats->d2h_ms += ms; break;
         case PH_TOTAL: stats->total_ms += ms; break;
+        case PH_PIPELINE: stats->pipeline_ms += ms; break;
         default:
           if (mk.kind >= 0 && mk.kind < 8) stats->kind_ms[mk.phase][mk.kind] += ms;
           break;

@@ -323,3 +323,103 @@ def test_cfg2_full_sampled(torch_gpu):
 def test_cfg3_full_sampled(torch_gpu):
     A, B = workloads.workload(3)
     sampled_check(torch_gpu, A, B, "cfg3", _rows(A, B, k=60, heavy=2))
+
+
+# ------------------------------------------- full-size cfg4 / cfg5 (tiled)
+
+def _check_structure(rp, col, P, N):
+    """Invariants that hold at any size: monotone int64 row_ptr, per-row
+    counts within the product bound, strictly increasing columns per row."""
+    lens = np.diff(rp)
+    assert rp[0] == 0 and np.all(lens >= 0)
+    assert np.all(lens <= np.minimum(P, N)) and np.all(lens >= (P > 0))
+    starts = np.zeros(len(col), dtype=bool)
+    starts[rp[:-1][lens > 0]] = True
+    step = 1 << 26
+    for s in range(0, len(col) - 1, step):
+        e = min(len(col), s + step + 1)
+        d = np.diff(col[s:e].astype(np.int64))
+        assert np.all((d > 0) | starts[s + 1:e]), "columns not increasing near entry %d" % s
+    assert col.min(initial=0) >= 0 and col.max(initial=0) < N
+
+
+def _check_rows(A, B, rp, col, val, rows):
+    for r in rows:
+        ref = oracle.spgemm(A, B, int(r), int(r) + 1)
+        s, e = int(rp[r]), int(rp[r + 1])
+        assert e - s == ref.nnz, "row %d nnz" % r
+        assert np.array_equal(col[s:e], ref.col), "row %d cols" % r
+        err = np.abs(val[s:e].astype(np.float64) - ref.val.astype(np.float64))
+        assert np.all(err <= TOL * (1 + np.abs(ref.val.astype(np.float64)))), "row %d vals" % r
+
+
+@pytest.mark.slow
+def test_cfg4_full_tiled(torch_gpu):
+    """8,388,608-node aggregation under a 64 GB budget, cut into row-block
+    tiles by a tile cap (Algorithm 1), device-resident operands."""
+    import paper_2507_02006_amd as aires
+    say("cfg4 full size: generating")
+    A, B = workloads.workload(4, verbose=True)
+    P = oracle.products(A, B)
+    say("cfg4 nnzA=%d nnzB=%d products=%d" % (A.nnz, B.nnz, int(P.sum())))
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    with aires.tile_plan(dA, dB, 64 << 30, max_tile_bytes=256 << 20, timing=True) as plan:
+        info = aires.plan_info(plan)
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        st = aires.plan_stats(plan)
+    say("cfg4 tiles=%d nnzC=%d total_ms=%.1f" % (info.ntiles, st["nnz_c"], st["total_ms"]))
+    assert info.ntiles >= 4
+    assert st["products"] == int(P.sum())
+    rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    del C
+    _check_structure(rp, col, P, B.ncols)
+    _check_rows(A, B, rp, col, val, _rows(A, B, k=300, heavy=5, seed=4))
+
+
+@pytest.mark.slow
+def test_cfg5_full_streamed(torch_gpu):
+    """68M-node aggregation, A (int64 row_ptr) and X in pinned host memory,
+    32 GB device budget: row-block tiles stream host to HBM double-buffered
+    and C tiles return to pinned host memory (Algorithm 2)."""
+    import paper_2507_02006_amd as aires
+    torch = torch_gpu
+    hold = []
+
+    def pinned(n, rp_dtype):
+        def out(nnz):
+            rp = torch.empty(n + 1, dtype=rp_dtype, pin_memory=True)
+            col = torch.empty(max(nnz, 1), dtype=torch.int32, pin_memory=True)[:nnz]
+            val = torch.empty(max(nnz, 1), dtype=torch.float32, pin_memory=True)[:nnz]
+            hold.append((rp, col, val))
+            return rp.numpy(), col.numpy(), val.numpy()
+        return out
+
+    n = workloads.CONFIGS[5]["n"]
+    say("cfg5 full size: generating into pinned memory")
+    A, B = workloads.workload(5, out_a=pinned(n, torch.int64), out_b=pinned(n, torch.int32), verbose=True)
+    assert A.rp.dtype == np.int64
+    tA = (A.nrows, A.ncols) + hold[0]
+    tB = (B.nrows, B.ncols) + hold[1]
+    P = oracle.products(A, B)
+    say("cfg5 nnzA=%d nnzB=%d products=%d" % (A.nnz, B.nnz, int(P.sum())))
+    with aires.tile_plan(tA, tB, 32 << 30, c_on_host=True, max_tile_bytes=768 << 20, timing=True) as plan:
+        info = aires.plan_info(plan)
+        say("cfg5 plan: %d tiles, peak %.2f GB of %d GB" % (info.ntiles, info.peak_bytes / 1e9, 32))
+        assert info.a_streamed and info.c_on_host and info.ntiles >= 8
+        assert info.peak_bytes <= 32 << 30
+        C = aires.spgemm(plan)
+        st = aires.plan_stats(plan)
+        compute_ms = sum(st[k] for k in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms"))
+        say("cfg5 streamed: nnzC=%d total_ms=%.1f pipeline_ms=%.1f h2d_ms=%.1f compute_ms=%.1f d2h_ms=%.1f "
+            "h2d=%.2fGB d2h=%.2fGB" % (st["nnz_c"], st["total_ms"], st["pipeline_ms"], st["h2d_ms"], compute_ms,
+                                       st["d2h_ms"], st["h2d_bytes"] / 1e9, st["d2h_bytes"] / 1e9))
+        assert st["products"] == int(P.sum())
+        assert st["host_syncs"] == info.ntiles
+        assert st["h2d_bytes"] == A.nbytes() + B.nbytes() + 8 * (info.ntiles - 1)
+        # transfers overlapped with compute: the pipeline is shorter than its parts in sequence
+        assert st["pipeline_ms"] < 0.9 * (st["h2d_ms"] + compute_ms + st["d2h_ms"])
+        assert C.on_host
+        _check_structure(C.rp, C.col, P, B.ncols)
+        _check_rows(A, B, C.rp, C.col, C.val, _rows(A, B, k=200, heavy=5, seed=5))
+        C.free()

@@ -14,6 +14,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys
 import subprocess
 from dataclasses import dataclass
 
@@ -47,7 +48,7 @@ def _load():
         lib = ctypes.CDLL(_LIB)
         i64, u64, dbl, vp = ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_void_p
         lib.rmat_build.restype = vp
-        lib.rmat_build.argtypes = [i64, dbl, dbl, dbl, dbl, u64]
+        lib.rmat_build.argtypes = [i64, dbl, dbl, dbl, dbl, u64, ctypes.c_int]
         for f in ("rmat_nnz", "rmat_samples", "rmat_self_samples"):
             getattr(lib, f).restype = i64
             getattr(lib, f).argtypes = [vp]
@@ -88,15 +89,16 @@ def _ptr(a: np.ndarray) -> int:
 
 
 def rmat_sym(n: int, avg_deg: float, seed: int, rp64: bool = False,
-             abcd=RMAT_ABCD, out=None) -> CSR:
+             abcd=RMAT_ABCD, out=None, verbose: bool = False) -> CSR:
     """Symmetric R-MAT graph, self-loops added, values 1/sqrt(d_i d_j) in fp32.
 
     ``out`` may supply preallocated (rp, col, val) buffers (e.g. pinned host
     memory viewed as numpy) of the right sizes; otherwise numpy allocates.
+    ``verbose`` prints a line to stderr as each generation stage ends.
     """
     lib = _load()
     a, b, c, _ = abcd
-    h = lib.rmat_build(int(n), float(avg_deg), a, b, c, int(seed))
+    h = lib.rmat_build(int(n), float(avg_deg), a, b, c, int(seed), int(bool(verbose)))
     if not h:
         raise MemoryError("rmat_build failed for n=%d" % n)
     try:
@@ -115,11 +117,14 @@ def rmat_sym(n: int, avg_deg: float, seed: int, rp64: bool = False,
     return CSR(n, n, rp, col, val)
 
 
-def features(n: int, F: int, rho: float, seed: int, rp64: bool = False, out=None) -> CSR:
+def features(n: int, F: int, rho: float, seed: int, rp64: bool = False, out=None,
+             verbose: bool = False) -> CSR:
     """n x F sparse features: each entry present w.p. rho, value U[-1, 1) as fp32."""
     lib = _load()
     lens = np.empty(n, dtype=np.int64)
     nnz = int(lib.feat_count(int(n), int(F), float(rho), int(seed), _ptr(lens)))
+    if verbose:
+        print("[gen] features %dx%d counted: nnz %d" % (n, F, nnz), file=sys.stderr, flush=True)
     rp64_tmp = np.zeros(n + 1, dtype=np.int64)
     np.cumsum(lens, out=rp64_tmp[1:])
     if out is None:
@@ -145,15 +150,15 @@ CONFIGS = {
 }
 
 
-def workload(cfg: int, n: int | None = None, out_a=None, out_b=None):
+def workload(cfg: int, n: int | None = None, out_a=None, out_b=None, verbose: bool = False):
     """Return (A, B) for workload ``cfg``; ``n`` overrides the node count
     (same degree, width and density) for scaled-down parity cases."""
     c = CONFIGS[cfg]
     nn = c["n"] if n is None else int(n)
-    A = rmat_sym(nn, c["deg"], seed=cfg, rp64=c["rp64"], out=out_a)
+    A = rmat_sym(nn, c["deg"], seed=cfg, rp64=c["rp64"], out=out_a, verbose=verbose)
     if c["F"] is None:
         return A, A
-    B = features(nn, c["F"], c["rho"], seed=1000 + cfg, out=out_b)
+    B = features(nn, c["F"], c["rho"], seed=1000 + cfg, out=out_b, verbose=verbose)
     return A, B
 
 

@@ -30,6 +30,7 @@
 #include <stdlib.h>
 #include <string.h>
 #include <omp.h>
+#include <stdio.h>
 
 static inline uint64_t sm64_mix(uint64_t z)
 {
@@ -99,8 +100,11 @@ static void rmat_sample(uint64_t seed, int64_t e, int levels, int64_t n,
  * failure.  deg_target is D (accepted samples = n*D/2).
  */
 rmat_graph *rmat_build(int64_t n, double deg_target, double a, double b, double c,
-                       uint64_t seed)
+                       uint64_t seed, int verbose)
 {
+    const double t0 = omp_get_wtime();
+#define GEN_STAGE(name) \
+    do { if (verbose) { fprintf(stderr, "[gen] n=%lld %s %.1fs\n", (long long)n, name, omp_get_wtime() - t0); fflush(stderr); } } while (0)
     if (n <= 0) return NULL;
     int levels = 0;
     while (((int64_t)1 << levels) < n) ++levels;
@@ -126,6 +130,7 @@ rmat_graph *rmat_build(int64_t n, double deg_target, double a, double b, double 
         int64_t j = (int64_t)(((unsigned __int128)h * (uint64_t)(i + 1)) >> 64);
         int32_t t = perm[i]; perm[i] = perm[j]; perm[j] = t;
     }
+    GEN_STAGE("permutation");
 
     /* Samples, relabelled; self samples marked with all-ones. */
     int64_t selfs = 0;
@@ -142,6 +147,7 @@ rmat_graph *rmat_build(int64_t n, double deg_target, double a, double b, double 
         cnt[pv]++;
     }
     g->self_samples = selfs;
+    GEN_STAGE("samples");
 
     /* Bucket both directions by row (+1 slot per row for the self-loop). */
     int64_t *off = (int64_t *)malloc(sizeof(int64_t) * ((size_t)n + 1));
@@ -167,6 +173,7 @@ rmat_graph *rmat_build(int64_t n, double deg_target, double a, double b, double 
         tmp[pv] = (int32_t)u;
     }
     free(pairs); pairs = NULL;
+    GEN_STAGE("bucketed");
 
     /* Sort + dedupe each row in place; record the unique length. */
     int64_t *len = cur;
@@ -185,6 +192,7 @@ rmat_graph *rmat_build(int64_t n, double deg_target, double a, double b, double 
     g->rp[0] = 0;
     for (int64_t i = 0; i < n; ++i) g->rp[i + 1] = g->rp[i] + len[i];
     g->nnz = g->rp[n];
+    GEN_STAGE("sorted and deduplicated");
     g->col = (int32_t *)malloc(sizeof(int32_t) * (size_t)(g->nnz > 0 ? g->nnz : 1));
     g->val = (float *)malloc(sizeof(float) * (size_t)(g->nnz > 0 ? g->nnz : 1));
     if (!g->col || !g->val) { free(off); free(tmp); goto fail; }
@@ -206,6 +214,8 @@ rmat_graph *rmat_build(int64_t n, double deg_target, double a, double b, double 
     }
     free(perm);
     free(cnt);
+    GEN_STAGE("normalised");
+#undef GEN_STAGE
     return g;
 
 fail:
