@@ -147,6 +147,11 @@ typedef struct aires_plan_opts {
     int64_t window_max_entries; /* C entries one window may hold, in
                                    [grain, 65535] (8192)                   */
     int64_t count_grains;       /* grains one symbolic item covers (32)    */
+    int64_t keep_bitmap_products; /* 0: default (65536), < 0: never.  The
+                                   symbolic phase keeps the presence bitmaps
+                                   of rows with more products than this for
+                                   the numeric phase (in-core runs, within a
+                                   fifth of the budget the plan leaves)    */
 } aires_plan_opts;
 
 /* Fill *o with defaults (struct_size set, validate 0, C on device). */

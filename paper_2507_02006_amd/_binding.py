@@ -53,7 +53,8 @@ class PlanOpts(ctypes.Structure):
                 ("timing", c_i32), ("_pad0", c_i32), ("max_tile_rows", c_i64), ("max_tile_bytes", c_i64),
                 ("m_a_bytes", c_i64), ("allocator", ctypes.POINTER(Allocator)), ("dense_max_cols", c_i64),
                 ("hash_max_products", c_i64), ("wave_max_products", c_i64), ("window_grain_cols", c_i64),
-                ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64)]
+                ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64),
+                ("keep_bitmap_products", c_i64)]
 
 
 class PlanInfo(ctypes.Structure):

@@ -52,6 +52,8 @@ constexpr int64_t kGrainCols = 8192;         // column grain of wide products
 constexpr int64_t kWindowMaxGrains = 16;     // grains one window may span
 constexpr int64_t kWindowMaxEntries = 8192;  // C entries one window may hold
 constexpr int64_t kCountGrains = 32;         // grains one symbolic item covers
+constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps kept for heavy rows
+constexpr int64_t kKeepBitmapProducts = 65536;           // rows above this many products keep them
 constexpr int64_t kWaveMaxProducts = 8192;   // rows up to this go to one wavefront
 constexpr int64_t kHashMaxProducts = 4096;   // = 8192-slot table at load <= 1/2
 constexpr int64_t kFixedWorkspace = 4 << 20; // scan partials, counters, slack
@@ -140,6 +142,8 @@ struct aires_plan {
   int wide = 0;
   int32_t G = 0, nG = 0;           // column grains (wide products)
   int32_t win_grains = 0, win_entries = 0, count_grains = 0;
+  int32_t ngg = 0;                 // symbolic items per wide row (runs of count_grains grains)
+  int64_t keep_bitmap = 0;         // rows with more products keep their symbolic bitmaps (-1: none)
   // host copies needed for streaming
   std::vector<int64_t> P_host;  // per-row products when computed on the host
   // timing events of the last call
@@ -189,6 +193,8 @@ void bin_plan(aires_plan* p) {
       p->win_entries = (int32_t)(o.window_max_entries > 0 ? o.window_max_entries
                                                           : std::max<int64_t>(kWindowMaxEntries, p->G));
       p->count_grains = (int32_t)(o.count_grains > 0 ? o.count_grains : kCountGrains);
+      p->ngg = (p->nG + p->count_grains - 1) / p->count_grains;
+      p->keep_bitmap = o.keep_bitmap_products == 0 ? kKeepBitmapProducts : o.keep_bitmap_products;
     }
   }
   th.nb = nb;
@@ -392,7 +398,7 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   int64_t per_row_ws = 8 + 4 + (p->wide ? 4 * nG + 8 : 0);
   if (!a_streamed) {
     // A and C.row_ptr resident; bin lists and window bookkeeping for all rows
-    resident += p->info.a_bytes + 8 * (m + 1) + (4 + (p->wide ? 4 * nG + 8 : 0)) * m;
+    resident += p->info.a_bytes + 8 * (m + 1) + (4 + (p->wide ? 4 * nG + 8 + 8 * p->ngg : 0)) * m;
     per_row_ws = 8;
   } else if (o.m_a_bytes == 0) {
     // C bound per row for the C slots (or for a device-resident C)
@@ -602,6 +608,10 @@ struct TileWs {
   int64_t nitems = 0;            // host copy of icount[n]
   int32_t* wcounter = nullptr;   // row counter of the window kernel
   void* scan_ws = nullptr;
+  int64_t* bm_off = nullptr;     // [n * ngg] kept bitmaps of the symbolic items (wide, in-core)
+  uint32_t* bm_cache = nullptr;  // shared bitmap cache (nullptr: none)
+  int64_t bm_cap = 0;
+  unsigned long long* bm_top = nullptr;
 };
 
 aires_status alloc_tile_ws(aires_plan* p, DevPool& ws, int64_t n, bool with_list_gcnt, TileWs& w) {
@@ -629,6 +639,12 @@ kern::WindowParams window_params(const aires_plan* p, const TileWs& w) {
   wp.item_count = w.icount;
   wp.items = w.items;
   wp.row_counter = w.wcounter;
+  wp.bm_cache = w.bm_cache;
+  wp.bm_cap = w.bm_cap;
+  wp.bm_top = w.bm_top;
+  wp.bm_off = w.bm_off;
+  wp.P = w.P;
+  wp.bm_min_products = p->keep_bitmap;
   return wp;
 }
 
@@ -733,10 +749,29 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   ST_TRY(ws.get_n(m, &list));
   ST_TRY(ws.get_n(nt * (kern::MAX_BINS + 1), &binoff));
   ST_TRY(ws.get_n(1, &prod));
+  int64_t* bm_off = nullptr;
+  uint32_t* bm_cache = nullptr;
+  unsigned long long* bm_top = nullptr;
+  int64_t bm_cap = 0;
   if (p->wide) {
     ST_TRY(ws.get_n(m * (int64_t)p->nG, &gcnt));
     ST_TRY(ws.get_n(m + nt, &icount));
     ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
+    if (p->keep_bitmap >= 0) {
+      ST_TRY(ws.get_n(m * (int64_t)p->ngg, &bm_off));
+      ST_TRY(ws.get_n(1, &bm_top));
+      // The kept bitmaps are a cache: they take up to a fifth of the budget
+      // the plan leaves free; items that do not fit are marked again by the
+      // numeric phase, and the cache is dropped if C then does not fit.
+      const int64_t spare = p->budget - p->info.peak_bytes;
+      bm_cap = spare > 0 ? std::min<int64_t>(spare / 5, kBitmapCacheBytes) / (int64_t)sizeof(uint32_t) : 0;
+      const int64_t words_all = m * (int64_t)p->nG * (p->G / 32);  // every row's bitmaps
+      if (words_all / std::max<int64_t>(m, 1) == (int64_t)p->nG * (p->G / 32)) bm_cap = std::min(bm_cap, words_all);
+      if (bm_cap > 0 && ws.get_n(bm_cap, &bm_cache) != AIRES_OK) {
+        bm_cache = nullptr;
+        bm_cap = 0;
+      }
+    }
   }
   auto tile_ws = [&](int64_t t) {
     const aires_tile& T = p->tiles[(size_t)t];
@@ -746,11 +781,18 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
     if (p->wide) {
       w.gcnt = gcnt + T.r0 * (int64_t)p->nG;
       w.icount = icount + T.r0 + t;
+      if (bm_cache) {
+        w.bm_cache = bm_cache;
+        w.bm_cap = bm_cap;
+        w.bm_top = bm_top;
+        w.bm_off = bm_off + T.r0 * (int64_t)p->ngg;
+      }
     }
     return w;
   };
   HIP_TRY(hipMemsetAsync(crp, 0, sizeof(int64_t), s));
   HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long), s));
+  if (bm_cache) HIP_TRY(hipMemsetAsync(bm_top, 0, sizeof(unsigned long long), s));
   if (p->wide) {
     const int ea = tm.record();
     HIP_TRY(kern::build_window_index(p->B.row_ptr, p->B.rp_type == AIRES_IDX_I64, p->B.col_idx, K, p->G, p->nG,
@@ -787,6 +829,14 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   if (resident + 8 * nnz > p->budget)
     return fail(AIRES_E_BUDGET, "C needs %lld bytes; budget %lld leaves %lld", (long long)(8 * nnz),
                 (long long)p->budget, (long long)(p->budget - resident));
+  if (bm_cache && p->info.peak_bytes + 4 * bm_cap + 8 * nnz > p->budget) {
+    // C and the kept bitmaps do not fit together: drop the bitmaps (the
+    // numeric phase then marks every window from the products)
+    ws.a.free(ws.a.ctx, bm_cache, (void*)s);
+    ws.detach(bm_cache);
+    bm_cache = nullptr;
+    bm_cap = 0;
+  }
   int32_t* ccol = nullptr;
   float* cval = nullptr;
   ST_TRY(ws.get_n(nnz, &ccol));

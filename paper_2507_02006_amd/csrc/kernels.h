@@ -64,12 +64,22 @@ struct WinItem {
 
 struct WindowParams {
   int32_t* gcnt;           // [row * nG + g] entries of C in grain g (per tile)
-  int32_t grains_per_count_item;  // grains one symbolic item covers
+  int32_t grains_per_count_item;  // grains one symbolic item covers (windows never straddle items)
   int32_t max_grains;      // grains one window may span
   int32_t max_entries;     // entries one window may hold (>= G)
   int64_t* item_count;     // [1 + d]: windows of the d-th row of the bins; scanned into offsets
   WinItem* items;          // filled in the numeric sweep
   int32_t* row_counter;    // zeroed before the numeric launch (dynamic row scheduling)
+  // Presence bitmaps kept by the symbolic phase for heavy rows (nullptr:
+  // none): the words of symbolic item (row, run of grains) start at
+  // bm_off[row * items_per_row + item] (-1: not kept), so the numeric phase
+  // reads them instead of marking the window from its products.
+  uint32_t* bm_cache;
+  int64_t bm_cap;                    // words the cache holds
+  unsigned long long* bm_top;        // words handed out so far (zeroed once per call)
+  int64_t* bm_off;                   // [row * items_per_row + item] per tile
+  const int64_t* P;                  // intermediate products per tile row
+  int64_t bm_min_products;           // rows with more products keep their bitmaps
 };
 
 // P_i per tile row and their total; rows longer than `long_row` entries are

@@ -588,25 +588,47 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 
 constexpr int WIN_BLOCK = 512;
 
+// Bitmaps of symbolic items and windows: each thread owns a run of `wpt`
+// consecutive words (a power of two, wpt * WIN_BLOCK >= words), and one pad
+// word follows every run so that the runs of a wavefront fall in distinct
+// banks.
+__host__ __device__ constexpr int window_wpt_log2(int maxw) {
+  int l = 0;
+  while ((1 << l) * WIN_BLOCK < maxw) ++l;
+  return l;
+}
+__host__ __device__ constexpr int window_words_padded(int maxw) {
+  return maxw + (maxw >> window_wpt_log2(maxw)) + 1;
+}
+
 template <typename S>
 __host__ __device__ constexpr size_t count_lds_bytes(int sg, int G) {
-  return align16((size_t)sg * (G / 32) * 4) + align16((size_t)sg * 4) + align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128;
+  return align16((size_t)window_words_padded(sg * (G / 32)) * 4) + align16((size_t)sg * 4) +
+         align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128 + 16;  // + the static list offset
 }
 
 template <typename RA, typename RB>
 __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op, const BinView bv,
                                                            const WindowParams wp) {
   extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int64_t s_off;
+  constexpr int64_t CACHE_CHUNK = 65536;  // cache words a workgroup takes from the shared buffer at once
+  int64_t chunk_cur = 0, chunk_end = 0;   // thread 0: the workgroup's current chunk
   const int SG = wp.grains_per_count_item;
   const int WPG = op.G / 32;  // bitmap words per grain
+  const int nwmax = SG * WPG;
+  const int lw = window_wpt_log2(nwmax);
+  const int wpt = 1 << lw;
   uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
-  int32_t* gc = reinterpret_cast<int32_t*>(smem + align16((size_t)SG * WPG * 4));
+  const size_t bm_bytes = align16((size_t)window_words_padded(nwmax) * 4);
+  int32_t* gc = reinterpret_cast<int32_t*>(smem + bm_bytes);
   using CH = Chunk<WIN_BLOCK, RB>;
-  CH& ch = *reinterpret_cast<CH*>(smem + align16((size_t)SG * WPG * 4) + align16((size_t)SG * 4));
+  CH& ch = *reinterpret_cast<CH*>(smem + bm_bytes + align16((size_t)SG * 4));
   Group<WIN_BLOCK, WIN_BLOCK> g;
   g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
   const int t = threadIdx.x;
-  for (int i = t; i < SG * WPG; i += WIN_BLOCK) bm[i] = 0u;
+  auto pidx = [&](int w) { return w + (w >> lw); };
+  for (int i = t; i < window_words_padded(nwmax); i += WIN_BLOCK) bm[i] = 0u;
   for (int i = t; i < SG; i += WIN_BLOCK) gc[i] = 0;
   __syncthreads();
 
@@ -622,26 +644,46 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
     const GrainRange seg{op.bidx + (int64_t)g0 * op.K, op.bidx + (int64_t)g1 * op.K};
     for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg, [&](int j, float) {
       j -= c0;
-      atomicOr(&bm[j >> 5], 1u << (j & 31));
+      atomicOr(&bm[pidx(j >> 5)], 1u << (j & 31));
     });
-    // per-grain popcounts (a wavefront's 64 words lie in one grain when
-    // grains are a multiple of 64 words; otherwise each lane adds its own)
+    // per-grain popcounts over each thread's run of words
     const int nw = (g1 - g0) * WPG;
-    const bool wave_grains = (WPG % WAVE) == 0;
-    for (int w0 = 0; w0 < nw; w0 += WIN_BLOCK) {
-      const int w = w0 + t;
-      int c = 0;
-      if (w < nw) {
-        c = __popc(bm[w]);
-        bm[w] = 0u;
+    const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
+    int c = 0, gcur = -1, gacc = 0;
+    for (int w = w0; w < w1; ++w) {
+      const int pc = __popc(bm[pidx(w)]);
+      c += pc;
+      const int gw = w / WPG;
+      if (gw != gcur) {
+        if (gacc) atomicAdd(&gc[gcur], gacc);
+        gcur = gw;
+        gacc = 0;
       }
-      if (wave_grains) {
-        c = wave_sum(c);
-        if (lane_id() == 0 && w < nw && c) atomicAdd(&gc[w / WPG], c);
-      } else if (w < nw && c) {
-        atomicAdd(&gc[w / WPG], c);
-      }
+      gacc += pc;
     }
+    if (gacc) atomicAdd(&gc[gcur], gacc);
+    if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
+      // heavy row: keep the item's bitmap for the numeric phase, in a slot
+      // taken from the workgroup's chunk of the shared cache
+      if (t == 0) {
+        if (chunk_cur + nw > chunk_end) {
+          const int64_t take = max<int64_t>(CACHE_CHUNK, nw);
+          chunk_cur = (int64_t)atomicAdd(wp.bm_top, (unsigned long long)take);
+          chunk_end = chunk_cur + take;
+        }
+        const int64_t off = chunk_cur + nw <= wp.bm_cap ? chunk_cur : -1;
+        chunk_cur += nw;
+        s_off = off;
+        wp.bm_off[row * ngg + gg] = off;
+      }
+      __syncthreads();
+      const int64_t off = s_off;
+      if (off >= 0)
+        for (int w = w0; w < w1; ++w) wp.bm_cache[off + w] = bm[pidx(w)];
+    } else if (wp.bm_cache && t == 0) {
+      wp.bm_off[row * ngg + gg] = -1;
+    }
+    for (int w = w0; w < w1; ++w) bm[pidx(w)] = 0u;
     __syncthreads();
     for (int k = t; k < g1 - g0; k += WIN_BLOCK) {
       wp.gcnt[row * op.nG + g0 + k] = gc[k];
@@ -652,16 +694,17 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
 }
 
 // Greedy windows of whole grains (at most max_grains grains and max_entries
-// entries); empty windows are skipped.  Calls f(g0, g1, n, roff).
+// entries, never across a symbolic item boundary, a multiple of sg grains);
+// empty windows are skipped.  Calls f(g0, g1, n, roff).
 template <typename F>
 __device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, int max_grains, int max_entries,
-                                                F&& f) {
+                                                int sg, F&& f) {
   int64_t roff = 0;
   int g0 = 0;
   while (g0 < nG) {
     int n = gc[g0];
     int g1 = g0 + 1;
-    while (g1 < nG && g1 - g0 < max_grains && n + gc[g1] <= max_entries) n += gc[g1++];
+    while (g1 < nG && g1 - g0 < max_grains && g1 % sg != 0 && n + gc[g1] <= max_entries) n += gc[g1++];
     if (n > 0) f(g0, g1, n, roff);
     roff += n;
     g0 = g1;
@@ -676,7 +719,7 @@ __global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, 
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t nwin = 0;
-    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries,
+    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries, wp.grains_per_count_item,
                                [&](int, int, int, int64_t) { ++nwin; });
     wp.item_count[1 + d] = nwin;
   }
@@ -688,7 +731,7 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t o = wp.item_count[d];  // scanned: windows of the rows before d
-    plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries,
+    plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries, wp.grains_per_count_item,
                  [&](int g0, int g1, int n, int64_t roff) {
                    WinItem w;
                    w.row = (int32_t)row;
@@ -702,17 +745,8 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
 }
 
 // A window's LDS: its presence bitmap and the rank of each word's first set
-// bit, both with one pad word after every `wpt` words (wpt = words a thread
-// owns in the rank scan) so the per-thread runs fall in distinct banks; the
-// window's fp32 values (reused to stage its column ids); the chunk.
-__host__ __device__ constexpr int window_wpt_log2(int maxw) {
-  int l = 0;
-  while ((1 << l) * WIN_BLOCK < maxw) ++l;
-  return l;
-}
-__host__ __device__ constexpr int window_words_padded(int maxw) {
-  return maxw + (maxw >> window_wpt_log2(maxw)) + 1;
-}
+// bit (padded as in the symbolic items); the window's fp32 values (reused
+// to stage its column ids); the chunk.
 
 template <typename S>
 __host__ __device__ constexpr size_t window_lds_bytes(int max_grains, int max_entries, int G) {
@@ -794,6 +828,17 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
       const int nw = (g1 - g0) * WPG;
       const int64_t base = rbase + I.roff;
       auto set_bit = [&](int j) { atomicOr(&bm[pidx(j >> 5)], 1u << (j & 31)); };
+      // Heavy rows: the symbolic phase kept the window's bitmap.
+      int64_t cached = -1;
+      if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
+        const int SG = wp.grains_per_count_item;
+        const int64_t o = wp.bm_off[row * ((op.nG + SG - 1) / SG) + g0 / SG];
+        if (o >= 0) cached = o + (int64_t)(g0 % SG) * WPG;  // windows never leave their item
+      }
+      auto load_bits = [&]() {
+        for (int w = t; w < nw; w += WIN_BLOCK) bm[pidx(w)] = wp.bm_cache[cached + w];
+        __syncthreads();
+      };
       auto add_at_rank = [&](int j, float v) {
         const int pw = pidx(j >> 5);
         const int rk = (int)pre[pw] + __popc(bm[pw] & ((1u << (j & 31)) - 1u));
@@ -866,8 +911,13 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
           for (int i = 0; i < SEG_PER_THREAD; ++i)
             if (jj[i] >= 0) add_at_rank(jj[i], vv[i]);
         } else {
-          // two passes over runs of the window's terms; the row's state stays
-          for (int pass = 0; pass < 2; ++pass) {
+          // two passes over runs of the window's terms (one with a kept
+          // bitmap); the row's state stays
+          if (cached >= 0) {
+            load_bits();
+            word_ranks();
+          }
+          for (int pass = cached >= 0 ? 1 : 0; pass < 2; ++pass) {
             for (int64_t r0 = 0; r0 < total; r0 += RUN) {
               const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
               seg_map(r0, rn);
@@ -913,8 +963,11 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
       } else {
         // long row: pass 1 presence bitmap, pass 2 add at the ranks
         const GrainRange seg{op.bidx + (int64_t)g0 * op.K, op.bidx + (int64_t)g1 * op.K};
-        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg,
-                                                       [&](int j, float) { set_bit(j - c0); });
+        if (cached >= 0)
+          load_bits();
+        else
+          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg,
+                                                         [&](int j, float) { set_bit(j - c0); });
         word_ranks();
         for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true>(op, g, ch, row, seg,
                                                       [&](int j, float v) { add_at_rank(j - c0, v); });

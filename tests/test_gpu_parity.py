@@ -134,6 +134,15 @@ def test_cfg3_scaled_wide(torch_gpu):
     assert st["kind_ms"]["numeric"]["windows"] > 0
 
 
+@pytest.mark.parametrize("keep", [1, -1])
+def test_cfg3_scaled_kept_bitmaps(torch_gpu, keep):
+    """Symbolic bitmaps kept for every wide row (keep=1) or for none (-1);
+    small windows so that windows of more than one run of terms occur."""
+    A, B = workloads.workload(3, n=40000)
+    check(torch_gpu, A, B, "cfg3 n=40000 keep_bitmap_products=%d" % keep, keep_bitmap_products=keep,
+          window_grain_cols=4096, window_max_grains=8, window_max_entries=16384, count_grains=4)
+
+
 def test_cfg3_scaled_small_windows(torch_gpu):
     """Many windows per row: 1024-column grains, windows of <= 4 grains and
     <= 1024 entries, 8 grains per symbolic item (64-word grains: wave sums)."""
@@ -266,6 +275,8 @@ def test_edge_hub_row(torch_gpu):
     check(torch_gpu, A, B, "hub row narrow")
     B2 = workloads.random_csr(rng, 5000, 40000, 0.0005)
     check(torch_gpu, A, B2, "hub row wide")
+    check(torch_gpu, A, B2, "hub row wide, kept bitmaps", keep_bitmap_products=1)
+    check(torch_gpu, A, B2, "hub row wide, no kept bitmaps", keep_bitmap_products=-1)
 
 
 def test_edge_stored_zeros_kept(torch_gpu):
