@@ -16,7 +16,8 @@
 //                 presence bitmap; compaction walks the bitmap, so the
 //                 output comes out sorted with no sort at all.
 //   hash          open addressing (linear probing) keyed by column; the
-//                 occupied slots are compacted and bitonic-sorted in LDS.
+//                 occupied slots are compacted and sorted (runs of 16 in
+//                 registers, then merge-path rounds in LDS).
 // A product's intermediate terms are spread over the threads of a group by
 // a flattened loop: the group loads up to GROUP entries (k, a_ik) of A_i,
 // scans the lengths of the matching B rows, and each thread takes every
@@ -470,6 +471,28 @@ struct HashLds {
   int64_t red[GROUP / WAVE + 1];
 };
 
+// Bitonic network over SORT_RUN (key, value) pairs held in registers.
+constexpr int SORT_RUN = 16;
+__device__ __forceinline__ void sort_run(int32_t (&k)[SORT_RUN], float (&v)[SORT_RUN]) {
+#pragma unroll
+  for (int size = 2; size <= SORT_RUN; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+#pragma unroll
+      for (int i = 0; i < SORT_RUN; ++i) {
+        const int l = i ^ stride;
+        if (l > i) {
+          const bool up = (i & size) == 0;
+          if ((k[i] > k[l]) == up) {
+            const int32_t tk = k[i]; k[i] = k[l]; k[l] = tk;
+            const float tv = v[i]; v[i] = v[l]; v[l] = tv;
+          }
+        }
+      }
+    }
+  }
+}
+
 template <int TABLE>
 __device__ __forceinline__ uint32_t hslot(int j) {
   constexpr int LOG2 = __builtin_ctz(TABLE);
@@ -478,7 +501,8 @@ __device__ __forceinline__ uint32_t hslot(int j) {
 
 // Light rows of wide products: open addressing keyed by column (linear
 // probing, load <= 1/2 since nnz(C_i) <= P_i <= TABLE/2), then the occupied
-// slots are compacted and bitonic-sorted in LDS.
+// slots are compacted and sorted: runs of 16 in registers, then merge-path
+// rounds between the two halves of the table.
 template <typename RA, typename RB, int TABLE, int GROUP, int BLOCK, bool NUM>
 __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView bv,
                                                 const Outputs out) {
@@ -538,31 +562,64 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 #pragma unroll
       for (int s = 0; s < SPT; ++s)
         if (kk[s] != -1) { L.key[o] = kk[s]; L.val[o] = vv[s]; ++o; }
-      int n2 = 1;
-      while (n2 < n) n2 <<= 1;
-      for (int i = (int)n + t; i < n2; i += GROUP) L.key[i] = 0x7fffffff;
       g.sync();
-      // bitonic sort of (key, val) pairs in [0, n2)
-      for (int k = 2; k <= n2; k <<= 1) {
-        for (int jj = k >> 1; jj > 0; jj >>= 1) {
-          for (int pi = t; pi < (n2 >> 1); pi += GROUP) {
-            const int i = ((pi & ~(jj - 1)) << 1) | (pi & (jj - 1));
-            const int l = i | jj;
-            const bool asc = (i & k) == 0;
-            const int ki = L.key[i], kl = L.key[l];
-            if ((ki > kl) == asc) {
-              const float vi = L.val[i], vl = L.val[l];
-              L.key[i] = kl; L.key[l] = ki;
-              L.val[i] = vl; L.val[l] = vi;
-            }
-          }
-          g.sync();
+      // sort the n compacted pairs by column: runs of SORT_RUN pairs sorted
+      // in registers, then merge-path rounds between the two halves of the
+      // table (n <= TABLE / 2)
+      const int npad = (int)((n + SORT_RUN - 1) / SORT_RUN) * SORT_RUN;
+      int32_t* ksrc = L.key;
+      float* vsrc = L.val;
+      int32_t* kdst = L.key + TABLE / 2;
+      float* vdst = L.val + TABLE / 2;
+      for (int p0 = t * SORT_RUN; p0 < npad; p0 += GROUP * SORT_RUN) {
+        int32_t rk[SORT_RUN];
+        float rv[SORT_RUN];
+#pragma unroll
+        for (int i = 0; i < SORT_RUN; ++i) {
+          const bool live = p0 + i < n;
+          rk[i] = live ? ksrc[p0 + i] : 0x7fffffff;
+          rv[i] = live ? vsrc[p0 + i] : 0.f;
         }
+        sort_run(rk, rv);
+#pragma unroll
+        for (int i = 0; i < SORT_RUN; ++i) {
+          ksrc[p0 + i] = rk[i];
+          vsrc[p0 + i] = rv[i];
+        }
+      }
+      g.sync();
+      for (int R = SORT_RUN; R < npad; R <<= 1) {
+        for (int p0 = t * SORT_RUN; p0 < npad; p0 += GROUP * SORT_RUN) {
+          const int lo = p0 / (2 * R) * (2 * R);
+          const int a0 = lo, la = min(R, npad - lo);
+          const int b0 = lo + la, lb = min(R, npad - b0);
+          const int d = p0 - lo;
+          // i = number of run-A pairs among the first d merged pairs
+          int i = max(0, d - lb), ihi = min(d, la);
+          while (i < ihi) {
+            const int mid = (i + ihi) >> 1;
+            if (ksrc[a0 + mid] <= ksrc[b0 + d - 1 - mid]) i = mid + 1; else ihi = mid;
+          }
+          int j = d - i;
+#pragma unroll 4
+          for (int q = 0; q < SORT_RUN; ++q) {
+            const int32_t ka = i < la ? ksrc[a0 + i] : 0x7fffffff;
+            const int32_t kb = j < lb ? ksrc[b0 + j] : 0x7fffffff;
+            const bool take_a = j >= lb || (i < la && ka <= kb);
+            kdst[p0 + q] = take_a ? ka : kb;
+            vdst[p0 + q] = take_a ? vsrc[a0 + i] : vsrc[b0 + j];
+            i += take_a;
+            j += !take_a;
+          }
+        }
+        g.sync();
+        int32_t* tk = ksrc; ksrc = kdst; kdst = tk;
+        float* tv = vsrc; vsrc = vdst; vdst = tv;
       }
       const int64_t o0 = out.crp[row];
       for (int i = t; i < n; i += GROUP) {
-        out.ccol[o0 + i] = L.key[i];
-        out.cval[o0 + i] = L.val[i];
+        out.ccol[o0 + i] = ksrc[i];
+        out.cval[o0 + i] = vsrc[i];
       }
       g.sync();
       for (int i = t; i < TABLE; i += GROUP) {
