@@ -101,6 +101,13 @@ struct Group {
   }
 };
 
+// C is written once and not read back by the kernels: stream it past the
+// caches so that B's rows stay resident there.
+template <typename T>
+__device__ __forceinline__ void store_stream(T* p, T v) {
+  __builtin_nontemporal_store(v, p);
+}
+
 template <typename RP>
 __device__ __forceinline__ int64_t ld_rp(const void* rp, int64_t i) {
   return (int64_t)static_cast<const RP*>(rp)[i];
@@ -110,21 +117,23 @@ __device__ __forceinline__ int64_t ld_rp(const void* rp, int64_t i) {
 
 constexpr int64_t kLongRow = 2048;  // longer A rows are summed by a whole workgroup
 
-// P_i for every tile row, 16 lanes per row; rows longer than kLongRow are
-// appended to long_list for k_analyze_long.
+// P_i for every tile row, 16 lanes per row, rows taken grid-stride; rows
+// longer than kLongRow are appended to long_list for k_analyze_long.  The
+// total is added once per workgroup.
 template <typename RA, typename RB>
 __global__ __launch_bounds__(256) void k_analyze(const Operands op, int64_t nrows, int64_t* P,
                                                  unsigned long long* total, int32_t* long_cnt,
                                                  int32_t* long_list) {
+  __shared__ int64_t red[256 / WAVE];
   const int sub = threadIdx.x & 15;
-  const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
-  int64_t s = 0;
-  bool is_long = false;
-  if (row < nrows) {
+  const int64_t nsub = (int64_t)gridDim.x * (blockDim.x / 16);
+  int64_t mine = 0;
+  for (int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4; row < nrows; row += nsub) {
+    int64_t s = 0;
     const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
     const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
-    if (p1 - p0 > kLongRow) {
-      is_long = true;
+    const bool is_long = p1 - p0 > kLongRow;  // uniform over the 16 lanes of the row
+    if (is_long) {
       if (sub == 0) long_list[atomicAdd(long_cnt, 1)] = (int32_t)row;
     } else {
       for (int64_t p = p0 + sub; p < p1; p += 64) {
@@ -136,13 +145,21 @@ __global__ __launch_bounds__(256) void k_analyze(const Operands op, int64_t nrow
           if (k[u] >= 0) s += ld_rp<RB>(op.brp, k[u] + 1) - ld_rp<RB>(op.brp, k[u]);
       }
     }
-  }
 #pragma unroll
-  for (int d = 8; d > 0; d >>= 1) s += __shfl_xor(s, d, 16);
-  if (row < nrows && sub == 0 && !is_long) P[row] = s;
-  int64_t w = (sub == 0) ? s : 0;
-  w = wave_sum(w);
-  if (lane_id() == 0 && w) atomicAdd(total, (unsigned long long)w);
+    for (int d = 8; d > 0; d >>= 1) s += __shfl_xor(s, d, 16);
+    if (sub == 0 && !is_long) {
+      P[row] = s;
+      mine += s;
+    }
+  }
+  mine = wave_sum(mine);
+  if (lane_id() == 0) red[threadIdx.x / WAVE] = mine;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t t = 0;
+    for (int i = 0; i < 256 / WAVE; ++i) t += red[i];
+    if (t) atomicAdd(total, (unsigned long long)t);
+  }
 }
 
 template <typename RA, typename RB>
@@ -186,13 +203,22 @@ __device__ __forceinline__ int bin_of(const BinThresholds& th, int64_t p) {
   return b;
 }
 
+// Bins are counted and filled per workgroup over a contiguous range of
+// rows, with one global atomic per bin and workgroup.
+__device__ __forceinline__ void block_rows(int64_t nrows, int64_t& r0, int64_t& r1) {
+  const int64_t per = (nrows + gridDim.x - 1) / gridDim.x;
+  r0 = min(nrows, (int64_t)blockIdx.x * per);
+  r1 = min(nrows, r0 + per);
+}
+
 __global__ __launch_bounds__(256) void k_bin_count(const int64_t* P, int64_t nrows,
                                                    const BinThresholds th, int32_t* cnt) {
   __shared__ int32_t h[MAX_BINS];
   if (threadIdx.x < MAX_BINS) h[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < nrows) atomicAdd(&h[bin_of(th, P[i])], 1);
+  int64_t r0, r1;
+  block_rows(nrows, r0, r1);
+  for (int64_t i = r0 + threadIdx.x; i < r1; i += blockDim.x) atomicAdd(&h[bin_of(th, P[i])], 1);
   __syncthreads();
   if (threadIdx.x < th.nb && h[threadIdx.x]) atomicAdd(&cnt[threadIdx.x], h[threadIdx.x]);
 }
@@ -211,16 +237,19 @@ __global__ __launch_bounds__(256) void k_bin_scatter(const int64_t* P, int64_t n
   }
   if (threadIdx.x < MAX_BINS) h[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int b = 0, r = 0;
-  if (i < nrows) {
-    b = bin_of(th, P[i]);
-    r = atomicAdd(&h[b], 1);
+  int64_t r0, r1;
+  block_rows(nrows, r0, r1);
+  for (int64_t i = r0 + threadIdx.x; i < r1; i += blockDim.x) atomicAdd(&h[bin_of(th, P[i])], 1);
+  __syncthreads();
+  if (threadIdx.x < th.nb) {
+    base[threadIdx.x] = h[threadIdx.x] ? atomicAdd(&cursor[threadIdx.x], h[threadIdx.x]) : 0;
+    h[threadIdx.x] = 0;
   }
   __syncthreads();
-  if (threadIdx.x < th.nb && h[threadIdx.x]) base[threadIdx.x] = atomicAdd(&cursor[threadIdx.x], h[threadIdx.x]);
-  __syncthreads();
-  if (i < nrows) list[off[b] + base[b] + r] = (int32_t)i;
+  for (int64_t i = r0 + threadIdx.x; i < r1; i += blockDim.x) {
+    const int b = bin_of(th, P[i]);
+    list[off[b] + base[b] + atomicAdd(&h[b], 1)] = (int32_t)i;
+  }
 }
 
 // ---------------------------------------------------- flattened product loop
@@ -448,8 +477,8 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
           before = g.incl_scan(present ? 1 : 0, &tot) - (present ? 1 : 0);
         }
         if (present) {
-          out.ccol[o0 + before] = j;
-          out.cval[o0 + before] = acc[j];
+          store_stream(&out.ccol[o0 + before], j);
+          store_stream(&out.cval[o0 + before], acc[j]);
           acc[j] = 0.f;
         }
         o0 += tot;
@@ -618,8 +647,8 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
       }
       const int64_t o0 = out.crp[row];
       for (int i = t; i < n; i += GROUP) {
-        out.ccol[o0 + i] = ksrc[i];
-        out.cval[o0 + i] = vsrc[i];
+        store_stream(&out.ccol[o0 + i], ksrc[i]);
+        store_stream(&out.cval[o0 + i], vsrc[i]);
       }
       g.sync();
       for (int i = t; i < TABLE; i += GROUP) {
@@ -1032,7 +1061,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
       __syncthreads();
       // values out (coalesced), then the column ids staged in the same LDS
       // array in rank order and written out coalesced as well
-      for (int kk = t; kk < n; kk += WIN_BLOCK) out.cval[base + kk] = vals[kk];
+      for (int kk = t; kk < n; kk += WIN_BLOCK) store_stream(&out.cval[base + kk], vals[kk]);
       __syncthreads();
       {
         const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
@@ -1051,7 +1080,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
       }
       __syncthreads();
       for (int kk = t; kk < n; kk += WIN_BLOCK) {
-        out.ccol[base + kk] = stage[kk];
+        store_stream(&out.ccol[base + kk], stage[kk]);
         vals[kk] = 0.f;
       }
     }
@@ -1278,7 +1307,8 @@ hipError_t win_numeric_t(const Operands& op, const BinView& bv, const WindowPara
 template <typename RA, typename RB>
 static hipError_t analyze_t(const Operands& op, int64_t nrows, int64_t* P, unsigned long long* total,
                             int32_t* long_cnt, int32_t* long_list, hipStream_t s) {
-  const int64_t grid = (nrows * 16 + 255) / 256;
+  int64_t grid = (nrows * 16 + 255) / 256;
+  if (grid > 8192) grid = 8192;
   hipLaunchKernelGGL((k_analyze<RA, RB>), dim3((unsigned)grid), dim3(256), 0, s, op, nrows, P, total, long_cnt,
                      long_list);
   int64_t lg = nrows / 64 + 1;
@@ -1296,7 +1326,8 @@ hipError_t analyze(const Operands& op, int64_t nrows, int64_t* P, unsigned long 
 
 hipError_t bin_rows(const int64_t* P, int64_t nrows, const BinThresholds& th, int32_t* cnt_cursor,
                     int32_t* binoff, int32_t* list, hipStream_t s) {
-  const int64_t grid = nrows > 0 ? (nrows + 255) / 256 : 1;
+  int64_t grid = nrows > 0 ? (nrows + 255) / 256 : 1;
+  if (grid > 2048) grid = 2048;
   hipLaunchKernelGGL(k_bin_count, dim3((unsigned)grid), dim3(256), 0, s, P, nrows, th, cnt_cursor);
   hipLaunchKernelGGL(k_bin_scatter, dim3((unsigned)grid), dim3(256), 0, s, P, nrows, th, cnt_cursor,
                      cnt_cursor + MAX_BINS, binoff, list);
