@@ -39,7 +39,7 @@ WORKLOAD_NAMES = {
     4: "large GCN aggregation: symmetric R-MAT n=8388608 deg 24 + self-loops; X 8388608x128 10% U(-1,1)",
 }
 
-KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows"]
+KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split"]
 
 
 def row_kinds(P: np.ndarray, N: int) -> np.ndarray:
@@ -47,7 +47,8 @@ def row_kinds(P: np.ndarray, N: int) -> np.ndarray:
     k = np.zeros(len(P), dtype=np.int8)
     if N <= 2048:
         k[(P > 0) & (P <= 8192)] = 1
-        k[P > 8192] = 2
+        k[(P > 8192) & (P <= 65536)] = 2
+        k[P > 65536] = 7
     else:
         k[(P > 0) & (P <= 64)] = 3
         k[(P > 64) & (P <= 512)] = 4

@@ -152,6 +152,12 @@ typedef struct aires_plan_opts {
                                    of rows with more products than this for
                                    the numeric phase (in-core runs, within a
                                    fifth of the budget the plan leaves)    */
+    int64_t split_min_products; /* 0: default (65536), < 0: never.  Rows of
+                                   a narrow product (N <= 2048) with more
+                                   products are split over workgroups      */
+    int64_t split_max_rows;     /* 0: default.  Cap on the rows given dense
+                                   slots for splitting; further rows of the
+                                   split bin take one workgroup each       */
 } aires_plan_opts;
 
 /* Fill *o with defaults (struct_size set, validate 0, C on device). */
@@ -267,7 +273,8 @@ typedef struct aires_stats {
     int64_t numeric_launches;   /* numeric-phase kernel launches           */
     /* milliseconds per kernel kind (index = kind id of the row bins:
        0 empty, 1 dense-wave, 2 dense-block, 3 hash-128, 4 hash-1024,
-       5 hash-8192, 6 column windows); [0] symbolic, [1] numeric phase     */
+       5 hash-8192, 6 column windows, 7 split rows); [0] symbolic, [1]
+       numeric phase                                                        */
     double kind_ms[2][8];
     /* streamed calls: from the first copy of Phase I to the last copy of
        Phase III (the tile pipeline, without the output allocation)       */

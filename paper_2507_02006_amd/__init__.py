@@ -64,7 +64,7 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
               max_tile_bytes: int = 0, m_a_bytes: int = 0, dense_max_cols: int = 0,
               hash_max_products: int = 0, wave_max_products: int = 0, window_grain_cols: int = 0,
               window_max_grains: int = 0, window_max_entries: int = 0, count_grains: int = 0,
-              keep_bitmap_products: int = 0,
+              keep_bitmap_products: int = 0, split_min_products: int = 0, split_max_rows: int = 0,
               torch_allocator: bool = True, device: int = 0) -> Plan:
     lib = B_.load()
     a = B_.make_csr(*_parts(A))
@@ -86,6 +86,8 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
     o.window_max_entries = window_max_entries
     o.count_grains = count_grains
     o.keep_bitmap_products = keep_bitmap_products
+    o.split_min_products = split_min_products
+    o.split_max_rows = split_max_rows
     alloc = None
     if torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
         alloc = B_.TorchAllocator(device)

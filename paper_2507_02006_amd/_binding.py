@@ -27,7 +27,7 @@ OK, E_INVALID_ARG, E_INVALID_CSR, E_DIM, E_BUDGET, E_OVERFLOW, E_OOM, E_HIP, E_S
 IDX_I32, IDX_I64 = 0, 1
 MEM_DEVICE, MEM_HOST_PINNED, MEM_HOST = 0, 1, 2
 CBOUND_PRODUCTS, CBOUND_DENSE, CBOUND_PAPER_EQ5 = 0, 1, 2
-KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows"]
+KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split"]
 
 
 class Csr(ctypes.Structure):
@@ -54,7 +54,8 @@ class PlanOpts(ctypes.Structure):
                 ("m_a_bytes", c_i64), ("allocator", ctypes.POINTER(Allocator)), ("dense_max_cols", c_i64),
                 ("hash_max_products", c_i64), ("wave_max_products", c_i64), ("window_grain_cols", c_i64),
                 ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64),
-                ("keep_bitmap_products", c_i64)]
+                ("keep_bitmap_products", c_i64), ("split_min_products", c_i64),
+                ("split_max_rows", c_i64)]
 
 
 class PlanInfo(ctypes.Structure):

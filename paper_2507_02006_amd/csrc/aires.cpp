@@ -55,6 +55,8 @@ constexpr int64_t kCountGrains = 32;         // grains one symbolic item covers
 constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps kept for heavy rows
 constexpr int64_t kKeepBitmapProducts = 65536;           // rows above this many products keep them
 constexpr int64_t kWaveMaxProducts = 8192;   // rows up to this go to one wavefront
+constexpr int64_t kSplitMinProducts = 65536; // narrow rows above this are split over workgroups
+constexpr int64_t kSplitWsBytes = int64_t(256) << 20;  // their dense slots
 constexpr int64_t kHashMaxProducts = 4096;   // = 8192-slot table at load <= 1/2
 constexpr int64_t kFixedWorkspace = 4 << 20; // scan partials, counters, slack
 
@@ -144,6 +146,9 @@ struct aires_plan {
   int32_t win_grains = 0, win_entries = 0, count_grains = 0;
   int32_t ngg = 0;                 // symbolic items per wide row (runs of count_grains grains)
   int64_t keep_bitmap = 0;         // rows with more products keep their symbolic bitmaps (-1: none)
+  int split = 0;                   // narrow product with a split-row bin
+  int64_t split_cap = 0;           // rows with dense slots for the split bin
+  int64_t split_ws = 0;            // bytes of those slots
   // host copies needed for streaming
   std::vector<int64_t> P_host;  // per-row products when computed on the host
   // timing events of the last call
@@ -162,6 +167,9 @@ void bin_plan(aires_plan* p) {
   const aires_plan_opts& o = p->opts;
   const int64_t dense_max = o.dense_max_cols > 0 ? std::min<int64_t>(o.dense_max_cols, kDenseMaxCols) : kDenseMaxCols;
   const int64_t wave_max = o.wave_max_products > 0 ? o.wave_max_products : kWaveMaxProducts;
+  const int64_t split_min = o.split_min_products > 0   ? o.split_min_products
+                            : o.split_min_products < 0 ? 0  // < 0: no split rows
+                                                       : kSplitMinProducts;
   const int64_t hash_max = o.hash_max_products > 0   ? std::min<int64_t>(o.hash_max_products, kHashMaxProducts)
                            : o.hash_max_products < 0 ? 0  // < 0: no hash bins
                                                      : kHashMaxProducts;
@@ -171,10 +179,17 @@ void bin_plan(aires_plan* p) {
   auto add = [&](int kind, int64_t maxp) { th.kind[nb] = kind; th.max_p[nb] = maxp; ++nb; };
   add(kern::KIND_EMPTY, 0);
   p->wide = 0;
+  p->split = 0;
   if (N <= std::min(kDenseWaveMaxN, dense_max)) {
     // narrow product: every row fits a dense LDS row
     add(kern::KIND_DENSE_WAVE, wave_max);
-    add(kern::KIND_DENSE_BLOCK, INT64_MAX);
+    if (split_min > 0) {
+      add(kern::KIND_DENSE_BLOCK, std::max(wave_max, split_min));
+      add(kern::KIND_DENSE_SPLIT, INT64_MAX);
+      p->split = 1;
+    } else {
+      add(kern::KIND_DENSE_BLOCK, INT64_MAX);
+    }
   } else {
     // light rows hash in LDS (load factor <= 1/2: nnz(C_i) <= P_i <= slots/2)
     if (hash_max > 0) add(kern::KIND_HASH_128, std::min<int64_t>(hash_max, 64));
@@ -430,6 +445,23 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     }
     if (!c_on_host) resident += 8 * p->info.c_bound_entries + 8 * (m + 1);
   }
+  if (p->split) {
+    // dense slots of the split rows, shared by all tiles (their kernels run
+    // on one stream): as many as rows above the split threshold when P_i is
+    // known on the host, else as many as fit kSplitWsBytes
+    const int64_t per = 4 * ((N + 31) / 32 + N);
+    int64_t rows = std::min<int64_t>(m, std::max<int64_t>(1, kSplitWsBytes / per));
+    if (!p->P_host.empty()) {
+      const int64_t lim = p->th.max_p[p->th.nb - 2];  // upper end of the bin before the split bin
+      rows = 0;
+      for (int64_t v : p->P_host) rows += v > lim;
+      rows = std::min(rows, std::max<int64_t>(1, kSplitWsBytes / per));
+    }
+    if (o.split_max_rows > 0) rows = std::min(rows, o.split_max_rows);
+    p->split_cap = rows;
+    p->split_ws = rows * per;
+    resident += p->split_ws;
+  }
 
   const int nslots = a_streamed ? 2 : 1;
   int64_t tile_budget;
@@ -608,6 +640,7 @@ struct TileWs {
   int64_t nitems = 0;            // host copy of icount[n]
   int32_t* wcounter = nullptr;   // row counter of the window kernel
   void* scan_ws = nullptr;
+  kern::SplitWs split{nullptr, nullptr, 0};  // dense slots of split rows (shared by all tiles)
   int64_t* bm_off = nullptr;     // [n * ngg] kept bitmaps of the symbolic items (wide, in-core)
   uint32_t* bm_cache = nullptr;  // shared bitmap cache (nullptr: none)
   int64_t bm_cap = 0;
@@ -627,6 +660,16 @@ aires_status alloc_tile_ws(aires_plan* p, DevPool& ws, int64_t n, bool with_list
   ST_TRY(ws.get_n(2 * kern::MAX_BINS + 1, &w.cntcur));
   ST_TRY(ws.get_n(1, &w.wcounter));
   ST_TRY(ws.get(kern::scan_workspace_bytes(n), &w.scan_ws));
+  return AIRES_OK;
+}
+
+aires_status alloc_split_ws(aires_plan* p, DevPool& ws, kern::SplitWs& sw) {
+  sw = kern::SplitWs{nullptr, nullptr, 0};
+  if (!p->split) return AIRES_OK;
+  const int64_t N = p->B.ncols;
+  ST_TRY(ws.get_n(p->split_cap * ((N + 31) / 32), &sw.bm));
+  ST_TRY(ws.get_n(p->split_cap * N, &sw.acc));
+  sw.cap = p->split_cap;
   return AIRES_OK;
 }
 
@@ -673,6 +716,8 @@ aires_status tile_symbolic(aires_plan* p, const kern::Operands& op, int64_t n, T
       while (bv.last() + 1 < p->th.nb && p->th.kind[bv.last() + 1] == kern::KIND_WINDOWS) bv.bin_last = bv.last() + 1;
       HIP_TRY(kern::windows_symbolic(op, bv, window_params(p, w), out, n, s));
       b = bv.last();
+    } else if (kind == kern::KIND_DENSE_SPLIT) {
+      HIP_TRY(kern::split_rows(0, op, bv, w.split, out, n, s));
     } else {
       HIP_TRY(kern::run_bin(kind, 0, op, bv, out, n, s));
     }
@@ -705,6 +750,8 @@ aires_status tile_numeric(aires_plan* p, const kern::Operands& op, int64_t n, co
       while (bv.last() + 1 < p->th.nb && p->th.kind[bv.last() + 1] == kern::KIND_WINDOWS) bv.bin_last = bv.last() + 1;
       HIP_TRY(kern::windows_numeric(op, bv, window_params(p, w), out, n, w.nitems, s));
       b = bv.last();
+    } else if (kind == kern::KIND_DENSE_SPLIT) {
+      HIP_TRY(kern::split_rows(1, op, bv, w.split, out, n, s));
     } else {
       HIP_TRY(kern::run_bin(kind, 1, op, bv, out, n, s));
     }
@@ -743,6 +790,7 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   ST_TRY(ws.get_n(m + 1, &crp));
   TileWs shared;
   ST_TRY(alloc_tile_ws(p, ws, max_rows, false, shared));
+  ST_TRY(alloc_split_ws(p, ws, shared.split));
   int32_t *list = nullptr, *binoff = nullptr, *gcnt = nullptr, *bidx = nullptr;
   int64_t* icount = nullptr;
   unsigned long long* prod = nullptr;
@@ -953,6 +1001,8 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   ST_TRY(ws.get_n(1, &prod));
   ST_TRY(ws.get_n(1, &running));
   if (p->wide) ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
+  kern::SplitWs split{nullptr, nullptr, 0};
+  ST_TRY(alloc_split_ws(p, ws, split));
   for (int s = 0; s < 2; ++s) {
     Slot& S = slot[s];
     S = Slot{};
@@ -960,6 +1010,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     ST_TRY(ws.get_n(max_q, &S.acol));
     ST_TRY(ws.get_n(max_q, &S.aval));
     ST_TRY(alloc_tile_ws(p, ws, max_rows, true, S.w));
+    S.w.split = split;
     ST_TRY(ws.get_n(max_rows + 1, &S.crp));
     if (c_on_host) {
       ST_TRY(ws.get_n(max_cb, &S.ccol));

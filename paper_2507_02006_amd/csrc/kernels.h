@@ -20,8 +20,9 @@ enum Kind : int {
   KIND_HASH_1024 = 4,   // one wavefront per row, LDS hash of 1024 slots
   KIND_HASH_8192 = 5,   // one workgroup per row, LDS hash of 8192 slots
   KIND_WINDOWS = 6,     // wide rows: per-grain counts, then bitmap-rank column windows
+  KIND_DENSE_SPLIT = 7, // heavy rows of a narrow product: runs of A entries per workgroup
 };
-constexpr int NUM_KINDS = 7;
+constexpr int NUM_KINDS = 8;
 
 struct BinThresholds {
   int32_t nb;                    // number of bins
@@ -43,6 +44,7 @@ struct BinView {
   const int32_t* binoff;   // [nb+1] offsets into list (device)
   int32_t bin;             // first bin of the view
   int32_t bin_last = -1;   // last bin of the view (-1: same as bin)
+  int32_t skip = 0;        // rows at the front of the bin left to another kernel
   __host__ __device__ int32_t last() const { return bin_last < 0 ? bin : bin_last; }
 };
 
@@ -92,6 +94,16 @@ hipError_t bin_rows(const int64_t* P, int64_t nrows, const BinThresholds& th,
 // phase: 0 symbolic, 1 numeric.  ub_rows: host upper bound on the bin size.
 hipError_t run_bin(int kind, int phase, const Operands& op, const BinView& bv,
                    const Outputs& out, int64_t ub_rows, hipStream_t s);
+// Dense slots of split rows: cap rows of N presence bits and N fp32 values.
+struct SplitWs {
+  uint32_t* bm;
+  float* acc;
+  int64_t cap;
+};
+// heavy narrow rows (phase 0 symbolic, 1 numeric); rows of the bin beyond
+// sw.cap take the one-workgroup-per-row kernel
+hipError_t split_rows(int phase, const Operands& op, const BinView& bv, const SplitWs& sw, const Outputs& out,
+                      int64_t ub_rows, hipStream_t s);
 // wide rows: symbolic grain counts + window plan (counts[row], item_count[1+d])
 hipError_t windows_symbolic(const Operands& op, const BinView& bv, const WindowParams& wp,
                             const Outputs& out, int64_t ub_rows, hipStream_t s);

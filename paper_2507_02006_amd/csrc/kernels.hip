@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace aires {
 namespace kern {
 namespace {
@@ -326,20 +328,19 @@ __device__ __forceinline__ int group_excl_max_scan(int v, const Group<GROUP, BLO
   }
 }
 
-// Calls f(column, a_ik * b_kj) (NUM) or f(column, 0) for every term of a row.
+// Calls f(column, a_ik * b_kj) (NUM) or f(column, 0) for every term of A
+// entries [p0, p1) (a row or a part of one).
 // Terms are numbered q = 0..total-1 over the chunk's segments; thread t
 // takes q = t, t + GROUP, ... so consecutive lanes read consecutive entries
 // of a B row.  The segment of each term comes from a map built per run of
 // GROUP * SEG_PER_THREAD terms: each segment's owner writes its id at its
 // first term, and a group max-scan carries ids forward.
-template <typename RA, int GROUP, int BLOCK, bool NUM, typename CH, typename SEG, typename F>
-__device__ __forceinline__ void for_each_term(const Operands& op, const Group<GROUP, BLOCK>& g,
-                                              CH& ch, int64_t row, const SEG& seg, F&& f) {
+template <int GROUP, int BLOCK, bool NUM, typename CH, typename SEG, typename F>
+__device__ __forceinline__ void for_each_term_in(const Operands& op, const Group<GROUP, BLOCK>& g,
+                                                 CH& ch, int64_t p0, int64_t p1, const SEG& seg, F&& f) {
   using S = typename CH::shift_t;
   constexpr int RUN = GROUP * SEG_PER_THREAD;
   const int t = g.t();
-  const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
-  const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
   for (int64_t cb = p0; cb < p1; cb += GROUP) {
     const int64_t p = cb + t;
     int64_t lo = 0, len = 0;
@@ -408,6 +409,15 @@ __device__ __forceinline__ void for_each_term(const Operands& op, const Group<GR
   }
 }
 
+// ... over the terms of A entries [p0, p1); the whole row:
+template <typename RA, int GROUP, int BLOCK, bool NUM, typename CH, typename SEG, typename F>
+__device__ __forceinline__ void for_each_term(const Operands& op, const Group<GROUP, BLOCK>& g,
+                                              CH& ch, int64_t row, const SEG& seg, F&& f) {
+  const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
+  const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
+  for_each_term_in<GROUP, BLOCK, NUM>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
+}
+
 // -------------------------------------------------- dense path (narrow N)
 
 // LDS layout of one group: [bitmap N/32 words][acc N floats if NUM][Chunk][red]
@@ -447,7 +457,7 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.bin + 1] - bv.binoff[bv.bin];
   const FullRows<RB> seg{op.brp};
-  for (int64_t it = (int64_t)blockIdx.x * NG + gi; it < cnt; it += (int64_t)gridDim.x * NG) {
+  for (int64_t it = (int64_t)blockIdx.x * NG + gi + bv.skip; it < cnt; it += (int64_t)gridDim.x * NG) {
     const int64_t row = list[it];
     for_each_term<RA, GROUP, BLOCK, NUM>(op, g, ch, row, seg, [&](int j, float v) {
       atomicOr(&bm[j >> 5], 1u << (j & 31));
@@ -487,6 +497,112 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
       for (int i = t; i < nwd; i += GROUP) bm[i] = 0u;
     }
     g.sync();
+  }
+}
+
+// ------------------------------------------- split rows (narrow N, heavy)
+//
+// The heaviest rows of a narrow product are cut into SPLIT_PARTS runs of
+// their A entries, one workgroup per run.  A run accumulates into a dense
+// LDS row as above and adds it into the row's dense slot in global memory
+// (presence bits by atomic OR, values by atomic add); a wavefront per row
+// then counts the slot (symbolic) or writes it out in column order.
+
+constexpr int SPLIT_BLOCK = 512;
+constexpr int SPLIT_PARTS = 32;
+
+template <typename RA, typename RB, bool NUM>
+__global__ __launch_bounds__(SPLIT_BLOCK) void k_split_parts(const Operands op, const BinView bv,
+                                                            const SplitWs sw) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int N = (int)op.N;
+  const int nwd = (N + 31) / 32;
+  uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
+  float* acc = reinterpret_cast<float*>(smem + align16((size_t)nwd * 4));
+  using CH = Chunk<SPLIT_BLOCK, RB>;
+  CH& ch = *reinterpret_cast<CH*>(smem + align16((size_t)nwd * 4) + (NUM ? align16((size_t)N * 4) : 0));
+  Group<SPLIT_BLOCK, SPLIT_BLOCK> g;
+  g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
+  const int t = threadIdx.x;
+  for (int i = t; i < nwd; i += SPLIT_BLOCK) bm[i] = 0u;
+  if constexpr (NUM)
+    for (int i = t; i < N; i += SPLIT_BLOCK) acc[i] = 0.f;
+  g.sync();
+  const int32_t* list = bv.list + bv.binoff[bv.bin];
+  const int64_t cnt = min((int64_t)(bv.binoff[bv.bin + 1] - bv.binoff[bv.bin]), sw.cap);
+  const FullRows<RB> seg{op.brp};
+  for (int64_t it = blockIdx.x; it < cnt * SPLIT_PARTS; it += gridDim.x) {
+    const int64_t d = it / SPLIT_PARTS;
+    const int64_t part = it - d * SPLIT_PARTS;
+    const int64_t row = list[d];
+    const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
+    const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
+    const int64_t len = (p1 - p0 + SPLIT_PARTS - 1) / SPLIT_PARTS;
+    const int64_t q0 = min(p1, p0 + part * len), q1 = min(p1, q0 + len);
+    if (q0 < q1)
+      for_each_term_in<SPLIT_BLOCK, SPLIT_BLOCK, NUM>(op, g, ch, q0, q1, seg, [&](int j, float v) {
+        atomicOr(&bm[j >> 5], 1u << (j & 31));
+        if constexpr (NUM) atomicAdd(&acc[j], v);
+      });
+    if constexpr (NUM) {
+      for (int j = t; j < N; j += SPLIT_BLOCK)
+        if ((bm[j >> 5] >> (j & 31)) & 1u) {
+          atomicAdd(&sw.acc[d * N + j], acc[j]);
+          acc[j] = 0.f;
+        }
+      __syncthreads();
+    }
+    for (int w = t; w < nwd; w += SPLIT_BLOCK) {
+      const uint32_t x = bm[w];
+      if (x) {
+        atomicOr(&sw.bm[d * nwd + w], x);
+        bm[w] = 0u;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Clears the slots of the rows the parts kernel takes.
+__global__ __launch_bounds__(256) void k_split_clear(const BinView bv, SplitWs sw, int32_t N, int num) {
+  const int nwd = (N + 31) / 32;
+  const int64_t cnt = min((int64_t)(bv.binoff[bv.bin + 1] - bv.binoff[bv.bin]), sw.cap);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cnt * nwd; i += stride) sw.bm[i] = 0u;
+  if (num)
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cnt * N; i += stride) sw.acc[i] = 0.f;
+}
+
+// One wavefront per split row: count its slot, or write it in column order.
+template <bool NUM>
+__global__ __launch_bounds__(256) void k_split_finish(const BinView bv, const SplitWs sw, int32_t N,
+                                                     const Outputs out) {
+  const int nwd = (N + 31) / 32;
+  const int32_t* list = bv.list + bv.binoff[bv.bin];
+  const int64_t cnt = min((int64_t)(bv.binoff[bv.bin + 1] - bv.binoff[bv.bin]), sw.cap);
+  const int64_t nw = (int64_t)gridDim.x * (blockDim.x / WAVE);
+  for (int64_t d = (int64_t)blockIdx.x * (blockDim.x / WAVE) + threadIdx.x / WAVE; d < cnt; d += nw) {
+    const int64_t row = list[d];
+    const uint32_t* words = sw.bm + d * nwd;
+    if constexpr (!NUM) {
+      int64_t c = 0;
+      for (int w = lane_id(); w < nwd; w += WAVE) c += __popc(words[w]);
+      c = wave_sum(c);
+      if (lane_id() == 0) out.counts[row] = c;
+    } else {
+      int64_t o0 = out.crp[row];
+      for (int j0 = 0; j0 < N; j0 += WAVE) {
+        const int j = j0 + lane_id();
+        const bool present = j < N && ((words[j >> 5] >> (j & 31)) & 1u);
+        const uint64_t mask = __ballot(present);
+        const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+        if (present) {
+          store_stream(&out.ccol[o0 + before], j);
+          store_stream(&out.cval[o0 + before], sw.acc[d * N + j]);
+        }
+        o0 += __popcll(mask);
+      }
+    }
   }
 }
 
@@ -1251,6 +1367,42 @@ hipError_t run_bin_t(int kind, const Operands& op, const BinView& bv, const Outp
   }
 }
 
+template <typename RA, typename RB, bool NUM>
+hipError_t split_t(const Operands& op, const BinView& bv, const SplitWs& sw, const Outputs& out,
+                   int64_t ub_rows, hipStream_t s) {
+  const int64_t cap_rows = std::min<int64_t>(ub_rows, sw.cap);
+  int64_t cg = (cap_rows * (((op.N + 31) / 32) + (NUM ? op.N : 0)) + 255) / 256;
+  if (cg > 4096) cg = 4096;
+  if (cg < 1) cg = 1;
+  hipLaunchKernelGGL(k_split_clear, dim3((unsigned)cg), dim3(256), 0, s, bv, sw, (int32_t)op.N, NUM ? 1 : 0);
+  auto kern = k_split_parts<RA, RB, NUM>;
+  const size_t lds = dense_group_bytes<SPLIT_BLOCK, NUM, RB>((int)op.N);
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t grid = grid_for(kern, SPLIT_BLOCK, lds, 1, cap_rows * SPLIT_PARTS);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(SPLIT_BLOCK), lds, s, op, bv, sw);
+  int64_t fg = (cap_rows + 3) / 4;
+  if (fg > 8192) fg = 8192;
+  if (fg < 1) fg = 1;
+  hipLaunchKernelGGL((k_split_finish<NUM>), dim3((unsigned)fg), dim3(256), 0, s, bv, sw, (int32_t)op.N, out);
+  // rows of the bin beyond the slots: one workgroup each
+  if (ub_rows > sw.cap) {
+    BinView rest = bv;
+    rest.skip = (int32_t)sw.cap;
+    hipError_t e = launch_dense<RA, RB, 512, 512, NUM>(op, rest, out, ub_rows - sw.cap, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipGetLastError();
+}
+
+template <typename RA, typename RB>
+hipError_t split_rp(int phase, const Operands& op, const BinView& bv, const SplitWs& sw, const Outputs& out,
+                    int64_t ub_rows, hipStream_t s) {
+  return phase ? split_t<RA, RB, true>(op, bv, sw, out, ub_rows, s) : split_t<RA, RB, false>(op, bv, sw, out, ub_rows, s);
+}
+
 template <typename RA, typename RB>
 hipError_t run_bin_rp(int kind, int phase, const Operands& op, const BinView& bv, const Outputs& out,
                       int64_t ub_rows, hipStream_t s) {
@@ -1340,6 +1492,12 @@ hipError_t run_bin(int kind, int phase, const Operands& op, const BinView& bv, c
   return AIRES_DISPATCH_RP(op, run_bin_rp, kind, phase, op, bv, out, ub_rows, s);
 }
 
+hipError_t split_rows(int phase, const Operands& op, const BinView& bv, const SplitWs& sw, const Outputs& out,
+                      int64_t ub_rows, hipStream_t s) {
+  if (ub_rows <= 0) return hipSuccess;
+  return AIRES_DISPATCH_RP(op, split_rp, phase, op, bv, sw, out, ub_rows, s);
+}
+
 hipError_t windows_symbolic(const Operands& op, const BinView& bv, const WindowParams& wp, const Outputs& out,
                             int64_t ub_rows, hipStream_t s) {
   if (ub_rows <= 0) return hipSuccess;
@@ -1384,6 +1542,7 @@ size_t lds_bytes(int kind, int phase, int32_t W) {
     case KIND_DENSE_WAVE:
       return 4 * (phase ? dense_group_bytes<64, true, int64_t>(W) : dense_group_bytes<64, false, int64_t>(W));
     case KIND_DENSE_BLOCK:
+    case KIND_DENSE_SPLIT:
       return phase ? dense_group_bytes<512, true, int64_t>(W) : dense_group_bytes<512, false, int64_t>(W);
     case KIND_HASH_128: return 4 * sizeof(HashLds<128, 64, true, int64_t>);
     case KIND_HASH_1024: return 4 * sizeof(HashLds<1024, 64, true, int64_t>);
@@ -1400,6 +1559,7 @@ size_t window_numeric_lds(int max_grains, int max_entries, int G) {
 int group_size(int kind) {
   switch (kind) {
     case KIND_DENSE_BLOCK: return 512;
+    case KIND_DENSE_SPLIT: return SPLIT_BLOCK;
     case KIND_HASH_8192: return 256;
     case KIND_WINDOWS: return WIN_BLOCK;
     default: return 64;

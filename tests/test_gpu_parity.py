@@ -97,6 +97,10 @@ PATHS = {
                                   window_max_grains=4, window_max_entries=200, count_grains=5),
     # 2048 < N <= 16384 handled as narrow: hash bins then workgroup dense rows
     "narrow_block_hash": dict(dense_max_cols=200, hash_max_products=512),
+    # narrow rows split over workgroups (dense slots in global memory); then
+    # with too few slots, the rest of the bin one workgroup per row
+    "dense_split": dict(wave_max_products=1, split_min_products=1),
+    "dense_split_capped": dict(wave_max_products=1, split_min_products=1, split_max_rows=7),
 }
 
 
@@ -162,6 +166,8 @@ def test_cfg3_scaled_narrow_block(torch_gpu):
 def test_cfg4_scaled(torch_gpu):
     A, B = workloads.workload(4, n=65536)
     check(torch_gpu, A, B, "cfg4 n=65536")
+    st, _, _ = check(torch_gpu, A, B, "cfg4 n=65536 split rows", split_min_products=4096)
+    assert st["kind_ms"]["numeric"]["split"] > 0
 
 
 def test_cfg5_scaled_int64_rowptr(torch_gpu):
