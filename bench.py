@@ -93,6 +93,26 @@ def cpu_baseline(A, B, P, seconds: float, seed: int = 7):
     }
 
 
+def measured_traffic(kernel_name: str, dom_bytes_launch: int):
+    """HBM bytes per launch of the dominant kernel, from the committed
+    rocprofv3 FETCH_SIZE/WRITE_SIZE summary (profiles/traffic.json), only
+    if it was taken on the kernel source as it is now; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    src = os.path.join(ROOT, "paper_2507_02006_amd", "csrc", "kernels.hip")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(src, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    ent = rec.get(kernel_name)
+    if not ent or ent.get("kernels_hip_sha256") != sha:
+        return None
+    return int(ent["traffic_bytes"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -187,8 +207,8 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "numeric/%s" % dom, "achieved": round(dom_gbs, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": None, "algorithmic_bytes": dom_bytes,
-                     "avg_launch_ms": round(num_ms[dom], 4)},
+                     "traffic": measured_traffic("cfg%d/numeric/%s" % (args.workload, dom), dom_bytes),
+                     "algorithmic_bytes": dom_bytes, "avg_launch_ms": round(num_ms[dom], 4)},
         "phases_ms": phase,
         "numeric_gflops": round(2 * total_products / (phase["numeric_ms"] * 1e-3) / 1e9, 2),
         "end_to_end_compulsory_gbs": round(compulsory / (ms_per_step * 1e-3) / 1e9, 2),
