@@ -947,8 +947,7 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
 }
 
 // A window's LDS: its presence bitmap and the rank of each word's first set
-// bit (padded as in the symbolic items); the window's fp32 values (reused
-// to stage its column ids); the chunk.
+// bit (padded as in the symbolic items); the window's fp32 values; the chunk.
 
 template <typename S>
 __host__ __device__ constexpr size_t window_lds_bytes(int max_grains, int max_entries, int G) {
@@ -979,7 +978,6 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
   uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
   uint16_t* pre = reinterpret_cast<uint16_t*>(smem + align16((size_t)npad * 4));
   float* vals = reinterpret_cast<float*>(smem + align16((size_t)npad * 4) + align16((size_t)npad * 2));
-  int32_t* stage = reinterpret_cast<int32_t*>(vals);  // column ids, once the values are out
   using CH = Chunk<WIN_BLOCK, RB>;
   CH& ch = *reinterpret_cast<CH*>(reinterpret_cast<unsigned char*>(vals) + align16((size_t)wp.max_entries * 4));
   Group<WIN_BLOCK, WIN_BLOCK> g;
@@ -1038,13 +1036,20 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         if (o >= 0) cached = o + (int64_t)(g0 % SG) * WPG;  // windows never leave their item
       }
       auto load_bits = [&]() {
+        __syncthreads();  // the previous window's bitmap is cleared
         for (int w = t; w < nw; w += WIN_BLOCK) bm[pidx(w)] = wp.bm_cache[cached + w];
         __syncthreads();
       };
+      // every term of a column writes the column id at the column's rank
+      // (the same value; the stores meet in L2), so no pass over the bitmap
+      // is needed to write C's columns
       auto add_at_rank = [&](int j, float v) {
         const int pw = pidx(j >> 5);
         const int rk = (int)pre[pw] + __popc(bm[pw] & ((1u << (j & 31)) - 1u));
-        if (rk < n) atomicAdd(&vals[rk], v);
+        if (rk < n) {
+          atomicAdd(&vals[rk], v);
+          out.ccol[base + rk] = c0 + j;
+        }
       };
       // exclusive popcount prefix over the window's words: each thread owns
       // a run of wpt consecutive words
@@ -1175,30 +1180,12 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
                                                       [&](int j, float v) { add_at_rank(j - c0, v); });
       }
       __syncthreads();
-      // values out (coalesced), then the column ids staged in the same LDS
-      // array in rank order and written out coalesced as well
-      for (int kk = t; kk < n; kk += WIN_BLOCK) store_stream(&out.cval[base + kk], vals[kk]);
-      __syncthreads();
-      {
-        const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
-        for (int w = w0; w < w1; ++w) {
-          const int pw = pidx(w);
-          uint32_t bits = bm[pw];
-          int kk = (int)pre[pw];
-          while (bits) {
-            const int b = __ffs(bits) - 1;
-            bits &= bits - 1;
-            if (kk < n) stage[kk] = c0 + w * 32 + b;
-            ++kk;
-          }
-          bm[pw] = 0u;
-        }
-      }
-      __syncthreads();
+      // values out (coalesced); clear the window's bitmap and values
       for (int kk = t; kk < n; kk += WIN_BLOCK) {
-        store_stream(&out.ccol[base + kk], stage[kk]);
+        store_stream(&out.cval[base + kk], vals[kk]);
         vals[kk] = 0.f;
       }
+      for (int w = t; w < nw; w += WIN_BLOCK) bm[pidx(w)] = 0u;
     }
   }
 }
