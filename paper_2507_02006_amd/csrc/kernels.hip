@@ -262,7 +262,7 @@ __global__ __launch_bounds__(256) void k_bin_scatter(const int64_t* P, int64_t n
 // chunk holds fewer than 2^31 terms: segments are at most one window or one
 // B row wide and a chunk has at most GROUP of them.
 #ifndef AIRES_SEG_PER_THREAD
-#define AIRES_SEG_PER_THREAD 16
+#define AIRES_SEG_PER_THREAD 8
 #endif
 constexpr int SEG_PER_THREAD = AIRES_SEG_PER_THREAD;
 
@@ -297,7 +297,7 @@ struct GrainRange {
 };
 
 #ifndef AIRES_UNROLL
-#define AIRES_UNROLL 4
+#define AIRES_UNROLL 2
 #endif
 constexpr int UNROLL = AIRES_UNROLL;  // independent B loads each thread keeps in flight
 
