@@ -256,11 +256,11 @@ __global__ __launch_bounds__(256) void k_bin_scatter(const int64_t* P, int64_t n
 
 // ---------------------------------------------------- flattened product loop
 
-// Per-group LDS for one chunk of A_i: the B position
-// of term 0 of each segment (shifted so pos = shift[c] + q), a_ik, and a
-// segment map for a run of SEG_PER_THREAD * GROUP consecutive terms.  A
-// chunk holds fewer than 2^31 terms: segments are at most one window or one
-// B row wide and a chunk has at most GROUP of them.
+// Per-group LDS for one chunk of A_i: the B position of term 0 of each
+// segment (shifted so pos = shift[c] + q), a_ik, the first term of each
+// segment, and per wavefront a segment map of SEG_PER_THREAD * WAVE
+// consecutive terms.  A chunk holds fewer than 2^31 terms: segments are at
+// most one window or one B row wide and a chunk has at most GROUP of them.
 #ifndef AIRES_SEG_PER_THREAD
 #define AIRES_SEG_PER_THREAD 8
 #endif
@@ -274,6 +274,7 @@ struct Chunk {
     float av;
   };
   Rec rec[GROUP];
+  int32_t ex[GROUP + 1];
   uint16_t seg[GROUP * SEG_PER_THREAD];
 };
 
@@ -301,46 +302,73 @@ struct GrainRange {
 #endif
 constexpr int UNROLL = AIRES_UNROLL;  // independent B loads each thread keeps in flight
 
-template <int GROUP, int BLOCK>
-__device__ __forceinline__ int group_excl_max_scan(int v, const Group<GROUP, BLOCK>& g) {
-  // exclusive max over the threads before t (-1 for the first)
-  int x = v;
+// Segment map of one wavefront's terms [lo, lo + len), len <= WAVE *
+// SEG_PER_THREAD: seg_w[x] = the segment holding term lo + x, from the
+// first terms ex[c] of segments c < nk (non-decreasing, ex[0] = 0,
+// lo < ex[nk]).  The segment holding lo is found with two ballots; each
+// later segment starting in the range writes its id at its first term and
+// a wavefront max-scan carries ids forward.  No workgroup barrier.
+__device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, int len, uint16_t* seg_w) {
+  const int l = lane_id();
+  wave_sync();  // the previous run's reads of seg_w are done
+  const int stride = (nk + WAVE - 1) / WAVE;
+  const int cs = l * stride;
+  const uint64_t b1 = __ballot(cs < nk && ex[cs] <= lo);
+  const int base = (63 - __clzll(b1)) * stride;
+  const int c2 = base + l;
+  const uint64_t b2 = __ballot(l < stride && c2 < nk && ex[c2] <= lo);
+  const int c0 = base + (63 - __clzll(b2));
+#pragma unroll
+  for (int i = 0; i < SEG_PER_THREAD; ++i) seg_w[l * SEG_PER_THREAD + i] = 0;
+  wave_sync();
+  const int hi = lo + len;
+  for (int c = c0 + 1 + l; c < nk; c += WAVE) {
+    const int e = ex[c];
+    if (e >= hi) break;
+    if (ex[c + 1] > e) seg_w[e - lo] = (uint16_t)c;
+  }
+  wave_sync();
+  int run[SEG_PER_THREAD];
+  int m = c0;
+#pragma unroll
+  for (int i = 0; i < SEG_PER_THREAD; ++i) {
+    m = max(m, (int)seg_w[l * SEG_PER_THREAD + i]);
+    run[i] = m;
+  }
+  int x = m;
 #pragma unroll
   for (int d = 1; d < WAVE; d <<= 1) {
     const int u = __shfl_up(x, d, WAVE);
-    if (lane_id() >= d) x = max(x, u);
+    if (l >= d) x = max(x, u);
   }
   int before = __shfl_up(x, 1, WAVE);
-  if (lane_id() == 0) before = -1;
-  if constexpr (GROUP == WAVE) {
-    return before;
-  } else {
-    const int w = threadIdx.x / WAVE;
-    int32_t* red = reinterpret_cast<int32_t*>(g.red);
-    if (lane_id() == WAVE - 1) red[w] = x;
-    __syncthreads();
-    int pre = -1;
+  if (l == 0) before = c0;
 #pragma unroll
-    for (int i = 0; i < GROUP / WAVE; ++i)
-      if (i < w) pre = max(pre, red[i]);
-    __syncthreads();
-    return max(before, pre);
-  }
+  for (int i = 0; i < SEG_PER_THREAD; ++i) seg_w[l * SEG_PER_THREAD + i] = (uint16_t)max(before, run[i]);
+  wave_sync();
+}
+
+// Terms of a run of rn each of nw wavefronts takes: an equal share rounded
+// up to whole wavefront loads (at most WAVE * SEG_PER_THREAD).
+__device__ __forceinline__ int wave_share(int rn, int nw) {
+  return ((rn + nw - 1) / nw + WAVE - 1) / WAVE * WAVE;
 }
 
 // Calls f(column, a_ik * b_kj) (NUM) or f(column, 0) for every term of A
-// entries [p0, p1) (a row or a part of one).
-// Terms are numbered q = 0..total-1 over the chunk's segments; thread t
-// takes q = t, t + GROUP, ... so consecutive lanes read consecutive entries
-// of a B row.  The segment of each term comes from a map built per run of
-// GROUP * SEG_PER_THREAD terms: each segment's owner writes its id at its
-// first term, and a group max-scan carries ids forward.
+// entries [p0, p1) (a row or a part of one).  Terms are numbered over the
+// chunk's segments; a run of up to GROUP * SEG_PER_THREAD terms is split
+// into equal contiguous parts, one per wavefront, whose lane l takes terms
+// l, l + WAVE, ..., so consecutive lanes read consecutive entries of a B row.
 template <int GROUP, int BLOCK, bool NUM, typename CH, typename SEG, typename F>
 __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group<GROUP, BLOCK>& g,
                                                  CH& ch, int64_t p0, int64_t p1, const SEG& seg, F&& f) {
   using S = typename CH::shift_t;
   constexpr int RUN = GROUP * SEG_PER_THREAD;
+  constexpr int WR = WAVE * SEG_PER_THREAD;  // terms of one wavefront per run
   const int t = g.t();
+  const int lane = lane_id();
+  const int w = t / WAVE;
+  uint16_t* seg_w = ch.seg + w * WR;
   for (int64_t cb = p0; cb < p1; cb += GROUP) {
     const int64_t p = cb + t;
     int64_t lo = 0, len = 0;
@@ -355,37 +383,29 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
     const int64_t excl = incl - len;
     ch.rec[t].shift = (S)(lo - excl);
     ch.rec[t].av = av;
+    ch.ex[t] = (int32_t)excl;
+    if (t == 0) ch.ex[GROUP] = (int32_t)total;
+    g.sync();
+    const int nk = (int)((p1 - cb) < GROUP ? (p1 - cb) : GROUP);
     for (int64_t r0 = 0; r0 < total; r0 += RUN) {
       const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
-      // segment map of terms [r0, r0 + rn)
-#pragma unroll
-      for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[i * GROUP + t] = 0;
-      g.sync();
-      if (len > 0 && incl > r0 && excl < r0 + rn) ch.seg[(excl > r0 ? excl : r0) - r0] = (uint16_t)t;
-      g.sync();
-      int run[SEG_PER_THREAD];
-      int m = -1;
-#pragma unroll
-      for (int i = 0; i < SEG_PER_THREAD; ++i) {
-        const int v = ch.seg[t * SEG_PER_THREAD + i];
-        m = max(m, v);
-        run[i] = m;
-      }
-      const int before = group_excl_max_scan(m, g);
-#pragma unroll
-      for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[t * SEG_PER_THREAD + i] = (uint16_t)max(before, run[i]);
-      g.sync();
-      for (int q0 = t; q0 < rn; q0 += GROUP * UNROLL) {
+      const int per = wave_share(rn, GROUP / WAVE);
+      const int wlo = w * per;
+      const int wlen = min(per, rn - wlo);
+      if (wlen <= 0) continue;
+      const int base = (int)r0 + wlo;
+      wave_seg_map(ch.ex, nk, base, wlen, seg_w);
+      for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
         int64_t pos[UNROLL];
         float am[UNROLL];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
-          const int q = q0 + u * GROUP;
+          const int q = q0 + u * WAVE;
           pos[u] = -1;
           am[u] = 0.f;
-          if (q < rn) {
-            const typename CH::Rec rc = ch.rec[ch.seg[q]];
-            pos[u] = (int64_t)rc.shift + r0 + q;
+          if (q < wlen) {
+            const typename CH::Rec rc = ch.rec[seg_w[q]];
+            pos[u] = (int64_t)rc.shift + base + q;
             am[u] = rc.av;
           }
         }
@@ -404,8 +424,8 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
         for (int u = 0; u < UNROLL; ++u)
           if (pos[u] >= 0) f(j[u], am[u] * bv[u]);
       }
-      g.sync();
     }
+    g.sync();
   }
 }
 
@@ -851,10 +871,9 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
     // per-grain popcounts over each thread's run of words
     const int nw = (g1 - g0) * WPG;
     const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
-    int c = 0, gcur = -1, gacc = 0;
+    int gcur = -1, gacc = 0;
     for (int w = w0; w < w1; ++w) {
       const int pc = __popc(bm[pidx(w)]);
-      c += pc;
       const int gw = w / WPG;
       if (gw != gcur) {
         if (gacc) atomicAdd(&gc[gcur], gacc);
@@ -1074,37 +1093,30 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         const int64_t excl = incl - len;
         ch.rec[t].shift = (RB)(cur - excl);
         ch.rec[t].av = a;
-        // segment map of terms [r0, r0 + rn)
-        auto seg_map = [&](int64_t r0, int rn) {
-#pragma unroll
-          for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[i * WIN_BLOCK + t] = 0;
-          __syncthreads();
-          if (len > 0 && incl > r0 && excl < r0 + rn) ch.seg[(excl > r0 ? excl : r0) - r0] = (uint16_t)t;
-          __syncthreads();
-          int runv[SEG_PER_THREAD];
-          int m = -1;
-#pragma unroll
-          for (int i = 0; i < SEG_PER_THREAD; ++i) {
-            m = max(m, (int)ch.seg[t * SEG_PER_THREAD + i]);
-            runv[i] = m;
-          }
-          const int before = group_excl_max_scan(m, g);
-#pragma unroll
-          for (int i = 0; i < SEG_PER_THREAD; ++i) ch.seg[t * SEG_PER_THREAD + i] = (uint16_t)max(before, runv[i]);
-          __syncthreads();
-        };
+        ch.ex[t] = (int32_t)excl;
+        if (t == 0) ch.ex[WIN_BLOCK] = (int32_t)total;
+        __syncthreads();
+        const int nk = (int)(p1 - p0);
+        constexpr int WR = WAVE * SEG_PER_THREAD;  // terms of one wavefront per run
+        const int lane = lane_id();
+        const int wi = t / WAVE;
+        uint16_t* seg_w = ch.seg + wi * WR;
         if (total <= RUN) {
-          seg_map(0, (int)total);
+          // every term of the window in registers
+          const int per = wave_share((int)total, WIN_BLOCK / WAVE);
+          const int wlo = wi * per;
+          const int wlen = min(per, (int)total - wlo);
+          if (wlen > 0) wave_seg_map(ch.ex, nk, wlo, wlen, seg_w);
           int jj[SEG_PER_THREAD];
           float vv[SEG_PER_THREAD];
 #pragma unroll
           for (int i = 0; i < SEG_PER_THREAD; ++i) {
-            const int q = t + i * WIN_BLOCK;
+            const int q = lane + i * WAVE;
             jj[i] = -1;
             vv[i] = 0.f;
-            if (q < total) {
-              const typename CH::Rec rc = ch.rec[ch.seg[q]];
-              const int64_t pos = (int64_t)rc.shift + q;
+            if (q < wlen) {
+              const typename CH::Rec rc = ch.rec[seg_w[q]];
+              const int64_t pos = (int64_t)rc.shift + wlo + q;
               jj[i] = op.bcol[pos] - c0;
               vv[i] = rc.av * op.bval[pos];
             }
@@ -1127,18 +1139,23 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
           for (int pass = cached >= 0 ? 1 : 0; pass < 2; ++pass) {
             for (int64_t r0 = 0; r0 < total; r0 += RUN) {
               const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
-              seg_map(r0, rn);
-              for (int q0 = t; q0 < rn; q0 += WIN_BLOCK * UNROLL) {
+              const int per = wave_share(rn, WIN_BLOCK / WAVE);
+              const int wlo = wi * per;
+              const int wlen = min(per, rn - wlo);
+              if (wlen <= 0) continue;
+              const int base = (int)r0 + wlo;
+              wave_seg_map(ch.ex, nk, base, wlen, seg_w);
+              for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
                 int64_t pos[UNROLL];
                 float am[UNROLL];
 #pragma unroll
                 for (int u = 0; u < UNROLL; ++u) {
-                  const int q = q0 + u * WIN_BLOCK;
+                  const int q = q0 + u * WAVE;
                   pos[u] = -1;
                   am[u] = 0.f;
-                  if (q < rn) {
-                    const typename CH::Rec rc = ch.rec[ch.seg[q]];
-                    pos[u] = (int64_t)rc.shift + r0 + q;
+                  if (q < wlen) {
+                    const typename CH::Rec rc = ch.rec[seg_w[q]];
+                    pos[u] = (int64_t)rc.shift + base + q;
                     am[u] = rc.av;
                   }
                 }
@@ -1160,8 +1177,8 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
                   else set_bit(jv[u]);
                 }
               }
-              __syncthreads();
             }
+            __syncthreads();
             if (pass == 0) word_ranks();
           }
         }
