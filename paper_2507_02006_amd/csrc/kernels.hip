@@ -265,6 +265,7 @@ __global__ __launch_bounds__(256) void k_bin_scatter(const int64_t* P, int64_t n
 #define AIRES_SEG_PER_THREAD 8
 #endif
 constexpr int SEG_PER_THREAD = AIRES_SEG_PER_THREAD;
+static_assert(SEG_PER_THREAD % 8 == 0, "segment maps move in 16-byte vectors");
 
 template <int GROUP, typename S>
 struct Chunk {
@@ -274,8 +275,8 @@ struct Chunk {
     float av;
   };
   Rec rec[GROUP];
-  int32_t ex[GROUP + 1];
-  uint16_t seg[GROUP * SEG_PER_THREAD];
+  int32_t ex[GROUP + 4];  // GROUP + 1 used; the padding keeps seg 16-byte aligned
+  alignas(16) uint16_t seg[GROUP * SEG_PER_THREAD];
 };
 
 // Where the terms of a k come from: the whole B row ...
@@ -318,8 +319,10 @@ __device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, 
   const int c2 = base + l;
   const uint64_t b2 = __ballot(l < stride && c2 < nk && ex[c2] <= lo);
   const int c0 = base + (63 - __clzll(b2));
+  // each lane's SEG_PER_THREAD entries are moved as 16-byte vectors
+  uint4* mine = reinterpret_cast<uint4*>(seg_w + l * SEG_PER_THREAD);
 #pragma unroll
-  for (int i = 0; i < SEG_PER_THREAD; ++i) seg_w[l * SEG_PER_THREAD + i] = 0;
+  for (int v = 0; v < SEG_PER_THREAD / 8; ++v) mine[v] = make_uint4(0u, 0u, 0u, 0u);
   wave_sync();
   const int hi = lo + len;
   for (int c = c0 + 1 + l; c < nk; c += WAVE) {
@@ -331,9 +334,14 @@ __device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, 
   int run[SEG_PER_THREAD];
   int m = c0;
 #pragma unroll
-  for (int i = 0; i < SEG_PER_THREAD; ++i) {
-    m = max(m, (int)seg_w[l * SEG_PER_THREAD + i]);
-    run[i] = m;
+  for (int v = 0; v < SEG_PER_THREAD / 8; ++v) {
+    const uint4 q = mine[v];
+    const uint32_t wv[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      m = max(m, (int)((wv[h >> 1] >> ((h & 1) * 16)) & 0xffffu));
+      run[v * 8 + h] = m;
+    }
   }
   int x = m;
 #pragma unroll
@@ -344,7 +352,13 @@ __device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, 
   int before = __shfl_up(x, 1, WAVE);
   if (l == 0) before = c0;
 #pragma unroll
-  for (int i = 0; i < SEG_PER_THREAD; ++i) seg_w[l * SEG_PER_THREAD + i] = (uint16_t)max(before, run[i]);
+  for (int v = 0; v < SEG_PER_THREAD / 8; ++v) {
+    uint32_t wv[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      wv[h] = (uint32_t)max(before, run[v * 8 + 2 * h]) | ((uint32_t)max(before, run[v * 8 + 2 * h + 1]) << 16);
+    mine[v] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+  }
   wave_sync();
 }
 
