@@ -1073,15 +1073,16 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         for (int w = t; w < nw; w += WIN_BLOCK) bm[pidx(w)] = wp.bm_cache[cached + w];
         __syncthreads();
       };
-      // every term of a column writes the column id at the column's rank
-      // (the same value; the stores meet in L2), so no pass over the bitmap
-      // is needed to write C's columns
+      // the term that finds its column's slot still at +0 (the first one,
+      // and any that follow a sum of exactly zero) writes the column id at
+      // the column's rank, so no pass over the bitmap is needed for C's
+      // columns
       auto add_at_rank = [&](int j, float v) {
         const int pw = pidx(j >> 5);
         const int rk = (int)pre[pw] + __popc(bm[pw] & ((1u << (j & 31)) - 1u));
         if (rk < n) {
-          atomicAdd(&vals[rk], v);
-          out.ccol[base + rk] = c0 + j;
+          const float old = atomicAdd(&vals[rk], v);
+          if (old == 0.f) out.ccol[base + rk] = c0 + j;
         }
       };
       // exclusive popcount prefix over the window's words: each thread owns
