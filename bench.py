@@ -13,7 +13,8 @@ roofline = the dominant kernel (the numeric launch with the largest time):
   achieved = its algorithmic bytes per launch / its average launch time,
   from HIP events the library records around that launch on the compute
   stream during the timed steps.
-cpu_baseline = the CPU oracle (serial) on a bounded random row sample.
+cpu_baseline = the CPU oracle (serial) on a bounded random row sample;
+cpu_baseline_all_cores = the same oracle calls over all host cores.
 """
 from __future__ import annotations
 
@@ -63,34 +64,61 @@ def row_products(A, B) -> np.ndarray:
     return np.bincount(rows, weights=lenB[A.col], minlength=A.nrows).astype(np.int64)
 
 
-def cpu_baseline(A, B, P, seconds: float, seed: int = 7):
-    """Time the serial CPU oracle on random rows whose products add up to
-    about `seconds` of oracle work (rate probed on a first small sample)."""
+def cpu_baseline(A, B, P, seconds: float, seed: int = 7, threads: int = 1):
+    """Time the CPU oracle on random contiguous row ranges whose products add
+    up to about `seconds` of work per thread (rate probed on a first small
+    range); one oracle call per range, the ranges spread over `threads` host
+    threads (the C oracle runs outside the GIL)."""
     import oracle
+    from concurrent.futures import ThreadPoolExecutor
     rng = np.random.default_rng(seed)
-    order = rng.permutation(A.nrows)
-    cum = np.cumsum(P[order])
+    cumr = np.concatenate([[0], np.cumsum(P)])
+    total = int(cumr[-1])
 
-    def run(nprod):
-        n = int(np.searchsorted(cum, nprod)) + 1
-        rows = np.sort(order[:n])
-        t0 = time.perf_counter()
-        prods = 0
-        for r in rows:
-            prods += oracle.spgemm(A, B, int(r), int(r) + 1).products
-        return prods, time.perf_counter() - t0, n
+    def ranges(nprod, parts):
+        out = []
+        for st in rng.integers(0, A.nrows, parts):
+            en = int(np.searchsorted(cumr, cumr[st] + nprod / parts)) + 1
+            out.append((int(st), min(A.nrows, max(en, int(st) + 1))))
+        return out
 
-    p0, t0, _ = run(2_000_000)
-    rate = p0 / max(t0, 1e-9)
-    prods, dt, n = run(rate * seconds)
+    def span(rg):
+        return oracle.spgemm(A, B, rg[0], rg[1]).products
+
+    t0 = time.perf_counter()
+    p0 = span(ranges(min(2_000_000, total), 1)[0])
+    rate = p0 / max(time.perf_counter() - t0, 1e-9)
+    rgs = ranges(min(rate * seconds * threads, total), threads * 4)
+    t0 = time.perf_counter()
+    if threads == 1:
+        prods = sum(span(r) for r in rgs)
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            prods = sum(ex.map(span, rgs))
+    dt = time.perf_counter() - t0
     return {
         "value": round(2 * prods / dt / 1e9, 4),
         "unit": "GFLOP/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "sample": "%d random rows (seed %d), %d intermediate products = %.2f%% of the workload, %.1f s serial"
-                  % (n, seed, prods, 100.0 * prods / max(int(P.sum()), 1), dt),
+        "sample": "%d random contiguous row ranges (seed %d), %d intermediate products = %.2f%% of the "
+                  "workload, %.1f s on %d thread(s)" % (len(rgs), seed, prods, 100.0 * prods / max(total, 1),
+                                                        dt, threads),
     }
+
+
+def host_cpu():
+    """Host CPU model and the cores this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
 
 
 def measured_traffic(kernel_name: str, dom_bytes_launch: int):
@@ -183,6 +211,10 @@ def main():
     sA = A.rp.dtype.itemsize
     dom_bytes = int((sA + 8 * alen[sel] + 8 + 8 * crow[sel]).sum()) + B.nbytes()
     dom_gbs = dom_bytes / (num_ms[dom] * 1e-3) / 1e9
+    # gather model (no reuse): B.row_ptr per A entry and 8 bytes of B per product
+    sB = B.rp.dtype.itemsize
+    dom_gather = int((sA + 8 * alen[sel] + 2 * sB * alen[sel] + 8 * P[sel] + 8 + 8 * crow[sel]).sum())
+    dom_gather_gbs = dom_gather / (num_ms[dom] * 1e-3) / 1e9
     del last
 
     phase = {k: round(float(np.mean([s[k] for s in stats])), 4)
@@ -208,7 +240,8 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "numeric/%s" % dom, "achieved": round(dom_gbs, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic("cfg%d/numeric/%s" % (args.workload, dom), dom_bytes),
-                     "algorithmic_bytes": dom_bytes, "avg_launch_ms": round(num_ms[dom], 4)},
+                     "algorithmic_bytes": dom_bytes, "avg_launch_ms": round(num_ms[dom], 4),
+                     "gather_model_gbs": round(dom_gather_gbs, 2)},
         "phases_ms": phase,
         "numeric_gflops": round(2 * total_products / (phase["numeric_ms"] * 1e-3) / 1e9, 2),
         "end_to_end_compulsory_gbs": round(compulsory / (ms_per_step * 1e-3) / 1e9, 2),
@@ -217,6 +250,11 @@ def main():
     }
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(A, B, P, args.cpu_seconds)
+        model, ncpu = host_cpu()
+        # a one-GPU share of the host: at most 16 threads
+        allc = cpu_baseline(A, B, P, args.cpu_seconds / 2, threads=max(1, min(ncpu, 16)))
+        allc["cpu_model"] = model
+        res["cpu_baseline_all_cores"] = allc
     print(json.dumps(res), flush=True)
 
 
