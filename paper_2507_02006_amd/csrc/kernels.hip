@@ -12,17 +12,23 @@
 //   numeric      C_i = sum_k a_ik B_k, written with strictly increasing columns
 //
 // Accumulators live in LDS:
-//   dense window  fp32 slots for a window of W consecutive columns plus a
-//                 presence bitmap; compaction walks the bitmap, so the
-//                 output comes out sorted with no sort at all.
+//   dense row     fp32 slots for all N columns of a narrow product plus a
+//                 presence bitmap; compaction by ballot walks the columns in
+//                 order, so the output comes out sorted with no sort at all
+//                 (heavy rows: runs of A entries per workgroup, merged in a
+//                 dense slot in global memory).
 //   hash          open addressing (linear probing) keyed by column; the
 //                 occupied slots are compacted and sorted (runs of 16 in
 //                 registers, then merge-path rounds in LDS).
+//   column window presence bitmap of a window of whole column grains, word
+//                 ranks from its popcounts, and a compact fp32 array indexed
+//                 by rank (wide products).
 // A product's intermediate terms are spread over the threads of a group by
-// a flattened loop: the group loads up to GROUP entries (k, a_ik) of A_i,
-// scans the lengths of the matching B rows, and each thread takes every
-// GROUP-th term, finding its B row by binary search in the scanned lengths.
-// Consecutive threads therefore read consecutive entries of a B row.
+// a flattened loop: the group loads up to GROUP entries (k, a_ik) of A_i and
+// scans the lengths of the matching B segments; each wavefront takes an
+// equal contiguous share of the terms and maps each term to its segment with
+// a segment map of its own.  Consecutive lanes read consecutive entries of a
+// B row.
 #include "kernels.h"
 
 #include <hip/hip_runtime.h>
@@ -814,13 +820,15 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 //
 // Wide products (N above the densest LDS row) split the columns into grains
 // of G columns.  Symbolic: a workgroup sets a presence bitmap for a run of
-// grains of one row and writes each grain's popcount.  A plan kernel then
-// cuts every row into windows of whole grains holding at most max_entries
-// entries and spanning at most max_grains grains.  Numeric, per window:
-// pass 1 sets the window's presence bitmap, a workgroup scan turns word
-// popcounts into ranks, pass 2 adds each term into a compact fp32 array at
-// the rank of its column, and the array and the bitmap's columns are written
-// out in column order.  LDS grows with the window's entries, not its width.
+// grains of one row (a symbolic item), writes each grain's popcount, and
+// for heavy rows keeps the bitmap in global memory.  A plan kernel then cuts
+// every row into windows of whole grains holding at most max_entries
+// entries, spanning at most max_grains grains and never leaving a symbolic
+// item.  Numeric, per window: the presence bitmap is set from the terms (or
+// loaded from the kept one), a workgroup scan turns word popcounts into
+// ranks, and each term is added into a compact fp32 array at the rank of
+// its column, the first one also writing the column id there; the array is
+// then written out.  LDS grows with the window's entries, not its width.
 
 constexpr int WIN_BLOCK = 512;
 
@@ -997,7 +1005,8 @@ __host__ __device__ constexpr size_t window_lds_bytes(int max_grains, int max_en
 // window needs one index lookup per k (its end), issued while the previous
 // window is processed.  A window with at most WIN_BLOCK * SEG_PER_THREAD
 // terms loads each term once into registers; larger windows make two
-// passes over the B segments, keeping the row's state in LDS.
+// passes over the B segments (one when the symbolic bitmap was kept),
+// keeping the row's state in LDS.
 template <typename RA, typename RB>
 __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, const BinView bv,
                                                            const WindowParams wp, const Outputs out) {
