@@ -273,6 +273,22 @@ __global__ __launch_bounds__(256) void k_bin_scatter(const int64_t* P, int64_t n
 constexpr int SEG_PER_THREAD = AIRES_SEG_PER_THREAD;
 static_assert(SEG_PER_THREAD % 8 == 0, "segment maps move in 16-byte vectors");
 
+// fp32 add into an LDS slot, returning the slot's previous value.  It is a
+// compare-and-swap loop on the slot's bits: on gfx950 the LDS float-add
+// atomic issues at roughly a seventh of the rate of the LDS integer atomics
+// and compare-swap, and a lane retries only when another lane changed the
+// slot between its read and its swap (at least one lane per slot succeeds
+// on every round, so the loop ends).
+__device__ __forceinline__ float lds_add(float* p, float v) {
+  uint32_t* q = reinterpret_cast<uint32_t*>(p);
+  uint32_t old = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  for (;;) {
+    const uint32_t prev = atomicCAS(q, old, __float_as_uint(__uint_as_float(old) + v));
+    if (prev == old) return __uint_as_float(old);
+    old = prev;
+  }
+}
+
 template <int GROUP, typename S>
 struct Chunk {
   using shift_t = S;  // B positions fit B's row-pointer type
@@ -501,7 +517,7 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
     const int64_t row = list[it];
     for_each_term<RA, GROUP, BLOCK, NUM>(op, g, ch, row, seg, [&](int j, float v) {
       atomicOr(&bm[j >> 5], 1u << (j & 31));
-      if constexpr (NUM) atomicAdd(&acc[j], v);
+      if constexpr (NUM) lds_add(&acc[j], v);
     });
     if constexpr (!NUM) {
       int64_t c = 0;
@@ -582,7 +598,7 @@ __global__ __launch_bounds__(SPLIT_BLOCK) void k_split_parts(const Operands op, 
     if (q0 < q1)
       for_each_term_in<SPLIT_BLOCK, SPLIT_BLOCK, NUM>(op, g, ch, q0, q1, seg, [&](int j, float v) {
         atomicOr(&bm[j >> 5], 1u << (j & 31));
-        if constexpr (NUM) atomicAdd(&acc[j], v);
+        if constexpr (NUM) lds_add(&acc[j], v);
       });
     if constexpr (NUM) {
       for (int j = t; j < N; j += SPLIT_BLOCK)
@@ -717,7 +733,7 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
       for (;;) {
         const int old = atomicCAS(&L.key[h], -1, j);
         if (old == -1 || old == j) {
-          if constexpr (NUM) atomicAdd(&L.val[h], v);
+          if constexpr (NUM) lds_add(&L.val[h], v);
           else mine += (old == -1);
           break;
         }
@@ -1090,7 +1106,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         const int pw = pidx(j >> 5);
         const int rk = (int)pre[pw] + __popc(bm[pw] & ((1u << (j & 31)) - 1u));
         if (rk < n) {
-          const float old = atomicAdd(&vals[rk], v);
+          const float old = lds_add(&vals[rk], v);
           if (old == 0.f) out.ccol[base + rk] = c0 + j;
         }
       };
