@@ -278,10 +278,13 @@ static_assert(SEG_PER_THREAD % 8 == 0, "segment maps move in 16-byte vectors");
 // atomic issues at roughly a seventh of the rate of the LDS integer atomics
 // and compare-swap, and a lane retries only when another lane changed the
 // slot between its read and its swap (at least one lane per slot succeeds
-// on every round, so the loop ends).
+// on every round, so the loop ends).  GUESS_EMPTY: the first swap assumes
+// the slot still holds +0 instead of reading it first, which saves the read
+// where most adds are a slot's first.
+template <bool GUESS_EMPTY>
 __device__ __forceinline__ float lds_add(float* p, float v) {
   uint32_t* q = reinterpret_cast<uint32_t*>(p);
-  uint32_t old = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  uint32_t old = GUESS_EMPTY ? 0u : __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   for (;;) {
     const uint32_t prev = atomicCAS(q, old, __float_as_uint(__uint_as_float(old) + v));
     if (prev == old) return __uint_as_float(old);
@@ -517,7 +520,7 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
     const int64_t row = list[it];
     for_each_term<RA, GROUP, BLOCK, NUM>(op, g, ch, row, seg, [&](int j, float v) {
       atomicOr(&bm[j >> 5], 1u << (j & 31));
-      if constexpr (NUM) lds_add(&acc[j], v);
+      if constexpr (NUM) lds_add<true>(&acc[j], v);
     });
     if constexpr (!NUM) {
       int64_t c = 0;
@@ -598,7 +601,7 @@ __global__ __launch_bounds__(SPLIT_BLOCK) void k_split_parts(const Operands op, 
     if (q0 < q1)
       for_each_term_in<SPLIT_BLOCK, SPLIT_BLOCK, NUM>(op, g, ch, q0, q1, seg, [&](int j, float v) {
         atomicOr(&bm[j >> 5], 1u << (j & 31));
-        if constexpr (NUM) lds_add(&acc[j], v);
+        if constexpr (NUM) lds_add<true>(&acc[j], v);
       });
     if constexpr (NUM) {
       for (int j = t; j < N; j += SPLIT_BLOCK)
@@ -733,7 +736,7 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
       for (;;) {
         const int old = atomicCAS(&L.key[h], -1, j);
         if (old == -1 || old == j) {
-          if constexpr (NUM) lds_add(&L.val[h], v);
+          if constexpr (NUM) lds_add<true>(&L.val[h], v);
           else mine += (old == -1);
           break;
         }
@@ -1106,7 +1109,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         const int pw = pidx(j >> 5);
         const int rk = (int)pre[pw] + __popc(bm[pw] & ((1u << (j & 31)) - 1u));
         if (rk < n) {
-          const float old = lds_add(&vals[rk], v);
+          const float old = lds_add<false>(&vals[rk], v);
           if (old == 0.f) out.ccol[base + rk] = c0 + j;
         }
       };
@@ -1405,7 +1408,7 @@ hipError_t run_bin_t(int kind, const Operands& op, const BinView& bv, const Outp
     case KIND_HASH_1024:
       return launch_hash<RA, RB, 1024, 64, 256, NUM>(op, bv, out, ub_rows, s);
     case KIND_HASH_8192:
-      return launch_hash<RA, RB, 8192, 256, 256, NUM>(op, bv, out, ub_rows, s);
+      return launch_hash<RA, RB, 8192, 512, 512, NUM>(op, bv, out, ub_rows, s);
     default:
       return hipErrorInvalidValue;
   }
@@ -1590,7 +1593,7 @@ size_t lds_bytes(int kind, int phase, int32_t W) {
       return phase ? dense_group_bytes<512, true, int64_t>(W) : dense_group_bytes<512, false, int64_t>(W);
     case KIND_HASH_128: return 4 * sizeof(HashLds<128, 64, true, int64_t>);
     case KIND_HASH_1024: return 4 * sizeof(HashLds<1024, 64, true, int64_t>);
-    case KIND_HASH_8192: return sizeof(HashLds<8192, 256, true, int64_t>);
+    case KIND_HASH_8192: return sizeof(HashLds<8192, 512, true, int64_t>);
     default: return 0;
   }
 }
@@ -1604,7 +1607,7 @@ int group_size(int kind) {
   switch (kind) {
     case KIND_DENSE_BLOCK: return 512;
     case KIND_DENSE_SPLIT: return SPLIT_BLOCK;
-    case KIND_HASH_8192: return 256;
+    case KIND_HASH_8192: return 512;
     case KIND_WINDOWS: return WIN_BLOCK;
     default: return 64;
   }
