@@ -52,21 +52,60 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <typename T>
-__device__ __forceinline__ T wave_incl_scan(T v) {
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    T u = __shfl_up(v, d, WAVE);
-    if (lane_id() >= d) v += u;
+// Cross-lane moves by DPP (data-parallel primitives of the GFX9 vector
+// ALU, no LDS traffic): row_shr:n = 0x110 + n shifts within rows of 16
+// lanes, row_bcast:15 = 0x142 and row_bcast:31 = 0x143 pass the last lane
+// of a row (of two rows) on to the rows that ROW_MASK enables, wave_shr:1 =
+// 0x138 shifts across the wavefront.  Lanes without a source read 0.
+template <int CTRL, int ROW_MASK, typename T>
+__device__ __forceinline__ T dpp_move(T x) {
+  static_assert(sizeof(T) == 4 || sizeof(T) == 8, "32- or 64-bit lanes");
+  if constexpr (sizeof(T) == 4) {
+    return (T)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xf, false);
+  } else {
+    const uint64_t u = (uint64_t)x;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROW_MASK, 0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROW_MASK, 0xf, false);
+    return (T)(((uint64_t)hi << 32) | lo);
   }
+}
+
+// Inclusive wavefront scan: Hillis-Steele steps 1, 2, 4, 8 inside rows of
+// 16 lanes, then the row totals are carried to rows 1 and 3 and to rows 2
+// and 3.  OP is + (SUM) or max (for non-negative values).
+template <bool SUM, typename T>
+__device__ __forceinline__ T wave_scan_op(T v) {
+  auto op = [](T a, T b) { return SUM ? a + b : (a > b ? a : b); };
+  v = op(v, dpp_move<0x111, 0xf>(v));
+  v = op(v, dpp_move<0x112, 0xf>(v));
+  v = op(v, dpp_move<0x114, 0xf>(v));
+  v = op(v, dpp_move<0x118, 0xf>(v));
+  v = op(v, dpp_move<0x142, 0xa>(v));
+  v = op(v, dpp_move<0x143, 0xc>(v));
   return v;
 }
 
 template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+  return wave_scan_op<true>(v);
+}
+
+// The value of lane 63 in every lane.
+template <typename T>
+__device__ __forceinline__ T wave_last(T x) {
+  if constexpr (sizeof(T) == 4) {
+    return (T)__builtin_amdgcn_readlane((int)x, WAVE - 1);
+  } else {
+    const uint64_t u = (uint64_t)x;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, WAVE - 1);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), WAVE - 1);
+    return (T)(((uint64_t)hi << 32) | lo);
+  }
+}
+
+template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
-#pragma unroll
-  for (int d = WAVE / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, WAVE);
-  return v;
+  return wave_last(wave_incl_scan(v));
 }
 
 // A cooperating group: one wavefront (GROUP == 64) or the whole block.
@@ -84,7 +123,7 @@ struct Group {
   __device__ __forceinline__ int64_t incl_scan(int64_t v, int64_t* total) const {
     int64_t x = wave_incl_scan(v);
     if constexpr (GROUP == WAVE) {
-      *total = __shfl(x, WAVE - 1, WAVE);
+      *total = wave_last(x);
       return x;
     } else {
       const int w = threadIdx.x / WAVE;
@@ -368,13 +407,8 @@ __device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, 
       run[v * 8 + h] = m;
     }
   }
-  int x = m;
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    const int u = __shfl_up(x, d, WAVE);
-    if (l >= d) x = max(x, u);
-  }
-  int before = __shfl_up(x, 1, WAVE);
+  const int x = wave_scan_op<false>(m);  // segment ids are >= 0
+  int before = dpp_move<0x138, 0xf>(x);  // the previous lane's
   if (l == 0) before = c0;
 #pragma unroll
   for (int v = 0; v < SEG_PER_THREAD / 8; ++v) {
