@@ -34,8 +34,8 @@ struct Operands {
   const void* arp; int rpa64; int64_t a_base; const int32_t* acol; const float* aval;
   const void* brp; int rpb64; const int32_t* bcol; const float* bval;
   int64_t K, N;
-  // Column grains of a wide product: bidx[g*K + k] = first position of B_k
-  // with column >= g*G, for g in [0, nG]; nullptr when N is narrow.
+  // Column grains of a wide product: bidx[k*(nG+1) + g] = first position of
+  // B_k with column >= g*G, for g in [0, nG]; nullptr when N is narrow.
   const int32_t* bidx; int32_t G; int32_t nG;
 };
 

@@ -354,11 +354,12 @@ struct FullRows {
 };
 // ... or the part of it in a run of column grains (two slabs of the index).
 struct GrainRange {
-  const int32_t* lo_slab;
-  const int32_t* hi_slab;
+  const int32_t* bidx;  // the grain index, nG + 1 entries per B row
+  int32_t stride, g0, g1;
   __device__ __forceinline__ void operator()(int64_t k, int64_t& lo, int64_t& len) const {
-    lo = lo_slab[k];
-    len = (int64_t)hi_slab[k] - lo;
+    const int32_t* r = bidx + k * stride;
+    lo = r[g0];
+    len = (int64_t)r[g1] - lo;
   }
 };
 
@@ -938,7 +939,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
     const int g0 = (int)(gg * SG);
     const int g1 = min((int)op.nG, g0 + SG);
     const int c0 = g0 * op.G;
-    const GrainRange seg{op.bidx + (int64_t)g0 * op.K, op.bidx + (int64_t)g1 * op.K};
+    const GrainRange seg{op.bidx, op.nG + 1, g0, g1};
     for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg, [&](int j, float) {
       j -= c0;
       atomicOr(&bm[pidx(j >> 5)], 1u << (j & 31));
@@ -1109,14 +1110,14 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
     WinItem nextI{};
     if (i0 < i1) {
       nextI = wp.items[i0];
-      if (k >= 0) nxt_hi = op.bidx[(int64_t)nextI.g1 * op.K + k];
+      if (k >= 0) nxt_hi = op.bidx[k * (op.nG + 1) + nextI.g1];
     }
     for (int64_t it = i0; it < i1; ++it) {
       const WinItem I = nextI;
       const int64_t hi = nxt_hi;
       if (it + 1 < i1) {  // next window's header and segment ends, in flight meanwhile
         nextI = wp.items[it + 1];
-        if (k >= 0) nxt_hi = op.bidx[(int64_t)nextI.g1 * op.K + k];
+        if (k >= 0) nxt_hi = op.bidx[k * (op.nG + 1) + nextI.g1];
       }
       const int g0 = I.g0, g1 = I.g1, n = I.n;
       const int c0 = g0 * op.G;
@@ -1163,7 +1164,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         __syncthreads();
       };
       if (short_row) {
-        if (k >= 0 && g0 != prev_g1) cur = op.bidx[(int64_t)g0 * op.K + k];
+        if (k >= 0 && g0 != prev_g1) cur = op.bidx[k * (op.nG + 1) + g0];
         const int64_t len = (k >= 0) ? hi - cur : 0;
         int64_t total;
         const int64_t incl = g.incl_scan(len, &total);
@@ -1263,7 +1264,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         prev_g1 = g1;
       } else {
         // long row: pass 1 presence bitmap, pass 2 add at the ranks
-        const GrainRange seg{op.bidx + (int64_t)g0 * op.K, op.bidx + (int64_t)g1 * op.K};
+        const GrainRange seg{op.bidx, op.nG + 1, g0, g1};
         if (cached >= 0)
           load_bits();
         else
@@ -1286,8 +1287,10 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
 
 // ------------------------------------------------------------ window index
 
-// bidx[g*K + k] = first position p of B_k with bcol[p] >= g*W (or the row
-// end), for grains g in [0, nwin]; W is the grain width.  One wavefront per B row.
+// bidx[k*(nwin+1) + g] = first position p of B_k with bcol[p] >= g*W (or
+// the row end), for grains g in [0, nwin]; W is the grain width.  A B row's
+// entries are contiguous, so the lookups of one k for successive windows
+// share cache lines.  One wavefront per B row.
 template <typename RB>
 __global__ __launch_bounds__(256) void k_window_index(const void* brp, const int32_t* bcol,
                                                       int64_t K, int32_t W, int32_t nwin,
@@ -1298,11 +1301,11 @@ __global__ __launch_bounds__(256) void k_window_index(const void* brp, const int
     for (int64_t p = s + lane_id(); p < e; p += WAVE) {
       const int wc = bcol[p] / W;
       const int wp = (p == s) ? -1 : bcol[p - 1] / W;
-      for (int w = wp + 1; w <= wc; ++w) bidx[(int64_t)w * K + k] = (int32_t)p;
+      for (int w = wp + 1; w <= wc; ++w) bidx[k * (nwin + 1) + w] = (int32_t)p;
     }
     if (lane_id() == 0) {
       const int wl = (e > s) ? bcol[e - 1] / W : -1;
-      for (int w = wl + 1; w <= nwin; ++w) bidx[(int64_t)w * K + k] = (int32_t)e;
+      for (int w = wl + 1; w <= nwin; ++w) bidx[k * (nwin + 1) + w] = (int32_t)e;
     }
   }
 }
