@@ -1041,13 +1041,13 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
   }
 }
 
-// A window's LDS: its presence bitmap and the rank of each word's first set
-// bit (padded as in the symbolic items); the window's fp32 values; the chunk.
+// A window's LDS: per bitmap word its presence bits and the rank of its
+// first set bit, side by side (a term's rank is one 8-byte read); the
+// window's fp32 values; the chunk.
 
 template <typename S>
 __host__ __device__ constexpr size_t window_lds_bytes(int max_grains, int max_entries, int G) {
-  return align16((size_t)window_words_padded(max_grains * (G / 32)) * 4) +
-         align16((size_t)window_words_padded(max_grains * (G / 32)) * 2) + align16((size_t)max_entries * 4) +
+  return align16((size_t)max_grains * (G / 32) * 8) + align16((size_t)max_entries * 4) +
          align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128 + 16;  // + the static row slot
 }
 
@@ -1068,20 +1068,15 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
   __shared__ int64_t s_row;
   const int WPG = op.G / 32;
   const int maxw = wp.max_grains * WPG;
-  const int lw = window_wpt_log2(maxw);
-  const int wpt = 1 << lw;
-  const int npad = window_words_padded(maxw);
-  uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
-  uint16_t* pre = reinterpret_cast<uint16_t*>(smem + align16((size_t)npad * 4));
-  float* vals = reinterpret_cast<float*>(smem + align16((size_t)npad * 4) + align16((size_t)npad * 2));
+  uint2* bw = reinterpret_cast<uint2*>(smem);  // (presence bits, rank of the word's first bit)
+  float* vals = reinterpret_cast<float*>(smem + align16((size_t)maxw * 8));
   using CH = Chunk<WIN_BLOCK, RB>;
   CH& ch = *reinterpret_cast<CH*>(reinterpret_cast<unsigned char*>(vals) + align16((size_t)wp.max_entries * 4));
   Group<WIN_BLOCK, WIN_BLOCK> g;
   g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
   const int t = threadIdx.x;
-  for (int i = t; i < npad; i += WIN_BLOCK) bm[i] = 0u;
+  for (int i = t; i < maxw; i += WIN_BLOCK) bw[i] = make_uint2(0u, 0u);
   for (int i = t; i < wp.max_entries; i += WIN_BLOCK) vals[i] = 0.f;
-  auto pidx = [&](int w) { return w + (w >> lw); };
   constexpr int RUN = WIN_BLOCK * SEG_PER_THREAD;
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
@@ -1123,7 +1118,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
       const int c0 = g0 * op.G;
       const int nw = (g1 - g0) * WPG;
       const int64_t base = rbase + I.roff;
-      auto set_bit = [&](int j) { atomicOr(&bm[pidx(j >> 5)], 1u << (j & 31)); };
+      auto set_bit = [&](int j) { atomicOr(&bw[j >> 5].x, 1u << (j & 31)); };
       // Heavy rows: the symbolic phase kept the window's bitmap.
       int64_t cached = -1;
       if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
@@ -1133,7 +1128,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
       }
       auto load_bits = [&]() {
         __syncthreads();  // the previous window's bitmap is cleared
-        for (int w = t; w < nw; w += WIN_BLOCK) bm[pidx(w)] = wp.bm_cache[cached + w];
+        for (int w = t; w < nw; w += WIN_BLOCK) bw[w].x = wp.bm_cache[cached + w];
         __syncthreads();
       };
       // the term that finds its column's slot still at +0 (the first one,
@@ -1141,25 +1136,34 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
       // the column's rank, so no pass over the bitmap is needed for C's
       // columns
       auto add_at_rank = [&](int j, float v) {
-        const int pw = pidx(j >> 5);
-        const int rk = (int)pre[pw] + __popc(bm[pw] & ((1u << (j & 31)) - 1u));
+        const uint2 e = bw[j >> 5];
+        const int rk = (int)e.y + __popc(e.x & ((1u << (j & 31)) - 1u));
         if (rk < n) {
           const float old = lds_add<false>(&vals[rk], v);
           if (old == 0.f) out.ccol[base + rk] = c0 + j;
         }
       };
-      // exclusive popcount prefix over the window's words: each thread owns
-      // a run of wpt consecutive words
+      // exclusive popcount prefix over the window's words: each wavefront
+      // takes a contiguous share, its lanes consecutive words, with one
+      // wavefront scan per 64 words and the shares' totals carried in
       auto word_ranks = [&]() {
-        const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
-        int64_t sw = 0;
-        for (int w = w0; w < w1; ++w) sw += __popc(bm[pidx(w)]);
-        int64_t tot;
-        int64_t r = g.incl_scan(sw, &tot) - sw;
-        for (int w = w0; w < w1; ++w) {
-          const int pw = pidx(w);
-          pre[pw] = (uint16_t)r;
-          r += __popc(bm[pw]);
+        constexpr int NWV = WIN_BLOCK / WAVE;
+        const int lane = lane_id(), wv = t / WAVE;
+        const int cw = (nw + NWV * WAVE - 1) / (NWV * WAVE) * WAVE;
+        const int a0 = wv * cw, a1 = min(nw, a0 + cw);
+        uint32_t sw = 0;
+        for (int w = a0 + lane; w < a1; w += WAVE) sw += __popc(bw[w].x);
+        sw = wave_sum(sw);
+        if (lane == 0) g.red[wv] = sw;
+        __syncthreads();
+        uint32_t carry = 0;
+        for (int i = 0; i < wv; ++i) carry += (uint32_t)g.red[i];
+        for (int b = a0; b < a1; b += WAVE) {
+          const int w = b + lane;
+          const uint32_t c = w < a1 ? __popc(bw[w].x) : 0u;
+          const uint32_t incl = wave_incl_scan(c);
+          if (w < a1) bw[w].y = carry + incl - c;
+          carry += wave_last(incl);
         }
         __syncthreads();
       };
@@ -1280,7 +1284,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         store_stream(&out.cval[base + kk], vals[kk]);
         vals[kk] = 0.f;
       }
-      for (int w = t; w < nw; w += WIN_BLOCK) bm[pidx(w)] = 0u;
+      for (int w = t; w < nw; w += WIN_BLOCK) bw[w].x = 0u;
     }
   }
 }
