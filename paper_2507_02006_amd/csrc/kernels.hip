@@ -1131,17 +1131,10 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         for (int w = t; w < nw; w += WIN_BLOCK) bw[w].x = wp.bm_cache[cached + w];
         __syncthreads();
       };
-      // the term that finds its column's slot still at +0 (the first one,
-      // and any that follow a sum of exactly zero) writes the column id at
-      // the column's rank, so no pass over the bitmap is needed for C's
-      // columns
       auto add_at_rank = [&](int j, float v) {
         const uint2 e = bw[j >> 5];
         const int rk = (int)e.y + __popc(e.x & ((1u << (j & 31)) - 1u));
-        if (rk < n) {
-          const float old = lds_add<false>(&vals[rk], v);
-          if (old == 0.f) out.ccol[base + rk] = c0 + j;
-        }
+        if (rk < n) lds_add<false>(&vals[rk], v);
       };
       // exclusive popcount prefix over the window's words: each wavefront
       // takes a contiguous share, its lanes consecutive words, with one
@@ -1279,12 +1272,30 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
                                                       [&](int j, float v) { add_at_rank(j - c0, v); });
       }
       __syncthreads();
-      // values out (coalesced); clear the window's bitmap and values
-      for (int kk = t; kk < n; kk += WIN_BLOCK) {
-        store_stream(&out.cval[base + kk], vals[kk]);
-        vals[kk] = 0.f;
+      // values out (coalesced); then the value slots take the column ids,
+      // written at their ranks from the bitmap words (a thread per word),
+      // and go out coalesced too: C's column array is written in whole
+      // lines rather than an entry at a time from the add loops
+      for (int kk = t; kk < n; kk += WIN_BLOCK) store_stream(&out.cval[base + kk], vals[kk]);
+      __syncthreads();
+      int32_t* cid = reinterpret_cast<int32_t*>(vals);
+      for (int w = t; w < nw; w += WIN_BLOCK) {
+        const uint2 e = bw[w];
+        uint32_t b = e.x;
+        int r = (int)e.y;
+        const int cw = c0 + (w << 5);
+        while (b) {
+          if (r < n) cid[r] = cw + __builtin_ctz(b);
+          ++r;
+          b &= b - 1u;
+        }
+        bw[w].x = 0u;
       }
-      for (int w = t; w < nw; w += WIN_BLOCK) bw[w].x = 0u;
+      __syncthreads();
+      for (int kk = t; kk < n; kk += WIN_BLOCK) {
+        store_stream(&out.ccol[base + kk], cid[kk]);
+        cid[kk] = 0;  // the bits of +0.0f: the slots are clear for the next window
+      }
     }
   }
 }
