@@ -48,10 +48,12 @@ aires_status fail(aires_status s, const char* fmt, ...) {
 
 constexpr int64_t kDenseWaveMaxN = 2048;     // widest dense row one wavefront holds
 constexpr int64_t kDenseMaxCols = 16384;     // widest dense row a workgroup holds
-constexpr int64_t kGrainCols = 8192;         // column grain of wide products
-constexpr int64_t kWindowMaxGrains = 16;     // grains one window may span
-constexpr int64_t kWindowMaxEntries = 8192;  // C entries one window may hold
-constexpr int64_t kCountGrains = 32;         // grains one symbolic item covers
+// Wide products: the window sizes keep a numeric workgroup's LDS at 52 KB,
+// so three 512-thread workgroups (24 wavefronts) share a CU.
+constexpr int64_t kGrainCols = 4096;         // column grain of wide products
+constexpr int64_t kWindowMaxGrains = 14;     // grains one window may span
+constexpr int64_t kWindowMaxEntries = 6144;  // C entries one window may hold
+constexpr int64_t kCountGrains = 64;         // grains one symbolic item covers
 constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps kept for heavy rows
 constexpr int64_t kKeepBitmapProducts = 65536;           // rows above this many products keep them
 constexpr int64_t kWaveMaxProducts = 8192;   // rows up to this go to one wavefront
@@ -384,7 +386,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     if (p->G < 32 || p->G % 32 || p->G > (1 << 20) || p->win_entries < p->G || p->win_entries > 65535 ||
         p->win_grains < 1 || p->count_grains < 1 ||
         kern::window_numeric_lds(p->win_grains, p->win_entries, p->G) > kern::kMaxLds ||
-        kern::grain_count_lds(p->count_grains, p->G) > kern::kMaxLds || p->nG > 65535) {
+        kern::grain_count_lds(p->count_grains, p->G) > kern::kMaxLds || p->nG > 65535 ||
+        (int64_t)p->count_grains * p->G * kern::group_size(kern::KIND_WINDOWS) >= (int64_t(1) << 31)) {
       aires_status st = fail(AIRES_E_INVALID_ARG,
                              "window options out of range (grain %d, windows of %d grains / %d entries, "
                              "%d grains per count item, %d grains)",

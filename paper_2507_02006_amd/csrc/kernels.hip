@@ -146,6 +146,28 @@ struct Group {
     incl_scan(v, &tot);
     return tot;
   }
+  // the same for 32-bit values whose group sum fits 32 bits
+  __device__ __forceinline__ int32_t incl_scan32(int32_t v, int32_t* total) const {
+    int32_t x = wave_incl_scan(v);
+    if constexpr (GROUP == WAVE) {
+      *total = wave_last(x);
+      return x;
+    } else {
+      const int w = threadIdx.x / WAVE;
+      if (lane_id() == WAVE - 1) red[w] = x;
+      __syncthreads();
+      int32_t pre = 0, tot = 0;
+#pragma unroll
+      for (int i = 0; i < NWAVES; ++i) {
+        const int32_t s = (int32_t)red[i];
+        pre += (i < w) ? s : 0;
+        tot += s;
+      }
+      __syncthreads();
+      *total = tot;
+      return x + pre;
+    }
+  }
 };
 
 // C is written once and not read back by the kernels: stream it past the
@@ -433,10 +455,12 @@ __device__ __forceinline__ int wave_share(int rn, int nw) {
 // chunk's segments; a run of up to GROUP * SEG_PER_THREAD terms is split
 // into equal contiguous parts, one per wavefront, whose lane l takes terms
 // l, l + WAVE, ..., so consecutive lanes read consecutive entries of a B row.
-template <int GROUP, int BLOCK, bool NUM, typename CH, typename SEG, typename F>
+// P32: B positions fit 32 bits (wide products, nnz(B) < 2^31).
+template <int GROUP, int BLOCK, bool NUM, bool P32 = false, typename CH, typename SEG, typename F>
 __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group<GROUP, BLOCK>& g,
                                                  CH& ch, int64_t p0, int64_t p1, const SEG& seg, F&& f) {
   using S = typename CH::shift_t;
+  using PI = std::conditional_t<P32, int32_t, int64_t>;
   constexpr int RUN = GROUP * SEG_PER_THREAD;
   constexpr int WR = WAVE * SEG_PER_THREAD;  // terms of one wavefront per run
   const int t = g.t();
@@ -452,16 +476,16 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
       if constexpr (NUM) av = op.aval[p];
       seg(k, lo, len);
     }
-    int64_t total;
-    const int64_t incl = g.incl_scan(len, &total);
-    const int64_t excl = incl - len;
+    int32_t total;  // a chunk holds fewer than 2^31 terms
+    const int32_t incl = g.incl_scan32((int32_t)len, &total);
+    const int32_t excl = incl - (int32_t)len;
     ch.rec[t].shift = (S)(lo - excl);
     ch.rec[t].av = av;
-    ch.ex[t] = (int32_t)excl;
-    if (t == 0) ch.ex[GROUP] = (int32_t)total;
+    ch.ex[t] = excl;
+    if (t == 0) ch.ex[GROUP] = total;
     g.sync();
     const int nk = (int)((p1 - cb) < GROUP ? (p1 - cb) : GROUP);
-    for (int64_t r0 = 0; r0 < total; r0 += RUN) {
+    for (int32_t r0 = 0; r0 < total; r0 += RUN) {
       const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
       const int per = wave_share(rn, GROUP / WAVE);
       const int wlo = w * per;
@@ -470,7 +494,7 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
       const int base = (int)r0 + wlo;
       wave_seg_map(ch.ex, nk, base, wlen, seg_w);
       for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
-        int64_t pos[UNROLL];
+        PI pos[UNROLL];
         float am[UNROLL];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
@@ -479,7 +503,7 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
           am[u] = 0.f;
           if (q < wlen) {
             const typename CH::Rec rc = ch.rec[seg_w[q]];
-            pos[u] = (int64_t)rc.shift + base + q;
+            pos[u] = (PI)rc.shift + base + q;
             am[u] = rc.av;
           }
         }
@@ -504,12 +528,12 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
 }
 
 // ... over the terms of A entries [p0, p1); the whole row:
-template <typename RA, int GROUP, int BLOCK, bool NUM, typename CH, typename SEG, typename F>
+template <typename RA, int GROUP, int BLOCK, bool NUM, bool P32 = false, typename CH, typename SEG, typename F>
 __device__ __forceinline__ void for_each_term(const Operands& op, const Group<GROUP, BLOCK>& g,
                                               CH& ch, int64_t row, const SEG& seg, F&& f) {
   const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
   const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
-  for_each_term_in<GROUP, BLOCK, NUM>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
+  for_each_term_in<GROUP, BLOCK, NUM, P32>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
 }
 
 // -------------------------------------------------- dense path (narrow N)
@@ -940,7 +964,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
     const int g1 = min((int)op.nG, g0 + SG);
     const int c0 = g0 * op.G;
     const GrainRange seg{op.bidx, op.nG + 1, g0, g1};
-    for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg, [&](int j, float) {
+    for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true>(op, g, ch, row, seg, [&](int j, float) {
       j -= c0;
       atomicOr(&bm[pidx(j >> 5)], 1u << (j & 31));
     });
@@ -1062,7 +1086,7 @@ __host__ __device__ constexpr size_t window_lds_bytes(int max_grains, int max_en
 // passes over the B segments (one when the symbolic bitmap was kept),
 // keeping the row's state in LDS.
 template <typename RA, typename RB>
-__global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, const BinView bv,
+__global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, const BinView bv,
                                                            const WindowParams wp, const Outputs out) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t s_row;
@@ -1094,25 +1118,25 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
     const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
     const int64_t rbase = out.crp[row];
     const bool short_row = (p1 - p0) <= WIN_BLOCK;
-    int64_t k = -1;
+    int32_t k = -1;  // B positions of a wide product fit 32 bits (nnz(B) < 2^31)
     float a = 0.f;
     if (short_row && p0 + t < p1) {
       k = op.acol[p0 + t];
       a = op.aval[p0 + t];
     }
-    int64_t cur = 0, nxt_hi = 0;
+    int32_t cur = 0, nxt_hi = 0;
     int prev_g1 = -1;
     WinItem nextI{};
     if (i0 < i1) {
       nextI = wp.items[i0];
-      if (k >= 0) nxt_hi = op.bidx[k * (op.nG + 1) + nextI.g1];
+      if (k >= 0) nxt_hi = op.bidx[(int64_t)k * (op.nG + 1) + nextI.g1];
     }
     for (int64_t it = i0; it < i1; ++it) {
       const WinItem I = nextI;
-      const int64_t hi = nxt_hi;
+      const int32_t hi = nxt_hi;
       if (it + 1 < i1) {  // next window's header and segment ends, in flight meanwhile
         nextI = wp.items[it + 1];
-        if (k >= 0) nxt_hi = op.bidx[k * (op.nG + 1) + nextI.g1];
+        if (k >= 0) nxt_hi = op.bidx[(int64_t)k * (op.nG + 1) + nextI.g1];
       }
       const int g0 = I.g0, g1 = I.g1, n = I.n;
       const int c0 = g0 * op.G;
@@ -1161,11 +1185,11 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         __syncthreads();
       };
       if (short_row) {
-        if (k >= 0 && g0 != prev_g1) cur = op.bidx[k * (op.nG + 1) + g0];
-        const int64_t len = (k >= 0) ? hi - cur : 0;
-        int64_t total;
-        const int64_t incl = g.incl_scan(len, &total);
-        const int64_t excl = incl - len;
+        if (k >= 0 && g0 != prev_g1) cur = op.bidx[(int64_t)k * (op.nG + 1) + g0];
+        const int32_t len = (k >= 0) ? hi - cur : 0;
+        int32_t total;
+        const int32_t incl = g.incl_scan32(len, &total);
+        const int32_t excl = incl - len;
         ch.rec[t].shift = (RB)(cur - excl);
         ch.rec[t].av = a;
         ch.ex[t] = (int32_t)excl;
@@ -1191,7 +1215,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
             vv[i] = 0.f;
             if (q < wlen) {
               const typename CH::Rec rc = ch.rec[seg_w[q]];
-              const int64_t pos = (int64_t)rc.shift + wlo + q;
+              const int32_t pos = (int32_t)rc.shift + wlo + q;
               jj[i] = op.bcol[pos] - c0;
               vv[i] = rc.av * op.bval[pos];
             }
@@ -1212,7 +1236,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
             word_ranks();
           }
           for (int pass = cached >= 0 ? 1 : 0; pass < 2; ++pass) {
-            for (int64_t r0 = 0; r0 < total; r0 += RUN) {
+            for (int32_t r0 = 0; r0 < total; r0 += RUN) {
               const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
               const int per = wave_share(rn, WIN_BLOCK / WAVE);
               const int wlo = wi * per;
@@ -1221,7 +1245,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
               const int base = (int)r0 + wlo;
               wave_seg_map(ch.ex, nk, base, wlen, seg_w);
               for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
-                int64_t pos[UNROLL];
+                int32_t pos[UNROLL];
                 float am[UNROLL];
 #pragma unroll
                 for (int u = 0; u < UNROLL; ++u) {
@@ -1230,7 +1254,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
                   am[u] = 0.f;
                   if (q < wlen) {
                     const typename CH::Rec rc = ch.rec[seg_w[q]];
-                    pos[u] = (int64_t)rc.shift + base + q;
+                    pos[u] = (int32_t)rc.shift + base + q;
                     am[u] = rc.av;
                   }
                 }
@@ -1265,11 +1289,11 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_win_rows(const Operands op, co
         if (cached >= 0)
           load_bits();
         else
-          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false>(op, g, ch, row, seg,
-                                                         [&](int j, float) { set_bit(j - c0); });
+          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true>(op, g, ch, row, seg,
+                                                               [&](int j, float) { set_bit(j - c0); });
         word_ranks();
-        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true>(op, g, ch, row, seg,
-                                                      [&](int j, float v) { add_at_rank(j - c0, v); });
+        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true>(op, g, ch, row, seg,
+                                                            [&](int j, float v) { add_at_rank(j - c0, v); });
       }
       __syncthreads();
       // values out (coalesced); then the value slots take the column ids,
