@@ -142,11 +142,11 @@ typedef struct aires_plan_opts {
                                    products are handled by one wavefront   */
     /* Wide products (N > dense_max_cols) cut columns into grains and rows
        into windows of whole grains; 0 = default for each.                 */
-    int64_t window_grain_cols;  /* grain width, multiple of 32 (8192)      */
-    int64_t window_max_grains;  /* grains one window may span (16)         */
+    int64_t window_grain_cols;  /* grain width, multiple of 32 (4096)      */
+    int64_t window_max_grains;  /* grains one window may span (64)         */
     int64_t window_max_entries; /* C entries one window may hold, in
-                                   [grain, 65535] (8192)                   */
-    int64_t count_grains;       /* grains one symbolic item covers (32)    */
+                                   [grain, 65535] (16384)                  */
+    int64_t count_grains;       /* grains one symbolic item covers (64)    */
     int64_t keep_bitmap_products; /* 0: default (65536), < 0: never.  The
                                    symbolic phase keeps the presence bitmaps
                                    of rows with more products than this for
@@ -158,6 +158,10 @@ typedef struct aires_plan_opts {
     int64_t split_max_rows;     /* 0: default.  Cap on the rows given dense
                                    slots for splitting; further rows of the
                                    split bin take one workgroup each       */
+    int64_t window_pool_bytes;  /* 0: default (38912).  LDS a window's
+                                   bitmap (8 bytes per 32 columns) and
+                                   values (4 bytes per entry) share; must
+                                   hold one full grain                     */
 } aires_plan_opts;
 
 /* Fill *o with defaults (struct_size set, validate 0, C on device). */

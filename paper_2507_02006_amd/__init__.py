@@ -65,7 +65,7 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
               hash_max_products: int = 0, wave_max_products: int = 0, window_grain_cols: int = 0,
               window_max_grains: int = 0, window_max_entries: int = 0, count_grains: int = 0,
               keep_bitmap_products: int = 0, split_min_products: int = 0, split_max_rows: int = 0,
-              torch_allocator: bool = True, device: int = 0) -> Plan:
+              window_pool_bytes: int = 0, torch_allocator: bool = True, device: int = 0) -> Plan:
     lib = B_.load()
     a = B_.make_csr(*_parts(A))
     b = B_.make_csr(*_parts(B))
@@ -88,6 +88,7 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
     o.keep_bitmap_products = keep_bitmap_products
     o.split_min_products = split_min_products
     o.split_max_rows = split_max_rows
+    o.window_pool_bytes = window_pool_bytes
     alloc = None
     if torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
         alloc = B_.TorchAllocator(device)

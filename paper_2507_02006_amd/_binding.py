@@ -55,7 +55,7 @@ class PlanOpts(ctypes.Structure):
                 ("hash_max_products", c_i64), ("wave_max_products", c_i64), ("window_grain_cols", c_i64),
                 ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64),
                 ("keep_bitmap_products", c_i64), ("split_min_products", c_i64),
-                ("split_max_rows", c_i64)]
+                ("split_max_rows", c_i64), ("window_pool_bytes", c_i64)]
 
 
 class PlanInfo(ctypes.Structure):

@@ -48,11 +48,13 @@ aires_status fail(aires_status s, const char* fmt, ...) {
 
 constexpr int64_t kDenseWaveMaxN = 2048;     // widest dense row one wavefront holds
 constexpr int64_t kDenseMaxCols = 16384;     // widest dense row a workgroup holds
-// Wide products: the window sizes keep a numeric workgroup's LDS at 52 KB,
-// so three 512-thread workgroups (24 wavefronts) share a CU.
+// Wide products: a window's bitmap and values share a pool of LDS sized so
+// that a numeric workgroup uses 52 KB and three 512-thread workgroups (24
+// wavefronts) share a CU; the grain and entry caps rarely bind.
 constexpr int64_t kGrainCols = 4096;         // column grain of wide products
-constexpr int64_t kWindowMaxGrains = 14;     // grains one window may span
-constexpr int64_t kWindowMaxEntries = 6144;  // C entries one window may hold
+constexpr int64_t kWindowMaxGrains = 64;     // grains one window may span
+constexpr int64_t kWindowMaxEntries = 16384; // C entries one window may hold
+constexpr int64_t kWindowPoolBytes = 38912;  // LDS shared by a window's bitmap and values
 constexpr int64_t kCountGrains = 64;         // grains one symbolic item covers
 constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps kept for heavy rows
 constexpr int64_t kKeepBitmapProducts = 65536;           // rows above this many products keep them
@@ -145,7 +147,7 @@ struct aires_plan {
   kern::BinThresholds th;
   int wide = 0;
   int32_t G = 0, nG = 0;           // column grains (wide products)
-  int32_t win_grains = 0, win_entries = 0, count_grains = 0;
+  int32_t win_grains = 0, win_entries = 0, count_grains = 0, win_pool_words = 0;
   int32_t ngg = 0;                 // symbolic items per wide row (runs of count_grains grains)
   int64_t keep_bitmap = 0;         // rows with more products keep their symbolic bitmaps (-1: none)
   int split = 0;                   // narrow product with a split-row bin
@@ -210,6 +212,7 @@ void bin_plan(aires_plan* p) {
       p->win_entries = (int32_t)(o.window_max_entries > 0 ? o.window_max_entries
                                                           : std::max<int64_t>(kWindowMaxEntries, p->G));
       p->count_grains = (int32_t)(o.count_grains > 0 ? o.count_grains : kCountGrains);
+      p->win_pool_words = (int32_t)((o.window_pool_bytes > 0 ? o.window_pool_bytes : kWindowPoolBytes) / 4);
       p->ngg = (p->nG + p->count_grains - 1) / p->count_grains;
       p->keep_bitmap = o.keep_bitmap_products == 0 ? kKeepBitmapProducts : o.keep_bitmap_products;
     }
@@ -385,7 +388,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   if (p->wide) {
     if (p->G < 32 || p->G % 32 || p->G > (1 << 20) || p->win_entries < p->G || p->win_entries > 65535 ||
         p->win_grains < 1 || p->count_grains < 1 ||
-        kern::window_numeric_lds(p->win_grains, p->win_entries, p->G) > kern::kMaxLds ||
+        kern::window_numeric_lds(p->win_pool_words) > kern::kMaxLds ||
+        2 * (int64_t)(p->G / 32) + p->G > p->win_pool_words ||  // one full grain fits the pool
         kern::grain_count_lds(p->count_grains, p->G) > kern::kMaxLds || p->nG > 65535 ||
         (int64_t)p->count_grains * p->G * kern::group_size(kern::KIND_WINDOWS) >= (int64_t(1) << 31)) {
       aires_status st = fail(AIRES_E_INVALID_ARG,
@@ -682,6 +686,7 @@ kern::WindowParams window_params(const aires_plan* p, const TileWs& w) {
   wp.grains_per_count_item = p->count_grains;
   wp.max_grains = p->win_grains;
   wp.max_entries = p->win_entries;
+  wp.pool_words = p->win_pool_words;
   wp.item_count = w.icount;
   wp.items = w.items;
   wp.row_counter = w.wcounter;

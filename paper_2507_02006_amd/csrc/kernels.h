@@ -69,6 +69,7 @@ struct WindowParams {
   int32_t grains_per_count_item;  // grains one symbolic item covers (windows never straddle items)
   int32_t max_grains;      // grains one window may span
   int32_t max_entries;     // entries one window may hold (>= G)
+  int32_t pool_words;      // LDS words a window's bitmap (2 per bitmap word) and values (1 per entry) share
   int64_t* item_count;     // [1 + d]: windows of the d-th row of the bins; scanned into offsets
   WinItem* items;          // filled in the numeric sweep
   int32_t* row_counter;    // zeroed before the numeric launch (dynamic row scheduling)
@@ -118,7 +119,7 @@ hipError_t scan_inplace(int64_t* x, int64_t n, void* ws, hipStream_t s);
 
 size_t lds_bytes(int kind, int phase, int32_t W);
 size_t grain_count_lds(int sg, int G);
-size_t window_numeric_lds(int max_grains, int max_entries, int G);
+size_t window_numeric_lds(int pool_words);
 constexpr size_t kMaxLds = 160 * 1024;  // LDS of one gfx950 workgroup
 int group_size(int kind);
 

@@ -1018,14 +1018,18 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
 // entries, never across a symbolic item boundary, a multiple of sg grains);
 // empty windows are skipped.  Calls f(g0, g1, n, roff).
 template <typename F>
-__device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, int max_grains, int max_entries,
-                                                int sg, F&& f) {
+__device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, const WindowParams& wp, int wpg, F&& f) {
+  const int sg = wp.grains_per_count_item;
   int64_t roff = 0;
   int g0 = 0;
   while (g0 < nG) {
     int n = gc[g0];
     int g1 = g0 + 1;
-    while (g1 < nG && g1 - g0 < max_grains && g1 % sg != 0 && n + gc[g1] <= max_entries) n += gc[g1++];
+    // the window's bitmap (two words per bitmap word: bits and rank) and its
+    // values share the LDS pool
+    while (g1 < nG && g1 - g0 < wp.max_grains && g1 % sg != 0 && n + gc[g1] <= wp.max_entries &&
+           2 * (g1 + 1 - g0) * wpg + n + gc[g1] <= wp.pool_words)
+      n += gc[g1++];
     if (n > 0) f(g0, g1, n, roff);
     roff += n;
     g0 = g1;
@@ -1033,27 +1037,25 @@ __device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, int m
   return roff;
 }
 
-__global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, const WindowParams wp,
+__global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, int32_t wpg, const WindowParams wp,
                                                   int64_t* counts) {
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t nwin = 0;
-    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries, wp.grains_per_count_item,
-                               [&](int, int, int, int64_t) { ++nwin; });
+    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp, wpg, [&](int, int, int, int64_t) { ++nwin; });
     wp.item_count[1 + d] = nwin;
   }
 }
 
-__global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, const WindowParams wp) {
+__global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, int32_t wpg, const WindowParams wp) {
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t o = wp.item_count[d];  // scanned: windows of the rows before d
-    plan_windows(wp.gcnt + row * nG, nG, wp.max_grains, wp.max_entries, wp.grains_per_count_item,
-                 [&](int g0, int g1, int n, int64_t roff) {
+    plan_windows(wp.gcnt + row * nG, nG, wp, wpg, [&](int g0, int g1, int n, int64_t roff) {
                    WinItem w;
                    w.row = (int32_t)row;
                    w.g0 = (uint16_t)g0;
@@ -1065,14 +1067,14 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
   }
 }
 
-// A window's LDS: per bitmap word its presence bits and the rank of its
-// first set bit, side by side (a term's rank is one 8-byte read); the
-// window's fp32 values; the chunk.
+// A window's LDS: a pool holding, per bitmap word, its presence bits and
+// the rank of its first set bit side by side (a term's rank is one 8-byte
+// read), followed by the window's fp32 values (a wide window with few
+// entries and a narrow one with many use the same pool); then the chunk.
 
 template <typename S>
-__host__ __device__ constexpr size_t window_lds_bytes(int max_grains, int max_entries, int G) {
-  return align16((size_t)max_grains * (G / 32) * 8) + align16((size_t)max_entries * 4) +
-         align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128 + 16;  // + the static row slot
+__host__ __device__ constexpr size_t window_lds_bytes(int pool_words) {
+  return align16((size_t)pool_words * 4) + align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128 + 16;  // + the static row slot
 }
 
 // Numeric phase of wide rows.  Workgroups take rows from a shared counter
@@ -1091,16 +1093,13 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t s_row;
   const int WPG = op.G / 32;
-  const int maxw = wp.max_grains * WPG;
   uint2* bw = reinterpret_cast<uint2*>(smem);  // (presence bits, rank of the word's first bit)
-  float* vals = reinterpret_cast<float*>(smem + align16((size_t)maxw * 8));
   using CH = Chunk<WIN_BLOCK, RB>;
-  CH& ch = *reinterpret_cast<CH*>(reinterpret_cast<unsigned char*>(vals) + align16((size_t)wp.max_entries * 4));
+  CH& ch = *reinterpret_cast<CH*>(smem + align16((size_t)wp.pool_words * 4));
   Group<WIN_BLOCK, WIN_BLOCK> g;
   g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
   const int t = threadIdx.x;
-  for (int i = t; i < maxw; i += WIN_BLOCK) bw[i] = make_uint2(0u, 0u);
-  for (int i = t; i < wp.max_entries; i += WIN_BLOCK) vals[i] = 0.f;
+  for (int i = t; i < wp.pool_words; i += WIN_BLOCK) reinterpret_cast<uint32_t*>(smem)[i] = 0u;  // pool clear
   constexpr int RUN = WIN_BLOCK * SEG_PER_THREAD;
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
@@ -1141,6 +1140,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       const int g0 = I.g0, g1 = I.g1, n = I.n;
       const int c0 = g0 * op.G;
       const int nw = (g1 - g0) * WPG;
+      float* vals = reinterpret_cast<float*>(bw + nw);  // the values follow this window's bitmap
       const int64_t base = rbase + I.roff;
       auto set_bit = [&](int j) { atomicOr(&bw[j >> 5].x, 1u << (j & 31)); };
       // Heavy rows: the symbolic phase kept the window's bitmap.
@@ -1313,7 +1313,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
           ++r;
           b &= b - 1u;
         }
-        bw[w].x = 0u;
+        bw[w] = make_uint2(0u, 0u);  // ranks too: the next window's values may lie here
       }
       __syncthreads();
       for (int kk = t; kk < n; kk += WIN_BLOCK) {
@@ -1547,7 +1547,7 @@ hipError_t win_symbolic_t(const Operands& op, const BinView& bv, const WindowPar
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WIN_BLOCK), lds, s, op, bv, wp);
   int64_t pg = (ub_rows + 255) / 256;
   if (pg > 8192) pg = 8192;
-  hipLaunchKernelGGL(k_win_plan, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, wp, out.counts);
+  hipLaunchKernelGGL(k_win_plan, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, op.G / 32, wp, out.counts);
   return hipGetLastError();
 }
 
@@ -1556,12 +1556,12 @@ hipError_t win_numeric_t(const Operands& op, const BinView& bv, const WindowPara
                          const Outputs& out, int64_t ub_rows, int64_t nitems, hipStream_t s) {
   int64_t pg = (ub_rows + 255) / 256;
   if (pg > 8192) pg = 8192;
-  hipLaunchKernelGGL(k_win_fill, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, wp);
+  hipLaunchKernelGGL(k_win_fill, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, op.G / 32, wp);
   if (nitems <= 0) return hipGetLastError();
   hipError_t ez = hipMemsetAsync(wp.row_counter, 0, sizeof(int32_t), s);
   if (ez != hipSuccess) return ez;
   auto kern = k_win_rows<RA, RB>;
-  const size_t lds = window_lds_bytes<RB>(wp.max_grains, wp.max_entries, op.G);
+  const size_t lds = window_lds_bytes<RB>(wp.pool_words);
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -1675,8 +1675,8 @@ size_t lds_bytes(int kind, int phase, int32_t W) {
 }
 
 size_t grain_count_lds(int sg, int G) { return count_lds_bytes<int64_t>(sg, G); }
-size_t window_numeric_lds(int max_grains, int max_entries, int G) {
-  return window_lds_bytes<int64_t>(max_grains, max_entries, G);
+size_t window_numeric_lds(int pool_words) {
+  return window_lds_bytes<int64_t>(pool_words);
 }
 
 int group_size(int kind) {

@@ -95,6 +95,11 @@ PATHS = {
                                   window_max_grains=1, window_max_entries=128, count_grains=1),
     "hash8192_then_windows": dict(dense_max_cols=160, hash_max_products=4096, window_grain_cols=96,
                                   window_max_grains=4, window_max_entries=200, count_grains=5),
+    # windows cut by the shared LDS pool (bitmap words + values), not by the
+    # grain or entry caps: a wide sparse window or a narrow dense one
+    "windows_pool": dict(dense_max_cols=64, hash_max_products=-1, window_grain_cols=64,
+                         window_max_grains=16, window_max_entries=1000, count_grains=8,
+                         window_pool_bytes=4 * 100),
     # 2048 < N <= 16384 handled as narrow: hash bins then workgroup dense rows
     "narrow_block_hash": dict(dense_max_cols=200, hash_max_products=512),
     # narrow rows split over workgroups (dense slots in global memory); then
