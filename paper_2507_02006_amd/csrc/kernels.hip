@@ -1179,7 +1179,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
           const int w = b + lane;
           const uint32_t c = w < a1 ? __popc(bw[w].x) : 0u;
           const uint32_t incl = wave_incl_scan(c);
-          if (w < a1) bw[w].y = carry + incl - c;
+          if (c) bw[w].y = carry + incl - c;  // only set bits are ranked: empty words stay all zero
           carry += wave_last(incl);
         }
         __syncthreads();
@@ -1306,13 +1306,14 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       for (int w = t; w < nw; w += WIN_BLOCK) {
         const uint2 e = bw[w];
         uint32_t b = e.x;
+        if (!b) continue;  // an empty word holds no rank either
         int r = (int)e.y;
         const int cw = c0 + (w << 5);
-        while (b) {
+        do {
           if (r < n) cid[r] = cw + __builtin_ctz(b);
           ++r;
           b &= b - 1u;
-        }
+        } while (b);
         bw[w] = make_uint2(0u, 0u);  // ranks too: the next window's values may lie here
       }
       __syncthreads();
