@@ -734,26 +734,16 @@ struct HashLds {
   int64_t red[GROUP / WAVE + 1];
 };
 
-// Bitonic network over SORT_RUN (key, value) pairs held in registers.
-constexpr int SORT_RUN = 16;
-__device__ __forceinline__ void sort_run(int32_t (&k)[SORT_RUN], float (&v)[SORT_RUN]) {
-#pragma unroll
-  for (int size = 2; size <= SORT_RUN; size <<= 1) {
-#pragma unroll
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-#pragma unroll
-      for (int i = 0; i < SORT_RUN; ++i) {
-        const int l = i ^ stride;
-        if (l > i) {
-          const bool up = (i & size) == 0;
-          if ((k[i] > k[l]) == up) {
-            const int32_t tk = k[i]; k[i] = k[l]; k[l] = tk;
-            const float tv = v[i]; v[i] = v[l]; v[l] = tv;
-          }
-        }
-      }
-    }
-  }
+// Buckets for ordering a hash row's columns: as many as the chunk's segment
+// maps hold as 32-bit counters (at most 1024), each 2^shift consecutive
+// columns wide so that NB buckets cover [0, N).
+__host__ __device__ constexpr int bucket_count(int group) {
+  return group * SEG_PER_THREAD / 2 < 1024 ? group * SEG_PER_THREAD / 2 : 1024;
+}
+__device__ __forceinline__ int bucket_shift(int64_t N, int nb) {
+  int sh = 0;
+  while (((N - 1) >> sh) >= nb) ++sh;
+  return sh;
 }
 
 template <int TABLE>
@@ -764,8 +754,8 @@ __device__ __forceinline__ uint32_t hslot(int j) {
 
 // Light rows of wide products: open addressing keyed by column (linear
 // probing, load <= 1/2 since nnz(C_i) <= P_i <= TABLE/2), then the occupied
-// slots are compacted and sorted: runs of 16 in registers, then merge-path
-// rounds between the two halves of the table.
+// slots are compacted and put in column order by bucket counts and a rank
+// within each bucket (a handful of columns per bucket).
 template <typename RA, typename RB, int TABLE, int GROUP, int BLOCK, bool NUM>
 __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView bv,
                                                 const Outputs out) {
@@ -826,59 +816,76 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
       for (int s = 0; s < SPT; ++s)
         if (kk[s] != -1) { L.key[o] = kk[s]; L.val[o] = vv[s]; ++o; }
       g.sync();
-      // sort the n compacted pairs by column: runs of SORT_RUN pairs sorted
-      // in registers, then merge-path rounds between the two halves of the
-      // table (n <= TABLE / 2)
-      const int npad = (int)((n + SORT_RUN - 1) / SORT_RUN) * SORT_RUN;
-      int32_t* ksrc = L.key;
-      float* vsrc = L.val;
-      int32_t* kdst = L.key + TABLE / 2;
-      float* vdst = L.val + TABLE / 2;
-      for (int p0 = t * SORT_RUN; p0 < npad; p0 += GROUP * SORT_RUN) {
-        int32_t rk[SORT_RUN];
-        float rv[SORT_RUN];
+      // order the n compacted pairs by column (the columns are distinct):
+      // count them into NB buckets of consecutive columns, place each pair
+      // in its bucket's range of the upper half of the table, then give it
+      // the rank start(bucket) + (pairs of the bucket with a smaller
+      // column) in the lower half (n <= TABLE / 2)
+      constexpr int NB = bucket_count(GROUP);
+      constexpr int EPT = (TABLE / 2 + GROUP - 1) / GROUP;  // pairs per thread
+      int32_t* cnt = reinterpret_cast<int32_t*>(L.ch.seg);   // the chunk's maps are free now
+      const int shift = bucket_shift(op.N, NB);
+      for (int b = t; b < NB; b += GROUP) cnt[b] = 0;
+      g.sync();
+      int32_t ek[EPT];
+      float ev[EPT];
+      int es[EPT];
 #pragma unroll
-        for (int i = 0; i < SORT_RUN; ++i) {
-          const bool live = p0 + i < n;
-          rk[i] = live ? ksrc[p0 + i] : 0x7fffffff;
-          rv[i] = live ? vsrc[p0 + i] : 0.f;
-        }
-        sort_run(rk, rv);
-#pragma unroll
-        for (int i = 0; i < SORT_RUN; ++i) {
-          ksrc[p0 + i] = rk[i];
-          vsrc[p0 + i] = rv[i];
+      for (int e = 0; e < EPT; ++e) {
+        const int i = t + e * GROUP;
+        ek[e] = 0;
+        ev[e] = 0.f;
+        es[e] = -1;
+        if (i < n) {
+          ek[e] = L.key[i];
+          ev[e] = L.val[i];
+          es[e] = atomicAdd(&cnt[ek[e] >> shift], 1);
         }
       }
       g.sync();
-      for (int R = SORT_RUN; R < npad; R <<= 1) {
-        for (int p0 = t * SORT_RUN; p0 < npad; p0 += GROUP * SORT_RUN) {
-          const int lo = p0 / (2 * R) * (2 * R);
-          const int a0 = lo, la = min(R, npad - lo);
-          const int b0 = lo + la, lb = min(R, npad - b0);
-          const int d = p0 - lo;
-          // i = number of run-A pairs among the first d merged pairs
-          int i = max(0, d - lb), ihi = min(d, la);
-          while (i < ihi) {
-            const int mid = (i + ihi) >> 1;
-            if (ksrc[a0 + mid] <= ksrc[b0 + d - 1 - mid]) i = mid + 1; else ihi = mid;
-          }
-          int j = d - i;
-#pragma unroll 4
-          for (int q = 0; q < SORT_RUN; ++q) {
-            const int32_t ka = i < la ? ksrc[a0 + i] : 0x7fffffff;
-            const int32_t kb = j < lb ? ksrc[b0 + j] : 0x7fffffff;
-            const bool take_a = j >= lb || (i < la && ka <= kb);
-            kdst[p0 + q] = take_a ? ka : kb;
-            vdst[p0 + q] = take_a ? vsrc[a0 + i] : vsrc[b0 + j];
-            i += take_a;
-            j += !take_a;
-          }
+      {
+        constexpr int BPT = NB / GROUP > 0 ? NB / GROUP : 1;  // buckets per thread
+        int c[BPT];
+        int32_t sum = 0;
+#pragma unroll
+        for (int q = 0; q < BPT; ++q) {
+          const int b = t * BPT + q;
+          c[q] = b < NB ? cnt[b] : 0;
+          sum += c[q];
         }
-        g.sync();
-        int32_t* tk = ksrc; ksrc = kdst; kdst = tk;
-        float* tv = vsrc; vsrc = vdst; vdst = tv;
+        int32_t tot;
+        int32_t run = g.incl_scan32(sum, &tot) - sum;
+#pragma unroll
+        for (int q = 0; q < BPT; ++q) {
+          const int b = t * BPT + q;
+          if (b < NB) cnt[b] = run;
+          run += c[q];
+        }
       }
+      g.sync();
+      int32_t* hk = L.key + TABLE / 2;
+      float* hv = L.val + TABLE / 2;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e)
+        if (es[e] >= 0) {
+          const int d = cnt[ek[e] >> shift] + es[e];
+          hk[d] = ek[e];
+          hv[d] = ev[e];
+        }
+      g.sync();
+#pragma unroll
+      for (int e = 0; e < EPT; ++e)
+        if (es[e] >= 0) {
+          const int b = ek[e] >> shift;
+          const int s0 = cnt[b], s1 = b + 1 < NB ? cnt[b + 1] : (int)n;
+          int r = s0;
+          for (int q = s0; q < s1; ++q) r += hk[q] < ek[e];
+          L.key[r] = ek[e];
+          L.val[r] = ev[e];
+        }
+      g.sync();
+      const int32_t* ksrc = L.key;
+      const float* vsrc = L.val;
       const int64_t o0 = out.crp[row];
       for (int i = t; i < n; i += GROUP) {
         store_stream(&out.ccol[o0 + i], ksrc[i]);
