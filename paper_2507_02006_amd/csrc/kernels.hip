@@ -396,7 +396,9 @@ constexpr int UNROLL = AIRES_UNROLL;  // independent B loads each thread keeps i
 // lo < ex[nk]).  The segment holding lo is found with two ballots; each
 // later segment starting in the range writes its id at its first term and
 // a wavefront max-scan carries ids forward.  No workgroup barrier.
-__device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, int len, uint16_t* seg_w) {
+// Returns that segment when it holds the whole range (no map is written:
+// long B segments make this common), else -1.
+__device__ __forceinline__ int wave_seg_map(const int32_t* ex, int nk, int lo, int len, uint16_t* seg_w) {
   const int l = lane_id();
   wave_sync();  // the previous run's reads of seg_w are done
   const int stride = (nk + WAVE - 1) / WAVE;
@@ -406,6 +408,7 @@ __device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, 
   const int c2 = base + l;
   const uint64_t b2 = __ballot(l < stride && c2 < nk && ex[c2] <= lo);
   const int c0 = base + (63 - __clzll(b2));
+  if (ex[c0 + 1] >= lo + len) return c0;  // the whole range lies in segment c0: no map
   // each lane's SEG_PER_THREAD entries are moved as 16-byte vectors
   uint4* mine = reinterpret_cast<uint4*>(seg_w + l * SEG_PER_THREAD);
 #pragma unroll
@@ -442,6 +445,7 @@ __device__ __forceinline__ void wave_seg_map(const int32_t* ex, int nk, int lo, 
     mine[v] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
   }
   wave_sync();
+  return -1;
 }
 
 // Terms of a run of rn each of nw wavefronts takes: an equal share rounded
@@ -492,35 +496,44 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
       const int wlen = min(per, rn - wlo);
       if (wlen <= 0) continue;
       const int base = (int)r0 + wlo;
-      wave_seg_map(ch.ex, nk, base, wlen, seg_w);
-      for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
-        PI pos[UNROLL];
-        float am[UNROLL];
+      // the wavefront's terms, each with the record of its segment
+      auto terms = [&](auto rec_of) {
+        for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
+          PI pos[UNROLL];
+          float am[UNROLL];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-          const int q = q0 + u * WAVE;
-          pos[u] = -1;
-          am[u] = 0.f;
-          if (q < wlen) {
-            const typename CH::Rec rc = ch.rec[seg_w[q]];
-            pos[u] = (PI)rc.shift + base + q;
-            am[u] = rc.av;
+          for (int u = 0; u < UNROLL; ++u) {
+            const int q = q0 + u * WAVE;
+            pos[u] = -1;
+            am[u] = 0.f;
+            if (q < wlen) {
+              const typename CH::Rec rc = rec_of(q);
+              pos[u] = (PI)rc.shift + base + q;
+              am[u] = rc.av;
+            }
           }
-        }
-        int j[UNROLL];
-        float bv[UNROLL];
+          int j[UNROLL];
+          float bv[UNROLL];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-          j[u] = 0;
-          bv[u] = 0.f;
-          if (pos[u] >= 0) {
-            j[u] = op.bcol[pos[u]];
-            if constexpr (NUM) bv[u] = op.bval[pos[u]];
+          for (int u = 0; u < UNROLL; ++u) {
+            j[u] = 0;
+            bv[u] = 0.f;
+            if (pos[u] >= 0) {
+              j[u] = op.bcol[pos[u]];
+              if constexpr (NUM) bv[u] = op.bval[pos[u]];
+            }
           }
-        }
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u)
-          if (pos[u] >= 0) f(j[u], am[u] * bv[u]);
+          for (int u = 0; u < UNROLL; ++u)
+            if (pos[u] >= 0) f(j[u], am[u] * bv[u]);
+        }
+      };
+      const int one = wave_seg_map(ch.ex, nk, base, wlen, seg_w);
+      if (one >= 0) {
+        const typename CH::Rec r1 = ch.rec[one];
+        terms([&](int) { return r1; });
+      } else {
+        terms([&](int q) { return ch.rec[seg_w[q]]; });
       }
     }
     g.sync();
@@ -1212,20 +1225,28 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
           const int per = wave_share((int)total, WIN_BLOCK / WAVE);
           const int wlo = wi * per;
           const int wlen = min(per, (int)total - wlo);
-          if (wlen > 0) wave_seg_map(ch.ex, nk, wlo, wlen, seg_w);
+          const int one = wlen > 0 ? wave_seg_map(ch.ex, nk, wlo, wlen, seg_w) : -1;
           int jj[SEG_PER_THREAD];
           float vv[SEG_PER_THREAD];
+          auto load_terms = [&](auto rec_of) {
 #pragma unroll
-          for (int i = 0; i < SEG_PER_THREAD; ++i) {
-            const int q = lane + i * WAVE;
-            jj[i] = -1;
-            vv[i] = 0.f;
-            if (q < wlen) {
-              const typename CH::Rec rc = ch.rec[seg_w[q]];
-              const int32_t pos = (int32_t)rc.shift + wlo + q;
-              jj[i] = op.bcol[pos] - c0;
-              vv[i] = rc.av * op.bval[pos];
+            for (int i = 0; i < SEG_PER_THREAD; ++i) {
+              const int q = lane + i * WAVE;
+              jj[i] = -1;
+              vv[i] = 0.f;
+              if (q < wlen) {
+                const typename CH::Rec rc = rec_of(q);
+                const int32_t pos = (int32_t)rc.shift + wlo + q;
+                jj[i] = op.bcol[pos] - c0;
+                vv[i] = rc.av * op.bval[pos];
+              }
             }
+          };
+          if (one >= 0) {
+            const typename CH::Rec r1 = ch.rec[one];
+            load_terms([&](int) { return r1; });
+          } else {
+            load_terms([&](int q) { return ch.rec[seg_w[q]]; });
           }
 #pragma unroll
           for (int i = 0; i < SEG_PER_THREAD; ++i)
@@ -1250,38 +1271,46 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
               const int wlen = min(per, rn - wlo);
               if (wlen <= 0) continue;
               const int base = (int)r0 + wlo;
-              wave_seg_map(ch.ex, nk, base, wlen, seg_w);
-              for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
-                int32_t pos[UNROLL];
-                float am[UNROLL];
+              auto terms = [&](auto rec_of) {
+                for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
+                  int32_t pos[UNROLL];
+                  float am[UNROLL];
 #pragma unroll
-                for (int u = 0; u < UNROLL; ++u) {
-                  const int q = q0 + u * WAVE;
-                  pos[u] = -1;
-                  am[u] = 0.f;
-                  if (q < wlen) {
-                    const typename CH::Rec rc = ch.rec[seg_w[q]];
-                    pos[u] = (int32_t)rc.shift + base + q;
-                    am[u] = rc.av;
+                  for (int u = 0; u < UNROLL; ++u) {
+                    const int q = q0 + u * WAVE;
+                    pos[u] = -1;
+                    am[u] = 0.f;
+                    if (q < wlen) {
+                      const typename CH::Rec rc = rec_of(q);
+                      pos[u] = (int32_t)rc.shift + base + q;
+                      am[u] = rc.av;
+                    }
+                  }
+                  int jv[UNROLL];
+                  float bv2[UNROLL];
+#pragma unroll
+                  for (int u = 0; u < UNROLL; ++u) {
+                    jv[u] = 0;
+                    bv2[u] = 0.f;
+                    if (pos[u] >= 0) {
+                      jv[u] = op.bcol[pos[u]] - c0;
+                      if (pass) bv2[u] = op.bval[pos[u]];
+                    }
+                  }
+#pragma unroll
+                  for (int u = 0; u < UNROLL; ++u) {
+                    if (pos[u] < 0) continue;
+                    if (pass) add_at_rank(jv[u], am[u] * bv2[u]);
+                    else set_bit(jv[u]);
                   }
                 }
-                int jv[UNROLL];
-                float bv2[UNROLL];
-#pragma unroll
-                for (int u = 0; u < UNROLL; ++u) {
-                  jv[u] = 0;
-                  bv2[u] = 0.f;
-                  if (pos[u] >= 0) {
-                    jv[u] = op.bcol[pos[u]] - c0;
-                    if (pass) bv2[u] = op.bval[pos[u]];
-                  }
-                }
-#pragma unroll
-                for (int u = 0; u < UNROLL; ++u) {
-                  if (pos[u] < 0) continue;
-                  if (pass) add_at_rank(jv[u], am[u] * bv2[u]);
-                  else set_bit(jv[u]);
-                }
+              };
+              const int one = wave_seg_map(ch.ex, nk, base, wlen, seg_w);
+              if (one >= 0) {
+                const typename CH::Rec r1 = ch.rec[one];
+                terms([&](int) { return r1; });
+              } else {
+                terms([&](int q) { return ch.rec[seg_w[q]]; });
               }
             }
             __syncthreads();
