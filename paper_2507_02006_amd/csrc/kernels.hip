@@ -1162,7 +1162,10 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       const int nw = (g1 - g0) * WPG;
       float* vals = reinterpret_cast<float*>(bw + nw);  // the values follow this window's bitmap
       const int64_t base = rbase + I.roff;
-      auto set_bit = [&](int j) { atomicOr(&bw[j >> 5].x, 1u << (j & 31)); };
+      // terms carry absolute columns: bwa is the bitmap seen from column 0
+      // (c0 is a multiple of 32, so a column's bit index is the same)
+      uint2* bwa = bw - (c0 >> 5);
+      auto set_bit = [&](int j) { atomicOr(&bwa[j >> 5].x, 1u << (j & 31)); };
       // Heavy rows: the symbolic phase kept the window's bitmap.
       int64_t cached = -1;
       if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
@@ -1176,7 +1179,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         __syncthreads();
       };
       auto add_at_rank = [&](int j, float v) {
-        const uint2 e = bw[j >> 5];
+        const uint2 e = bwa[j >> 5];
         const int rk = (int)e.y + __popc(e.x & ((1u << (j & 31)) - 1u));
         if (rk < n) lds_add<false>(&vals[rk], v);
       };
@@ -1237,7 +1240,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
               if (q < wlen) {
                 const typename CH::Rec rc = rec_of(q);
                 const int32_t pos = (int32_t)rc.shift + wlo + q;
-                jj[i] = op.bcol[pos] - c0;
+                jj[i] = op.bcol[pos];
                 vv[i] = rc.av * op.bval[pos];
               }
             }
@@ -1293,7 +1296,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                     jv[u] = 0;
                     bv2[u] = 0.f;
                     if (pos[u] >= 0) {
-                      jv[u] = op.bcol[pos[u]] - c0;
+                      jv[u] = op.bcol[pos[u]];
                       if (pass) bv2[u] = op.bval[pos[u]];
                     }
                   }
@@ -1326,10 +1329,10 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
           load_bits();
         else
           for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true>(op, g, ch, row, seg,
-                                                               [&](int j, float) { set_bit(j - c0); });
+                                                               [&](int j, float) { set_bit(j); });
         word_ranks();
         for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true>(op, g, ch, row, seg,
-                                                            [&](int j, float v) { add_at_rank(j - c0, v); });
+                                                            [&](int j, float v) { add_at_rank(j, v); });
       }
       __syncthreads();
       // values out (coalesced); then the value slots take the column ids,
