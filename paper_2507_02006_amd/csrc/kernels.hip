@@ -920,33 +920,21 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 // of G columns.  Symbolic: a workgroup sets a presence bitmap for a run of
 // grains of one row (a symbolic item), writes each grain's popcount, and
 // for heavy rows keeps the bitmap in global memory.  A plan kernel then cuts
-// every row into windows of whole grains holding at most max_entries
-// entries, spanning at most max_grains grains and never leaving a symbolic
-// item.  Numeric, per window: the presence bitmap is set from the terms (or
-// loaded from the kept one), a workgroup scan turns word popcounts into
-// ranks, and each term is added into a compact fp32 array at the rank of
-// its column, the first one also writing the column id there; the array is
-// then written out.  LDS grows with the window's entries, not its width.
+// every row into windows of whole grains whose bitmap and values fit one
+// LDS pool (and at most max_entries entries and max_grains grains), never
+// leaving a symbolic item.  Numeric, per window: the presence bitmap is set
+// from the terms (or loaded from the kept one), wavefront scans turn word
+// popcounts into ranks, and each term is added into a compact fp32 array at
+// the rank of its column; the values are written out, then the column ids,
+// staged at their ranks from the bitmap.  LDS grows with the window's
+// entries, not its width.
 
 constexpr int WIN_BLOCK = 512;
 
-// Bitmaps of symbolic items and windows: each thread owns a run of `wpt`
-// consecutive words (a power of two, wpt * WIN_BLOCK >= words), and one pad
-// word follows every run so that the runs of a wavefront fall in distinct
-// banks.
-__host__ __device__ constexpr int window_wpt_log2(int maxw) {
-  int l = 0;
-  while ((1 << l) * WIN_BLOCK < maxw) ++l;
-  return l;
-}
-__host__ __device__ constexpr int window_words_padded(int maxw) {
-  return maxw + (maxw >> window_wpt_log2(maxw)) + 1;
-}
-
 template <typename S>
 __host__ __device__ constexpr size_t count_lds_bytes(int sg, int G) {
-  return align16((size_t)window_words_padded(sg * (G / 32)) * 4) + align16((size_t)sg * 4) +
-         align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128 + 16;  // + the static list offset
+  return align16((size_t)sg * (G / 32) * 4) + align16((size_t)sg * 4) + align16(sizeof(Chunk<WIN_BLOCK, S>)) + 128 +
+         16;  // + the static list offset
 }
 
 template <typename RA, typename RB>
@@ -955,23 +943,21 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t s_off;
   constexpr int64_t CACHE_CHUNK = 65536;  // cache words a workgroup takes from the shared buffer at once
+  constexpr int NWV = WIN_BLOCK / WAVE;
   int64_t chunk_cur = 0, chunk_end = 0;   // thread 0: the workgroup's current chunk
   const int SG = wp.grains_per_count_item;
   const int WPG = op.G / 32;  // bitmap words per grain
   const int nwmax = SG * WPG;
-  const int lw = window_wpt_log2(nwmax);
-  const int wpt = 1 << lw;
   uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
-  const size_t bm_bytes = align16((size_t)window_words_padded(nwmax) * 4);
+  const size_t bm_bytes = align16((size_t)nwmax * 4);
   int32_t* gc = reinterpret_cast<int32_t*>(smem + bm_bytes);
   using CH = Chunk<WIN_BLOCK, RB>;
   CH& ch = *reinterpret_cast<CH*>(smem + bm_bytes + align16((size_t)SG * 4));
   Group<WIN_BLOCK, WIN_BLOCK> g;
   g.red = reinterpret_cast<int64_t*>(reinterpret_cast<unsigned char*>(&ch) + align16(sizeof(CH)));
   const int t = threadIdx.x;
-  auto pidx = [&](int w) { return w + (w >> lw); };
-  for (int i = t; i < window_words_padded(nwmax); i += WIN_BLOCK) bm[i] = 0u;
-  for (int i = t; i < SG; i += WIN_BLOCK) gc[i] = 0;
+  const int lane = lane_id(), wv = t / WAVE;
+  for (int i = t; i < nwmax; i += WIN_BLOCK) bm[i] = 0u;
   __syncthreads();
 
   const int32_t* list = bv.list + bv.binoff[bv.bin];
@@ -984,25 +970,20 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
     const int g1 = min((int)op.nG, g0 + SG);
     const int c0 = g0 * op.G;
     const GrainRange seg{op.bidx, op.nG + 1, g0, g1};
+    // terms carry absolute columns: bma is the bitmap seen from column 0
+    // (c0 is a multiple of 32, so a column's bit index is the same)
+    uint32_t* bma = bm - (c0 >> 5);
     for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true>(op, g, ch, row, seg, [&](int j, float) {
-      j -= c0;
-      atomicOr(&bm[pidx(j >> 5)], 1u << (j & 31));
+      atomicOr(&bma[j >> 5], 1u << (j & 31));
     });
-    // per-grain popcounts over each thread's run of words
+    // per-grain popcounts: a wavefront per grain, lanes on consecutive words
     const int nw = (g1 - g0) * WPG;
-    const int w0 = t * wpt, w1 = min(nw, w0 + wpt);
-    int gcur = -1, gacc = 0;
-    for (int w = w0; w < w1; ++w) {
-      const int pc = __popc(bm[pidx(w)]);
-      const int gw = w / WPG;
-      if (gw != gcur) {
-        if (gacc) atomicAdd(&gc[gcur], gacc);
-        gcur = gw;
-        gacc = 0;
-      }
-      gacc += pc;
+    for (int gi = wv; gi < g1 - g0; gi += NWV) {
+      uint32_t c = 0;
+      for (int w = gi * WPG + lane; w < (gi + 1) * WPG; w += WAVE) c += __popc(bm[w]);
+      c = wave_sum(c);
+      if (lane == 0) gc[gi] = (int32_t)c;
     }
-    if (gacc) atomicAdd(&gc[gcur], gacc);
     if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
       // heavy row: keep the item's bitmap for the numeric phase, in a slot
       // taken from the workgroup's chunk of the shared cache
@@ -1020,16 +1001,13 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
       __syncthreads();
       const int64_t off = s_off;
       if (off >= 0)
-        for (int w = w0; w < w1; ++w) wp.bm_cache[off + w] = bm[pidx(w)];
+        for (int w = t; w < nw; w += WIN_BLOCK) wp.bm_cache[off + w] = bm[w];  // coalesced
     } else if (wp.bm_cache && t == 0) {
       wp.bm_off[row * ngg + gg] = -1;
     }
-    for (int w = w0; w < w1; ++w) bm[pidx(w)] = 0u;
-    __syncthreads();
-    for (int k = t; k < g1 - g0; k += WIN_BLOCK) {
-      wp.gcnt[row * op.nG + g0 + k] = gc[k];
-      gc[k] = 0;
-    }
+    __syncthreads();  // counts and cache copies have read the bitmap
+    for (int w = t; w < nw; w += WIN_BLOCK) bm[w] = 0u;
+    for (int k = t; k < g1 - g0; k += WIN_BLOCK) wp.gcnt[row * op.nG + g0 + k] = gc[k];
     __syncthreads();
   }
 }
