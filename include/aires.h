@@ -285,6 +285,31 @@ typedef struct aires_stats {
     double pipeline_ms;
 } aires_stats;
 
+/* Activation applied by aires_spmm. */
+typedef enum aires_act { AIRES_ACT_NONE = 0, AIRES_ACT_RELU = 1 } aires_act;
+
+/*
+ * aires_spmm -- Y = act(A * W) for a sparse A and a dense W: the
+ * combination step of a GCN layer (Sec. II-A, Eq. 3: the aggregated
+ * features times the layer's weights, then the activation sigma, e.g.
+ * ReLU), and, with a dense feature matrix in place of W, the aggregation of
+ * Eq. 1 (the backward pass of a layer multiplies by the symmetric A_norm
+ * the same way).
+ *
+ * A: CSR descriptor with A->mem == AIRES_MEM_DEVICE (borrowed; rows m =
+ * A->nrows, K = A->ncols).  W: device, row-major K x F, row stride ldw >= F
+ * elements.  Y: device, row-major m x F, row stride ldy >= F, owned by the
+ * caller; every element of the m x F block is overwritten (rows of A with
+ * no entries give act(0) = 0); columns between F and ldy are untouched.
+ * Work is enqueued on `stream` (a hipStream_t); the call allocates nothing
+ * and returns once the kernels are enqueued.  Each element is a sum in
+ * fp32 over the row's entries in an unspecified order.
+ * Errors: AIRES_E_INVALID_ARG (NULL arrays, ldw < F, ldy < F, bad act),
+ * AIRES_E_UNSUPPORTED (A not on the device, F >= 2^31), AIRES_E_HIP.
+ */
+aires_status aires_spmm(const aires_csr *A, const float *W, int64_t ldw, int64_t F, float *Y, int64_t ldy,
+                        aires_act act, void *stream);
+
 /* Statistics of the last aires_spgemm / aires_stream_tiles on the plan. */
 aires_status aires_plan_stats(const aires_plan *plan, aires_stats *stats);
 

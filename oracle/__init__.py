@@ -3,7 +3,8 @@ benchmark's CPU-baseline leg).  The GPU library never imports it.
 
 Python front end to ``oracle.c``: a serial CPU Gustavson sparse product
 (Sec. II-A, Eq. 1, with both operands compressed), the per-row
-intermediate-product counts, the RoBW row-block partition of Algorithm 1
+intermediate-product counts, the sparse-times-dense combination product of
+a GCN layer (Eq. 3, in double), the RoBW row-block partition of Algorithm 1
 (Sec. III-A) and a canonical-CSR validator.  Matrices are any object with
 ``nrows, ncols, rp, col, val`` numpy attributes.
 """
@@ -58,6 +59,8 @@ def _load():
         lib.oracle_robw.argtypes = [i64, vp, i64, i64, vp, i64]
         lib.oracle_validate.restype = ci
         lib.oracle_validate.argtypes = [i64, i64, i64, vp, vp]
+        lib.oracle_spmm.restype = None
+        lib.oracle_spmm.argtypes = [i64, vp, vp, vp, vp, i64, i64, ctypes.c_int, vp, vp]
         _lib = lib
     return _lib
 
@@ -118,6 +121,23 @@ def spgemm(A, B, r0: int = 0, r1: int | None = None, f64: bool = False) -> Produ
     finally:
         lib.oracle_result_free(h)
     return Product(r0, r1, B.ncols, rp, col, val, prods, v64, a64)
+
+
+def spmm(A, W: np.ndarray, relu: bool = False) -> tuple[np.ndarray, np.ndarray]:
+    """Y = act(A * W) in double (Sec. II-A, Eq. 3) and the sums of |a_ik w_kj|
+    for each entry: A a CSR, W a float32 (A.ncols x F) array."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    if W.ndim != 2 or W.shape[0] != A.ncols:
+        raise ValueError("W must be (A.ncols x F)")
+    lib = _load()
+    m, F = A.nrows, W.shape[1]
+    arp, acol, aval = _rp64(A.rp), _c(A.col, np.int32), _c(A.val, np.float32)
+    Y = np.empty((m, F), dtype=np.float64)
+    Ya = np.empty((m, F), dtype=np.float64)
+    if m and F:
+        lib.oracle_spmm(int(m), arp.ctypes.data, acol.ctypes.data, aval.ctypes.data, W.ctypes.data, int(F), int(F),
+                        1 if relu else 0, Y.ctypes.data, Ya.ctypes.data)
+    return Y, Ya
 
 
 def products(A, B, r0: int = 0, r1: int | None = None) -> np.ndarray:

@@ -32,6 +32,12 @@
  *    paper's loop would not advance).
  * 4. oracle_validate: canonical CSR check (row_ptr starts at 0, is
  *    non-decreasing, ends at nnz; columns strictly increasing in range).
+ * 5. oracle_spmm: Y = act(A * W) for a CSR A and a dense row-major W, the
+ *    combination step of a GCN layer (Sec. II-A, Eq. 3: aggregated features
+ *    times the weights, then the activation sigma, ReLU here), written out
+ *    from its definition: y_ij = act(sum over stored k of A_i of
+ *    a_ik * w_kj), accumulated in double in ascending k, together with the
+ *    sum of |a_ik * w_kj| for the standard summation error bound.
  *
  * Row pointers are passed as int64 (the Python side widens int32 arrays).
  */
@@ -226,4 +232,26 @@ int oracle_validate(int64_t m, int64_t ncols, int64_t nnz, const int64_t *rp, co
             if (p > rp[i] && col[p] <= col[p - 1]) return 5;
         }
     return 0;
+}
+
+/* Y (m x F, double, row-major) = act(A * W) with act = ReLU when relu;
+   Yabs = sum over k of |a_ik * w_kj| (before the activation). */
+void oracle_spmm(int64_t m, const int64_t *arp, const int32_t *acol, const float *aval, const float *W,
+                 int64_t ldw, int64_t F, int relu, double *Y, double *Yabs)
+{
+    for (int64_t i = 0; i < m; ++i) {
+        double *y = Y + i * F, *ya = Yabs + i * F;
+        for (int64_t j = 0; j < F; ++j) { y[j] = 0.0; ya[j] = 0.0; }
+        for (int64_t p = arp[i]; p < arp[i + 1]; ++p) {
+            const double a = (double)aval[p];
+            const float *w = W + (int64_t)acol[p] * ldw;
+            for (int64_t j = 0; j < F; ++j) {
+                const double t = a * (double)w[j];
+                y[j] += t;
+                ya[j] += t < 0 ? -t : t;
+            }
+        }
+        if (relu)
+            for (int64_t j = 0; j < F; ++j) if (y[j] < 0.0) y[j] = 0.0;
+    }
 }

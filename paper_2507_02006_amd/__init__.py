@@ -20,7 +20,7 @@ from dataclasses import dataclass
 
 from . import _binding as B_
 
-__all__ = ["tile_plan", "spgemm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
+__all__ = ["tile_plan", "spgemm", "spmm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
            "Plan", "Output", "AiresError", "to_device", "to_pinned"]
 
 AiresError = B_.AiresError
@@ -191,6 +191,27 @@ def _stream_handle(stream):
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
+
+
+def spmm(A, W, relu: bool = False, out=None, stream=None):
+    """Y = act(A * W) (aires_spmm): A a device CSR (a tuple as from
+    ``to_device``, or an ``Output`` of ``spgemm``), W a dense device float32
+    matrix with A.ncols rows (row stride W.stride(0)); act is ReLU when
+    ``relu``.  Returns Y (m x F float32, a new tensor unless ``out`` is
+    given); valid once ``stream`` reaches the enqueued kernels."""
+    import torch
+    m, k, rp, col, val = _parts(A)
+    if W.dim() != 2 or W.dtype != torch.float32 or W.stride(1) != 1 or W.shape[0] != k:
+        raise ValueError("W must be a float32 (A.ncols x F) matrix with unit column stride")
+    F = int(W.shape[1])
+    if out is None:
+        out = torch.empty((m, F), dtype=torch.float32, device=W.device)
+    if out.dim() != 2 or out.shape[0] != m or out.shape[1] != F or out.stride(1) != 1 or out.dtype != torch.float32:
+        raise ValueError("out must be a float32 (m x F) matrix with unit column stride")
+    a = B_.make_csr(m, k, rp, col, val)
+    B_.check(B_.load().aires_spmm(ctypes.byref(a), W.data_ptr(), W.stride(0), F, out.data_ptr(), out.stride(0),
+                                  B_.ACT_RELU if relu else B_.ACT_NONE, _stream_handle(stream)), "aires_spmm")
+    return out
 
 
 def spgemm(plan: Plan, stream=None) -> Output:

@@ -1245,6 +1245,22 @@ aires_status aires_stream_tiles(aires_plan* plan, void* h2d, void* compute, void
   return st;
 }
 
+aires_status aires_spmm(const aires_csr* A, const float* W, int64_t ldw, int64_t F, float* Y, int64_t ldy,
+                        aires_act act, void* stream) {
+  ST_TRY(check_csr_desc(A, "A"));
+  if (A->mem != AIRES_MEM_DEVICE) return fail(AIRES_E_UNSUPPORTED, "aires_spmm needs A on the device");
+  if (F < 0 || F >= (int64_t(1) << 31)) return fail(AIRES_E_UNSUPPORTED, "F = %lld out of range", (long long)F);
+  if (act != AIRES_ACT_NONE && act != AIRES_ACT_RELU) return fail(AIRES_E_INVALID_ARG, "act %d invalid", (int)act);
+  if (A->nrows == 0 || F == 0) return AIRES_OK;
+  if (ldw < F || ldy < F) return fail(AIRES_E_INVALID_ARG, "ldw %lld / ldy %lld below F %lld", (long long)ldw,
+                                      (long long)ldy, (long long)F);
+  if (!Y || !A->row_ptr || (A->nnz > 0 && (!W || !A->col_idx || !A->vals)))
+    return fail(AIRES_E_INVALID_ARG, "NULL array");
+  HIP_TRY(kern::spmm(A->row_ptr, A->rp_type == AIRES_IDX_I64, A->col_idx, A->vals, A->nrows, W, ldw, F, Y, ldy,
+                     act == AIRES_ACT_RELU, (hipStream_t)stream));
+  return AIRES_OK;
+}
+
 aires_status aires_plan_stats(const aires_plan* plan, aires_stats* stats) {
   if (!plan || !stats) return fail(AIRES_E_INVALID_ARG, "NULL argument");
   *stats = plan->stats;

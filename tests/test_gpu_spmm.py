@@ -1,0 +1,159 @@
+"""GPU parity of the combination step Y = act(A * W) (aires_spmm, Sec. II-A
+Eq. 3) through the C-ABI against the oracle's double-precision product.
+
+Bar: every entry within the fp32 summation error bound of the GPU's
+arbitrary order with fused multiply-adds,
+    |y - y64| <= (n_i + 2) * 2^-24 * sum_k |a_ik w_kj| + 2^-24 * |y64|,
+where n_i is the number of stored entries of row i (the standard bound
+gamma_n for a sum of n_i rounded terms, plus the final rounding); exact
+(bit-equal to the integer product) when every value is a small integer."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from workloads import CSR
+
+pytestmark = pytest.mark.gpu
+
+U = 2.0 ** -24
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    return torch
+
+
+def say(msg):
+    print("[gpu-case] " + msg, flush=True)
+
+
+def dev_csr(torch, A, rp64=False):
+    rp = A.rp.astype(np.int64 if rp64 else np.int32)
+    return (A.nrows, A.ncols, torch.from_numpy(rp).cuda(), torch.from_numpy(A.col.astype(np.int32)).cuda(),
+            torch.from_numpy(A.val.astype(np.float32)).cuda())
+
+
+def check(torch, A, W, relu=False, rp64=False, ldw_pad=0, ldy_pad=0, w_offset=0, exact=False, name=""):
+    import paper_2507_02006_amd as aires
+    say("%s m=%d K=%d F=%d relu=%d rp64=%d pads=(%d,%d) off=%d" % (name, A.nrows, A.ncols, W.shape[1], relu, rp64,
+                                                                  ldw_pad, ldy_pad, w_offset))
+    K, F = W.shape
+    buf = torch.zeros(K * (F + ldw_pad) + w_offset + 1, dtype=torch.float32, device="cuda")
+    Wd = buf[w_offset:w_offset + K * (F + ldw_pad)].view(K, F + ldw_pad)[:, :F]
+    Wd.copy_(torch.from_numpy(W))
+    ybuf = torch.full((A.nrows, F + ldy_pad), 7.0, dtype=torch.float32, device="cuda")
+    Y = aires.spmm(dev_csr(torch, A, rp64), Wd, relu=relu, out=ybuf[:, :F])
+    torch.cuda.synchronize()
+    y = Y.cpu().numpy().astype(np.float64)
+    if ldy_pad:
+        assert np.all(ybuf[:, F:].cpu().numpy() == 7.0), "columns past F were written"
+    ref, refabs = oracle.spmm(A, W, relu=relu)
+    if exact:
+        assert np.array_equal(y, ref), name
+        return
+    n = np.diff(A.rp.astype(np.int64))[:, None]
+    tol = (n + 2) * U * refabs + U * np.abs(ref)
+    err = np.abs(y - ref)
+    bad = err > tol
+    assert not bad.any(), "%s: %d entries over the bound, worst %g" % (name, bad.sum(), (err - tol).max())
+
+
+@pytest.mark.parametrize("F", [1, 7, 64, 100, 128, 200, 256, 512, 700])
+def test_widths(torch_gpu, F):
+    """One wavefront pass covers 64*V columns (V = 1, 2, 4, 8); 700 takes two
+    passes; F not a multiple of the vector takes the scalar tail."""
+    rng = np.random.default_rng(F)
+    A = workloads.random_csr(rng, 300, 90, 0.05)
+    W = rng.uniform(-1, 1, (90, F)).astype(np.float32)
+    check(torch_gpu, A, W, name="width %d" % F)
+
+
+@pytest.mark.parametrize("relu", [False, True])
+def test_integer_values_exact(torch_gpu, relu):
+    """Small integers: every product and partial sum is exact in fp32, so Y
+    equals the integer product whatever the order."""
+    rng = np.random.default_rng(5)
+    Ad = rng.integers(-3, 4, (257, 129)) * (rng.random((257, 129)) < 0.1)
+    A = CSR(257, 129, *_csr_parts(Ad))
+    W = rng.integers(-3, 4, (129, 96)).astype(np.float32)
+    check(torch_gpu, A, W, relu=relu, exact=True, name="integer relu=%d" % relu)
+
+
+def _csr_parts(D):
+    rows, cols = np.nonzero(D)
+    rp = np.zeros(D.shape[0] + 1, dtype=np.int64)
+    np.add.at(rp, rows + 1, 1)
+    return np.cumsum(rp).astype(np.int32), cols.astype(np.int32), D[rows, cols].astype(np.float32)
+
+
+def test_heavy_rows_split_over_a_workgroup(torch_gpu):
+    """Rows above 512 entries take the workgroup kernel (four wavefronts
+    and an LDS reduction); mixed with light and empty rows."""
+    rng = np.random.default_rng(7)
+    K = 3000
+    lens = np.array([0, 3, 513, 512, 2999, 0, 1, 1500, 700, 5] * 4)
+    rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    col = np.concatenate([np.sort(rng.choice(K, L, replace=False)) for L in lens]).astype(np.int32)
+    val = rng.uniform(-1, 1, len(col)).astype(np.float32)
+    A = CSR(len(lens), K, rp, col, val)
+    for F in (64, 256, 600):
+        W = rng.uniform(-1, 1, (K, F)).astype(np.float32)
+        check(torch_gpu, A, W, relu=True, name="heavy F=%d" % F)
+
+
+def test_strides_offsets_and_rp64(torch_gpu):
+    """Row strides above F (padding untouched), a W base that is not
+    vector-aligned (scalar loads), and 64-bit row pointers."""
+    rng = np.random.default_rng(8)
+    A = workloads.random_csr(rng, 200, 70, 0.1)
+    W = rng.uniform(-1, 1, (70, 256)).astype(np.float32)
+    check(torch_gpu, A, W, ldw_pad=3, ldy_pad=5, name="pads")
+    check(torch_gpu, A, W, w_offset=1, name="unaligned W")
+    check(torch_gpu, A, W, rp64=True, relu=True, name="rp64")
+
+
+def test_edges(torch_gpu):
+    import paper_2507_02006_amd as aires
+    torch = torch_gpu
+    rng = np.random.default_rng(9)
+    E = CSR(6, 10, np.zeros(7, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+    W = rng.uniform(-1, 1, (10, 33)).astype(np.float32)
+    check(torch, E, W, name="all rows empty")
+    Y = aires.spmm(dev_csr(torch, CSR(0, 10, np.zeros(1, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))),
+                   torch.from_numpy(W).cuda())
+    assert Y.shape == (0, 33)
+    A = workloads.random_csr(rng, 8, 10, 0.5)
+    Y = aires.spmm(dev_csr(torch, A), torch.zeros((10, 0), device="cuda"))
+    assert Y.shape == (8, 0)
+    with pytest.raises(ValueError):
+        aires.spmm(dev_csr(torch, A), torch.zeros((11, 4), device="cuda"))
+
+
+def test_gcn_layer_on_aggregated_features(torch_gpu):
+    """A GCN layer H' = relu((A_norm X) W) (Eqs. 1-3): the aggregation from
+    aires_spgemm, then the combination on its CSR output (int64 row
+    pointers), against the oracle on the oracle's aggregation."""
+    import paper_2507_02006_amd as aires
+    torch = torch_gpu
+    A, X = workloads.workload(2, n=8192)  # cfg2 scaled down: F_in = 512 features at 5 %
+    rng = np.random.default_rng(10)
+    W = rng.uniform(-0.5, 0.5, (X.ncols, 64)).astype(np.float32)
+    say("gcn layer m=%d nnzA=%d F_in=%d F_out=64" % (A.nrows, A.nnz, X.ncols))
+    with aires.tile_plan(aires.to_device(A), aires.to_device(X), 0) as plan:
+        C = aires.spgemm(plan)
+        Wd = torch.from_numpy(W).cuda()
+        H = aires.spmm((C.nrows, C.ncols, C.rp, C.col, C.val), Wd, relu=True)
+        torch.cuda.synchronize()
+        h = H.cpu().numpy().astype(np.float64)
+    Co = oracle.spgemm(A, X)
+    ref, refabs = oracle.spmm(CSR(Co.r1 - Co.r0, Co.ncols, Co.rp, Co.col, Co.val), W, relu=True)
+    # C itself differs from the oracle's by at most 1e-5 (1 + |c|) per entry
+    n = np.diff(Co.rp)[:, None]
+    cabs, _ = oracle.spmm(CSR(Co.r1 - Co.r0, Co.ncols, Co.rp, Co.col, np.abs(Co.val)), np.abs(W))
+    tol = (n + 2) * U * refabs + U * np.abs(ref) + 1e-5 * (np.abs(W).sum(0)[None, :] + cabs)
+    assert np.all(np.abs(h - ref) <= tol)

@@ -370,3 +370,83 @@ def test_generator_properties():
     assert oracle.validate(X) == 0
     assert abs(X.nnz / (4096 * 256) - 0.1) < 0.005
     assert X.val.min() >= -1.0 and X.val.max() <= 1.0
+
+
+# --------------------------------------- combination step (Eq. 3): A * W
+
+def test_spmm_identity_and_relu():
+    """A = I: Y = W exactly; with the activation, Y = max(W, 0)."""
+    rng = np.random.default_rng(11)
+    W = rng.standard_normal((37, 19)).astype(np.float32)
+    I = from_dense(np.eye(37))
+    Y, Ya = oracle.spmm(I, W)
+    assert np.array_equal(Y, W.astype(np.float64))
+    assert np.array_equal(Ya, np.abs(W).astype(np.float64))
+    Yr, _ = oracle.spmm(I, W, relu=True)
+    assert np.array_equal(Yr, np.maximum(W, 0).astype(np.float64))
+
+
+@pytest.mark.parametrize("density", [0.0, 0.05, 0.3, 1.0])
+def test_spmm_integer_matches_integer_matmul(density):
+    """Small integers: every product and partial sum is exact in double, so
+    Y equals the exact integer product of the dense operands."""
+    rng = np.random.default_rng(int(density * 100) + 3)
+    Ad = rng.integers(-4, 5, (23, 31)) * (rng.random((23, 31)) < density)
+    W = rng.integers(-4, 5, (31, 45))
+    A = from_dense(Ad.astype(np.float32), pattern=(Ad != 0))
+    Y, Ya = oracle.spmm(A, W.astype(np.float32))
+    assert np.array_equal(Y, (Ad.astype(np.int64) @ W.astype(np.int64)).astype(np.float64))
+    assert np.array_equal(Ya, (np.abs(Ad).astype(np.int64) @ np.abs(W).astype(np.int64)).astype(np.float64))
+    Yr, _ = oracle.spmm(A, W.astype(np.float32), relu=True)
+    assert np.all(Yr >= 0) and np.array_equal(Yr, np.maximum(Y, 0))
+
+
+def test_spmm_permutation_empty_rows_and_average():
+    rng = np.random.default_rng(12)
+    W = rng.standard_normal((16, 9)).astype(np.float32)
+    perm = rng.permutation(16)
+    Y, _ = oracle.spmm(from_dense(np.eye(16)[perm]), W)           # row i = W[perm[i]]
+    assert np.array_equal(Y, W[perm].astype(np.float64))
+    E = CSR(5, 16, np.zeros(6, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+    Y, Ya = oracle.spmm(E, W, relu=True)                           # empty rows: act(0) = 0
+    assert np.array_equal(Y, np.zeros((5, 9))) and np.array_equal(Ya, np.zeros((5, 9)))
+    # K_16 with self-loops: A_norm = J/16 exactly, so every row is the mean of W's rows
+    A = _sym_graph(16, [(u, v) for u in range(16) for v in range(u + 1, 16)])
+    Wi = rng.integers(-8, 9, (16, 9)).astype(np.float32)
+    Y, _ = oracle.spmm(A, Wi)
+    assert np.array_equal(Y, np.tile(Wi.astype(np.float64).sum(0) / 16, (16, 1)))
+
+
+def test_spmm_brute_force_triples():
+    """Tiny random inputs: the sum over stored (i, k) entries of a_ik w_kj
+    enumerated directly."""
+    rng = np.random.default_rng(13)
+    for trial in range(20):
+        m, K, F = rng.integers(1, 7, 3)
+        Ad = rng.standard_normal((m, K)) * (rng.random((m, K)) < 0.5)
+        A = from_dense(Ad.astype(np.float32), pattern=(Ad != 0))
+        W = rng.standard_normal((K, F)).astype(np.float32)
+        want = np.zeros((m, F))
+        rp = A.rp.astype(np.int64)
+        for i in range(m):
+            for p in range(rp[i], rp[i + 1]):
+                for j in range(F):
+                    want[i, j] += float(A.val[p]) * float(W[A.col[p], j])
+        Y, _ = oracle.spmm(A, W)
+        assert np.allclose(Y, want, rtol=0, atol=1e-12)
+
+
+def test_spmm_gcn_layer_composes():
+    """A GCN layer H' = relu((A_norm X) W) from the two oracle products
+    equals relu(A_norm (X W)) up to double rounding (associativity)."""
+    rng = np.random.default_rng(14)
+    A = _sym_graph(40, [tuple(e) for e in rng.integers(0, 40, (60, 2)) if e[0] != e[1]])
+    X = workloads.random_csr(rng, 40, 24, 0.3)
+    W = rng.standard_normal((24, 8)).astype(np.float32)
+    C = oracle.spgemm(A, X, f64=True)
+    Cd = CSR(40, 24, C.rp, C.col, C.val)
+    H1, _ = oracle.spmm(Cd, W, relu=True)
+    Dx = np.zeros((40, 24)); Dx[pattern_dense(X)] = X.val
+    Da = np.zeros((40, 40)); Da[pattern_dense(A)] = A.val
+    H2 = np.maximum(Da @ (Dx @ W.astype(np.float64)), 0)
+    assert np.allclose(H1, H2, rtol=1e-5, atol=1e-6)
