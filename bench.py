@@ -7,6 +7,7 @@ symbolic phase, scan, the nnz read-back, C allocation, numeric phase
 (aires_spgemm), until C is ready on the stream.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload 3] [--cpu-seconds S]
+  python bench.py --workload 2 --combine 256    (the combination step, Eq. 3)
 
 value  = whole-job GFLOP/s (2 flops per intermediate product) per step.
 roofline = the dominant kernel (the numeric launch with the largest time):
@@ -141,6 +142,88 @@ def measured_traffic(kernel_name: str, dom_bytes_launch: int):
     return int(ent["traffic_bytes"])
 
 
+def combine(args, A, B, dA, dB, gen_s):
+    """The combination step relu(C W) on the aggregated features C = A B."""
+    import torch
+    import paper_2507_02006_amd as aires
+    F = args.combine
+    with aires.tile_plan(dA, dB, 0) as plan:
+        C = aires.spgemm(plan)
+        torch.cuda.synchronize()
+    Cd = (C.nrows, C.ncols, C.rp, C.col, C.val)
+    g = torch.Generator(device="cuda").manual_seed(17)
+    W = (torch.rand((C.ncols, F), generator=g, device="cuda") - 0.5) / float(np.sqrt(C.ncols))
+    Y = torch.empty((C.nrows, F), dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        aires.spmm(Cd, W, relu=True, out=Y)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record()
+        aires.spmm(Cd, W, relu=True, out=Y)
+        e1.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = 1e3 * elapsed / args.steps
+    launch_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    nnz, m = int(C.nnz), int(C.nrows)
+    flops = 2.0 * nnz * F
+    compulsory = 8 * (m + 1) + 8 * nnz + 4 * C.ncols * F + 4 * m * F  # C, W once, Y
+    gather = 8 * (m + 1) + 8 * nnz + 4 * nnz * F + 4 * m * F          # a row of W per entry of C
+    res = {
+        "metric": "SpMM GFLOP/s of the GCN combination step relu(C W) (Eq. 3) on 1 MI355X",
+        "value": round(flops / (ms_per_step * 1e-3) / 1e9, 3),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded R-MAT graph and uniform sparse features; uniform random weights)",
+        "config": {"workload": "combination of cfg%d %s: C (%d x %d, %d nnz) times W (%d x %d), ReLU"
+                               % (args.workload, WORKLOAD_NAMES[args.workload], m, C.ncols, nnz, C.ncols, F),
+                   "m": m, "k": int(C.ncols), "f_out": F, "nnz_c": nnz, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "k_spmm_rows + k_spmm_heavy",
+                     "achieved": round(compulsory / (launch_ms * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(compulsory / (launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "algorithmic_bytes": compulsory, "avg_launch_ms": round(launch_ms, 4),
+                     "gather_model_gbs": round(gather / (launch_ms * 1e-3) / 1e9, 2),
+                     "fp32_tflops": round(flops / (launch_ms * 1e-3) / 1e12, 3)},
+        "generation_s": round(gen_s, 2),
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_combine_baseline(C, W, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_combine_baseline(C, W, seconds):
+    """The oracle's double-precision product on leading row blocks of C,
+    one core, until about `seconds` of work."""
+    import oracle
+    from workloads import CSR
+    rp = C.rp.cpu().numpy()
+    Wn = W.cpu().numpy()
+    F = Wn.shape[1]
+    col, val = C.col.cpu().numpy(), C.val.cpu().numpy()
+    done = 0
+    t0 = time.perf_counter()
+    r0 = 0
+    while time.perf_counter() - t0 < seconds and r0 < C.nrows:
+        r1 = min(C.nrows, r0 + 4096)
+        blk = CSR(r1 - r0, C.ncols, rp[r0:r1 + 1] - rp[r0], col[rp[r0]:rp[r1]], val[rp[r0]:rp[r1]])
+        oracle.spmm(blk, Wn, relu=True)
+        done += int(rp[r1] - rp[r0])
+        r0 = r1
+    dt = time.perf_counter() - t0
+    return {"value": round(2.0 * done * F / dt / 1e9, 4), "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
+            "sample": "leading rows of C in blocks of 4096: %d of %d entries = %.2f%% of the workload, %.1f s"
+                      % (done, int(C.nnz), 100.0 * done / max(1, int(C.nnz)), dt)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +232,10 @@ def main():
     ap.add_argument("--workload", type=int, default=3, choices=sorted(WORKLOAD_NAMES))
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--combine", type=int, default=0, metavar="F_OUT",
+                    help="instead of the aggregation, time the combination step of the GCN layer "
+                         "(Eq. 3): relu(C * W) with C the workload's aggregated features (computed once, "
+                         "untimed) and a random dense W with F_OUT columns (aires_spmm)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run one device copy of this many MiB (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -173,6 +260,8 @@ def main():
     A, B = workloads.workload(args.workload)
     gen_s = time.perf_counter() - t0
     dA, dB = aires.to_device(A), aires.to_device(B)
+    if args.combine:
+        return combine(args, A, B, dA, dB, gen_s)
     torch.cuda.synchronize()
     P = row_products(A, B)
     total_products = int(P.sum())

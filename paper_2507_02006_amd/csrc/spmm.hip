@@ -6,8 +6,8 @@
 //
 // Rows with at most kHeavy entries take one wavefront: lane l owns V
 // consecutive columns of a 64*V-column block, the row's (k, a_ik) pairs are
-// read once per block (the same for every lane, so they come through the
-// scalar cache), and four rows of W are in flight at a time.  Longer rows
+// read 64 at a time (a lane each) and broadcast with readlane, and several
+// rows of W are in flight at a time.  Longer rows
 // take a 256-thread workgroup whose four wavefronts split the entries and
 // add their partial rows in LDS.  The activation is applied before the
 // store; every element of Y is written exactly once.
@@ -57,28 +57,43 @@ __device__ __forceinline__ void load_w(const float* wr, int c, int F, float (&w)
   for (int v = 0; v < V; ++v) w[v] = c + v < F ? wr[c + v] : 0.f;
 }
 
-// acc += a_ik * W[k, c .. c+V) over the entries [p0, p1), four at a time.
+// acc += a_ik * W[k, c .. c+V) over the entries [p0, p1).  The entries
+// come in 64 at a time, one per lane (a coalesced load), and are handed to
+// the whole wavefront with readlane, so that U rows of W are in flight per
+// step with no scalar load on the path.
 template <int V, bool VEC>
 __device__ __forceinline__ void row_block(const int32_t* acol, const float* aval, int64_t p0, int64_t p1,
                                           const float* W, int64_t ldw, int c, int F, float (&acc)[V]) {
-  int64_t p = p0;
-  for (; p + 4 <= p1; p += 4) {
-    float w[4][V];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) load_w<V, VEC>(W + (int64_t)acol[p + u] * ldw, c, F, w[u]);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float a = aval[p + u];
-#pragma unroll
-      for (int v = 0; v < V; ++v) acc[v] = fmaf(a, w[u][v], acc[v]);
+  constexpr int U = V <= 2 ? 8 : 4;
+  const int lane = threadIdx.x % WAVE;
+  for (int64_t pb = p0; pb < p1; pb += WAVE) {
+    const int cnt = (int)(p1 - pb < WAVE ? p1 - pb : WAVE);
+    int kl = 0;
+    float al = 0.f;
+    if (lane < cnt) {
+      kl = acol[pb + lane];
+      al = aval[pb + lane];
     }
-  }
-  for (; p < p1; ++p) {
-    float w[V];
-    load_w<V, VEC>(W + (int64_t)acol[p] * ldw, c, F, w);
-    const float a = aval[p];
+    int j = 0;
+    for (; j + U <= cnt; j += U) {
+      float w[U][V];
 #pragma unroll
-    for (int v = 0; v < V; ++v) acc[v] = fmaf(a, w[v], acc[v]);
+      for (int u = 0; u < U; ++u)
+        load_w<V, VEC>(W + (int64_t)__builtin_amdgcn_readlane(kl, j + u) * ldw, c, F, w[u]);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(al), j + u));
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] = fmaf(a, w[u][v], acc[v]);
+      }
+    }
+    for (; j < cnt; ++j) {
+      float w[V];
+      load_w<V, VEC>(W + (int64_t)__builtin_amdgcn_readlane(kl, j) * ldw, c, F, w);
+      const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(al), j));
+#pragma unroll
+      for (int v = 0; v < V; ++v) acc[v] = fmaf(a, w[v], acc[v]);
+    }
   }
 }
 
