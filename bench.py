@@ -8,6 +8,7 @@ symbolic phase, scan, the nnz read-back, C allocation, numeric phase
 
   python bench.py [--steps K] [--warmup W] [--workload 3] [--cpu-seconds S]
   python bench.py --workload 2 --combine 256    (the combination step, Eq. 3)
+  python bench.py --workload 3 --dense-h 256    (aggregation with dense features)
 
 value  = whole-job GFLOP/s (2 flops per intermediate product) per step.
 roofline = the dominant kernel (the numeric launch with the largest time):
@@ -224,6 +225,50 @@ def cpu_combine_baseline(C, W, seconds):
                       % (done, int(C.nnz), 100.0 * done / max(1, int(C.nnz)), dt)}
 
 
+def dense_aggregate(args, A, dA, gen_s):
+    """Y = A_norm * H for a dense H (aires_spmm without activation)."""
+    import torch
+    import paper_2507_02006_amd as aires
+    F = args.dense_h
+    g = torch.Generator(device="cuda").manual_seed(19)
+    H = torch.rand((A.ncols, F), generator=g, device="cuda") * 2 - 1
+    Y = torch.empty((A.nrows, F), dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        aires.spmm(dA, H, out=Y)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record()
+        aires.spmm(dA, H, out=Y)
+        e1.record()
+    torch.cuda.synchronize()
+    ms_per_step = 1e3 * (time.perf_counter() - t_start) / args.steps
+    launch_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    nnz, m, sA = int(A.nnz), int(A.nrows), A.rp.dtype.itemsize
+    flops = 2.0 * nnz * F
+    compulsory = sA * (m + 1) + 8 * nnz + 4 * A.ncols * F + 4 * m * F  # A, H once, Y
+    gather = sA * (m + 1) + 8 * nnz + 4 * nnz * F + 4 * m * F          # a row of H per entry of A
+    res = {
+        "metric": "SpMM GFLOP/s of the aggregation A_norm H with dense features (Eq. 1) on 1 MI355X",
+        "value": round(flops / (ms_per_step * 1e-3) / 1e9, 3),
+        "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded R-MAT graph; uniform random dense features)",
+        "config": {"workload": "cfg%d graph (%d nodes, %d nnz) times dense H (%d x %d)"
+                               % (args.workload, m, nnz, A.ncols, F),
+                   "m": m, "k": int(A.ncols), "f": F, "nnz_a": nnz, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "k_spmm_rows + k_spmm_heavy",
+                     "achieved": round(gather / (launch_ms * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gather / (launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "algorithmic_bytes": gather, "avg_launch_ms": round(launch_ms, 4),
+                     "compulsory_gbs": round(compulsory / (launch_ms * 1e-3) / 1e9, 2)},
+        "generation_s": round(gen_s, 2),
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -236,6 +281,9 @@ def main():
                     help="instead of the aggregation, time the combination step of the GCN layer "
                          "(Eq. 3): relu(C * W) with C the workload's aggregated features (computed once, "
                          "untimed) and a random dense W with F_OUT columns (aires_spmm)")
+    ap.add_argument("--dense-h", type=int, default=0, metavar="F",
+                    help="instead, time the next layer's aggregation A_norm * H with a dense H of F "
+                         "columns (Eq. 1 with dense features; aires_spmm), A the workload's graph")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run one device copy of this many MiB (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -262,6 +310,8 @@ def main():
     dA, dB = aires.to_device(A), aires.to_device(B)
     if args.combine:
         return combine(args, A, B, dA, dB, gen_s)
+    if args.dense_h:
+        return dense_aggregate(args, A, dA, gen_s)
     torch.cuda.synchronize()
     P = row_products(A, B)
     total_products = int(P.sum())
