@@ -386,7 +386,7 @@ struct GrainRange {
 };
 
 #ifndef AIRES_UNROLL
-#define AIRES_UNROLL 2
+#define AIRES_UNROLL 4
 #endif
 constexpr int UNROLL = AIRES_UNROLL;  // independent B loads each thread keeps in flight
 
