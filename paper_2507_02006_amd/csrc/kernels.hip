@@ -460,7 +460,7 @@ __device__ __forceinline__ int wave_share(int rn, int nw) {
 // into equal contiguous parts, one per wavefront, whose lane l takes terms
 // l, l + WAVE, ..., so consecutive lanes read consecutive entries of a B row.
 // P32: B positions fit 32 bits (wide products, nnz(B) < 2^31).
-template <int GROUP, int BLOCK, bool NUM, bool P32 = false, typename CH, typename SEG, typename F>
+template <int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, typename CH, typename SEG, typename F>
 __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group<GROUP, BLOCK>& g,
                                                  CH& ch, int64_t p0, int64_t p1, const SEG& seg, F&& f) {
   using S = typename CH::shift_t;
@@ -498,11 +498,11 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
       const int base = (int)r0 + wlo;
       // the wavefront's terms, each with the record of its segment
       auto terms = [&](auto rec_of) {
-        for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
-          PI pos[UNROLL];
-          float am[UNROLL];
+        for (int q0 = lane; q0 < wlen; q0 += WAVE * UR) {
+          PI pos[UR];
+          float am[UR];
 #pragma unroll
-          for (int u = 0; u < UNROLL; ++u) {
+          for (int u = 0; u < UR; ++u) {
             const int q = q0 + u * WAVE;
             pos[u] = -1;
             am[u] = 0.f;
@@ -512,10 +512,10 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
               am[u] = rc.av;
             }
           }
-          int j[UNROLL];
-          float bv[UNROLL];
+          int j[UR];
+          float bv[UR];
 #pragma unroll
-          for (int u = 0; u < UNROLL; ++u) {
+          for (int u = 0; u < UR; ++u) {
             j[u] = 0;
             bv[u] = 0.f;
             if (pos[u] >= 0) {
@@ -524,7 +524,7 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
             }
           }
 #pragma unroll
-          for (int u = 0; u < UNROLL; ++u)
+          for (int u = 0; u < UR; ++u)
             if (pos[u] >= 0) f(j[u], am[u] * bv[u]);
         }
       };
@@ -541,12 +541,13 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
 }
 
 // ... over the terms of A entries [p0, p1); the whole row:
-template <typename RA, int GROUP, int BLOCK, bool NUM, bool P32 = false, typename CH, typename SEG, typename F>
+template <typename RA, int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, typename CH, typename SEG,
+          typename F>
 __device__ __forceinline__ void for_each_term(const Operands& op, const Group<GROUP, BLOCK>& g,
                                               CH& ch, int64_t row, const SEG& seg, F&& f) {
   const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
   const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
-  for_each_term_in<GROUP, BLOCK, NUM, P32>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
+  for_each_term_in<GROUP, BLOCK, NUM, P32, UR>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
 }
 
 // -------------------------------------------------- dense path (narrow N)
@@ -930,6 +931,7 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 // entries, not its width.
 
 constexpr int WIN_BLOCK = 512;
+constexpr int WIN_UNROLL = 2;  // the numeric window kernel keeps fewer loads in flight (registers)
 
 template <typename S>
 __host__ __device__ constexpr size_t count_lds_bytes(int sg, int G) {
@@ -1253,11 +1255,11 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
               if (wlen <= 0) continue;
               const int base = (int)r0 + wlo;
               auto terms = [&](auto rec_of) {
-                for (int q0 = lane; q0 < wlen; q0 += WAVE * UNROLL) {
-                  int32_t pos[UNROLL];
-                  float am[UNROLL];
+                for (int q0 = lane; q0 < wlen; q0 += WAVE * WIN_UNROLL) {
+                  int32_t pos[WIN_UNROLL];
+                  float am[WIN_UNROLL];
 #pragma unroll
-                  for (int u = 0; u < UNROLL; ++u) {
+                  for (int u = 0; u < WIN_UNROLL; ++u) {
                     const int q = q0 + u * WAVE;
                     pos[u] = -1;
                     am[u] = 0.f;
@@ -1267,10 +1269,10 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                       am[u] = rc.av;
                     }
                   }
-                  int jv[UNROLL];
-                  float bv2[UNROLL];
+                  int jv[WIN_UNROLL];
+                  float bv2[WIN_UNROLL];
 #pragma unroll
-                  for (int u = 0; u < UNROLL; ++u) {
+                  for (int u = 0; u < WIN_UNROLL; ++u) {
                     jv[u] = 0;
                     bv2[u] = 0.f;
                     if (pos[u] >= 0) {
@@ -1279,7 +1281,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                     }
                   }
 #pragma unroll
-                  for (int u = 0; u < UNROLL; ++u) {
+                  for (int u = 0; u < WIN_UNROLL; ++u) {
                     if (pos[u] < 0) continue;
                     if (pass) add_at_rank(jv[u], am[u] * bv2[u]);
                     else set_bit(jv[u]);
@@ -1306,10 +1308,10 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         if (cached >= 0)
           load_bits();
         else
-          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true>(op, g, ch, row, seg,
+          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, WIN_UNROLL>(op, g, ch, row, seg,
                                                                [&](int j, float) { set_bit(j); });
         word_ranks();
-        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true>(op, g, ch, row, seg,
+        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true, WIN_UNROLL>(op, g, ch, row, seg,
                                                             [&](int j, float v) { add_at_rank(j, v); });
       }
       __syncthreads();
