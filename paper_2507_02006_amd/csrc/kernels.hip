@@ -975,7 +975,8 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
     // terms carry absolute columns: bma is the bitmap seen from column 0
     // (c0 is a multiple of 32, so a column's bit index is the same)
     uint32_t* bma = bm - (c0 >> 5);
-    for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true>(op, g, ch, row, seg, [&](int j, float) {
+    // eight B loads in flight per thread: the symbolic loop reads columns only
+    for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, row, seg, [&](int j, float) {
       atomicOr(&bma[j >> 5], 1u << (j & 31));
     });
     // per-grain popcounts: a wavefront per grain, lanes on consecutive words
