@@ -32,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
 METRIC = "SpGEMM GFLOP/s and achieved HBM GB/s (% of peak) on 1 MI355X; end-to-end latency"
 
 WORKLOAD_NAMES = {
@@ -143,6 +144,33 @@ def measured_traffic(kernel_name: str, dom_bytes_launch: int):
     return int(ent["traffic_bytes"])
 
 
+def spmm_kernels(algo, nnz, m, k):
+    """Kernel names aires_spmm launches for `algo` (its AUTO rule: dense
+    tiles from one entry in eight)."""
+    dense = algo == "dense_tiles" or (algo == "auto" and 8 * nnz >= m * k and k <= 1 << 30)
+    return "k_spmm_dense" if dense else "k_spmm_rows + k_spmm_heavy"
+
+
+def spmm_roofline(algo, m, k, F, nnz, flops, compulsory, gather, launch_ms):
+    """Entry gather: HBM-bound on the compulsory bytes (C, W once, Y).
+    Dense tiles: bound by the fp32 matrix cores on the m*K*F multiply-adds
+    they execute (the product's own 2*nnz*F flops beside it)."""
+    kern = spmm_kernels(algo, nnz, m, k)
+    sec = launch_ms * 1e-3
+    if kern == "k_spmm_dense":
+        dense_flops = 2.0 * m * k * F
+        return {"bound": "mfma", "kernel": kern, "achieved": round(dense_flops / sec / 1e12, 3),
+                "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(dense_flops / sec / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                "algorithmic_flops": dense_flops, "avg_launch_ms": round(launch_ms, 4),
+                "product_tflops": round(flops / sec / 1e12, 3),
+                "compulsory_gbs": round(compulsory / sec / 1e9, 2)}
+    return {"bound": "hbm", "kernel": kern, "achieved": round(compulsory / sec / 1e9, 2), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(compulsory / sec / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
+            "algorithmic_bytes": compulsory, "avg_launch_ms": round(launch_ms, 4),
+            "gather_model_gbs": round(gather / sec / 1e9, 2), "fp32_tflops": round(flops / sec / 1e12, 3)}
+
+
 def combine(args, A, B, dA, dB, gen_s):
     """The combination step relu(C W) on the aggregated features C = A B."""
     import torch
@@ -156,13 +184,13 @@ def combine(args, A, B, dA, dB, gen_s):
     W = (torch.rand((C.ncols, F), generator=g, device="cuda") - 0.5) / float(np.sqrt(C.ncols))
     Y = torch.empty((C.nrows, F), dtype=torch.float32, device="cuda")
     for _ in range(args.warmup):
-        aires.spmm(Cd, W, relu=True, out=Y)
+        aires.spmm(Cd, W, relu=True, out=Y, algo=args.spmm_algo)
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     t_start = time.perf_counter()
     for e0, e1 in ev:
         e0.record()
-        aires.spmm(Cd, W, relu=True, out=Y)
+        aires.spmm(Cd, W, relu=True, out=Y, algo=args.spmm_algo)
         e1.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
@@ -188,12 +216,7 @@ def combine(args, A, B, dA, dB, gen_s):
         "config": {"workload": "combination of cfg%d %s: C (%d x %d, %d nnz) times W (%d x %d), ReLU"
                                % (args.workload, WORKLOAD_NAMES[args.workload], m, C.ncols, nnz, C.ncols, F),
                    "m": m, "k": int(C.ncols), "f_out": F, "nnz_c": nnz, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "k_spmm_rows + k_spmm_heavy",
-                     "achieved": round(compulsory / (launch_ms * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(compulsory / (launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "traffic": None, "algorithmic_bytes": compulsory, "avg_launch_ms": round(launch_ms, 4),
-                     "gather_model_gbs": round(gather / (launch_ms * 1e-3) / 1e9, 2),
-                     "fp32_tflops": round(flops / (launch_ms * 1e-3) / 1e12, 3)},
+        "roofline": spmm_roofline(args.spmm_algo, m, int(C.ncols), F, nnz, flops, compulsory, gather, launch_ms),
         "generation_s": round(gen_s, 2),
     }
     if not args.no_cpu:
@@ -234,13 +257,13 @@ def dense_aggregate(args, A, dA, gen_s):
     H = torch.rand((A.ncols, F), generator=g, device="cuda") * 2 - 1
     Y = torch.empty((A.nrows, F), dtype=torch.float32, device="cuda")
     for _ in range(args.warmup):
-        aires.spmm(dA, H, out=Y)
+        aires.spmm(dA, H, out=Y, algo=args.spmm_algo)
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     t_start = time.perf_counter()
     for e0, e1 in ev:
         e0.record()
-        aires.spmm(dA, H, out=Y)
+        aires.spmm(dA, H, out=Y, algo=args.spmm_algo)
         e1.record()
     torch.cuda.synchronize()
     ms_per_step = 1e3 * (time.perf_counter() - t_start) / args.steps
@@ -259,7 +282,7 @@ def dense_aggregate(args, A, dA, gen_s):
         "config": {"workload": "cfg%d graph (%d nodes, %d nnz) times dense H (%d x %d)"
                                % (args.workload, m, nnz, A.ncols, F),
                    "m": m, "k": int(A.ncols), "f": F, "nnz_a": nnz, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "k_spmm_rows + k_spmm_heavy",
+        "roofline": {"bound": "hbm", "kernel": spmm_kernels(args.spmm_algo, nnz, m, int(A.ncols)),
                      "achieved": round(gather / (launch_ms * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gather / (launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": None, "algorithmic_bytes": gather, "avg_launch_ms": round(launch_ms, 4),
@@ -281,6 +304,8 @@ def main():
                     help="instead of the aggregation, time the combination step of the GCN layer "
                          "(Eq. 3): relu(C * W) with C the workload's aggregated features (computed once, "
                          "untimed) and a random dense W with F_OUT columns (aires_spmm)")
+    ap.add_argument("--spmm-algo", default="auto", choices=["auto", "rows", "dense_tiles"],
+                    help="kernel family of aires_spmm for --combine / --dense-h")
     ap.add_argument("--dense-h", type=int, default=0, metavar="F",
                     help="instead, time the next layer's aggregation A_norm * H with a dense H of F "
                          "columns (Eq. 1 with dense features; aires_spmm), A the workload's graph")

@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define AIRES_ABI_VERSION 1
+#define AIRES_ABI_VERSION 2
 
 typedef enum aires_status {
     AIRES_OK = 0,
@@ -288,6 +288,15 @@ typedef struct aires_stats {
 /* Activation applied by aires_spmm. */
 typedef enum aires_act { AIRES_ACT_NONE = 0, AIRES_ACT_RELU = 1 } aires_act;
 
+/* Kernel family of aires_spmm. */
+typedef enum aires_spmm_algo {
+    AIRES_SPMM_AUTO = 0,        /* DENSE_TILES when nnz(A) >= m*K/8 and K <= 2^30,
+                                   else ROWS                                 */
+    AIRES_SPMM_ROWS = 1,        /* each entry a_ik scales row k of W         */
+    AIRES_SPMM_DENSE_TILES = 2  /* 64-row tiles of A densified in LDS, fp32
+                                   matrix cores; work ~ m*K*F, K <= 2^30    */
+} aires_spmm_algo;
+
 /*
  * aires_spmm -- Y = act(A * W) for a sparse A and a dense W: the
  * combination step of a GCN layer (Sec. II-A, Eq. 3: the aggregated
@@ -297,18 +306,24 @@ typedef enum aires_act { AIRES_ACT_NONE = 0, AIRES_ACT_RELU = 1 } aires_act;
  * the same way).
  *
  * A: CSR descriptor with A->mem == AIRES_MEM_DEVICE (borrowed; rows m =
- * A->nrows, K = A->ncols).  W: device, row-major K x F, row stride ldw >= F
- * elements.  Y: device, row-major m x F, row stride ldy >= F, owned by the
- * caller; every element of the m x F block is overwritten (rows of A with
- * no entries give act(0) = 0); columns between F and ldy are untouched.
+ * A->nrows, K = A->ncols; canonical: columns in [0, K), strictly increasing
+ * per row).  W: device, row-major K x F, row stride ldw >= F elements.
+ * Y: device, row-major m x F, row stride ldy >= F, owned by the caller;
+ * every element of the m x F block is overwritten (rows of A with no
+ * entries give act(0) = 0); columns between F and ldy are untouched.
  * Work is enqueued on `stream` (a hipStream_t); the call allocates nothing
  * and returns once the kernels are enqueued.  Each element is a sum in
- * fp32 over the row's entries in an unspecified order.
- * Errors: AIRES_E_INVALID_ARG (NULL arrays, ldw < F, ldy < F, bad act),
- * AIRES_E_UNSUPPORTED (A not on the device, F >= 2^31), AIRES_E_HIP.
+ * fp32 over the row's products a_ik * w_kj in an unspecified order.
+ * DENSE_TILES also multiplies the row's absent entries, as zeros, with W:
+ * for finite W that adds exact zeros and changes nothing, but an Inf or NaN
+ * in row k of W then reaches every row of Y, not only rows with an entry
+ * in column k.  AUTO assumes W is finite (as layer weights are).
+ * Errors: AIRES_E_INVALID_ARG (NULL arrays, ldw < F, ldy < F, bad act or
+ * algo), AIRES_E_UNSUPPORTED (A not on the device, F >= 2^31, DENSE_TILES
+ * with K > 2^30), AIRES_E_HIP.
  */
 aires_status aires_spmm(const aires_csr *A, const float *W, int64_t ldw, int64_t F, float *Y, int64_t ldy,
-                        aires_act act, void *stream);
+                        aires_act act, aires_spmm_algo algo, void *stream);
 
 /* Statistics of the last aires_spgemm / aires_stream_tiles on the plan. */
 aires_status aires_plan_stats(const aires_plan *plan, aires_stats *stats);

@@ -193,13 +193,20 @@ def _stream_handle(stream):
     return stream.cuda_stream
 
 
-def spmm(A, W, relu: bool = False, out=None, stream=None):
+_SPMM_ALGOS = {"auto": 0, "rows": 1, "dense_tiles": 2}
+
+
+def spmm(A, W, relu: bool = False, out=None, stream=None, algo: str = "auto"):
     """Y = act(A * W) (aires_spmm): A a device CSR (a tuple as from
     ``to_device``, or an ``Output`` of ``spgemm``), W a dense device float32
     matrix with A.ncols rows (row stride W.stride(0)); act is ReLU when
-    ``relu``.  Returns Y (m x F float32, a new tensor unless ``out`` is
-    given); valid once ``stream`` reaches the enqueued kernels."""
+    ``relu``.  ``algo``: "auto", "rows" (entry gather) or "dense_tiles"
+    (densified 64-row tiles on the matrix cores).  Returns Y (m x F
+    float32, a new tensor unless ``out`` is given); valid once ``stream``
+    reaches the enqueued kernels."""
     import torch
+    if algo not in _SPMM_ALGOS:
+        raise ValueError("algo must be one of %s" % sorted(_SPMM_ALGOS))
     m, k, rp, col, val = _parts(A)
     if W.dim() != 2 or W.dtype != torch.float32 or W.stride(1) != 1 or W.shape[0] != k:
         raise ValueError("W must be a float32 (A.ncols x F) matrix with unit column stride")
@@ -210,7 +217,8 @@ def spmm(A, W, relu: bool = False, out=None, stream=None):
         raise ValueError("out must be a float32 (m x F) matrix with unit column stride")
     a = B_.make_csr(m, k, rp, col, val)
     B_.check(B_.load().aires_spmm(ctypes.byref(a), W.data_ptr(), W.stride(0), F, out.data_ptr(), out.stride(0),
-                                  B_.ACT_RELU if relu else B_.ACT_NONE, _stream_handle(stream)), "aires_spmm")
+                                  B_.ACT_RELU if relu else B_.ACT_NONE, _SPMM_ALGOS[algo],
+                                  _stream_handle(stream)), "aires_spmm")
     return out
 
 

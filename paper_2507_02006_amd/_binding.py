@@ -106,7 +106,8 @@ def load() -> ctypes.CDLL:
         "aires_plan_stats": (ctypes.c_int, [c_vp, P(Stats)]),
         "aires_csr_out_free": (None, [P(CsrOut)]),
         "aires_plan_destroy": (None, [c_vp]),
-        "aires_spmm": (ctypes.c_int, [P(Csr), c_vp, c_i64, c_i64, c_vp, c_i64, ctypes.c_int, c_vp]),
+        "aires_spmm": (ctypes.c_int, [P(Csr), c_vp, c_i64, c_i64, c_vp, c_i64, ctypes.c_int, ctypes.c_int,
+                                       c_vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -117,6 +118,7 @@ def load() -> ctypes.CDLL:
 
 
 ACT_NONE, ACT_RELU = 0, 1
+SPMM_AUTO, SPMM_ROWS, SPMM_DENSE_TILES = 0, 1, 2
 
 
 class AiresError(RuntimeError):

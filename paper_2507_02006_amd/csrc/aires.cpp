@@ -1246,18 +1246,28 @@ aires_status aires_stream_tiles(aires_plan* plan, void* h2d, void* compute, void
 }
 
 aires_status aires_spmm(const aires_csr* A, const float* W, int64_t ldw, int64_t F, float* Y, int64_t ldy,
-                        aires_act act, void* stream) {
+                        aires_act act, aires_spmm_algo algo, void* stream) {
   ST_TRY(check_csr_desc(A, "A"));
   if (A->mem != AIRES_MEM_DEVICE) return fail(AIRES_E_UNSUPPORTED, "aires_spmm needs A on the device");
   if (F < 0 || F >= (int64_t(1) << 31)) return fail(AIRES_E_UNSUPPORTED, "F = %lld out of range", (long long)F);
   if (act != AIRES_ACT_NONE && act != AIRES_ACT_RELU) return fail(AIRES_E_INVALID_ARG, "act %d invalid", (int)act);
+  if (algo != AIRES_SPMM_AUTO && algo != AIRES_SPMM_ROWS && algo != AIRES_SPMM_DENSE_TILES)
+    return fail(AIRES_E_INVALID_ARG, "algo %d invalid", (int)algo);
+  if (algo == AIRES_SPMM_DENSE_TILES && !kern::spmm_dense_fits(A->ncols) && A->nrows > 0 && F > 0)
+    return fail(AIRES_E_UNSUPPORTED, "dense tiles need K <= 2^30 (K = %lld)", (long long)A->ncols);
   if (A->nrows == 0 || F == 0) return AIRES_OK;
   if (ldw < F || ldy < F) return fail(AIRES_E_INVALID_ARG, "ldw %lld / ldy %lld below F %lld", (long long)ldw,
                                       (long long)ldy, (long long)F);
   if (!Y || !A->row_ptr || (A->nnz > 0 && (!W || !A->col_idx || !A->vals)))
     return fail(AIRES_E_INVALID_ARG, "NULL array");
-  HIP_TRY(kern::spmm(A->row_ptr, A->rp_type == AIRES_IDX_I64, A->col_idx, A->vals, A->nrows, W, ldw, F, Y, ldy,
-                     act == AIRES_ACT_RELU, (hipStream_t)stream));
+  // dense tiles do m*K*F multiply-adds against nnz*F gathered rows: worth it
+  // from about one entry in eight (measured on 512-column aggregates)
+  bool dense = algo == AIRES_SPMM_DENSE_TILES;
+  if (algo == AIRES_SPMM_AUTO)
+    dense = kern::spmm_dense_fits(A->ncols) && (double)A->nnz * 8.0 >= (double)A->nrows * (double)A->ncols;
+  if (dense && !W && A->ncols > 0) return fail(AIRES_E_INVALID_ARG, "NULL W (dense tiles read W)");
+  HIP_TRY(kern::spmm(A->row_ptr, A->rp_type == AIRES_IDX_I64, A->col_idx, A->vals, A->nrows, A->ncols, W, ldw, F,
+                     Y, ldy, act == AIRES_ACT_RELU, dense, (hipStream_t)stream));
   return AIRES_OK;
 }
 

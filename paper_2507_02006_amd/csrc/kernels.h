@@ -117,10 +117,13 @@ hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, i
 size_t scan_workspace_bytes(int64_t n);
 hipError_t scan_inplace(int64_t* x, int64_t n, void* ws, hipStream_t s);
 
-// Y = act(A * W) for CSR A (m rows) and dense row-major W (ldw) and Y (ldy),
-// F columns; relu != 0 applies max(0, .) before the store.
-hipError_t spmm(const void* arp, int rpa64, const int32_t* acol, const float* aval, int64_t m, const float* W,
-                int64_t ldw, int64_t F, float* Y, int64_t ldy, int relu, hipStream_t s);
+// Y = act(A * W) for CSR A (m x K) and dense row-major W (ldw) and Y (ldy),
+// F columns; relu != 0 applies max(0, .) before the store.  dense != 0
+// takes the MFMA dense-tile kernel (K must satisfy spmm_dense_fits), else
+// the entry-gather kernels.
+bool spmm_dense_fits(int64_t K);
+hipError_t spmm(const void* arp, int rpa64, const int32_t* acol, const float* aval, int64_t m, int64_t K,
+                const float* W, int64_t ldw, int64_t F, float* Y, int64_t ldy, int relu, int dense, hipStream_t s);
 
 size_t lds_bytes(int kind, int phase, int32_t W);
 size_t grain_count_lds(int sg, int G);

@@ -160,6 +160,186 @@ __global__ __launch_bounds__(SPMM_BLOCK) void k_spmm_heavy(const void* arp, cons
   }
 }
 
+// ---------------------------------------------------------------------------
+// Dense tiles on the matrix cores.  When A is dense enough (the aggregated
+// features of Eq. 3 typically are), reading one row of W per entry of A
+// costs more than a dense product over the zeros: a workgroup takes a
+// 64-row x 16*NT-column tile of Y, densifies A's rows 64 columns at a time
+// into LDS, stages the matching 64 x 16*NT block of W (transposed, k
+// contiguous), and accumulates with v_mfma_f32_16x16x4_f32.  Each wavefront
+// owns 16 rows and NT 16-column blocks of the tile.
+//
+// k order: for a 16-wide block of k, lane l (group g = l / 16, c = l % 16)
+// reads k = 4g .. 4g+3 of its row (A) and of its column (W) as one 16-byte
+// LDS load, and the four MFMA steps take those four k's in turn, so every
+// product a_ik w_kj meets its partner in the same step.  Absent entries are
+// zeros in the tile, and x + 0 * w = x exactly for finite w, so each
+// element is still a sum of the row's own products.
+constexpr int DT_M = 64;        // rows per tile
+constexpr int DT_K = 64;        // k per LDS chunk
+constexpr int DT_S = DT_K + 4;  // LDS row stride in floats: lanes c and c+1 sit 4 banks apart
+constexpr int DT_BLOCK = 256;   // four wavefronts, 16 rows each
+constexpr int DT_ENTRIES = 8;   // entries a thread loads per round (four threads per row)
+constexpr int NXCD = 8;         // gfx950 hands workgroups round-robin to its 8 XCDs
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// a wavefront-uniform 64-bit value in scalar registers
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// raw buffer over n 4-byte elements (gfx9 resource word 3: 32-bit data format)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)(4 * n), 0x00020000);
+}
+
+// Occupancy is LDS-bound at four (NT = 4) or three (NT = 8) workgroups per
+// CU; the register budget is set to match.
+template <typename RP, int NT, bool VEC, bool RELU>
+__global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 3 : 4) void k_spmm_dense(
+    const void* arp, const int32_t* acol, const float* aval, int64_t m, int K, const float* W, int64_t ldw, int F,
+    float* Y, int64_t ldy, int64_t nrt, int64_t nct, int64_t ntiles) {
+  constexpr int BN = 16 * NT;
+  __shared__ __align__(16) float As[DT_M * DT_S];  // [row][k]
+  __shared__ __align__(16) float Wt[BN * DT_S];    // [column][k]
+  const int t = threadIdx.x, lane = t % WAVE, wv = t / WAVE;
+  const int r = t / 4, q = t % 4;          // densify: four threads per row
+  const int g = lane / 16, c = lane % 16;  // MFMA operand position
+  // W staging: pass e moves columns 16e .. 16e+15 of the block; the thread
+  // takes row wk = 16 wv + c and columns 16e + 4g .. +3, so a row's 64 bytes
+  // come from one load of four lanes and the transposed LDS stores of a
+  // wavefront hit 64 distinct banks.
+  const int wk = 16 * wv + c;
+  // The grid is a multiple of 8 blocks, so a block's tiles all have its
+  // index mod 8 and stay on its XCD; the column tiles of one row tile are
+  // consecutive there and share A's entries through that XCD's L2.
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t x = tile % NXCD, i = tile / NXCD;
+    const int64_t rt = (i / nct) * NXCD + x, ct = i % nct;
+    if (rt >= nrt) continue;  // uniform over the workgroup
+    const int64_t row0 = rt * DT_M;
+    const int n0 = (int)ct * BN;
+    // A's entries of the tile go through buffer resources: a load past the
+    // tile's last entry returns 0 instead of touching memory, so the loads
+    // need no branches (the tile holds < 2^28 entries, K <= 2^22)
+    const int64_t e0 = uniform64(rp_at<RP>(arp, row0));
+    const int64_t e1 = uniform64(rp_at<RP>(arp, row0 + DT_M < m ? row0 + DT_M : m));
+    const __amdgpu_buffer_rsrc_t rc = make_rsrc(acol + e0, e1 - e0);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(aval + e0, e1 - e0);
+    int64_t cur = e0, p1 = e0;
+    if (row0 + r < m) {
+      cur = rp_at<RP>(arp, row0 + r);
+      p1 = rp_at<RP>(arp, row0 + r + 1);
+    }
+    int kc[DT_ENTRIES];
+    float kv[DT_ENTRIES];
+    int nval = 0;  // kc[e] belongs to the row while 4e < nval
+    float w[NT][4];
+    // the next 32 entries of the row; nothing here waits for the loads
+    auto load_entries = [&]() {
+      const int64_t left = p1 - cur - q;  // entries of the row at or after this thread's first
+      nval = left < 4 * DT_ENTRIES ? (int)left : 4 * DT_ENTRIES;
+      const int off = 4 * ((int)(cur - e0) + q);
+#pragma unroll
+      for (int e = 0; e < DT_ENTRIES; ++e) {
+        kc[e] = __builtin_amdgcn_raw_buffer_load_b32(rc, off + 16 * e, 0, 0);
+        kv[e] = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rv, off + 16 * e, 0, 0));
+      }
+    };
+    // this thread's share of W[k0 .. k0+64, n0 .. n0+BN); zeros past K and F.
+    // Whole chunks of interior tiles take plain 16-byte loads (a uniform branch).
+    auto load_w = [&](int k0) {
+      if (VEC && n0 + BN <= F && k0 + DT_K <= K) {
+        const float* wr = W + (int64_t)(k0 + wk) * ldw + n0 + 4 * g;
+#pragma unroll
+        for (int e = 0; e < NT; ++e) {
+          const float4 v = *reinterpret_cast<const float4*>(wr + 16 * e);
+          w[e][0] = v.x; w[e][1] = v.y; w[e][2] = v.z; w[e][3] = v.w;
+        }
+        return;
+      }
+#pragma unroll
+      for (int e = 0; e < NT; ++e) {
+        const int n = n0 + 16 * e + 4 * g;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          w[e][u] = k0 + wk < K && n + u < F ? W[(int64_t)(k0 + wk) * ldw + n + u] : 0.f;
+      }
+    };
+    f32x4 acc[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (K > 0) {
+      load_entries();
+      load_w(0);
+    }
+    for (int k0 = 0; k0 < K; k0 += DT_K) {
+      const int kend = k0 + DT_K;
+      __syncthreads();  // the previous chunk's operands have been read
+      // zero this thread's quarter of its row; the scatter below runs in the
+      // same wavefront after it, and LDS executes a wavefront's accesses in order
+#pragma unroll
+      for (int e = 0; e < DT_K / 16; ++e)
+        *reinterpret_cast<f32x4*>(&As[r * DT_S + q * 16 + 4 * e]) = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int e = 0; e < NT; ++e)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) Wt[(16 * e + 4 * g + u) * DT_S + wk] = w[e][u];
+      for (;;) {
+        int n_in = 0;
+#pragma unroll
+        for (int e = 0; e < DT_ENTRIES; ++e) {
+          // every entry is stored: one of another chunk (or a malformed
+          // column below k0) lands in the row's padding column DT_K, which
+          // the products never read, so the store needs no branch
+          const bool in = 4 * e < nval && kc[e] < kend;
+          const int kk = in && kc[e] >= k0 ? kc[e] - k0 : DT_K;
+          As[r * DT_S + kk] = kv[e];
+          n_in += in;
+        }
+        n_in += __shfl_xor(n_in, 1);
+        n_in += __shfl_xor(n_in, 2);
+        cur += n_in;
+        if (n_in < 4 * DT_ENTRIES) break;
+        load_entries();  // all 32 were below kend: the row has more in this chunk
+      }
+      // the next chunk's operands travel while this one is multiplied
+      if (kend < K) {
+        load_entries();
+        load_w(kend);
+      }
+      __syncthreads();
+      // 64 k in four blocks of 16; per step the NT accumulators are
+      // independent, so consecutive MFMAs never wait on each other
+#pragma unroll
+      for (int kb = 0; kb < DT_K; kb += 16) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(&As[(wv * 16 + c) * DT_S + kb + 4 * g]);
+        f32x4 b[NT];
+#pragma unroll
+        for (int j = 0; j < NT; ++j) b[j] = *reinterpret_cast<const f32x4*>(&Wt[(j * 16 + c) * DT_S + kb + 4 * g]);
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[j][s], acc[j], 0, 0, 0);
+      }
+    }
+    // the lane holds rows 4g .. 4g+3 of its wavefront's 16, column c of each block
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const int col = n0 + j * 16 + c;
+      if (col >= F) continue;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t row = row0 + wv * 16 + 4 * g + u;
+        if (row < m) Y[row * ldy + col] = RELU ? fmaxf(acc[j][u], 0.f) : acc[j][u];
+      }
+    }
+  }
+}
+
 template <typename RP, int V, bool VEC, bool RELU>
 hipError_t spmm_t(const void* arp, const int32_t* acol, const float* aval, int64_t m, const float* W, int64_t ldw,
                   int F, float* Y, int64_t ldy, hipStream_t s) {
@@ -200,11 +380,44 @@ hipError_t spmm_rp(int relu, const void* arp, const int32_t* acol, const float* 
   }
 }
 
+template <typename RP, int NT, bool VEC>
+hipError_t dense_t(int relu, const void* arp, const int32_t* acol, const float* aval, int64_t m, int K,
+                   const float* W, int64_t ldw, int F, float* Y, int64_t ldy, hipStream_t s) {
+  const int64_t nrt = (m + DT_M - 1) / DT_M, nct = (F + 16 * NT - 1) / (16 * NT);
+  const int64_t ntiles = (nrt + NXCD - 1) / NXCD * NXCD * nct;  // a multiple of NXCD
+  const int64_t grid = ntiles < 65536 ? ntiles : 65536;          // so is this
+  if (relu)
+    hipLaunchKernelGGL((k_spmm_dense<RP, NT, VEC, true>), dim3((unsigned)grid), dim3(DT_BLOCK), 0, s, arp, acol,
+                       aval, m, K, W, ldw, F, Y, ldy, nrt, nct, ntiles);
+  else
+    hipLaunchKernelGGL((k_spmm_dense<RP, NT, VEC, false>), dim3((unsigned)grid), dim3(DT_BLOCK), 0, s, arp, acol,
+                       aval, m, K, W, ldw, F, Y, ldy, nrt, nct, ntiles);
+  return hipGetLastError();
+}
+
+template <typename RP>
+hipError_t dense_rp(int relu, const void* arp, const int32_t* acol, const float* aval, int64_t m, int K,
+                    const float* W, int64_t ldw, int F, float* Y, int64_t ldy, hipStream_t s) {
+  const bool vec = ldw % 4 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
+  if (F > 64)
+    return vec ? dense_t<RP, 8, true>(relu, arp, acol, aval, m, K, W, ldw, F, Y, ldy, s)
+               : dense_t<RP, 8, false>(relu, arp, acol, aval, m, K, W, ldw, F, Y, ldy, s);
+  return vec ? dense_t<RP, 4, true>(relu, arp, acol, aval, m, K, W, ldw, F, Y, ldy, s)
+             : dense_t<RP, 4, false>(relu, arp, acol, aval, m, K, W, ldw, F, Y, ldy, s);
+}
+
 }  // namespace
 
-hipError_t spmm(const void* arp, int rpa64, const int32_t* acol, const float* aval, int64_t m, const float* W,
-                int64_t ldw, int64_t F, float* Y, int64_t ldy, int relu, hipStream_t s) {
+bool spmm_dense_fits(int64_t K) { return K >= 0 && K <= (int64_t(1) << 22); }
+
+hipError_t spmm(const void* arp, int rpa64, const int32_t* acol, const float* aval, int64_t m, int64_t K,
+                const float* W, int64_t ldw, int64_t F, float* Y, int64_t ldy, int relu, int dense, hipStream_t s) {
   if (m <= 0 || F <= 0) return hipSuccess;
+  if (dense) {
+    if (!spmm_dense_fits(K)) return hipErrorInvalidValue;
+    return rpa64 ? dense_rp<int64_t>(relu, arp, acol, aval, m, (int)K, W, ldw, (int)F, Y, ldy, s)
+                 : dense_rp<int32_t>(relu, arp, acol, aval, m, (int)K, W, ldw, (int)F, Y, ldy, s);
+  }
   return rpa64 ? spmm_rp<int64_t>(relu, arp, acol, aval, m, W, ldw, (int)F, Y, ldy, s)
                : spmm_rp<int32_t>(relu, arp, acol, aval, m, W, ldw, (int)F, Y, ldy, s);
 }

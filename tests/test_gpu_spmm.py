@@ -6,7 +6,10 @@ arbitrary order with fused multiply-adds,
     |y - y64| <= (n_i + 2) * 2^-24 * sum_k |a_ik w_kj| + 2^-24 * |y64|,
 where n_i is the number of stored entries of row i (the standard bound
 gamma_n for a sum of n_i rounded terms, plus the final rounding); exact
-(bit-equal to the integer product) when every value is a small integer."""
+(bit-equal to the integer product) when every value is a small integer.
+Both kernel families are held to it: the entry gather ("rows") and the
+densified tiles on the matrix cores ("dense_tiles"), whose extra products
+with absent entries are exact zeros for finite W."""
 import numpy as np
 import pytest
 
@@ -17,6 +20,7 @@ from workloads import CSR
 pytestmark = pytest.mark.gpu
 
 U = 2.0 ** -24
+ALGOS = ["rows", "dense_tiles"]
 
 
 @pytest.fixture(scope="module")
@@ -38,16 +42,17 @@ def dev_csr(torch, A, rp64=False):
             torch.from_numpy(A.val.astype(np.float32)).cuda())
 
 
-def check(torch, A, W, relu=False, rp64=False, ldw_pad=0, ldy_pad=0, w_offset=0, exact=False, name=""):
+def check(torch, A, W, relu=False, rp64=False, ldw_pad=0, ldy_pad=0, w_offset=0, exact=False, name="",
+          algo="auto"):
     import paper_2507_02006_amd as aires
-    say("%s m=%d K=%d F=%d relu=%d rp64=%d pads=(%d,%d) off=%d" % (name, A.nrows, A.ncols, W.shape[1], relu, rp64,
-                                                                  ldw_pad, ldy_pad, w_offset))
+    say("%s algo=%s m=%d K=%d F=%d relu=%d rp64=%d pads=(%d,%d) off=%d" % (
+        name, algo, A.nrows, A.ncols, W.shape[1], relu, rp64, ldw_pad, ldy_pad, w_offset))
     K, F = W.shape
     buf = torch.zeros(K * (F + ldw_pad) + w_offset + 1, dtype=torch.float32, device="cuda")
     Wd = buf[w_offset:w_offset + K * (F + ldw_pad)].view(K, F + ldw_pad)[:, :F]
     Wd.copy_(torch.from_numpy(W))
     ybuf = torch.full((A.nrows, F + ldy_pad), 7.0, dtype=torch.float32, device="cuda")
-    Y = aires.spmm(dev_csr(torch, A, rp64), Wd, relu=relu, out=ybuf[:, :F])
+    Y = aires.spmm(dev_csr(torch, A, rp64), Wd, relu=relu, out=ybuf[:, :F], algo=algo)
     torch.cuda.synchronize()
     y = Y.cpu().numpy().astype(np.float64)
     if ldy_pad:
@@ -63,25 +68,28 @@ def check(torch, A, W, relu=False, rp64=False, ldw_pad=0, ldy_pad=0, w_offset=0,
     assert not bad.any(), "%s: %d entries over the bound, worst %g" % (name, bad.sum(), (err - tol).max())
 
 
-@pytest.mark.parametrize("F", [1, 7, 64, 100, 128, 200, 256, 512, 700])
-def test_widths(torch_gpu, F):
-    """One wavefront pass covers 64*V columns (V = 1, 2, 4, 8); 700 takes two
-    passes; F not a multiple of the vector takes the scalar tail."""
+@pytest.mark.parametrize("algo", ALGOS)
+@pytest.mark.parametrize("F", [1, 7, 64, 65, 100, 128, 129, 200, 256, 512, 700])
+def test_widths(torch_gpu, F, algo):
+    """Rows: one wavefront pass covers 64*V columns (V = 1, 2, 4, 8); 700
+    takes two passes; F not a multiple of the vector takes the scalar tail.
+    Dense tiles: 64- or 128-column tiles, ragged in m (300), K (90) and F."""
     rng = np.random.default_rng(F)
     A = workloads.random_csr(rng, 300, 90, 0.05)
     W = rng.uniform(-1, 1, (90, F)).astype(np.float32)
-    check(torch_gpu, A, W, name="width %d" % F)
+    check(torch_gpu, A, W, name="width %d" % F, algo=algo)
 
 
+@pytest.mark.parametrize("algo", ALGOS)
 @pytest.mark.parametrize("relu", [False, True])
-def test_integer_values_exact(torch_gpu, relu):
+def test_integer_values_exact(torch_gpu, relu, algo):
     """Small integers: every product and partial sum is exact in fp32, so Y
     equals the integer product whatever the order."""
     rng = np.random.default_rng(5)
     Ad = rng.integers(-3, 4, (257, 129)) * (rng.random((257, 129)) < 0.1)
     A = CSR(257, 129, *_csr_parts(Ad))
     W = rng.integers(-3, 4, (129, 96)).astype(np.float32)
-    check(torch_gpu, A, W, relu=relu, exact=True, name="integer relu=%d" % relu)
+    check(torch_gpu, A, W, relu=relu, exact=True, name="integer relu=%d" % relu, algo=algo)
 
 
 def _csr_parts(D):
@@ -91,9 +99,12 @@ def _csr_parts(D):
     return np.cumsum(rp).astype(np.int32), cols.astype(np.int32), D[rows, cols].astype(np.float32)
 
 
-def test_heavy_rows_split_over_a_workgroup(torch_gpu):
+@pytest.mark.parametrize("algo", ALGOS)
+def test_heavy_rows_split_over_a_workgroup(torch_gpu, algo):
     """Rows above 512 entries take the workgroup kernel (four wavefronts
-    and an LDS reduction); mixed with light and empty rows."""
+    and an LDS reduction); mixed with light and empty rows.  For dense
+    tiles, rows with more than 32 entries in a 64-column chunk take several
+    load rounds."""
     rng = np.random.default_rng(7)
     K = 3000
     lens = np.array([0, 3, 513, 512, 2999, 0, 1, 1500, 700, 5] * 4)
@@ -103,18 +114,20 @@ def test_heavy_rows_split_over_a_workgroup(torch_gpu):
     A = CSR(len(lens), K, rp, col, val)
     for F in (64, 256, 600):
         W = rng.uniform(-1, 1, (K, F)).astype(np.float32)
-        check(torch_gpu, A, W, relu=True, name="heavy F=%d" % F)
+        check(torch_gpu, A, W, relu=True, name="heavy F=%d" % F, algo=algo)
 
 
-def test_strides_offsets_and_rp64(torch_gpu):
+@pytest.mark.parametrize("algo", ALGOS)
+def test_strides_offsets_and_rp64(torch_gpu, algo):
     """Row strides above F (padding untouched), a W base that is not
     vector-aligned (scalar loads), and 64-bit row pointers."""
     rng = np.random.default_rng(8)
     A = workloads.random_csr(rng, 200, 70, 0.1)
     W = rng.uniform(-1, 1, (70, 256)).astype(np.float32)
-    check(torch_gpu, A, W, ldw_pad=3, ldy_pad=5, name="pads")
-    check(torch_gpu, A, W, w_offset=1, name="unaligned W")
-    check(torch_gpu, A, W, rp64=True, relu=True, name="rp64")
+    check(torch_gpu, A, W, ldw_pad=3, ldy_pad=5, name="pads", algo=algo)
+    check(torch_gpu, A, W, ldw_pad=4, name="aligned pad", algo=algo)
+    check(torch_gpu, A, W, w_offset=1, name="unaligned W", algo=algo)
+    check(torch_gpu, A, W, rp64=True, relu=True, name="rp64", algo=algo)
 
 
 def test_edges(torch_gpu):
@@ -123,7 +136,10 @@ def test_edges(torch_gpu):
     rng = np.random.default_rng(9)
     E = CSR(6, 10, np.zeros(7, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
     W = rng.uniform(-1, 1, (10, 33)).astype(np.float32)
-    check(torch, E, W, name="all rows empty")
+    for algo in ALGOS:
+        check(torch, E, W, name="all rows empty", algo=algo)
+    check(torch, CSR(5, 0, np.zeros(6, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32)),
+          np.zeros((0, 20), np.float32), name="K = 0", algo="dense_tiles")
     Y = aires.spmm(dev_csr(torch, CSR(0, 10, np.zeros(1, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))),
                    torch.from_numpy(W).cuda())
     assert Y.shape == (0, 33)
@@ -132,6 +148,43 @@ def test_edges(torch_gpu):
     assert Y.shape == (8, 0)
     with pytest.raises(ValueError):
         aires.spmm(dev_csr(torch, A), torch.zeros((11, 4), device="cuda"))
+    with pytest.raises(ValueError):
+        aires.spmm(dev_csr(torch, A), torch.zeros((10, 4), device="cuda"), algo="gemm")
+
+
+@pytest.mark.parametrize("density", [0.3, 1.0])
+def test_dense_tiles_dense_rows(torch_gpu, density):
+    """Fully dense and 30 % rows: 64 entries per 64-column chunk (two load
+    rounds of 32 and a third that finds the chunk's end), K not a multiple
+    of 64, several column tiles on the XCD-ordered grid."""
+    rng = np.random.default_rng(int(density * 10))
+    A = workloads.random_csr(rng, 517, 333, density)
+    for F in (48, 300):
+        W = rng.uniform(-1, 1, (333, F)).astype(np.float32)
+        check(torch_gpu, A, W, relu=True, name="dense rows %.1f F=%d" % (density, F), algo="dense_tiles")
+
+
+def test_dense_tiles_grid_loop(torch_gpu):
+    """More tiles than the grid (65536 blocks): the second sweep of the
+    persistent loop, checked on sampled rows and the last rows (1 075 200
+    rows, one entry each, K = 16, F = 512: 67200 tiles)."""
+    import paper_2507_02006_amd as aires
+    torch = torch_gpu
+    rng = np.random.default_rng(12)
+    m, K, F = 1075200, 16, 512
+    rp = np.arange(m + 1, dtype=np.int32)
+    col = (np.arange(m) * 7 % K).astype(np.int32)
+    val = rng.integers(-4, 5, m).astype(np.float32)
+    A = CSR(m, K, rp, col, val)
+    W = rng.integers(-8, 9, (K, F)).astype(np.float32)
+    say("grid loop m=%d K=%d F=%d" % (m, K, F))
+    Y = aires.spmm(dev_csr(torch, A), torch.from_numpy(W).cuda(), algo="dense_tiles")
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([rng.integers(0, m, 2000), np.arange(m - 3000, m)]))
+    y = Y[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+    sub = CSR(len(rows), K, np.arange(len(rows) + 1, dtype=np.int32), col[rows], val[rows])
+    ref, _ = oracle.spmm(sub, W)
+    assert np.array_equal(y, ref)
 
 
 def test_gcn_layer_on_aggregated_features(torch_gpu):
