@@ -147,7 +147,7 @@ def measured_traffic(kernel_name: str, dom_bytes_launch: int):
 def spmm_kernels(algo, nnz, m, k):
     """Kernel names aires_spmm launches for `algo` (its AUTO rule: dense
     tiles from one entry in eight)."""
-    dense = algo == "dense_tiles" or (algo == "auto" and 8 * nnz >= m * k and k <= 1 << 30)
+    dense = algo == "dense_tiles" or (algo == "auto" and 8 * nnz >= m * k and k <= 1 << 20)
     return "k_spmm_dense" if dense else "k_spmm_rows + k_spmm_heavy"
 
 

@@ -290,11 +290,11 @@ typedef enum aires_act { AIRES_ACT_NONE = 0, AIRES_ACT_RELU = 1 } aires_act;
 
 /* Kernel family of aires_spmm. */
 typedef enum aires_spmm_algo {
-    AIRES_SPMM_AUTO = 0,        /* DENSE_TILES when nnz(A) >= m*K/8 and K <= 2^30,
-                                   else ROWS                                 */
+    AIRES_SPMM_AUTO = 0,        /* DENSE_TILES when nnz(A) >= m*K/8, K <= 2^20
+                                   and ldw < 2^23, else ROWS                 */
     AIRES_SPMM_ROWS = 1,        /* each entry a_ik scales row k of W         */
     AIRES_SPMM_DENSE_TILES = 2  /* 64-row tiles of A densified in LDS, fp32
-                                   matrix cores; work ~ m*K*F, K <= 2^30    */
+                                   matrix cores; work ~ m*K*F               */
 } aires_spmm_algo;
 
 /*
@@ -320,7 +320,7 @@ typedef enum aires_spmm_algo {
  * in column k.  AUTO assumes W is finite (as layer weights are).
  * Errors: AIRES_E_INVALID_ARG (NULL arrays, ldw < F, ldy < F, bad act or
  * algo), AIRES_E_UNSUPPORTED (A not on the device, F >= 2^31, DENSE_TILES
- * with K > 2^30), AIRES_E_HIP.
+ * with K > 2^20 or ldw >= 2^23), AIRES_E_HIP.
  */
 aires_status aires_spmm(const aires_csr *A, const float *W, int64_t ldw, int64_t F, float *Y, int64_t ldy,
                         aires_act act, aires_spmm_algo algo, void *stream);

@@ -1253,8 +1253,9 @@ aires_status aires_spmm(const aires_csr* A, const float* W, int64_t ldw, int64_t
   if (act != AIRES_ACT_NONE && act != AIRES_ACT_RELU) return fail(AIRES_E_INVALID_ARG, "act %d invalid", (int)act);
   if (algo != AIRES_SPMM_AUTO && algo != AIRES_SPMM_ROWS && algo != AIRES_SPMM_DENSE_TILES)
     return fail(AIRES_E_INVALID_ARG, "algo %d invalid", (int)algo);
-  if (algo == AIRES_SPMM_DENSE_TILES && !kern::spmm_dense_fits(A->ncols) && A->nrows > 0 && F > 0)
-    return fail(AIRES_E_UNSUPPORTED, "dense tiles need K <= 2^30 (K = %lld)", (long long)A->ncols);
+  if (algo == AIRES_SPMM_DENSE_TILES && !kern::spmm_dense_fits(A->ncols, ldw) && A->nrows > 0 && F > 0)
+    return fail(AIRES_E_UNSUPPORTED, "dense tiles need K <= 2^20 and ldw < 2^23 (K = %lld, ldw = %lld)",
+                (long long)A->ncols, (long long)ldw);
   if (A->nrows == 0 || F == 0) return AIRES_OK;
   if (ldw < F || ldy < F) return fail(AIRES_E_INVALID_ARG, "ldw %lld / ldy %lld below F %lld", (long long)ldw,
                                       (long long)ldy, (long long)F);
@@ -1264,7 +1265,7 @@ aires_status aires_spmm(const aires_csr* A, const float* W, int64_t ldw, int64_t
   // from about one entry in eight (measured on 512-column aggregates)
   bool dense = algo == AIRES_SPMM_DENSE_TILES;
   if (algo == AIRES_SPMM_AUTO)
-    dense = kern::spmm_dense_fits(A->ncols) && (double)A->nnz * 8.0 >= (double)A->nrows * (double)A->ncols;
+    dense = kern::spmm_dense_fits(A->ncols, ldw) && (double)A->nnz * 8.0 >= (double)A->nrows * (double)A->ncols;
   if (dense && !W && A->ncols > 0) return fail(AIRES_E_INVALID_ARG, "NULL W (dense tiles read W)");
   HIP_TRY(kern::spmm(A->row_ptr, A->rp_type == AIRES_IDX_I64, A->col_idx, A->vals, A->nrows, A->ncols, W, ldw, F,
                      Y, ldy, act == AIRES_ACT_RELU, dense, (hipStream_t)stream));

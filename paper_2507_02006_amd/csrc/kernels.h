@@ -119,9 +119,9 @@ hipError_t scan_inplace(int64_t* x, int64_t n, void* ws, hipStream_t s);
 
 // Y = act(A * W) for CSR A (m x K) and dense row-major W (ldw) and Y (ldy),
 // F columns; relu != 0 applies max(0, .) before the store.  dense != 0
-// takes the MFMA dense-tile kernel (K must satisfy spmm_dense_fits), else
+// takes the MFMA dense-tile kernel (K, ldw must satisfy spmm_dense_fits), else
 // the entry-gather kernels.
-bool spmm_dense_fits(int64_t K);
+bool spmm_dense_fits(int64_t K, int64_t ldw);
 hipError_t spmm(const void* arp, int rpa64, const int32_t* acol, const float* aval, int64_t m, int64_t K,
                 const float* W, int64_t ldw, int64_t F, float* Y, int64_t ldy, int relu, int dense, hipStream_t s);
 

@@ -164,25 +164,35 @@ __global__ __launch_bounds__(SPMM_BLOCK) void k_spmm_heavy(const void* arp, cons
 // Dense tiles on the matrix cores.  When A is dense enough (the aggregated
 // features of Eq. 3 typically are), reading one row of W per entry of A
 // costs more than a dense product over the zeros: a workgroup takes a
-// 64-row x 16*NT-column tile of Y, densifies A's rows 64 columns at a time
-// into LDS, stages the matching 64 x 16*NT block of W (transposed, k
-// contiguous), and accumulates with v_mfma_f32_16x16x4_f32.  Each wavefront
-// owns 16 rows and NT 16-column blocks of the tile.
+// 64-row x 16*NT-column tile of Y, densifies A's rows 32 columns at a time
+// into LDS, stages the matching 32 x 16*NT block of W (transposed, k
+// contiguous), and accumulates with v_mfma_f32_32x32x2_f32 (it sustains a
+// larger share of the fp32 matrix peak than the 16x16x4 form).  Each
+// wavefront owns 32 rows and 8*NT columns (NT/4 blocks of 32) of the tile.
 //
-// k order: for a 16-wide block of k, lane l (group g = l / 16, c = l % 16)
-// reads k = 4g .. 4g+3 of its row (A) and of its column (W) as one 16-byte
-// LDS load, and the four MFMA steps take those four k's in turn, so every
+// k order: for an 8-wide block of k, lane l (h = l / 32, c = l % 32) reads
+// k = 4h .. 4h+3 of its row (A) and of its column (W) as one 16-byte LDS
+// load, and the four MFMA steps take those four k's in turn, so every
 // product a_ik w_kj meets its partner in the same step.  Absent entries are
 // zeros in the tile, and x + 0 * w = x exactly for finite w, so each
 // element is still a sum of the row's own products.
+//
+// Pipeline: LDS holds two chunks.  While the wavefronts multiply chunk c
+// from one buffer they write chunk c+1 (loaded during chunk c-1) into the
+// other and issue the loads of chunk c+2, so one barrier per chunk
+// suffices and the staging work interleaves with the MFMAs.  Every load
+// goes through a buffer resource: out-of-range offsets read 0 without
+// touching memory, so the loop body has no branches.
 constexpr int DT_M = 64;        // rows per tile
-constexpr int DT_K = 64;        // k per LDS chunk
-constexpr int DT_S = DT_K + 4;  // LDS row stride in floats: lanes c and c+1 sit 4 banks apart
+constexpr int DT_K = 32;        // k per LDS chunk
+constexpr int DT_S = DT_K + 4;  // LDS row stride in floats: 16-byte reads of 16 rows hit 64 distinct banks
 constexpr int DT_BLOCK = 256;   // four wavefronts, 16 rows each
-constexpr int DT_ENTRIES = 8;   // entries a thread loads per round (four threads per row)
+constexpr int DT_ENTRIES = DT_K / 4;  // four threads per row: one round of loads covers a chunk
 constexpr int NXCD = 8;         // gfx950 hands workgroups round-robin to its 8 XCDs
+constexpr int kOutOfRange = INT32_MIN;  // a buffer offset no resource here reaches (reads 0)
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // a wavefront-uniform 64-bit value in scalar registers
 __device__ __forceinline__ int64_t uniform64(int64_t v) {
@@ -191,28 +201,32 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-// raw buffer over n 4-byte elements (gfx9 resource word 3: 32-bit data format)
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t n) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)(4 * n), 0x00020000);
+// raw buffer over `bytes` bytes (gfx9 resource word 3: 32-bit data format)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-// Occupancy is LDS-bound at four (NT = 4) or three (NT = 8) workgroups per
-// CU; the register budget is set to match.
+// Occupancy is LDS-bound (two chunks per workgroup): four workgroups per CU
+// at NT = 4, two at NT = 8; the register budget is set to match.
 template <typename RP, int NT, bool VEC, bool RELU>
-__global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 3 : 4) void k_spmm_dense(
+__global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 2 : 4) void k_spmm_dense(
     const void* arp, const int32_t* acol, const float* aval, int64_t m, int K, const float* W, int64_t ldw, int F,
     float* Y, int64_t ldy, int64_t nrt, int64_t nct, int64_t ntiles) {
   constexpr int BN = 16 * NT;
-  __shared__ __align__(16) float As[DT_M * DT_S];  // [row][k]
-  __shared__ __align__(16) float Wt[BN * DT_S];    // [column][k]
+  constexpr int WL = NT / 2;  // 16-byte W loads per thread per chunk (32 x BN floats over 256 threads)
+  __shared__ __align__(16) float As[2][DT_M * DT_S];  // [row][k]
+  __shared__ __align__(16) float Wt[2][BN * DT_S];    // [column][k]
+  constexpr int NB = BN / 64;  // 32-column MFMA blocks per wavefront
   const int t = threadIdx.x, lane = t % WAVE, wv = t / WAVE;
-  const int r = t / 4, q = t % 4;          // densify: four threads per row
-  const int g = lane / 16, c = lane % 16;  // MFMA operand position
-  // W staging: pass e moves columns 16e .. 16e+15 of the block; the thread
-  // takes row wk = 16 wv + c and columns 16e + 4g .. +3, so a row's 64 bytes
-  // come from one load of four lanes and the transposed LDS stores of a
-  // wavefront hit 64 distinct banks.
-  const int wk = 16 * wv + c;
+  const int r = t / 4, q = t % 4;             // densify: four threads per row
+  const int h = lane / 32, c = lane % 32;     // MFMA operand position
+  const int mr = 32 * (wv >> 1), mc = (wv & 1) * (BN / 2);  // the wavefront's rows and columns
+  // W staging: the thread takes row wk of the chunk and, for e < WL, the
+  // columns wc + 16e .. +3; a row's 64 bytes come from four lanes, and the
+  // transposed LDS stores of a wavefront hit 64 distinct banks.
+  const int wk = lane % 16 + 16 * (wv & 1);
+  const int wc = (wv >> 1) * (BN / 2) + 4 * (lane / 16);
+  const int nch = (K + DT_K - 1) / DT_K;
   // The grid is a multiple of 8 blocks, so a block's tiles all have its
   // index mod 8 and stay on its XCD; the column tiles of one row tile are
   // consecutive there and share A's entries through that XCD's L2.
@@ -222,119 +236,125 @@ __global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 3 : 4) void k_spmm_dense(
     if (rt >= nrt) continue;  // uniform over the workgroup
     const int64_t row0 = rt * DT_M;
     const int n0 = (int)ct * BN;
-    // A's entries of the tile go through buffer resources: a load past the
-    // tile's last entry returns 0 instead of touching memory, so the loads
-    // need no branches (the tile holds < 2^28 entries, K <= 2^22)
+    // A's entries of the tile (< 2^26 of them: K <= 2^20), positions relative to e0
     const int64_t e0 = uniform64(rp_at<RP>(arp, row0));
     const int64_t e1 = uniform64(rp_at<RP>(arp, row0 + DT_M < m ? row0 + DT_M : m));
-    const __amdgpu_buffer_rsrc_t rc = make_rsrc(acol + e0, e1 - e0);
-    const __amdgpu_buffer_rsrc_t rv = make_rsrc(aval + e0, e1 - e0);
-    int64_t cur = e0, p1 = e0;
+    const __amdgpu_buffer_rsrc_t rc = make_rsrc(acol + e0, 4 * (e1 - e0));
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(aval + e0, 4 * (e1 - e0));
+    // the row's entries as tile-local positions [cur, p1)
+    int cur = 0, p1 = 0;
     if (row0 + r < m) {
-      cur = rp_at<RP>(arp, row0 + r);
-      p1 = rp_at<RP>(arp, row0 + r + 1);
+      cur = (int)(rp_at<RP>(arp, row0 + r) - e0);
+      p1 = (int)(rp_at<RP>(arp, row0 + r + 1) - e0);
     }
     int kc[DT_ENTRIES];
     float kv[DT_ENTRIES];
     int nval = 0;  // kc[e] belongs to the row while 4e < nval
-    float w[NT][4];
-    // the next 32 entries of the row; nothing here waits for the loads
+    f32x4 w[WL];
+    // the row's next 32 entries; nothing here waits for the loads
     auto load_entries = [&]() {
-      const int64_t left = p1 - cur - q;  // entries of the row at or after this thread's first
-      nval = left < 4 * DT_ENTRIES ? (int)left : 4 * DT_ENTRIES;
-      const int off = 4 * ((int)(cur - e0) + q);
+      nval = p1 - cur - q;  // entries of the row at or after this thread's first
+      const int off = 4 * (cur + q);
 #pragma unroll
       for (int e = 0; e < DT_ENTRIES; ++e) {
         kc[e] = __builtin_amdgcn_raw_buffer_load_b32(rc, off + 16 * e, 0, 0);
         kv[e] = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rv, off + 16 * e, 0, 0));
       }
     };
-    // this thread's share of W[k0 .. k0+64, n0 .. n0+BN); zeros past K and F.
-    // Whole chunks of interior tiles take plain 16-byte loads (a uniform branch).
+    // this thread's share of rows k0 .. k0+32 of W[:, n0 .. n0+BN): rows
+    // past K are outside the resource, columns past F get an out-of-range
+    // offset, so both read as zeros (F <= ldw < 2^23 keeps offsets in int)
     auto load_w = [&](int k0) {
-      if (VEC && n0 + BN <= F && k0 + DT_K <= K) {
-        const float* wr = W + (int64_t)(k0 + wk) * ldw + n0 + 4 * g;
+      const int rows = K - k0 < DT_K ? (K - k0 > 0 ? K - k0 : 0) : DT_K;
+      const __amdgpu_buffer_rsrc_t rw = make_rsrc(W + (int64_t)k0 * ldw + n0, 4 * (int64_t)rows * ldw);
 #pragma unroll
-        for (int e = 0; e < NT; ++e) {
-          const float4 v = *reinterpret_cast<const float4*>(wr + 16 * e);
-          w[e][0] = v.x; w[e][1] = v.y; w[e][2] = v.z; w[e][3] = v.w;
+      for (int e = 0; e < WL; ++e) {
+        const int n = wc + 16 * e;  // column within the tile
+        const int base = 4 * (wk * (int)ldw + n);
+        if constexpr (VEC) {
+          // n0 + n, F and ldw are multiples of 4: the 16 bytes are all
+          // columns below F or all past it
+          w[e] = __builtin_bit_cast(
+              f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, n0 + n < F ? base : kOutOfRange, 0, 0));
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            w[e][u] = __int_as_float(
+                __builtin_amdgcn_raw_buffer_load_b32(rw, n0 + n + u < F ? base + 4 * u : kOutOfRange, 0, 0));
         }
-        return;
-      }
-#pragma unroll
-      for (int e = 0; e < NT; ++e) {
-        const int n = n0 + 16 * e + 4 * g;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          w[e][u] = k0 + wk < K && n + u < F ? W[(int64_t)(k0 + wk) * ldw + n + u] : 0.f;
       }
     };
-    f32x4 acc[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (K > 0) {
-      load_entries();
-      load_w(0);
-    }
-    for (int k0 = 0; k0 < K; k0 += DT_K) {
-      const int kend = k0 + DT_K;
-      __syncthreads();  // the previous chunk's operands have been read
+    // chunk k0 from the registers into LDS buffer b
+    auto write_chunk = [&](int b, int k0) {
       // zero this thread's quarter of its row; the scatter below runs in the
       // same wavefront after it, and LDS executes a wavefront's accesses in order
 #pragma unroll
       for (int e = 0; e < DT_K / 16; ++e)
-        *reinterpret_cast<f32x4*>(&As[r * DT_S + q * 16 + 4 * e]) = f32x4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<f32x4*>(&As[b][r * DT_S + q * (DT_K / 4) + 4 * e]) = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int e = 0; e < NT; ++e)
+      for (int e = 0; e < WL; ++e)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) Wt[(16 * e + 4 * g + u) * DT_S + wk] = w[e][u];
-      for (;;) {
-        int n_in = 0;
+        for (int u = 0; u < 4; ++u) Wt[b][(wc + 16 * e + u) * DT_S + wk] = w[e][u];
+      // 32 entries cover the 32 columns: every entry of the row in the
+      // chunk is here.  Each is stored; one of a later chunk lands in the
+      // padding column DT_K, which the products never read.
+      int n_in = 0;
 #pragma unroll
-        for (int e = 0; e < DT_ENTRIES; ++e) {
-          // every entry is stored: one of another chunk (or a malformed
-          // column below k0) lands in the row's padding column DT_K, which
-          // the products never read, so the store needs no branch
-          const bool in = 4 * e < nval && kc[e] < kend;
-          const int kk = in && kc[e] >= k0 ? kc[e] - k0 : DT_K;
-          As[r * DT_S + kk] = kv[e];
-          n_in += in;
-        }
-        n_in += __shfl_xor(n_in, 1);
-        n_in += __shfl_xor(n_in, 2);
-        cur += n_in;
-        if (n_in < 4 * DT_ENTRIES) break;
-        load_entries();  // all 32 were below kend: the row has more in this chunk
+      for (int e = 0; e < DT_ENTRIES; ++e) {
+        // a canonical row has no column below k0 left, so this is kc < kend
+        const bool in = 4 * e < nval && (unsigned)(kc[e] - k0) < (unsigned)DT_K;
+        As[b][r * DT_S + (in ? kc[e] - k0 : DT_K)] = kv[e];
+        n_in += in;
       }
-      // the next chunk's operands travel while this one is multiplied
-      if (kend < K) {
-        load_entries();
-        load_w(kend);
-      }
+      n_in += __shfl_xor(n_in, 1);
+      n_in += __shfl_xor(n_in, 2);
+      cur += n_in;
+    };
+    f32x16 acc[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+    if (nch > 0) {
+      load_entries();
+      load_w(0);
+      write_chunk(0, 0);
+      load_entries();
+      load_w(DT_K);
       __syncthreads();
-      // 64 k in four blocks of 16; per step the NT accumulators are
-      // independent, so consecutive MFMAs never wait on each other
+    }
+    for (int ch = 0; ch < nch; ++ch) {
+      const int b = ch & 1;
 #pragma unroll
-      for (int kb = 0; kb < DT_K; kb += 16) {
-        const f32x4 a = *reinterpret_cast<const f32x4*>(&As[(wv * 16 + c) * DT_S + kb + 4 * g]);
-        f32x4 b[NT];
+      for (int kb = 0; kb < DT_K; kb += 8) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(&As[b][(mr + c) * DT_S + kb + 4 * h]);
+        f32x4 bw[NB];
 #pragma unroll
-        for (int j = 0; j < NT; ++j) b[j] = *reinterpret_cast<const f32x4*>(&Wt[(j * 16 + c) * DT_S + kb + 4 * g]);
+        for (int j = 0; j < NB; ++j)
+          bw[j] = *reinterpret_cast<const f32x4*>(&Wt[b][(mc + 32 * j + c) * DT_S + kb + 4 * h]);
 #pragma unroll
         for (int s = 0; s < 4; ++s)
 #pragma unroll
-          for (int j = 0; j < NT; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[j][s], acc[j], 0, 0, 0);
+          for (int j = 0; j < NB; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], bw[j][s], acc[j], 0, 0, 0);
       }
+      // chunk ch+1 into the other buffer (read last in chunk ch-1, before the
+      // barrier), then the loads of chunk ch+2.  Past the last chunk both are
+      // harmless: the rows are exhausted and W's rows are out of range.
+      write_chunk(b ^ 1, (ch + 1) * DT_K);
+      load_entries();
+      load_w((ch + 2) * DT_K);
+      __syncthreads();
     }
-    // the lane holds rows 4g .. 4g+3 of its wavefront's 16, column c of each block
+    // register v of block j holds row 8(v/4) + 4h + v%4 of the wavefront's
+    // 32, column c of the block
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int col = n0 + j * 16 + c;
+    for (int j = 0; j < NB; ++j) {
+      const int col = n0 + mc + 32 * j + c;
       if (col >= F) continue;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int64_t row = row0 + wv * 16 + 4 * g + u;
-        if (row < m) Y[row * ldy + col] = RELU ? fmaxf(acc[j][u], 0.f) : acc[j][u];
+      for (int v = 0; v < 16; ++v) {
+        const int64_t row = row0 + mr + 8 * (v / 4) + 4 * h + v % 4;
+        if (row < m) Y[row * ldy + col] = RELU ? fmaxf(acc[j][v], 0.f) : acc[j][v];
       }
     }
   }
@@ -398,7 +418,7 @@ hipError_t dense_t(int relu, const void* arp, const int32_t* acol, const float* 
 template <typename RP>
 hipError_t dense_rp(int relu, const void* arp, const int32_t* acol, const float* aval, int64_t m, int K,
                     const float* W, int64_t ldw, int F, float* Y, int64_t ldy, hipStream_t s) {
-  const bool vec = ldw % 4 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
+  const bool vec = ldw % 4 == 0 && F % 4 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
   if (F > 64)
     return vec ? dense_t<RP, 8, true>(relu, arp, acol, aval, m, K, W, ldw, F, Y, ldy, s)
                : dense_t<RP, 8, false>(relu, arp, acol, aval, m, K, W, ldw, F, Y, ldy, s);
@@ -408,13 +428,15 @@ hipError_t dense_rp(int relu, const void* arp, const int32_t* acol, const float*
 
 }  // namespace
 
-bool spmm_dense_fits(int64_t K) { return K >= 0 && K <= (int64_t(1) << 22); }
+bool spmm_dense_fits(int64_t K, int64_t ldw) {
+  return K >= 0 && K <= (int64_t(1) << 20) && ldw < (int64_t(1) << 23);
+}
 
 hipError_t spmm(const void* arp, int rpa64, const int32_t* acol, const float* aval, int64_t m, int64_t K,
                 const float* W, int64_t ldw, int64_t F, float* Y, int64_t ldy, int relu, int dense, hipStream_t s) {
   if (m <= 0 || F <= 0) return hipSuccess;
   if (dense) {
-    if (!spmm_dense_fits(K)) return hipErrorInvalidValue;
+    if (!spmm_dense_fits(K, ldw)) return hipErrorInvalidValue;
     return rpa64 ? dense_rp<int64_t>(relu, arp, acol, aval, m, (int)K, W, ldw, (int)F, Y, ldy, s)
                  : dense_rp<int32_t>(relu, arp, acol, aval, m, (int)K, W, ldw, (int)F, Y, ldy, s);
   }
