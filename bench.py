@@ -292,12 +292,102 @@ def dense_aggregate(args, A, dA, gen_s):
     print(json.dumps(res), flush=True)
 
 
+def streamed(args):
+    """Out-of-core aggregation (Alg. 2): A and X in pinned host memory, row-block
+    tiles streamed to HBM double-buffered and C tiles returned to pinned host
+    memory, under each device budget of --budget-gb and each feature width of
+    --features (analogues of the paper's budget and feature-size studies).
+    One JSON line per (width, budget); each line's steps are whole calls,
+    planning included, with the host C allocation."""
+    import torch
+    import workloads
+    import paper_2507_02006_amd as aires
+    cfg = workloads.CONFIGS[args.workload]
+    if cfg["F"] is None:
+        sys.exit("bench.py --stream: workload %d is not a feature aggregation" % args.workload)
+    n = args.nodes or cfg["n"]
+    feats = [int(x) for x in args.features.split(",")] if args.features else [cfg["F"]]
+    budgets = [float(x) for x in args.budget_gb.split(",")] if args.budget_gb else [32.0]
+    hold = []
+
+    def pinned(rp_dtype):
+        def out(nnz):
+            rp = torch.empty(n + 1, dtype=rp_dtype, pin_memory=True)
+            col = torch.empty(max(nnz, 1), dtype=torch.int32, pin_memory=True)[:nnz]
+            val = torch.empty(max(nnz, 1), dtype=torch.float32, pin_memory=True)[:nnz]
+            hold.append((rp, col, val))
+            return rp.numpy(), col.numpy(), val.numpy()
+        return out
+
+    t0 = time.perf_counter()
+    A = workloads.rmat_sym(n, cfg["deg"], seed=args.workload, rp64=cfg["rp64"],
+                           out=pinned(torch.int64 if cfg["rp64"] else torch.int32), verbose=True)
+    tA = (A.nrows, A.ncols) + hold[-1]
+    gen_a = time.perf_counter() - t0
+    for F in feats:
+        t0 = time.perf_counter()
+        B = workloads.features(n, F, cfg["rho"], seed=1000 + args.workload, out=pinned(torch.int32), verbose=True)
+        tB = (B.nrows, B.ncols) + hold[-1]
+        gen_s = gen_a + time.perf_counter() - t0
+        for budget in budgets:
+            runs = []
+            for it in range(args.warmup + args.steps):
+                t1 = time.perf_counter()
+                with aires.tile_plan(tA, tB, int(budget * (1 << 30)), c_on_host=True, timing=True,
+                                     max_tile_bytes=args.max_tile_mb << 20) as plan:
+                    t2 = time.perf_counter()
+                    info = aires.plan_info(plan)
+                    C = aires.spgemm(plan)
+                    torch.cuda.synchronize()
+                    t3 = time.perf_counter()
+                    st = aires.plan_stats(plan)
+                    st["_plan_ms"], st["_call_ms"] = 1e3 * (t2 - t1), 1e3 * (t3 - t2)
+                    t4 = time.perf_counter()
+                    C.free()
+                    st["_free_ms"] = 1e3 * (time.perf_counter() - t4)
+                wall = time.perf_counter() - t1
+                if it >= args.warmup:
+                    runs.append((wall, st))
+                print("[stream] F=%d budget=%.1f GB run %d: %.1f ms, %d tiles" % (F, budget, it, 1e3 * wall,
+                                                                               info.ntiles), file=sys.stderr, flush=True)
+            walls = sorted(r[0] for r in runs)
+            wall = walls[len(walls) // 2]
+            st = [r[1] for r in runs if r[0] == wall][0]
+            compute = sum(st[k] for k in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms"))
+            flops = 2.0 * st["products"]
+            res = {
+                "metric": "SpGEMM GFLOP/s end to end, A and X streamed from pinned host memory and C returned "
+                          "to it (Alg. 2) on 1 MI355X",
+                "value": round(flops / wall / 1e9, 3), "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps,
+                "warmup": args.warmup, "ms_per_step": round(1e3 * wall, 2), "higher_is_better": True,
+                "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+                "data": "synthetic (seeded R-MAT graph and uniform sparse features, in pinned host memory)",
+                "config": {"workload": "cfg%d-shaped streamed aggregation: n=%d, X %d x %d at %g" %
+                                       (args.workload, n, n, F, cfg["rho"]),
+                           "budget_gb": budget, "f": F, "nnz_a": A.nnz, "nnz_b": B.nnz,
+                           "products": st["products"], "nnz_c": st["nnz_c"], "tiles": info.ntiles,
+                           "peak_device_gb": round(info.peak_bytes / 1e9, 2), "parallelism": "single GPU"},
+                "plan_ms": round(st["_plan_ms"], 2), "call_ms": round(st["_call_ms"], 2),
+                "free_c_ms": round(st["_free_ms"], 2), "library_total_ms": round(st["total_ms"], 2),
+                "pipeline_ms": round(st["pipeline_ms"], 2), "h2d_ms": round(st["h2d_ms"], 2),
+                "d2h_ms": round(st["d2h_ms"], 2), "compute_ms": round(compute, 2),
+                "parts_in_sequence_ms": round(st["h2d_ms"] + compute + st["d2h_ms"], 2),
+                "h2d_gb": round(st["h2d_bytes"] / 1e9, 3), "d2h_gb": round(st["d2h_bytes"] / 1e9, 3),
+                "h2d_gbs": round(st["h2d_bytes"] / max(st["h2d_ms"], 1e-9) / 1e6, 2),
+                "d2h_gbs": round(st["d2h_bytes"] / max(st["d2h_ms"], 1e-9) / 1e6, 2),
+                "generation_s": round(gen_s, 2),
+            }
+            print(json.dumps(res), flush=True)
+        del B, tB
+        hold.pop()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", type=int, default=3, choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--combine", type=int, default=0, metavar="F_OUT",
@@ -309,6 +399,13 @@ def main():
     ap.add_argument("--dense-h", type=int, default=0, metavar="F",
                     help="instead, time the next layer's aggregation A_norm * H with a dense H of F "
                          "columns (Eq. 1 with dense features; aires_spmm), A the workload's graph")
+    ap.add_argument("--stream", action="store_true",
+                    help="instead, the out-of-core schedule: A and X in pinned host memory, C back to "
+                         "pinned host memory, one line per (feature width, budget)")
+    ap.add_argument("--budget-gb", default="", help="--stream: comma-separated device budgets in GB (32)")
+    ap.add_argument("--features", default="", help="--stream: comma-separated feature widths (the workload's)")
+    ap.add_argument("--nodes", type=int, default=0, help="--stream: graph nodes (the workload's)")
+    ap.add_argument("--max-tile-mb", type=int, default=0, help="--stream: cap on a tile's A bytes (0: none)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run one device copy of this many MiB (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -323,6 +420,10 @@ def main():
     import paper_2507_02006_amd as aires
 
     torch.cuda.set_device(0)
+    if args.stream:
+        return streamed(args)
+    if args.workload not in WORKLOAD_NAMES:
+        sys.exit("bench.py: workload %d is timed with --stream" % args.workload)
     if args.copy_probe_mib:
         src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)

@@ -57,6 +57,8 @@ constexpr int64_t kWindowMaxEntries = 16384; // C entries one window may hold
 constexpr int64_t kWindowPoolBytes = 38912;  // LDS shared by a window's bitmap and values
 constexpr int64_t kCountGrains = 64;         // grains one symbolic item covers
 constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps kept for heavy rows
+constexpr int64_t kStreamTiles = 16;                       // default tile count of a streamed A
+constexpr int64_t kMinStreamTileBytes = int64_t(32) << 20;  // ... with at least this much of A per tile
 constexpr int64_t kKeepBitmapProducts = 65536;           // rows above this many products keep them
 constexpr int64_t kWaveMaxProducts = 8192;   // rows up to this go to one wavefront
 constexpr int64_t kSplitMinProducts = 65536; // narrow rows above this are split over workgroups
@@ -512,9 +514,14 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     const int64_t k = r1 - r0, q = arp[(size_t)r1] - arp[(size_t)r0];
     return k * per_row_ws + (k + 1) * sA + 8 * q + 8 * (cpre[(size_t)r1] - cpre[(size_t)r0]) + 8 * (k + 1);
   };
+  // Streamed A with no cap given: about kStreamTiles tiles, so that the
+  // copies of one tile overlap the products of another (Algorithm 2)
+  int64_t max_tile_bytes = o.max_tile_bytes;
+  if (a_streamed && max_tile_bytes == 0 && o.m_a_bytes == 0)
+    max_tile_bytes = std::max<int64_t>(p->info.a_bytes / kStreamTiles, kMinStreamTileBytes);
   auto fits = [&](int64_t r0, int64_t r1) -> bool {
     if (o.max_tile_rows > 0 && r1 - r0 > o.max_tile_rows) return false;
-    if (o.max_tile_bytes > 0 && (r1 - r0 + 1) * sA + 8 * (arp[(size_t)r1] - arp[(size_t)r0]) > o.max_tile_bytes)
+    if (max_tile_bytes > 0 && (r1 - r0 + 1) * sA + 8 * (arp[(size_t)r1] - arp[(size_t)r0]) > max_tile_bytes)
       return false;
     return slot_bytes_fast(r0, r1) <= tile_budget;
   };
