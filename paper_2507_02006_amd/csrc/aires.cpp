@@ -156,7 +156,6 @@ struct aires_plan {
   int64_t split_cap = 0;           // rows with dense slots for the split bin
   int64_t split_ws = 0;            // bytes of those slots
   // host copies needed for streaming
-  std::vector<int64_t> P_host;  // per-row products when computed on the host
   // timing events of the last call
   std::vector<hipEvent_t> ev;
   struct Mark { int kind; int phase; int a, b; };  // elapsed(ev[a], ev[b])
@@ -257,26 +256,122 @@ aires_status validate_host(const aires_csr& M, const char* name) {
 }
 
 // P_i on the host: A and B.rp in host memory; multithreaded over row ranges.
-void host_products(const aires_csr& A, const std::vector<int64_t>& brp, std::vector<int64_t>& P) {
-  const int64_t m = A.nrows;
-  P.assign((size_t)m, 0);
-  unsigned nt = std::max(1u, std::min(32u, std::thread::hardware_concurrency()));
-  if (m < 65536) nt = 1;
-  std::vector<std::thread> th;
-  for (unsigned t = 0; t < nt; ++t) {
-    th.emplace_back([&, t]() {
-      const int64_t r0 = m * t / nt, r1 = m * (t + 1) / nt;
-      for (int64_t i = r0; i < r1; ++i) {
-        int64_t s = 0;
-        for (int64_t q = host_rp(A, i); q < host_rp(A, i + 1); ++q) {
-          const int64_t k = A.col_idx[q];
-          s += brp[(size_t)k + 1] - brp[(size_t)k];
-        }
-        P[(size_t)i] = s;
-      }
-    });
+// Runs fn(lo, hi, t) over [0, n) cut into contiguous ranges, one per host
+// thread t < nt (up to 16 threads; one below 2^16 items).
+template <typename Fn>
+int parallel_ranges(int64_t n, Fn fn) {
+  int nt = (int)std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  if (n < 65536) nt = 1;
+  if (nt == 1) {
+    fn((int64_t)0, n, 0);
+    return 1;
   }
+  std::vector<std::thread> th;
+  for (int t = 0; t < nt; ++t) th.emplace_back([&, t]() { fn(n * t / nt, n * (t + 1) / nt, t); });
   for (auto& x : th) x.join();
+  return nt;
+}
+
+// nnz(B_k) for every row of B (rows hold at most N < 2^31 entries)
+aires_status host_row_lengths(const aires_csr& B, std::vector<int32_t>& len, int64_t* max_len) {
+  const int64_t K = B.nrows;
+  len.resize((size_t)K);
+  if (B.mem == AIRES_MEM_DEVICE) {
+    std::vector<int64_t> brp((size_t)K + 1);
+    if (B.rp_type == AIRES_IDX_I64) {
+      HIP_TRY(hipMemcpy(brp.data(), B.row_ptr, brp.size() * 8, hipMemcpyDeviceToHost));
+    } else {
+      std::vector<int32_t> tmp(brp.size());
+      HIP_TRY(hipMemcpy(tmp.data(), B.row_ptr, tmp.size() * 4, hipMemcpyDeviceToHost));
+      for (size_t i = 0; i < tmp.size(); ++i) brp[i] = tmp[i];
+    }
+    int64_t mx = 0;
+    for (int64_t k = 0; k < K; ++k) {
+      len[(size_t)k] = (int32_t)(brp[(size_t)k + 1] - brp[(size_t)k]);
+      mx = std::max<int64_t>(mx, len[(size_t)k]);
+    }
+    *max_len = mx;
+    return AIRES_OK;
+  }
+  std::vector<int64_t> mx(16, 0);
+  const int nt = parallel_ranges(K, [&](int64_t lo, int64_t hi, int t) {
+    int32_t x = 0;
+    if (B.rp_type == AIRES_IDX_I64) {
+      const int64_t* r = static_cast<const int64_t*>(B.row_ptr);
+      for (int64_t k = lo; k < hi; ++k) x = std::max(x, len[(size_t)k] = (int32_t)(r[k + 1] - r[k]));
+    } else {
+      const int32_t* r = static_cast<const int32_t*>(B.row_ptr);
+      for (int64_t k = lo; k < hi; ++k) x = std::max(x, len[(size_t)k] = r[k + 1] - r[k]);
+    }
+    mx[(size_t)t] = x;
+  });
+  *max_len = *std::max_element(mx.begin(), mx.begin() + nt);
+  return AIRES_OK;
+}
+
+// C bound per row, u_i = min(N, P_i) with P_i = sum over A_i of nnz(B_k),
+// its running sum (cpre[0] = 0, m + 1 entries), and the number of rows
+// with P_i > lim.  The gather of nnz(B_k) is random over B's rows: the
+// lengths are read from the narrowest table that holds them (a byte each
+// for feature matrices), each thread requests them a fixed distance ahead
+// of their use, and a row stops once its sum reaches N, or max(N, lim + 1)
+// if it could pass lim (|A_i| * max_k nnz(B_k) > lim): min(N, P_i) and
+// P_i > lim stay exact.
+template <typename L>
+void host_bounds_t(const aires_csr& A, const int64_t* arp, const L* len, int64_t max_len, int64_t N, int64_t lim,
+                   std::vector<int64_t>& cu, std::vector<int64_t>& cpre, int64_t* above) {
+  constexpr int64_t kAhead = 64;
+  const int64_t m = A.nrows;
+  const int32_t* col = A.col_idx;
+  cu.resize((size_t)m);
+  cpre.assign((size_t)m + 1, 0);
+  std::vector<int64_t> part(17, 0), cnt(17, 0);
+  const int nt = parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
+    int64_t sum = 0, c = 0;
+    const int64_t qend = arp[hi];
+    const int64_t heavy_stop = lim < INT64_MAX ? std::max(N, lim + 1) : N;
+    for (int64_t i = lo; i < hi; ++i) {
+      int64_t P = 0;
+      const int64_t stop = (arp[i + 1] - arp[i]) * max_len > lim ? heavy_stop : N;
+      for (int64_t q = arp[i]; q < arp[i + 1] && P < stop; ++q) {
+        if (q + kAhead < qend) __builtin_prefetch(len + col[q + kAhead], 0, 0);
+        P += len[col[q]];
+      }
+      const int64_t u = std::min<int64_t>(N, P);
+      cu[(size_t)i] = u;
+      sum += u;
+      c += P > lim;
+    }
+    part[(size_t)t + 1] = sum;
+    cnt[(size_t)t] = c;
+  });
+  for (int t = 0; t < nt; ++t) part[(size_t)t + 1] += part[(size_t)t];
+  parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
+    int64_t run = part[(size_t)t];
+    for (int64_t i = lo; i < hi; ++i) {
+      run += cu[(size_t)i];
+      cpre[(size_t)i + 1] = run;
+    }
+  });
+  int64_t a = 0;
+  for (int t = 0; t < nt; ++t) a += cnt[(size_t)t];
+  *above = a;
+}
+
+void host_bounds(const aires_csr& A, const int64_t* arp, const std::vector<int32_t>& lenB, int64_t max_len,
+                 int64_t N, int64_t lim, std::vector<int64_t>& cu, std::vector<int64_t>& cpre, int64_t* above) {
+  const int64_t K = (int64_t)lenB.size();
+  auto narrow = [&](auto tag) {
+    using L = decltype(tag);
+    std::vector<L> t((size_t)K);
+    parallel_ranges(K, [&](int64_t lo, int64_t hi, int) {
+      for (int64_t k = lo; k < hi; ++k) t[(size_t)k] = (L)lenB[(size_t)k];
+    });
+    host_bounds_t(A, arp, t.data(), max_len, N, lim, cu, cpre, above);
+  };
+  if (max_len <= 255) narrow(uint8_t{});
+  else if (max_len <= 65535) narrow(uint16_t{});
+  else host_bounds_t(A, arp, lenB.data(), max_len, N, lim, cu, cpre, above);
 }
 
 aires_status host_row_ptr(const aires_csr& M, std::vector<int64_t>& out) {
@@ -290,7 +385,14 @@ aires_status host_row_ptr(const aires_csr& M, std::vector<int64_t>& out) {
       for (size_t i = 0; i < tmp.size(); ++i) out[i] = tmp[i];
     }
   } else {
-    for (int64_t i = 0; i <= M.nrows; ++i) out[(size_t)i] = host_rp(M, i);
+    parallel_ranges(M.nrows + 1, [&](int64_t lo, int64_t hi, int) {
+      if (M.rp_type == AIRES_IDX_I64) {
+        std::memcpy(out.data() + lo, static_cast<const int64_t*>(M.row_ptr) + lo, (size_t)(hi - lo) * 8);
+      } else {
+        const int32_t* r = static_cast<const int32_t*>(M.row_ptr);
+        for (int64_t i = lo; i < hi; ++i) out[(size_t)i] = r[i];
+      }
+    });
   }
   return AIRES_OK;
 }
@@ -409,14 +511,24 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   const int64_t nG = p->wide ? p->nG : 0;
   const int64_t index_bytes = p->wide ? 4 * (nG + 1) * K : 0;
 
-  std::vector<int64_t> arp;
-  aires_status st = host_row_ptr(*A, arp);
-  if (st != AIRES_OK) { delete p; return st; }
+  // A's row pointers on the host as int64 (in place when they already are)
+  std::vector<int64_t> arp_own;
+  const int64_t* arp = nullptr;
+  aires_status st = AIRES_OK;
+  if (A->mem != AIRES_MEM_DEVICE && A->rp_type == AIRES_IDX_I64) {
+    arp = static_cast<const int64_t*>(A->row_ptr);
+  } else {
+    st = host_row_ptr(*A, arp_own);
+    if (st != AIRES_OK) { delete p; return st; }
+    arp = arp_own.data();
+  }
 
   // Per-row and per-tile bytes of one tile slot.
   // ws per row: P_i (8) + bin list (4) + window counts (4 per window) + C row
   // pointer of the tile (8, streamed only).
-  std::vector<int64_t> cu;  // C bound per row (entries), streamed + host C
+  std::vector<int64_t> cu;    // C bound per row (entries), streamed + host C
+  std::vector<int64_t> cpre;  // its running sum when C is placed in host memory
+  int64_t split_rows = -1;    // rows above the split threshold (when P_i is computed)
   int64_t resident = p->info.b_bytes + kFixedWorkspace + index_bytes;
   // (+ per-grain counts and per-row window counts of wide products)
   int64_t per_row_ws = 8 + 4 + (p->wide ? 4 * nG + 8 : 0);
@@ -427,14 +539,13 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   } else if (o.m_a_bytes == 0) {
     // C bound per row for the C slots (or for a device-resident C)
     if (o.c_bound == AIRES_CBOUND_PRODUCTS) {
-      std::vector<int64_t> brp;
-      st = host_row_ptr(*B, brp);
+      std::vector<int32_t> lenB;
+      int64_t max_len = 0;
+      st = host_row_lengths(*B, lenB, &max_len);
       if (st != AIRES_OK) { delete p; return st; }
-      host_products(*A, brp, p->P_host);
-      cu.resize((size_t)m);
-      int64_t tot = 0;
-      for (int64_t i = 0; i < m; ++i) { cu[(size_t)i] = std::min<int64_t>(N, p->P_host[(size_t)i]); tot += cu[(size_t)i]; }
-      p->info.c_bound_entries = tot;
+      const int64_t lim = p->split ? p->th.max_p[p->th.nb - 2] : INT64_MAX;
+      host_bounds(*A, arp, lenB, max_len, N, lim, cu, cpre, &split_rows);
+      p->info.c_bound_entries = cpre[(size_t)m];
     } else if (o.c_bound == AIRES_CBOUND_DENSE) {
       cu.assign((size_t)m, N);
       p->info.c_bound_entries = m * N;
@@ -446,7 +557,7 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
       cu.resize((size_t)m);
       int64_t tot = 0;
       for (int64_t i = 0; i < m; ++i) {
-        const double share = A->nnz ? mc_entries * (double)(arp[(size_t)i + 1] - arp[(size_t)i]) / (double)A->nnz : 0.0;
+        const double share = A->nnz ? mc_entries * (double)(arp[i + 1] - arp[i]) / (double)A->nnz : 0.0;
         cu[(size_t)i] = std::min<int64_t>(N, (int64_t)std::ceil(share));
         tot += cu[(size_t)i];
       }
@@ -460,12 +571,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     // known on the host, else as many as fit kSplitWsBytes
     const int64_t per = 4 * ((N + 31) / 32 + N);
     int64_t rows = std::min<int64_t>(m, std::max<int64_t>(1, kSplitWsBytes / per));
-    if (!p->P_host.empty()) {
-      const int64_t lim = p->th.max_p[p->th.nb - 2];  // upper end of the bin before the split bin
-      rows = 0;
-      for (int64_t v : p->P_host) rows += v > lim;
-      rows = std::min(rows, std::max<int64_t>(1, kSplitWsBytes / per));
-    }
+    if (split_rows >= 0)  // P_i known: rows above the upper end of the bin before the split bin
+      rows = std::min(split_rows, std::max<int64_t>(1, kSplitWsBytes / per));
     if (o.split_max_rows > 0) rows = std::min(rows, o.split_max_rows);
     p->split_cap = rows;
     p->split_ws = rows * per;
@@ -488,7 +595,7 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
 
   // bytes of a slot holding rows [r0, r1)
   auto slot_bytes = [&](int64_t r0, int64_t r1) -> int64_t {
-    const int64_t k = r1 - r0, q = arp[(size_t)r1] - arp[(size_t)r0];
+    const int64_t k = r1 - r0, q = arp[r1] - arp[r0];
     if (o.m_a_bytes > 0) return (k + 1) * sA + 8 * q;  // calcMem of Algorithm 1
     int64_t b = k * per_row_ws;
     if (a_streamed) {
@@ -504,14 +611,14 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   // Greedy maximal blocks of whole rows (Algorithm 1).  Costs grow with
   // every added row, so the longest feasible block is found by doubling
   // and bisection; this yields exactly the linear scan's blocks.
-  std::vector<int64_t> cpre;
-  if (a_streamed && c_on_host && o.m_a_bytes == 0) {
+  if (a_streamed && c_on_host && o.m_a_bytes == 0 && cpre.empty()) {
     cpre.assign((size_t)m + 1, 0);
     for (int64_t i = 0; i < m; ++i) cpre[(size_t)i + 1] = cpre[(size_t)i] + cu[(size_t)i];
   }
+  if (!(a_streamed && c_on_host && o.m_a_bytes == 0)) cpre.clear();
   auto slot_bytes_fast = [&](int64_t r0, int64_t r1) -> int64_t {
     if (cpre.empty()) return slot_bytes(r0, r1);
-    const int64_t k = r1 - r0, q = arp[(size_t)r1] - arp[(size_t)r0];
+    const int64_t k = r1 - r0, q = arp[r1] - arp[r0];
     return k * per_row_ws + (k + 1) * sA + 8 * q + 8 * (cpre[(size_t)r1] - cpre[(size_t)r0]) + 8 * (k + 1);
   };
   // Streamed A with no cap given: about kStreamTiles tiles, so that the
@@ -521,7 +628,7 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     max_tile_bytes = std::max<int64_t>(p->info.a_bytes / kStreamTiles, kMinStreamTileBytes);
   auto fits = [&](int64_t r0, int64_t r1) -> bool {
     if (o.max_tile_rows > 0 && r1 - r0 > o.max_tile_rows) return false;
-    if (max_tile_bytes > 0 && (r1 - r0 + 1) * sA + 8 * (arp[(size_t)r1] - arp[(size_t)r0]) > max_tile_bytes)
+    if (max_tile_bytes > 0 && (r1 - r0 + 1) * sA + 8 * (arp[r1] - arp[r0]) > max_tile_bytes)
       return false;
     return slot_bytes_fast(r0, r1) <= tile_budget;
   };
@@ -557,8 +664,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     aires_tile t;
     t.r0 = r0;
     t.r1 = lo;
-    t.nnz0 = arp[(size_t)r0];
-    t.nnz1 = arp[(size_t)lo];
+    t.nnz0 = arp[r0];
+    t.nnz1 = arp[lo];
     t.a_bytes = (lo - r0 + 1) * sA + 8 * (t.nnz1 - t.nnz0);
     t.c_bound_entries = cpre.empty() ? -1 : cpre[(size_t)lo] - cpre[(size_t)r0];
     t.tile_bytes = slot_bytes_fast(r0, lo);

@@ -165,3 +165,31 @@ def test_eq5_bound_mode():
     rho = Bm.nnz / (Bm.nrows * Bm.ncols)
     mc = 12 * A.nnz * (1 + Bm.ncols / A.nrows + rho) / 8
     assert abs(info.c_bound_entries - mc) <= A.nrows + 1   # per-row ceil, capped at N
+
+
+@pytest.mark.parametrize("N,row_max", [(8, 40), (300, 300), (70000, 70000)])
+def test_streamed_c_bound_exact(N, row_max):
+    """The planner's C bound is sum_i min(N, P_i) with P_i from the oracle,
+    whatever the width of B's row lengths (byte, 16-bit, 32-bit tables) and
+    with rows that reach N after a few entries (the bound pass stops
+    summing a row there) next to rows that do not."""
+    rng = np.random.default_rng(N)
+    K, m = 400, 70000
+    lens = rng.integers(0, row_max + 1, K)
+    lens[:3] = [row_max, 0, 1]
+    cols = [np.sort(rng.choice(N, min(int(L), N), replace=False)) for L in lens]
+    brp = np.concatenate([[0], np.cumsum([len(c) for c in cols])]).astype(np.int64)
+    Bm = workloads.CSR(K, N, brp.astype(np.int32), np.concatenate(cols).astype(np.int32),
+                       np.ones(int(brp[-1]), np.float32))
+    alen = rng.integers(0, 6, m)
+    alen[:5] = [0, 1, K, 2, 50]
+    acol = np.concatenate([np.sort(rng.choice(K, int(L), replace=False)) for L in alen]).astype(np.int32)
+    arp = np.concatenate([[0], np.cumsum(alen)]).astype(np.int32)
+    A = workloads.CSR(m, K, arp, acol, np.ones(len(acol), np.float32))
+    P = oracle.products(A, Bm)
+    with aires.tile_plan(_host(A), _host(Bm), 1 << 40, c_on_host=True) as p:
+        info = aires.plan_info(p)
+        tiles = aires.plan_tiles(p)
+    assert info.c_bound_entries == int(np.minimum(P, N).sum())
+    for t in tiles:
+        assert t["c_bound_entries"] == int(np.minimum(P[t["r0"]:t["r1"]], N).sum())
