@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <string>
 #include <thread>
 #include <vector>
@@ -256,6 +257,24 @@ aires_status validate_host(const aires_csr& M, const char* name) {
 }
 
 // P_i on the host: A and B.rp in host memory; multithreaded over row ranges.
+// n int64 values left uninitialised: the parallel passes that fill them
+// also touch their pages first.
+struct I64Array {
+  std::unique_ptr<int64_t[]> v;
+  int64_t n = 0;
+  void alloc(int64_t k) {
+    v.reset(new int64_t[(size_t)std::max<int64_t>(k, 1)]);
+    n = k;
+  }
+  void clear() {
+    v.reset();
+    n = 0;
+  }
+  bool empty() const { return n == 0; }
+  int64_t& operator[](size_t i) { return v[i]; }
+  const int64_t& operator[](size_t i) const { return v[i]; }
+};
+
 // Runs fn(lo, hi, t) over [0, n) cut into contiguous ranges, one per host
 // thread t < nt (up to 16 threads; one below 2^16 items).
 template <typename Fn>
@@ -319,12 +338,13 @@ aires_status host_row_lengths(const aires_csr& B, std::vector<int32_t>& len, int
 // P_i > lim stay exact.
 template <typename L>
 void host_bounds_t(const aires_csr& A, const int64_t* arp, const L* len, int64_t max_len, int64_t N, int64_t lim,
-                   std::vector<int64_t>& cu, std::vector<int64_t>& cpre, int64_t* above) {
+                   I64Array& cu, I64Array& cpre, int64_t* above) {
   constexpr int64_t kAhead = 64;
   const int64_t m = A.nrows;
   const int32_t* col = A.col_idx;
-  cu.resize((size_t)m);
-  cpre.assign((size_t)m + 1, 0);
+  cu.alloc(m);
+  cpre.alloc(m + 1);
+  cpre[0] = 0;
   std::vector<int64_t> part(17, 0), cnt(17, 0);
   const int nt = parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
     int64_t sum = 0, c = 0;
@@ -359,7 +379,7 @@ void host_bounds_t(const aires_csr& A, const int64_t* arp, const L* len, int64_t
 }
 
 void host_bounds(const aires_csr& A, const int64_t* arp, const std::vector<int32_t>& lenB, int64_t max_len,
-                 int64_t N, int64_t lim, std::vector<int64_t>& cu, std::vector<int64_t>& cpre, int64_t* above) {
+                 int64_t N, int64_t lim, I64Array& cu, I64Array& cpre, int64_t* above) {
   const int64_t K = (int64_t)lenB.size();
   auto narrow = [&](auto tag) {
     using L = decltype(tag);
@@ -526,8 +546,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   // Per-row and per-tile bytes of one tile slot.
   // ws per row: P_i (8) + bin list (4) + window counts (4 per window) + C row
   // pointer of the tile (8, streamed only).
-  std::vector<int64_t> cu;    // C bound per row (entries), streamed + host C
-  std::vector<int64_t> cpre;  // its running sum when C is placed in host memory
+  I64Array cu;    // C bound per row (entries), streamed + host C
+  I64Array cpre;  // its running sum when C is placed in host memory
   int64_t split_rows = -1;    // rows above the split threshold (when P_i is computed)
   int64_t resident = p->info.b_bytes + kFixedWorkspace + index_bytes;
   // (+ per-grain counts and per-row window counts of wide products)
@@ -547,14 +567,15 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
       host_bounds(*A, arp, lenB, max_len, N, lim, cu, cpre, &split_rows);
       p->info.c_bound_entries = cpre[(size_t)m];
     } else if (o.c_bound == AIRES_CBOUND_DENSE) {
-      cu.assign((size_t)m, N);
+      cu.alloc(m);
+      for (int64_t i = 0; i < m; ++i) cu[(size_t)i] = N;
       p->info.c_bound_entries = m * N;
     } else {
       // Eq. 5 with alpha_A read as dense value bytes: M_C = 12 nnzA (1 + N/m + rho_B),
       // shared out over rows in proportion to their A entries.
       const double rhoB = (K > 0 && N > 0) ? (double)B->nnz / ((double)K * (double)N) : 0.0;
       const double mc_entries = 12.0 * (double)A->nnz * (1.0 + (m ? (double)N / (double)m : 0.0) + rhoB) / 8.0;
-      cu.resize((size_t)m);
+      cu.alloc(m);
       int64_t tot = 0;
       for (int64_t i = 0; i < m; ++i) {
         const double share = A->nnz ? mc_entries * (double)(arp[i + 1] - arp[i]) / (double)A->nnz : 0.0;
@@ -612,7 +633,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   // every added row, so the longest feasible block is found by doubling
   // and bisection; this yields exactly the linear scan's blocks.
   if (a_streamed && c_on_host && o.m_a_bytes == 0 && cpre.empty()) {
-    cpre.assign((size_t)m + 1, 0);
+    cpre.alloc(m + 1);
+    cpre[0] = 0;
     for (int64_t i = 0; i < m; ++i) cpre[(size_t)i + 1] = cpre[(size_t)i] + cu[(size_t)i];
   }
   if (!(a_streamed && c_on_host && o.m_a_bytes == 0)) cpre.clear();
