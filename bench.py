@@ -333,8 +333,10 @@ def streamed(args):
             runs = []
             for it in range(args.warmup + args.steps):
                 t1 = time.perf_counter()
-                with aires.tile_plan(tA, tB, int(budget * (1 << 30)), c_on_host=True, timing=True,
-                                     max_tile_bytes=args.max_tile_mb << 20) as plan:
+                a_in = tA[:4] + (None,) if args.sym_norm else tA
+                with aires.tile_plan(a_in, tB, int(budget * (1 << 30)), c_on_host=True, timing=True,
+                                     max_tile_bytes=args.max_tile_mb << 20,
+                                     a_values="sym_norm" if args.sym_norm else "given") as plan:
                     t2 = time.perf_counter()
                     info = aires.plan_info(plan)
                     C = aires.spgemm(plan)
@@ -365,6 +367,7 @@ def streamed(args):
                 "config": {"workload": "cfg%d-shaped streamed aggregation: n=%d, X %d x %d at %g" %
                                        (args.workload, n, n, F, cfg["rho"]),
                            "budget_gb": budget, "f": F, "nnz_a": A.nnz, "nnz_b": B.nnz,
+                           "a_values": "derived on the device (Eq. 2)" if args.sym_norm else "copied",
                            "products": st["products"], "nnz_c": st["nnz_c"], "tiles": info.ntiles,
                            "peak_device_gb": round(info.peak_bytes / 1e9, 2), "parallelism": "single GPU"},
                 "plan_ms": round(st["_plan_ms"], 2), "call_ms": round(st["_call_ms"], 2),
@@ -406,6 +409,8 @@ def main():
     ap.add_argument("--features", default="", help="--stream: comma-separated feature widths (the workload's)")
     ap.add_argument("--nodes", type=int, default=0, help="--stream: graph nodes (the workload's)")
     ap.add_argument("--max-tile-mb", type=int, default=0, help="--stream: cap on a tile's A bytes (0: none)")
+    ap.add_argument("--sym-norm", action="store_true",
+                    help="--stream: A's values derived on the device from its pattern (Eq. 2) instead of copied")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run one device copy of this many MiB (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")

@@ -112,6 +112,20 @@ typedef struct aires_allocator {
     void *ctx;
 } aires_allocator;
 
+/*
+ * Where A's values come from.  SYM_NORM: A is square and its values are
+ * those of the normalised adjacency of Sec. II-A, Eq. 2,
+ * a_ik = 1 / sqrt(r_i * r_k) with r_x the number of entries stored in row
+ * x (D^-1/2 (A + I) D^-1/2 when the pattern is the symmetric adjacency with
+ * its self-loops); they are computed on the device in double and rounded
+ * once to fp32, A->vals is not read and may be NULL.  A streamed A then
+ * sends only its row pointers (once) and column indices over the host link.
+ */
+typedef enum aires_avalues {
+    AIRES_AVALUES_GIVEN = 0,
+    AIRES_AVALUES_SYM_NORM = 1
+} aires_avalues;
+
 /* Upper bound used for the size of C when planning. */
 typedef enum aires_cbound {
     AIRES_CBOUND_PRODUCTS = 0,  /* u_i = min(N, P_i), P_i = sum nnz(B_k)   */
@@ -164,6 +178,9 @@ typedef struct aires_plan_opts {
                                    bitmap (8 bytes per 32 columns) and
                                    values (4 bytes per entry) share; must
                                    hold one full grain                     */
+    int32_t a_values;           /* aires_avalues: where A's values come
+                                   from (AIRES_AVALUES_GIVEN)              */
+    int32_t _reserved0;
 } aires_plan_opts;
 
 /* Fill *o with defaults (struct_size set, validate 0, C on device). */

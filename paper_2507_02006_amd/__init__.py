@@ -65,7 +65,11 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
               hash_max_products: int = 0, wave_max_products: int = 0, window_grain_cols: int = 0,
               window_max_grains: int = 0, window_max_entries: int = 0, count_grains: int = 0,
               keep_bitmap_products: int = 0, split_min_products: int = 0, split_max_rows: int = 0,
-              window_pool_bytes: int = 0, torch_allocator: bool = True, device: int = 0) -> Plan:
+              window_pool_bytes: int = 0, a_values: str = "given", torch_allocator: bool = True,
+              device: int = 0) -> Plan:
+    """Plan C = A * B under a device budget (aires_tile_plan).  a_values:
+    "given" (A's values) or "sym_norm" (a_ik = 1/sqrt(r_i r_k) of A's
+    pattern, Eq. 2, derived on the device; A's vals may then be None)."""
     lib = B_.load()
     a = B_.make_csr(*_parts(A))
     b = B_.make_csr(*_parts(B))
@@ -89,6 +93,9 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
     o.split_min_products = split_min_products
     o.split_max_rows = split_max_rows
     o.window_pool_bytes = window_pool_bytes
+    if a_values not in ("given", "sym_norm"):
+        raise ValueError("a_values must be 'given' or 'sym_norm'")
+    o.a_values = B_.AVALUES_SYM_NORM if a_values == "sym_norm" else B_.AVALUES_GIVEN
     alloc = None
     if torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
         alloc = B_.TorchAllocator(device)

@@ -55,7 +55,8 @@ class PlanOpts(ctypes.Structure):
                 ("hash_max_products", c_i64), ("wave_max_products", c_i64), ("window_grain_cols", c_i64),
                 ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64),
                 ("keep_bitmap_products", c_i64), ("split_min_products", c_i64),
-                ("split_max_rows", c_i64), ("window_pool_bytes", c_i64)]
+                ("split_max_rows", c_i64), ("window_pool_bytes", c_i64), ("a_values", c_i32),
+                ("_reserved0", c_i32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -119,6 +120,7 @@ def load() -> ctypes.CDLL:
 
 ACT_NONE, ACT_RELU = 0, 1
 SPMM_AUTO, SPMM_ROWS, SPMM_DENSE_TILES = 0, 1, 2
+AVALUES_GIVEN, AVALUES_SYM_NORM = 0, 1
 
 
 class AiresError(RuntimeError):
@@ -159,18 +161,20 @@ def _dtype_name(x) -> str:
 def make_csr(nrows: int, ncols: int, rp, col, val) -> Csr:
     """Descriptor over caller arrays (numpy, pinned or device torch tensors).
     All three arrays must live in the same memory and be contiguous."""
-    mems = {_mem_of(rp), _mem_of(col), _mem_of(val)}
+    arrays = (rp, col) if val is None else (rp, col, val)
+    mems = {_mem_of(x) for x in arrays}
     if len(mems) != 1:
         raise ValueError("row_ptr, col_idx and vals must live in the same memory")
     rpt = _dtype_name(rp)
-    if rpt not in ("int32", "int64") or _dtype_name(col) != "int32" or _dtype_name(val) != "float32":
+    if rpt not in ("int32", "int64") or _dtype_name(col) != "int32" or \
+            (val is not None and _dtype_name(val) != "float32"):
         raise TypeError("expected int32/int64 row_ptr, int32 col_idx, float32 vals")
-    for x in (rp, col, val):
+    for x in arrays:
         if not (x.flags["C_CONTIGUOUS"] if isinstance(x, np.ndarray) else x.is_contiguous()):
             raise ValueError("arrays must be contiguous")
     nnz = int(col.shape[0])
     return Csr(int(nrows), int(ncols), nnz, IDX_I64 if rpt == "int64" else IDX_I32, mems.pop(),
-               _ptr(rp) or None, _ptr(col) or None, _ptr(val) or None)
+               _ptr(rp) or None, _ptr(col) or None, (_ptr(val) or None) if val is not None else None)
 
 
 # -------------------------------------------------------------- allocator

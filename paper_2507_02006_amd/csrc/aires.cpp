@@ -222,7 +222,7 @@ void bin_plan(aires_plan* p) {
   th.nb = nb;
 }
 
-aires_status check_csr_desc(const aires_csr* M, const char* name) {
+aires_status check_csr_desc(const aires_csr* M, const char* name, bool need_vals = true) {
   if (!M) return fail(AIRES_E_INVALID_ARG, "%s is NULL", name);
   if (M->nrows < 0 || M->ncols < 0 || M->nnz < 0)
     return fail(AIRES_E_DIM, "%s has a negative size", name);
@@ -231,14 +231,15 @@ aires_status check_csr_desc(const aires_csr* M, const char* name) {
   if (M->mem != AIRES_MEM_DEVICE && M->mem != AIRES_MEM_HOST_PINNED && M->mem != AIRES_MEM_HOST)
     return fail(AIRES_E_INVALID_ARG, "%s.mem %d invalid", name, M->mem);
   if (!M->row_ptr) return fail(AIRES_E_INVALID_ARG, "%s.row_ptr is NULL", name);
-  if (M->nnz > 0 && (!M->col_idx || !M->vals)) return fail(AIRES_E_INVALID_ARG, "%s arrays are NULL", name);
+  if (M->nnz > 0 && (!M->col_idx || (need_vals && !M->vals)))
+    return fail(AIRES_E_INVALID_ARG, "%s arrays are NULL", name);
   if (M->ncols > INT32_MAX) return fail(AIRES_E_OVERFLOW, "%s.ncols exceeds int32 column indices", name);
   if (M->rp_type == AIRES_IDX_I32 && M->nnz > INT32_MAX)
     return fail(AIRES_E_OVERFLOW, "%s.nnz needs int64 row pointers", name);
   return AIRES_OK;
 }
 
-aires_status validate_host(const aires_csr& M, const char* name) {
+aires_status validate_host(const aires_csr& M, const char* name, bool check_vals = true) {
   if (host_rp(M, 0) != 0) return fail(AIRES_E_INVALID_CSR, "%s.row_ptr[0] != 0", name);
   if (host_rp(M, M.nrows) != M.nnz) return fail(AIRES_E_INVALID_CSR, "%s.row_ptr[nrows] != nnz", name);
   for (int64_t i = 0; i < M.nrows; ++i) {
@@ -250,7 +251,8 @@ aires_status validate_host(const aires_csr& M, const char* name) {
         return fail(AIRES_E_INVALID_CSR, "%s column %d out of range in row %lld", name, c, (long long)i);
       if (q > a && c <= M.col_idx[q - 1])
         return fail(AIRES_E_INVALID_CSR, "%s columns not strictly increasing in row %lld", name, (long long)i);
-      if (!std::isfinite(M.vals[q])) return fail(AIRES_E_INVALID_CSR, "%s has a non-finite value", name);
+      if (check_vals && !std::isfinite(M.vals[q]))
+        return fail(AIRES_E_INVALID_CSR, "%s has a non-finite value", name);
     }
   }
   return AIRES_OK;
@@ -454,8 +456,16 @@ aires_status aires_plan_opts_default(aires_plan_opts* o) {
 aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hbm_budget,
                              const aires_plan_opts* opts, aires_plan** out) {
   if (!out) return fail(AIRES_E_INVALID_ARG, "out is NULL");
-  ST_TRY(check_csr_desc(A, "A"));
+  if (opts && opts->struct_size != sizeof(aires_plan_opts))
+    return fail(AIRES_E_INVALID_ARG, "opts.struct_size %u != %zu", opts->struct_size, sizeof(aires_plan_opts));
+  const bool a_sym_norm = opts && opts->a_values == AIRES_AVALUES_SYM_NORM;
+  ST_TRY(check_csr_desc(A, "A", !a_sym_norm));
   ST_TRY(check_csr_desc(B, "B"));
+  if (opts && opts->a_values != AIRES_AVALUES_GIVEN && opts->a_values != AIRES_AVALUES_SYM_NORM)
+    return fail(AIRES_E_INVALID_ARG, "opts.a_values %d invalid", opts->a_values);
+  if (a_sym_norm && A->nrows != A->ncols)
+    return fail(AIRES_E_DIM, "a_values = SYM_NORM needs a square A (%lld x %lld)", (long long)A->nrows,
+                (long long)A->ncols);
   if (A->ncols != B->nrows)
     return fail(AIRES_E_DIM, "A.ncols (%lld) != B.nrows (%lld)", (long long)A->ncols, (long long)B->nrows);
   if (A->nrows > INT32_MAX - 1) return fail(AIRES_E_OVERFLOW, "A.nrows exceeds int32 row ids");
@@ -473,7 +483,7 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   if (o.max_tile_rows < 0 || o.max_tile_bytes < 0 || o.m_a_bytes < 0)
     return fail(AIRES_E_INVALID_ARG, "negative tile cap");
   if (o.validate) {
-    if (A->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*A, "A"));
+    if (A->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*A, "A", !a_sym_norm));
     if (B->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*B, "B"));
   }
 
@@ -552,6 +562,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   int64_t resident = p->info.b_bytes + kFixedWorkspace + index_bytes;
   // (+ per-grain counts and per-row window counts of wide products)
   int64_t per_row_ws = 8 + 4 + (p->wide ? 4 * nG + 8 : 0);
+  // derived values of a streamed A need all of A's row pointers on the device
+  if (a_streamed && a_sym_norm) resident += (m + 1) * sA;
   if (!a_streamed) {
     // A and C.row_ptr resident; bin lists and window bookkeeping for all rows
     resident += p->info.a_bytes + 8 * (m + 1) + (4 + (p->wide ? 4 * nG + 8 + 8 * p->ngg : 0)) * m;
@@ -941,6 +953,15 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   ST_TRY(ws.get_n(m, &list));
   ST_TRY(ws.get_n(nt * (kern::MAX_BINS + 1), &binoff));
   ST_TRY(ws.get_n(1, &prod));
+  // A's values: given, or derived from its pattern (Eq. 2) into the workspace
+  const float* avals = p->A.vals;
+  if (p->opts.a_values == AIRES_AVALUES_SYM_NORM && p->A.nnz > 0) {
+    float* v = nullptr;
+    ST_TRY(ws.get_n(p->A.nnz, &v));
+    HIP_TRY(kern::sym_norm_values(p->A.row_ptr, p->A.rp_type == AIRES_IDX_I64, 0, m, 0, p->A.col_idx, v, p->A.nnz,
+                                  s));
+    avals = v;
+  }
   int64_t* bm_off = nullptr;
   uint32_t* bm_cache = nullptr;
   unsigned long long* bm_top = nullptr;
@@ -997,7 +1018,7 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
     const aires_tile& T = p->tiles[(size_t)t];
     TileWs w = tile_ws(t);
     const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
-    kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, p->A.vals, p->B.row_ptr, p->B.col_idx,
+    kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, avals, p->B.row_ptr, p->B.col_idx,
                                       p->B.vals, bidx);
     ST_TRY(tile_symbolic(p, op, T.r1 - T.r0, w, crp + T.r0, prod, s, tm));
   }
@@ -1049,7 +1070,7 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
       w.nitems = hb[2 + t];
     }
     const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
-    kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, p->A.vals, p->B.row_ptr, p->B.col_idx,
+    kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, avals, p->B.row_ptr, p->B.col_idx,
                                       p->B.vals, bidx);
     ST_TRY(tile_numeric(p, op, T.r1 - T.r0, w, crp + T.r0, ccol, cval, 0, s, tm));
   }
@@ -1205,21 +1226,37 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     bval = (const float*)d_bval;
   }
 
+  // Derived values (Eq. 2): all of A's row pointers stay on the device (they
+  // give every row's length); a tile then sends only its column indices.
+  const bool sym_norm = p->opts.a_values == AIRES_AVALUES_SYM_NORM;
+  void* d_arp_all = nullptr;
+  if (sym_norm) {
+    ST_TRY(ws.get((size_t)(m + 1) * sA, &d_arp_all));
+    HIP_TRY(hipEventRecord(ev_ws, sc));
+    HIP_TRY(hipStreamWaitEvent(sh, ev_ws, 0));
+    const int ea = th.record();
+    HIP_TRY(hipMemcpyAsync(d_arp_all, A.row_ptr, (size_t)(m + 1) * sA, hipMemcpyHostToDevice, sh));
+    th.mark(PH_H2D, 0, ea, th.record());
+    p->stats.h2d_bytes += (m + 1) * sA;
+  }
+
   auto issue_h2d = [&](int64_t t) -> aires_status {
     const aires_tile& T = p->tiles[(size_t)t];
     Slot& S = slot[t % 2];
     if (t >= 2) HIP_TRY(hipStreamWaitEvent(sh, ev_done[(size_t)t - 2], 0));
     const int ea = th.record();
     const int64_t k = T.r1 - T.r0, q = T.nnz1 - T.nnz0;
-    HIP_TRY(hipMemcpyAsync(S.arp, static_cast<const char*>(A.row_ptr) + T.r0 * sA, (size_t)(k + 1) * sA,
-                           hipMemcpyHostToDevice, sh));
+    if (!sym_norm)
+      HIP_TRY(hipMemcpyAsync(S.arp, static_cast<const char*>(A.row_ptr) + T.r0 * sA, (size_t)(k + 1) * sA,
+                             hipMemcpyHostToDevice, sh));
     if (q > 0) {
       HIP_TRY(hipMemcpyAsync(S.acol, A.col_idx + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
-      HIP_TRY(hipMemcpyAsync(S.aval, A.vals + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
+      if (!sym_norm)
+        HIP_TRY(hipMemcpyAsync(S.aval, A.vals + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
     }
     HIP_TRY(hipEventRecord(ev_in[(size_t)t], sh));
     th.mark(PH_H2D, 0, ea, th.record());
-    p->stats.h2d_bytes += (k + 1) * sA + 8 * q;
+    p->stats.h2d_bytes += sym_norm ? 4 * q : (k + 1) * sA + 8 * q;
     return AIRES_OK;
   };
 
@@ -1236,7 +1273,13 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     const int64_t k = T.r1 - T.r0;
     HIP_TRY(hipStreamWaitEvent(sc, ev_in[(size_t)t], 0));
     if (t >= 2 && c_on_host) HIP_TRY(hipStreamWaitEvent(sc, ev_cfree[t % 2], 0));
-    kern::Operands op = tile_operands(p, S.arp, T.nnz0, S.acol, S.aval, brp, bcol, bval, bidx);
+    const void* tile_rp = S.arp;
+    if (sym_norm) {
+      tile_rp = static_cast<const char*>(d_arp_all) + T.r0 * sA;
+      HIP_TRY(kern::sym_norm_values(d_arp_all, A.rp_type == AIRES_IDX_I64, T.r0, k, T.nnz0, S.acol, S.aval,
+                                    T.nnz1 - T.nnz0, sc));
+    }
+    kern::Operands op = tile_operands(p, tile_rp, T.nnz0, S.acol, S.aval, brp, bcol, bval, bidx);
     // running base of C.row_ptr for this tile: crp[0] = total so far
     HIP_TRY(hipMemcpyAsync(S.crp, running, sizeof(int64_t), hipMemcpyDeviceToDevice, sc));
     ST_TRY(tile_symbolic(p, op, k, S.w, S.crp, prod, sc, tm));

@@ -125,6 +125,12 @@ bool spmm_dense_fits(int64_t K, int64_t ldw);
 hipError_t spmm(const void* arp, int rpa64, const int32_t* acol, const float* aval, int64_t m, int64_t K,
                 const float* W, int64_t ldw, int64_t F, float* Y, int64_t ldy, int relu, int dense, hipStream_t s);
 
+// a_ik = 1/sqrt(r_i r_k) (Eq. 2) for the nnz entries of rows [row0, row0 +
+// nrows) of a square CSR: rp holds the whole matrix's row pointers on the
+// device, acol/aval are indexed by (entry position - a_base).
+hipError_t sym_norm_values(const void* rp, int rp64, int64_t row0, int64_t nrows, int64_t a_base,
+                           const int32_t* acol, float* aval, int64_t nnz, hipStream_t s);
+
 size_t lds_bytes(int kind, int phase, int32_t W);
 size_t grain_count_lds(int sg, int G);
 size_t window_numeric_lds(int pool_words);

@@ -193,3 +193,20 @@ def test_streamed_c_bound_exact(N, row_max):
     assert info.c_bound_entries == int(np.minimum(P, N).sum())
     for t in tiles:
         assert t["c_bound_entries"] == int(np.minimum(P[t["r0"]:t["r1"]], N).sum())
+
+
+def test_sym_norm_plan():
+    """a_values='sym_norm': A's values may be absent; a streamed plan keeps
+    all of A's row pointers on the device (counted in the budget); A must be
+    square."""
+    A, Bm = workloads.workload(1, n=1024)
+    budget = Bm.nbytes() + (4 << 20) + 600_000
+    hA = _host(A)
+    with aires.tile_plan(hA[:4] + (None,), _host(Bm), budget, c_on_host=True, a_values="sym_norm") as p:
+        info = aires.plan_info(p)
+    assert info.tile_budget == (budget - (Bm.nbytes() + (4 << 20) + 4 * (A.nrows + 1))) // 2
+    with pytest.raises(aires.AiresError):
+        aires.tile_plan(_host(Bm)[:4] + (None,), _host(workloads.random_csr(np.random.default_rng(1), 256, 7, 0.3)),
+                        1 << 30, c_on_host=True, a_values="sym_norm")
+    with pytest.raises(ValueError):
+        aires.tile_plan(hA, _host(Bm), budget, c_on_host=True, a_values="normalised")

@@ -445,3 +445,98 @@ def test_cfg5_full_streamed(torch_gpu):
         _check_structure(C.rp, C.col, P, B.ncols)
         _check_rows(A, B, C.rp, C.col, C.val, _rows(A, B, k=200, heavy=5, seed=5))
         C.free()
+
+
+# ------------------------------------------- values derived from the pattern (Eq. 2)
+
+def _identity(n):
+    return CSR(n, n, np.arange(n + 1, dtype=np.int32), np.arange(n, dtype=np.int32), np.ones(n, np.float32))
+
+
+def test_sym_norm_values_bitwise(torch_gpu):
+    """a_values='sym_norm': C = A_norm * I reproduces the generator's values
+    1/sqrt(d_i d_j) bit for bit (double arithmetic, one rounding to fp32),
+    with A's own values not passed at all."""
+    import paper_2507_02006_amd as aires
+    A, _ = workloads.workload(3, n=20000)
+    dA = aires.to_device(A)
+    say("sym_norm values n=20000 nnz=%d" % A.nnz)
+    with aires.tile_plan(dA[:4] + (None,), aires.to_device(_identity(A.ncols)), 0, a_values="sym_norm") as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(rp, A.rp.astype(np.int64))
+    assert np.array_equal(col, A.col)
+    assert np.array_equal(val.view(np.uint32), A.val.view(np.uint32))
+
+
+def test_sym_norm_values_sparse_rows(torch_gpu):
+    """Derived values when runs of empty rows make a 2048-entry chunk span
+    more rows than the kernel stages in LDS (its global-search branch):
+    C = A_norm * I against Eq. 2 evaluated in double on the host."""
+    import paper_2507_02006_amd as aires
+    rng = np.random.default_rng(31)
+    m = 200000
+    full = np.arange(0, m, 97)  # non-empty rows; columns only among them
+    lens = np.zeros(m, np.int64)
+    lens[full] = rng.integers(1, 60, len(full))
+    cols = [np.sort(rng.choice(full, int(L), replace=False)) for L in lens[full]]
+    rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    col = np.concatenate(cols).astype(np.int32)
+    A = CSR(m, m, rp, col, np.zeros(len(col), np.float32))
+    rows = np.repeat(np.arange(m), lens)
+    want = (1.0 / np.sqrt(lens[rows].astype(np.float64) * lens[col].astype(np.float64))).astype(np.float32)
+    dA = aires.to_device(A)
+    say("sym_norm sparse rows m=%d nnz=%d" % (m, len(col)))
+    with aires.tile_plan(dA[:4] + (None,), aires.to_device(_identity(m)), 0, a_values="sym_norm") as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        c_col, c_val = C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(c_col, col)
+    assert np.array_equal(c_val.view(np.uint32), want.view(np.uint32))
+
+
+def test_sym_norm_incore_equals_given(torch_gpu):
+    """In-core tiles with derived values: the same structure as with the
+    given values and both within the bar of the oracle (the order of the
+    fp32 sums in LDS differs from run to run, so values are not compared
+    bit for bit; the derived values themselves are, above)."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(2, n=8192)
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    say("sym_norm in-core cfg2 n=8192")
+    out = []
+    for mode, a in (("given", dA), ("sym_norm", dA[:4] + (None,))):
+        with aires.tile_plan(a, dB, 0, a_values=mode, max_tile_rows=3001) as plan:
+            C = aires.spgemm(plan)
+            torch_gpu.cuda.synchronize()
+            out.append((C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()))
+    ref = oracle.spgemm(A, B)
+    for rp, col, val in out:
+        assert_match(rp, col, val, ref)
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
+
+
+def test_sym_norm_streamed_equals_given(torch_gpu):
+    """Streamed tiles with derived values: A's row pointers cross the host
+    link once and each tile sends only its column indices; the structure
+    equals that of the given values and both meet the oracle's bar."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(5, n=60000)
+    pA, pB = aires.to_pinned(A), aires.to_pinned(B)
+    budget = B.nbytes() + (4 << 20) + 8 * (A.nrows + 1) + 2 * 1_500_000
+    say("sym_norm streamed cfg5 n=60000 budget=%d" % budget)
+    out = []
+    for mode, a in (("given", pA), ("sym_norm", pA[:4] + (None,))):
+        with aires.tile_plan(a, pB, budget, c_on_host=True, timing=True, a_values=mode) as plan:
+            info = aires.plan_info(plan)
+            C = aires.spgemm(plan)
+            st = aires.plan_stats(plan)
+            assert info.ntiles >= 3
+            out.append((C.rp.copy(), C.col.copy(), C.val.copy()))
+            C.free()
+    assert st["h2d_bytes"] == 8 * (A.nrows + 1) + 4 * A.nnz + B.nbytes()
+    ref = oracle.spgemm(A, B)
+    for rp, col, val in out:
+        assert_match(rp, col, val, ref)
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
