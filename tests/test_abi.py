@@ -210,3 +210,27 @@ def test_sym_norm_plan():
                         1 << 30, c_on_host=True, a_values="sym_norm")
     with pytest.raises(ValueError):
         aires.tile_plan(hA, _host(Bm), budget, c_on_host=True, a_values="normalised")
+
+
+def test_spmm_argument_errors():
+    """aires_spmm rejects bad arguments before touching the device: unknown
+    activation or kernel family, W/Y strides below F, an A outside device
+    memory, and dense tiles past their K and ldw limits."""
+    lib = B_.load()
+    fake = 1 << 40  # never dereferenced: every case fails validation first
+
+    def call(A, ldw=64, F=64, ldy=64, act=B_.ACT_NONE, algo=B_.SPMM_AUTO):
+        return lib.aires_spmm(ctypes.byref(A), fake, ldw, F, fake, ldy, act, algo, None)
+
+    def csr(m=10, k=20, mem=B_.MEM_DEVICE):
+        return B_.Csr(m, k, 5, B_.IDX_I32, mem, fake, fake, fake)
+
+    assert call(csr(), act=5) == -1
+    assert call(csr(), algo=7) == -1
+    assert call(csr(), ldw=63) == -1
+    assert call(csr(), ldy=10) == -1
+    assert call(csr(mem=B_.MEM_HOST)) == -9
+    assert call(csr(k=(1 << 20) + 1), algo=B_.SPMM_DENSE_TILES) == -9
+    assert "dense tiles" in lib.aires_last_error().decode()
+    assert call(csr(), ldw=1 << 23, algo=B_.SPMM_DENSE_TILES) == -9
+    assert call(csr(), F=1 << 31) == -9
