@@ -210,3 +210,34 @@ def test_gcn_layer_on_aggregated_features(torch_gpu):
     cabs, _ = oracle.spmm(CSR(Co.r1 - Co.r0, Co.ncols, Co.rp, Co.col, np.abs(Co.val)), np.abs(W))
     tol = (n + 2) * U * refabs + U * np.abs(ref) + 1e-5 * (np.abs(W).sum(0)[None, :] + cabs)
     assert np.all(np.abs(h - ref) <= tol)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("algo", ALGOS)
+def test_full_cfg2_combination_sampled(torch_gpu, algo):
+    """The combination step at the size the bench times: relu(C W) with C
+    the aggregate of the full cfg2 (262144 x 512, 39.2 M entries) from
+    aires_spgemm and W 512 x 256, checked on sampled rows and the heaviest
+    rows against the oracle's product of the oracle's aggregate rows."""
+    import paper_2507_02006_amd as aires
+    torch = torch_gpu
+    A, X = workloads.workload(2)
+    rng = np.random.default_rng(21)
+    W = rng.uniform(-0.05, 0.05, (X.ncols, 256)).astype(np.float32)
+    say("full cfg2 combination algo=%s" % algo)
+    with aires.tile_plan(aires.to_device(A), aires.to_device(X), 0) as plan:
+        C = aires.spgemm(plan)
+        H = aires.spmm((C.nrows, C.ncols, C.rp, C.col, C.val), torch.from_numpy(W).cuda(), relu=True, algo=algo)
+        torch.cuda.synchronize()
+        crow = np.diff(C.rp.cpu().numpy())
+        rows = np.unique(np.concatenate([rng.choice(A.nrows, 200, replace=False), np.argsort(crow)[-5:],
+                                         [0, A.nrows - 1]]))
+        h = H[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+    for r, hr in zip(rows, h):
+        Co = oracle.spgemm(A, X, int(r), int(r) + 1)
+        row = CSR(1, Co.ncols, Co.rp, Co.col, Co.val)
+        ref, refabs = oracle.spmm(row, W, relu=True)
+        cabs, _ = oracle.spmm(CSR(1, Co.ncols, Co.rp, Co.col, np.abs(Co.val)), np.abs(W))
+        n = len(Co.col)
+        tol = (n + 2) * U * refabs + U * np.abs(ref) + 1e-5 * (np.abs(W).sum(0)[None, :] + cabs)
+        assert np.all(np.abs(hr[None, :] - ref) <= tol), "row %d" % r
