@@ -185,7 +185,6 @@ __global__ __launch_bounds__(SPMM_BLOCK) void k_spmm_heavy(const void* arp, cons
 // touching memory, so the loop body has no branches.
 constexpr int DT_M = 64;        // rows per tile
 constexpr int DT_K = 32;        // k per LDS chunk
-constexpr int DT_S = DT_K + 4;  // LDS row stride in floats: 16-byte reads of 16 rows hit 64 distinct banks
 constexpr int DT_BLOCK = 256;   // four wavefronts, 16 rows each
 constexpr int DT_ENTRIES = DT_K / 4;  // four threads per row: one round of loads covers a chunk
 constexpr int NXCD = 8;         // gfx950 hands workgroups round-robin to its 8 XCDs
@@ -193,6 +192,24 @@ constexpr int kOutOfRange = INT32_MIN;  // a buffer offset no resource here reac
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Row layout of a tile chunk in LDS (element k of row r, DT_K per row).
+// Padded: rows of DT_K + 4 floats, so the 16-byte operand reads of 16 rows
+// fall on distinct banks; column DT_K of each row takes the entries of later
+// chunks.  Swizzled (less LDS, used where it buys one more workgroup per
+// CU): unpadded rows whose 16-byte groups are permuted by the row's low
+// three bits, so eight consecutive rows' reads of one group fall on
+// distinct banks; one dump slot per row after the rows.
+template <bool SWZ>
+struct TileLayout {
+  static constexpr int S = SWZ ? DT_K : DT_K + 4;                // floats per row
+  static constexpr int A_FLOATS = SWZ ? DT_M * DT_K + DT_M : DT_M * S;
+  __device__ static __forceinline__ int at(int r, int k) {
+    if constexpr (SWZ) return r * DT_K + ((((k >> 2) ^ (r & 7)) << 2) | (k & 3));
+    else return r * S + k;
+  }
+  __device__ static __forceinline__ int dump(int r) { return SWZ ? DT_M * DT_K + r : r * S + DT_K; }
+};
 
 // a wavefront-uniform 64-bit value in scalar registers
 __device__ __forceinline__ int64_t uniform64(int64_t v) {
@@ -207,15 +224,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
 }
 
 // Occupancy is LDS-bound (two chunks per workgroup): four workgroups per CU
-// at NT = 4, two at NT = 8; the register budget is set to match.
+// at NT = 4, three at NT = 8; the register budget is set to match.
 template <typename RP, int NT, bool VEC, bool RELU>
-__global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 2 : 4) void k_spmm_dense(
+__global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 3 : 4) void k_spmm_dense(
     const void* arp, const int32_t* acol, const float* aval, int64_t m, int K, const float* W, int64_t ldw, int F,
     float* Y, int64_t ldy, int64_t nrt, int64_t nct, int64_t ntiles) {
   constexpr int BN = 16 * NT;
   constexpr int WL = NT / 2;  // 16-byte W loads per thread per chunk (32 x BN floats over 256 threads)
-  __shared__ __align__(16) float As[2][DT_M * DT_S];  // [row][k]
-  __shared__ __align__(16) float Wt[2][BN * DT_S];    // [column][k]
+  using L = TileLayout<(NT > 4)>;
+  __shared__ __align__(16) float As[2][L::A_FLOATS];  // [row][k]
+  __shared__ __align__(16) float Wt[2][BN * L::S];    // [column][k]
   constexpr int NB = BN / 64;  // 32-column MFMA blocks per wavefront
   const int t = threadIdx.x, lane = t % WAVE, wv = t / WAVE;
   const int r = t / 4, q = t % 4;             // densify: four threads per row
@@ -290,20 +308,20 @@ __global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 2 : 4) void k_spmm_dense(
       // same wavefront after it, and LDS executes a wavefront's accesses in order
 #pragma unroll
       for (int e = 0; e < DT_K / 16; ++e)
-        *reinterpret_cast<f32x4*>(&As[b][r * DT_S + q * (DT_K / 4) + 4 * e]) = f32x4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<f32x4*>(&As[b][L::at(r, q * (DT_K / 4) + 4 * e)]) = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int e = 0; e < WL; ++e)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) Wt[b][(wc + 16 * e + u) * DT_S + wk] = w[e][u];
+        for (int u = 0; u < 4; ++u) Wt[b][L::at(wc + 16 * e + u, wk)] = w[e][u];
       // 32 entries cover the 32 columns: every entry of the row in the
       // chunk is here.  Each is stored; one of a later chunk lands in the
-      // padding column DT_K, which the products never read.
+      // row's dump slot, which the products never read.
       int n_in = 0;
 #pragma unroll
       for (int e = 0; e < DT_ENTRIES; ++e) {
         // a canonical row has no column below k0 left, so this is kc < kend
         const bool in = 4 * e < nval && (unsigned)(kc[e] - k0) < (unsigned)DT_K;
-        As[b][r * DT_S + (in ? kc[e] - k0 : DT_K)] = kv[e];
+        As[b][in ? L::at(r, kc[e] - k0) : L::dump(r)] = kv[e];
         n_in += in;
       }
       n_in += __shfl_xor(n_in, 1);
@@ -327,11 +345,11 @@ __global__ __launch_bounds__(DT_BLOCK, NT > 4 ? 2 : 4) void k_spmm_dense(
       const int b = ch & 1;
 #pragma unroll
       for (int kb = 0; kb < DT_K; kb += 8) {
-        const f32x4 a = *reinterpret_cast<const f32x4*>(&As[b][(mr + c) * DT_S + kb + 4 * h]);
+        const f32x4 a = *reinterpret_cast<const f32x4*>(&As[b][L::at(mr + c, kb + 4 * h)]);
         f32x4 bw[NB];
 #pragma unroll
         for (int j = 0; j < NB; ++j)
-          bw[j] = *reinterpret_cast<const f32x4*>(&Wt[b][(mc + 32 * j + c) * DT_S + kb + 4 * h]);
+          bw[j] = *reinterpret_cast<const f32x4*>(&Wt[b][L::at(mc + 32 * j + c, kb + 4 * h)]);
 #pragma unroll
         for (int s = 0; s < 4; ++s)
 #pragma unroll
