@@ -540,3 +540,24 @@ def test_sym_norm_streamed_equals_given(torch_gpu):
     for rp, col, val in out:
         assert_match(rp, col, val, ref)
     assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
+
+
+def test_sym_norm_streamed_device_c(torch_gpu):
+    """Derived values with a streamed A and C kept in device memory (the
+    schedule with no copies back), against the oracle on the generator's
+    values; two tiles or more under the budget."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(4, n=40000)
+    ref = oracle.spgemm(A, B)
+    pA = aires.to_pinned(A)
+    dB = aires.to_device(B)
+    budget = B.nbytes() + (4 << 20) + 8 * 40001 + 8 * int(np.minimum(oracle.products(A, B), 128).sum()) \
+        + 4 * 40001 + 2 * 400_000
+    say("sym_norm streamed cfg4 n=40000 device C")
+    with aires.tile_plan(pA[:4] + (None,), dB, budget, a_values="sym_norm", timing=True) as plan:
+        assert aires.plan_info(plan).ntiles >= 2
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        st = aires.plan_stats(plan)
+        assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
+    assert st["h2d_bytes"] == 4 * (A.nrows + 1) + 4 * A.nnz
