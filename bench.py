@@ -336,7 +336,8 @@ def streamed(args):
                 a_in = tA[:4] + (None,) if args.sym_norm else tA
                 with aires.tile_plan(a_in, tB, int(budget * (1 << 30)), c_on_host=not args.c_on_device, timing=True,
                                      max_tile_bytes=args.max_tile_mb << 20,
-                                     a_values="sym_norm" if args.sym_norm else "given") as plan:
+                                     a_values="sym_norm" if args.sym_norm else "given",
+                                     c_bound=3 if args.c_bound == "rows" else 0) as plan:
                     t2 = time.perf_counter()
                     info = aires.plan_info(plan)
                     C = aires.spgemm(plan)
@@ -371,6 +372,7 @@ def streamed(args):
                            "budget_gb": budget, "f": F, "nnz_a": A.nnz, "nnz_b": B.nnz,
                            "a_values": "derived on the device (Eq. 2)" if args.sym_norm else "copied",
                            "c_placement": "device" if args.c_on_device else "pinned host",
+                           "c_bound": args.c_bound, "c_bound_entries": info.c_bound_entries,
                            "products": st["products"], "nnz_c": st["nnz_c"], "tiles": info.ntiles,
                            "peak_device_gb": round(info.peak_bytes / 1e9, 2), "parallelism": "single GPU"},
                 "plan_ms": round(st["_plan_ms"], 2), "call_ms": round(st["_call_ms"], 2),
@@ -414,6 +416,9 @@ def main():
     ap.add_argument("--max-tile-mb", type=int, default=0, help="--stream: cap on a tile's A bytes (0: none)")
     ap.add_argument("--c-on-device", action="store_true",
                     help="--stream: C stays in device memory instead of returning to pinned host memory")
+    ap.add_argument("--c-bound", default="products", choices=["products", "rows"],
+                    help="--stream: C bound of the plan, min(N, P_i) (a gather over A's columns) or "
+                         "min(N, nnz(A_i) max_k nnz(B_k)) (row pointers only)")
     ap.add_argument("--sym-norm", action="store_true",
                     help="--stream: A's values derived on the device from its pattern (Eq. 2) instead of copied")
     ap.add_argument("--copy-probe-mib", type=int, default=0,

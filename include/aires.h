@@ -130,8 +130,11 @@ typedef enum aires_avalues {
 typedef enum aires_cbound {
     AIRES_CBOUND_PRODUCTS = 0,  /* u_i = min(N, P_i), P_i = sum nnz(B_k)   */
     AIRES_CBOUND_DENSE = 1,     /* u_i = N                                 */
-    AIRES_CBOUND_PAPER_EQ5 = 2  /* the paper's Eq. 5 estimate (not a bound;
+    AIRES_CBOUND_PAPER_EQ5 = 2, /* the paper's Eq. 5 estimate (not a bound;
                                    for planning experiments only)          */
+    AIRES_CBOUND_ROWS = 3       /* u_i = min(N, nnz(A_i) * max_k nnz(B_k)):
+                                   looser than PRODUCTS, but the planner
+                                   reads no column of A (no gather)       */
 } aires_cbound;
 
 typedef struct aires_plan_opts {

@@ -26,7 +26,7 @@ OK, E_INVALID_ARG, E_INVALID_CSR, E_DIM, E_BUDGET, E_OVERFLOW, E_OOM, E_HIP, E_S
     E_UNSUPPORTED, E_CAPACITY = 0, -1, -2, -3, -4, -5, -6, -7, -8, -9, -10
 IDX_I32, IDX_I64 = 0, 1
 MEM_DEVICE, MEM_HOST_PINNED, MEM_HOST = 0, 1, 2
-CBOUND_PRODUCTS, CBOUND_DENSE, CBOUND_PAPER_EQ5 = 0, 1, 2
+CBOUND_PRODUCTS, CBOUND_DENSE, CBOUND_PAPER_EQ5, CBOUND_ROWS = 0, 1, 2, 3
 KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split"]
 
 

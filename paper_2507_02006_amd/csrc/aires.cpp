@@ -396,6 +396,52 @@ void host_bounds(const aires_csr& A, const int64_t* arp, const std::vector<int32
   else host_bounds_t(A, arp, lenB.data(), max_len, N, lim, cu, cpre, above);
 }
 
+// max_k nnz(B_k) from B's row pointers
+aires_status host_max_row_length(const aires_csr& B, int64_t* max_len) {
+  const int64_t K = B.nrows;
+  if (B.mem == AIRES_MEM_DEVICE) {
+    std::vector<int32_t> len;
+    return host_row_lengths(B, len, max_len);
+  }
+  std::vector<int64_t> mx(16, 0);
+  const int nt = parallel_ranges(K, [&](int64_t lo, int64_t hi, int t) {
+    int64_t x = 0;
+    for (int64_t k = lo; k < hi; ++k) x = std::max<int64_t>(x, host_rp(B, k + 1) - host_rp(B, k));
+    mx[(size_t)t] = x;
+  });
+  *max_len = K > 0 ? *std::max_element(mx.begin(), mx.begin() + nt) : 0;
+  return AIRES_OK;
+}
+
+// u_i = min(N, nnz(A_i) * max_len) and its running sum, from A's row
+// pointers alone
+void host_row_bounds(const aires_csr& A, const int64_t* arp, int64_t max_len, int64_t N, I64Array& cu,
+                     I64Array& cpre) {
+  const int64_t m = A.nrows;
+  cu.alloc(m);
+  cpre.alloc(m + 1);
+  cpre[0] = 0;
+  std::vector<int64_t> part(17, 0);
+  const int nt = parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
+    int64_t sum = 0;
+    for (int64_t i = lo; i < hi; ++i) {
+      const int64_t len = arp[i + 1] - arp[i];
+      const int64_t u = len > 0 && max_len > N / len ? N : std::min<int64_t>(N, len * max_len);
+      cu[(size_t)i] = u;
+      sum += u;
+    }
+    part[(size_t)t + 1] = sum;
+  });
+  for (int t = 0; t < nt; ++t) part[(size_t)t + 1] += part[(size_t)t];
+  parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
+    int64_t run = part[(size_t)t];
+    for (int64_t i = lo; i < hi; ++i) {
+      run += cu[(size_t)i];
+      cpre[(size_t)i + 1] = run;
+    }
+  });
+}
+
 aires_status host_row_ptr(const aires_csr& M, std::vector<int64_t>& out) {
   out.resize((size_t)M.nrows + 1);
   if (M.mem == AIRES_MEM_DEVICE) {
@@ -478,7 +524,7 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   }
   if (o.c_placement != AIRES_MEM_DEVICE && o.c_placement != AIRES_MEM_HOST_PINNED)
     return fail(AIRES_E_INVALID_ARG, "opts.c_placement %d invalid", o.c_placement);
-  if (o.c_bound < AIRES_CBOUND_PRODUCTS || o.c_bound > AIRES_CBOUND_PAPER_EQ5)
+  if (o.c_bound < AIRES_CBOUND_PRODUCTS || o.c_bound > AIRES_CBOUND_ROWS)
     return fail(AIRES_E_INVALID_ARG, "opts.c_bound %d invalid", o.c_bound);
   if (o.max_tile_rows < 0 || o.max_tile_bytes < 0 || o.m_a_bytes < 0)
     return fail(AIRES_E_INVALID_ARG, "negative tile cap");
@@ -577,6 +623,12 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
       if (st != AIRES_OK) { delete p; return st; }
       const int64_t lim = p->split ? p->th.max_p[p->th.nb - 2] : INT64_MAX;
       host_bounds(*A, arp, lenB, max_len, N, lim, cu, cpre, &split_rows);
+      p->info.c_bound_entries = cpre[(size_t)m];
+    } else if (o.c_bound == AIRES_CBOUND_ROWS) {
+      int64_t max_len = 0;
+      st = host_max_row_length(*B, &max_len);
+      if (st != AIRES_OK) { delete p; return st; }
+      host_row_bounds(*A, arp, max_len, N, cu, cpre);
       p->info.c_bound_entries = cpre[(size_t)m];
     } else if (o.c_bound == AIRES_CBOUND_DENSE) {
       cu.alloc(m);

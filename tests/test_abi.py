@@ -234,3 +234,22 @@ def test_spmm_argument_errors():
     assert "dense tiles" in lib.aires_last_error().decode()
     assert call(csr(), ldw=1 << 23, algo=B_.SPMM_DENSE_TILES) == -9
     assert call(csr(), F=1 << 31) == -9
+
+
+@pytest.mark.parametrize("N", [8, 256, 5000])
+def test_streamed_rows_bound(N):
+    """c_bound = ROWS: u_i = min(N, nnz(A_i) * max_k nnz(B_k)) from the row
+    pointers alone; never below the exact bound min(N, P_i)."""
+    rng = np.random.default_rng(N + 7)
+    A = workloads.random_csr(rng, 70000, 300, 0.01)
+    Bm = workloads.random_csr(rng, 300, N, min(1.0, 40.0 / N))
+    alen = np.diff(A.rp.astype(np.int64))
+    maxlen = int(np.diff(Bm.rp.astype(np.int64)).max())
+    want = np.minimum(N, alen * maxlen)
+    with aires.tile_plan(_host(A), _host(Bm), 1 << 40, c_on_host=True, c_bound=B_.CBOUND_ROWS) as p:
+        info = aires.plan_info(p)
+        tiles = aires.plan_tiles(p)
+    assert info.c_bound_entries == int(want.sum())
+    for t in tiles:
+        assert t["c_bound_entries"] == int(want[t["r0"]:t["r1"]].sum())
+    assert info.c_bound_entries >= int(np.minimum(oracle.products(A, Bm), N).sum())

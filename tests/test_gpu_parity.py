@@ -561,3 +561,21 @@ def test_sym_norm_streamed_device_c(torch_gpu):
         st = aires.plan_stats(plan)
         assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
     assert st["h2d_bytes"] == 4 * (A.nrows + 1) + 4 * A.nnz
+
+
+def test_streamed_rows_bound(torch_gpu):
+    """Streamed tiles planned with the gather-free C bound (c_bound = ROWS):
+    the same C as the oracle."""
+    import paper_2507_02006_amd as aires
+    from paper_2507_02006_amd import _binding as B_
+    A, B = workloads.workload(5, n=60000)
+    ref = oracle.spgemm(A, B)
+    pA, pB = aires.to_pinned(A), aires.to_pinned(B)
+    # P_i is not computed on the host, so the split rows' slots take their cap
+    budget = B.nbytes() + (24 << 20) + 2 * 3_000_000
+    say("streamed cfg5 n=60000 rows bound budget=%d" % budget)
+    with aires.tile_plan(pA, pB, budget, c_on_host=True, c_bound=B_.CBOUND_ROWS) as plan:
+        assert aires.plan_info(plan).ntiles >= 3
+        C = aires.spgemm(plan)
+        assert_match(C.rp, C.col, C.val, ref)
+        C.free()
