@@ -124,22 +124,30 @@ def host_cpu():
     return model, len(os.sched_getaffinity(0))
 
 
+def traffic_sources_sha256() -> str:
+    """SHA-256 over kernels.hip followed by aires.cpp."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("kernels.hip", "aires.cpp"):
+        with open(os.path.join(ROOT, "paper_2507_02006_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def measured_traffic(kernel_name: str, dom_bytes_launch: int):
     """HBM bytes per launch of the dominant kernel, from the committed
     rocprofv3 FETCH_SIZE/WRITE_SIZE summary (profiles/traffic.json), only
-    if it was taken on the kernel source as it is now; else None."""
-    import hashlib
+    if it was taken on the kernels and the planner (whose defaults shape
+    the launches) as they are now; else None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
-    src = os.path.join(ROOT, "paper_2507_02006_amd", "csrc", "kernels.hip")
     try:
         with open(path) as f:
             rec = json.load(f)
-        with open(src, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
+        sha = traffic_sources_sha256()
     except OSError:
         return None
     ent = rec.get(kernel_name)
-    if not ent or ent.get("kernels_hip_sha256") != sha:
+    if not ent or ent.get("sources_sha256") != sha:
         return None
     return int(ent["traffic_bytes"])
 

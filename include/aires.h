@@ -161,11 +161,11 @@ typedef struct aires_plan_opts {
                                    products are handled by one wavefront   */
     /* Wide products (N > dense_max_cols) cut columns into grains and rows
        into windows of whole grains; 0 = default for each.                 */
-    int64_t window_grain_cols;  /* grain width, multiple of 32 (4096)      */
+    int64_t window_grain_cols;  /* grain width, multiple of 32 (8192)      */
     int64_t window_max_grains;  /* grains one window may span (64)         */
     int64_t window_max_entries; /* C entries one window may hold, in
                                    [grain, 65535] (16384)                  */
-    int64_t count_grains;       /* grains one symbolic item covers (64)    */
+    int64_t count_grains;       /* grains one symbolic item covers (32)    */
     int64_t keep_bitmap_products; /* 0: default (65536), < 0: never.  The
                                    symbolic phase keeps the presence bitmaps
                                    of rows with more products than this for

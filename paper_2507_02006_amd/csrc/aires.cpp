@@ -51,12 +51,15 @@ constexpr int64_t kDenseWaveMaxN = 2048;     // widest dense row one wavefront h
 constexpr int64_t kDenseMaxCols = 16384;     // widest dense row a workgroup holds
 // Wide products: a window's bitmap and values share a pool of LDS sized so
 // that a numeric workgroup uses 52 KB and three 512-thread workgroups (24
-// wavefronts) share a CU; the grain and entry caps rarely bind.
-constexpr int64_t kGrainCols = 4096;         // column grain of wide products
+// wavefronts) share a CU; the grain and entry caps rarely bind. A symbolic
+// item's bitmap (grains x columns / 8 bytes) stays at 32 KB so that four
+// 512-thread counting workgroups share a CU; wider grains mean fewer grain
+// steps per item at the same LDS.
+constexpr int64_t kGrainCols = 8192;         // column grain of wide products
 constexpr int64_t kWindowMaxGrains = 64;     // grains one window may span
 constexpr int64_t kWindowMaxEntries = 16384; // C entries one window may hold
 constexpr int64_t kWindowPoolBytes = 38912;  // LDS shared by a window's bitmap and values
-constexpr int64_t kCountGrains = 64;         // grains one symbolic item covers
+constexpr int64_t kCountGrains = 32;         // grains one symbolic item covers
 constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps kept for heavy rows
 constexpr int64_t kStreamTiles = 16;                       // default tile count of a streamed A
 constexpr int64_t kMinStreamTileBytes = int64_t(32) << 20;  // ... with at least this much of A per tile

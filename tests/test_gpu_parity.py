@@ -162,6 +162,14 @@ def test_cfg3_scaled_small_windows(torch_gpu):
           window_max_entries=1024, count_grains=5)
 
 
+def test_cfg3_scaled_wide_grains(torch_gpu):
+    """8192-column grains (256 bitmap words per grain) with symbolic items of
+    2 grains over 5 grains (a ragged last item) and windows of <= 2 grains."""
+    A, B = workloads.workload(3, n=40000)
+    check(torch_gpu, A, B, "cfg3 n=40000 8192-col grains", window_grain_cols=8192, window_max_grains=2,
+          window_max_entries=8192, count_grains=2)
+
+
 def test_cfg3_scaled_narrow_block(torch_gpu):
     """A*A with 2048 < N <= 16384: hash bins plus single-window workgroup rows."""
     A, B = workloads.workload(3, n=12000)
