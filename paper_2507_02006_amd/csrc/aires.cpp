@@ -333,9 +333,10 @@ aires_status host_row_lengths(const aires_csr& B, std::vector<int32_t>& len, int
   return AIRES_OK;
 }
 
-// C bound per row, u_i = min(N, P_i) with P_i = sum over A_i of nnz(B_k),
-// its running sum (cpre[0] = 0, m + 1 entries), and the number of rows
-// with P_i > lim.  The gather of nnz(B_k) is random over B's rows: the
+// C bound per row, u_i = min(N, P_i) with P_i = sum over A_i of nnz(B_k):
+// its total, its running sum when cpre is given (cpre[0] = 0, m + 1
+// entries; u_i is parked in cpre[i + 1] and summed in place), and the
+// number of rows with P_i > lim.  The gather of nnz(B_k) is random over B's rows: the
 // lengths are read from the narrowest table that holds them (a byte each
 // for feature matrices), each thread requests them a fixed distance ahead
 // of their use, and a row stops once its sum reaches N, or max(N, lim + 1)
@@ -343,13 +344,15 @@ aires_status host_row_lengths(const aires_csr& B, std::vector<int32_t>& len, int
 // P_i > lim stay exact.
 template <typename L>
 void host_bounds_t(const aires_csr& A, const int64_t* arp, const L* len, int64_t max_len, int64_t N, int64_t lim,
-                   I64Array& cu, I64Array& cpre, int64_t* above) {
+                   I64Array* cpre, int64_t* total, int64_t* above) {
   constexpr int64_t kAhead = 64;
   const int64_t m = A.nrows;
   const int32_t* col = A.col_idx;
-  cu.alloc(m);
-  cpre.alloc(m + 1);
-  cpre[0] = 0;
+  if (cpre) {
+    cpre->alloc(m + 1);
+    (*cpre)[0] = 0;
+  }
+  int64_t* u_out = cpre ? &(*cpre)[1] : nullptr;
   std::vector<int64_t> part(17, 0), cnt(17, 0);
   const int nt = parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
     int64_t sum = 0, c = 0;
@@ -363,7 +366,7 @@ void host_bounds_t(const aires_csr& A, const int64_t* arp, const L* len, int64_t
         P += len[col[q]];
       }
       const int64_t u = std::min<int64_t>(N, P);
-      cu[(size_t)i] = u;
+      if (u_out) u_out[i] = u;
       sum += u;
       c += P > lim;
     }
@@ -371,20 +374,23 @@ void host_bounds_t(const aires_csr& A, const int64_t* arp, const L* len, int64_t
     cnt[(size_t)t] = c;
   });
   for (int t = 0; t < nt; ++t) part[(size_t)t + 1] += part[(size_t)t];
-  parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
-    int64_t run = part[(size_t)t];
-    for (int64_t i = lo; i < hi; ++i) {
-      run += cu[(size_t)i];
-      cpre[(size_t)i + 1] = run;
-    }
-  });
+  if (u_out) {
+    parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
+      int64_t run = part[(size_t)t];
+      for (int64_t i = lo; i < hi; ++i) {
+        run += u_out[i];
+        u_out[i] = run;
+      }
+    });
+  }
+  *total = part[(size_t)nt];
   int64_t a = 0;
   for (int t = 0; t < nt; ++t) a += cnt[(size_t)t];
   *above = a;
 }
 
 void host_bounds(const aires_csr& A, const int64_t* arp, const std::vector<int32_t>& lenB, int64_t max_len,
-                 int64_t N, int64_t lim, I64Array& cu, I64Array& cpre, int64_t* above) {
+                 int64_t N, int64_t lim, I64Array* cpre, int64_t* total, int64_t* above) {
   const int64_t K = (int64_t)lenB.size();
   auto narrow = [&](auto tag) {
     using L = decltype(tag);
@@ -392,11 +398,11 @@ void host_bounds(const aires_csr& A, const int64_t* arp, const std::vector<int32
     parallel_ranges(K, [&](int64_t lo, int64_t hi, int) {
       for (int64_t k = lo; k < hi; ++k) t[(size_t)k] = (L)lenB[(size_t)k];
     });
-    host_bounds_t(A, arp, t.data(), max_len, N, lim, cu, cpre, above);
+    host_bounds_t(A, arp, t.data(), max_len, N, lim, cpre, total, above);
   };
   if (max_len <= 255) narrow(uint8_t{});
   else if (max_len <= 65535) narrow(uint16_t{});
-  else host_bounds_t(A, arp, lenB.data(), max_len, N, lim, cu, cpre, above);
+  else host_bounds_t(A, arp, lenB.data(), max_len, N, lim, cpre, total, above);
 }
 
 // max_k nnz(B_k) from B's row pointers
@@ -407,40 +413,45 @@ aires_status host_max_row_length(const aires_csr& B, int64_t* max_len) {
     return host_row_lengths(B, len, max_len);
   }
   std::vector<int64_t> mx(16, 0);
-  const int nt = parallel_ranges(K, [&](int64_t lo, int64_t hi, int t) {
-    int64_t x = 0;
-    for (int64_t k = lo; k < hi; ++k) x = std::max<int64_t>(x, host_rp(B, k + 1) - host_rp(B, k));
-    mx[(size_t)t] = x;
-  });
+  auto scan = [&](const auto* r) {
+    return parallel_ranges(K, [&, r](int64_t lo, int64_t hi, int t) {
+      int64_t x = 0;
+      for (int64_t k = lo; k < hi; ++k) x = std::max<int64_t>(x, (int64_t)r[k + 1] - (int64_t)r[k]);
+      mx[(size_t)t] = x;
+    });
+  };
+  const int nt = B.rp_type == AIRES_IDX_I64 ? scan(static_cast<const int64_t*>(B.row_ptr))
+                                            : scan(static_cast<const int32_t*>(B.row_ptr));
   *max_len = K > 0 ? *std::max_element(mx.begin(), mx.begin() + nt) : 0;
   return AIRES_OK;
 }
 
-// u_i = min(N, nnz(A_i) * max_len) and its running sum, from A's row
-// pointers alone
-void host_row_bounds(const aires_csr& A, const int64_t* arp, int64_t max_len, int64_t N, I64Array& cu,
-                     I64Array& cpre) {
+// u_i = min(N, nnz(A_i) * max_len) from A's row pointers alone: its total,
+// and its running sum when cpre is given (a second pass recomputes u_i)
+void host_row_bounds(const aires_csr& A, const int64_t* arp, int64_t max_len, int64_t N, I64Array* cpre,
+                     int64_t* total) {
   const int64_t m = A.nrows;
-  cu.alloc(m);
-  cpre.alloc(m + 1);
-  cpre[0] = 0;
+  auto u_of = [&](int64_t i) -> int64_t {
+    const int64_t len = arp[i + 1] - arp[i];
+    return len > 0 && max_len > N / len ? N : std::min<int64_t>(N, len * max_len);
+  };
   std::vector<int64_t> part(17, 0);
   const int nt = parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
     int64_t sum = 0;
-    for (int64_t i = lo; i < hi; ++i) {
-      const int64_t len = arp[i + 1] - arp[i];
-      const int64_t u = len > 0 && max_len > N / len ? N : std::min<int64_t>(N, len * max_len);
-      cu[(size_t)i] = u;
-      sum += u;
-    }
+    for (int64_t i = lo; i < hi; ++i) sum += u_of(i);
     part[(size_t)t + 1] = sum;
   });
   for (int t = 0; t < nt; ++t) part[(size_t)t + 1] += part[(size_t)t];
+  *total = part[(size_t)nt];
+  if (!cpre) return;
+  cpre->alloc(m + 1);
+  (*cpre)[0] = 0;
+  int64_t* run_out = &(*cpre)[1];
   parallel_ranges(m, [&](int64_t lo, int64_t hi, int t) {
     int64_t run = part[(size_t)t];
     for (int64_t i = lo; i < hi; ++i) {
-      run += cu[(size_t)i];
-      cpre[(size_t)i + 1] = run;
+      run += u_of(i);
+      run_out[i] = run;
     }
   });
 }
@@ -605,8 +616,8 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   // Per-row and per-tile bytes of one tile slot.
   // ws per row: P_i (8) + bin list (4) + window counts (4 per window) + C row
   // pointer of the tile (8, streamed only).
-  I64Array cu;    // C bound per row (entries), streamed + host C
-  I64Array cpre;  // its running sum when C is placed in host memory
+  I64Array cu;    // C bound per row (entries), for the bounds built row by row
+  I64Array cpre;  // running sum of the C bound when C is placed in host memory
   int64_t split_rows = -1;    // rows above the split threshold (when P_i is computed)
   int64_t resident = p->info.b_bytes + kFixedWorkspace + index_bytes;
   // (+ per-grain counts and per-row window counts of wide products)
@@ -625,14 +636,13 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
       st = host_row_lengths(*B, lenB, &max_len);
       if (st != AIRES_OK) { delete p; return st; }
       const int64_t lim = p->split ? p->th.max_p[p->th.nb - 2] : INT64_MAX;
-      host_bounds(*A, arp, lenB, max_len, N, lim, cu, cpre, &split_rows);
-      p->info.c_bound_entries = cpre[(size_t)m];
+      host_bounds(*A, arp, lenB, max_len, N, lim, c_on_host ? &cpre : nullptr, &p->info.c_bound_entries,
+                  &split_rows);
     } else if (o.c_bound == AIRES_CBOUND_ROWS) {
       int64_t max_len = 0;
       st = host_max_row_length(*B, &max_len);
       if (st != AIRES_OK) { delete p; return st; }
-      host_row_bounds(*A, arp, max_len, N, cu, cpre);
-      p->info.c_bound_entries = cpre[(size_t)m];
+      host_row_bounds(*A, arp, max_len, N, c_on_host ? &cpre : nullptr, &p->info.c_bound_entries);
     } else if (o.c_bound == AIRES_CBOUND_DENSE) {
       cu.alloc(m);
       for (int64_t i = 0; i < m; ++i) cu[(size_t)i] = N;
