@@ -193,6 +193,10 @@ def test_streamed_c_bound_exact(N, row_max):
     assert info.c_bound_entries == int(np.minimum(P, N).sum())
     for t in tiles:
         assert t["c_bound_entries"] == int(np.minimum(P[t["r0"]:t["r1"]], N).sum())
+    # C on the device: the plan needs (and keeps) only the total
+    with aires.tile_plan(_host(A), _host(Bm), 1 << 40) as p:
+        assert aires.plan_info(p).c_bound_entries == int(np.minimum(P, N).sum())
+        assert all(t["c_bound_entries"] == -1 for t in aires.plan_tiles(p))
 
 
 def test_sym_norm_plan():
@@ -253,3 +257,6 @@ def test_streamed_rows_bound(N):
     for t in tiles:
         assert t["c_bound_entries"] == int(want[t["r0"]:t["r1"]].sum())
     assert info.c_bound_entries >= int(np.minimum(oracle.products(A, Bm), N).sum())
+    with aires.tile_plan(_host(A), _host(Bm), 1 << 40, c_bound=B_.CBOUND_ROWS) as p:
+        assert aires.plan_info(p).c_bound_entries == int(want.sum())
+        assert all(t["c_bound_entries"] == -1 for t in aires.plan_tiles(p))
