@@ -36,23 +36,28 @@ def say(msg):
     print("[gpu-case] " + msg, flush=True)
 
 
-def dev_csr(torch, A, rp64=False):
+def dev_csr(torch, A, rp64=False, a_offset=0):
+    """A on the device; a_offset > 0 starts its column and value arrays that
+    many elements into their allocations (off 16-byte alignment for 1-3)."""
     rp = A.rp.astype(np.int64 if rp64 else np.int32)
-    return (A.nrows, A.ncols, torch.from_numpy(rp).cuda(), torch.from_numpy(A.col.astype(np.int32)).cuda(),
-            torch.from_numpy(A.val.astype(np.float32)).cuda())
+    col = torch.zeros(A.nnz + a_offset, dtype=torch.int32, device="cuda")[a_offset:]
+    val = torch.zeros(A.nnz + a_offset, dtype=torch.float32, device="cuda")[a_offset:]
+    col.copy_(torch.from_numpy(A.col.astype(np.int32)))
+    val.copy_(torch.from_numpy(A.val.astype(np.float32)))
+    return (A.nrows, A.ncols, torch.from_numpy(rp).cuda(), col, val)
 
 
 def check(torch, A, W, relu=False, rp64=False, ldw_pad=0, ldy_pad=0, w_offset=0, exact=False, name="",
-          algo="auto"):
+          algo="auto", a_offset=0):
     import paper_2507_02006_amd as aires
-    say("%s algo=%s m=%d K=%d F=%d relu=%d rp64=%d pads=(%d,%d) off=%d" % (
-        name, algo, A.nrows, A.ncols, W.shape[1], relu, rp64, ldw_pad, ldy_pad, w_offset))
+    say("%s algo=%s m=%d K=%d F=%d relu=%d rp64=%d pads=(%d,%d) off=%d a_off=%d" % (
+        name, algo, A.nrows, A.ncols, W.shape[1], relu, rp64, ldw_pad, ldy_pad, w_offset, a_offset))
     K, F = W.shape
     buf = torch.zeros(K * (F + ldw_pad) + w_offset + 1, dtype=torch.float32, device="cuda")
     Wd = buf[w_offset:w_offset + K * (F + ldw_pad)].view(K, F + ldw_pad)[:, :F]
     Wd.copy_(torch.from_numpy(W))
     ybuf = torch.full((A.nrows, F + ldy_pad), 7.0, dtype=torch.float32, device="cuda")
-    Y = aires.spmm(dev_csr(torch, A, rp64), Wd, relu=relu, out=ybuf[:, :F], algo=algo)
+    Y = aires.spmm(dev_csr(torch, A, rp64, a_offset), Wd, relu=relu, out=ybuf[:, :F], algo=algo)
     torch.cuda.synchronize()
     y = Y.cpu().numpy().astype(np.float64)
     if ldy_pad:
@@ -128,6 +133,8 @@ def test_strides_offsets_and_rp64(torch_gpu, algo):
     check(torch_gpu, A, W, ldw_pad=4, name="aligned pad", algo=algo)
     check(torch_gpu, A, W, w_offset=1, name="unaligned W", algo=algo)
     check(torch_gpu, A, W, rp64=True, relu=True, name="rp64", algo=algo)
+    for off in (1, 2, 4):  # A's arrays off 16-byte alignment (single-entry loads), then back on it
+        check(torch_gpu, A, W, a_offset=off, name="A offset %d" % off, algo=algo)
 
 
 def test_edges(torch_gpu):
@@ -162,6 +169,8 @@ def test_dense_tiles_dense_rows(torch_gpu, density):
     for F in (48, 300):
         W = rng.uniform(-1, 1, (333, F)).astype(np.float32)
         check(torch_gpu, A, W, relu=True, name="dense rows %.1f F=%d" % (density, F), algo="dense_tiles")
+        check(torch_gpu, A, W, name="dense rows %.1f F=%d A offset 1" % (density, F), algo="dense_tiles",
+              a_offset=1)
 
 
 def test_dense_tiles_grid_loop(torch_gpu):
