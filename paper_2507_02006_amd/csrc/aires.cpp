@@ -296,40 +296,25 @@ int parallel_ranges(int64_t n, Fn fn) {
   return nt;
 }
 
-// nnz(B_k) for every row of B (rows hold at most N < 2^31 entries)
+// nnz(B_k) for every row of a device-resident B (rows hold at most N < 2^31
+// entries), from its row pointers copied to the host
 aires_status host_row_lengths(const aires_csr& B, std::vector<int32_t>& len, int64_t* max_len) {
   const int64_t K = B.nrows;
   len.resize((size_t)K);
-  if (B.mem == AIRES_MEM_DEVICE) {
-    std::vector<int64_t> brp((size_t)K + 1);
-    if (B.rp_type == AIRES_IDX_I64) {
-      HIP_TRY(hipMemcpy(brp.data(), B.row_ptr, brp.size() * 8, hipMemcpyDeviceToHost));
-    } else {
-      std::vector<int32_t> tmp(brp.size());
-      HIP_TRY(hipMemcpy(tmp.data(), B.row_ptr, tmp.size() * 4, hipMemcpyDeviceToHost));
-      for (size_t i = 0; i < tmp.size(); ++i) brp[i] = tmp[i];
-    }
-    int64_t mx = 0;
-    for (int64_t k = 0; k < K; ++k) {
-      len[(size_t)k] = (int32_t)(brp[(size_t)k + 1] - brp[(size_t)k]);
-      mx = std::max<int64_t>(mx, len[(size_t)k]);
-    }
-    *max_len = mx;
-    return AIRES_OK;
+  std::vector<int64_t> brp((size_t)K + 1);
+  if (B.rp_type == AIRES_IDX_I64) {
+    HIP_TRY(hipMemcpy(brp.data(), B.row_ptr, brp.size() * 8, hipMemcpyDeviceToHost));
+  } else {
+    std::vector<int32_t> tmp(brp.size());
+    HIP_TRY(hipMemcpy(tmp.data(), B.row_ptr, tmp.size() * 4, hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < tmp.size(); ++i) brp[i] = tmp[i];
   }
-  std::vector<int64_t> mx(16, 0);
-  const int nt = parallel_ranges(K, [&](int64_t lo, int64_t hi, int t) {
-    int32_t x = 0;
-    if (B.rp_type == AIRES_IDX_I64) {
-      const int64_t* r = static_cast<const int64_t*>(B.row_ptr);
-      for (int64_t k = lo; k < hi; ++k) x = std::max(x, len[(size_t)k] = (int32_t)(r[k + 1] - r[k]));
-    } else {
-      const int32_t* r = static_cast<const int32_t*>(B.row_ptr);
-      for (int64_t k = lo; k < hi; ++k) x = std::max(x, len[(size_t)k] = r[k + 1] - r[k]);
-    }
-    mx[(size_t)t] = x;
-  });
-  *max_len = *std::max_element(mx.begin(), mx.begin() + nt);
+  int64_t mx = 0;
+  for (int64_t k = 0; k < K; ++k) {
+    len[(size_t)k] = (int32_t)(brp[(size_t)k + 1] - brp[(size_t)k]);
+    mx = std::max<int64_t>(mx, len[(size_t)k]);
+  }
+  *max_len = mx;
   return AIRES_OK;
 }
 
@@ -389,20 +374,34 @@ void host_bounds_t(const aires_csr& A, const int64_t* arp, const L* len, int64_t
   *above = a;
 }
 
-void host_bounds(const aires_csr& A, const int64_t* arp, const std::vector<int32_t>& lenB, int64_t max_len,
-                 int64_t N, int64_t lim, I64Array* cpre, int64_t* total, int64_t* above) {
-  const int64_t K = (int64_t)lenB.size();
+// B's row lengths in the narrowest table that holds them (max_len known),
+// read from B's row pointers in host memory or from lenB when B is on the
+// device (its row pointers were copied to the host to measure them)
+void host_bounds(const aires_csr& A, const int64_t* arp, const aires_csr& B, const std::vector<int32_t>& lenB,
+                 int64_t max_len, int64_t N, int64_t lim, I64Array* cpre, int64_t* total, int64_t* above) {
+  const int64_t K = B.nrows;
   auto narrow = [&](auto tag) {
     using L = decltype(tag);
     std::vector<L> t((size_t)K);
-    parallel_ranges(K, [&](int64_t lo, int64_t hi, int) {
-      for (int64_t k = lo; k < hi; ++k) t[(size_t)k] = (L)lenB[(size_t)k];
-    });
+    auto fill = [&](const auto* r) {
+      parallel_ranges(K, [&, r](int64_t lo, int64_t hi, int) {
+        for (int64_t k = lo; k < hi; ++k) t[(size_t)k] = (L)(r[k + 1] - r[k]);
+      });
+    };
+    if (B.mem == AIRES_MEM_DEVICE) {
+      parallel_ranges(K, [&](int64_t lo, int64_t hi, int) {
+        for (int64_t k = lo; k < hi; ++k) t[(size_t)k] = (L)lenB[(size_t)k];
+      });
+    } else if (B.rp_type == AIRES_IDX_I64) {
+      fill(static_cast<const int64_t*>(B.row_ptr));
+    } else {
+      fill(static_cast<const int32_t*>(B.row_ptr));
+    }
     host_bounds_t(A, arp, t.data(), max_len, N, lim, cpre, total, above);
   };
   if (max_len <= 255) narrow(uint8_t{});
   else if (max_len <= 65535) narrow(uint16_t{});
-  else host_bounds_t(A, arp, lenB.data(), max_len, N, lim, cpre, total, above);
+  else narrow(int32_t{});
 }
 
 // max_k nnz(B_k) from B's row pointers
@@ -631,12 +630,12 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   } else if (o.m_a_bytes == 0) {
     // C bound per row for the C slots (or for a device-resident C)
     if (o.c_bound == AIRES_CBOUND_PRODUCTS) {
-      std::vector<int32_t> lenB;
+      std::vector<int32_t> lenB;  // B on the device only
       int64_t max_len = 0;
-      st = host_row_lengths(*B, lenB, &max_len);
+      st = B->mem == AIRES_MEM_DEVICE ? host_row_lengths(*B, lenB, &max_len) : host_max_row_length(*B, &max_len);
       if (st != AIRES_OK) { delete p; return st; }
       const int64_t lim = p->split ? p->th.max_p[p->th.nb - 2] : INT64_MAX;
-      host_bounds(*A, arp, lenB, max_len, N, lim, c_on_host ? &cpre : nullptr, &p->info.c_bound_entries,
+      host_bounds(*A, arp, *B, lenB, max_len, N, lim, c_on_host ? &cpre : nullptr, &p->info.c_bound_entries,
                   &split_rows);
     } else if (o.c_bound == AIRES_CBOUND_ROWS) {
       int64_t max_len = 0;
