@@ -223,6 +223,7 @@ def test_streamed_tiles_host_c(torch_gpu):
         C = aires.spgemm(plan)
         st = aires.plan_stats(plan)
         assert info.ntiles >= 3
+        assert info.c_bound_entries == int(np.minimum(oracle.products(A, B), B.ncols).sum())
         assert C.on_host
         assert_match(C.rp, C.col, C.val, ref)
         assert st["host_syncs"] == info.ntiles
@@ -242,6 +243,8 @@ def test_streamed_tiles_device_c(torch_gpu):
     say("streamed cfg4 n=40000 device C")
     with aires.tile_plan(pA, dB, budget) as plan:
         assert aires.plan_info(plan).ntiles >= 2
+        # exact bound with B's row lengths read from its device row pointers
+        assert aires.plan_info(plan).c_bound_entries == int(np.minimum(oracle.products(A, B), B.ncols).sum())
         C = aires.spgemm(plan)
         torch_gpu.cuda.synchronize()
         assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
