@@ -398,6 +398,167 @@ def streamed(args):
         hold.pop()
 
 
+def in_core_run(A, B, dA, dB, steps, warmup):
+    """Time `steps` whole in-core steps (plan + spgemm until C is ready, C
+    dropped) after `warmup`; per-phase and per-kind times from the library's
+    HIP events; the dominant numeric launch against the HBM roofline."""
+    import torch
+    import paper_2507_02006_amd as aires
+    P = row_products(A, B)
+    total_products = int(P.sum())
+
+    def step():
+        with aires.tile_plan(dA, dB, 0, timing=True) as plan:
+            C = aires.spgemm(plan)
+            torch.cuda.synchronize()
+            st = aires.plan_stats(plan)
+        return C, st
+
+    for _ in range(warmup):
+        C, _ = step()
+        del C
+    torch.cuda.synchronize()
+    stats = []
+    t_start = time.perf_counter()
+    for _ in range(steps):
+        C, st = step()
+        stats.append(st)
+        last_rp = C.rp  # only the row pointers outlive the step, as for a caller that consumes C
+        del C
+    torch.cuda.synchronize()
+    ms_per_step = 1e3 * (time.perf_counter() - t_start) / steps
+    assert all(s["products"] == total_products for s in stats)
+    nnz_c = stats[-1]["nnz_c"]
+    # dominant kernel: numeric launch of the kind with the largest time
+    num_ms = {k: np.mean([s["kind_ms"]["numeric"][k] for s in stats]) for k in KIND_NAMES}
+    dom = max(num_ms, key=num_ms.get)
+    kinds = row_kinds(P, B.ncols)
+    sel = kinds == KIND_NAMES.index(dom)
+    crow = np.diff(last_rp.cpu().numpy())
+    alen = np.diff(A.rp.astype(np.int64))
+    sA = A.rp.dtype.itemsize
+    dom_bytes = int((sA + 8 * alen[sel] + 8 + 8 * crow[sel]).sum()) + B.nbytes()
+    dom_gbs = dom_bytes / (num_ms[dom] * 1e-3) / 1e9
+    # gather model (no reuse): B.row_ptr per A entry and 8 bytes of B per product
+    sB = B.rp.dtype.itemsize
+    dom_gather = int((sA + 8 * alen[sel] + 2 * sB * alen[sel] + 8 * P[sel] + 8 + 8 * crow[sel]).sum())
+    phase = {k: round(float(np.mean([s[k] for s in stats])), 4)
+             for k in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "total_ms")}
+    compulsory = A.nbytes() + B.nbytes() + 8 * (A.nrows + 1) + 8 * nnz_c
+    return {
+        "ms_per_step": ms_per_step, "P": P, "products": total_products, "nnz_c": nnz_c,
+        "tiles": stats[-1]["ntiles"], "dominant": dom,
+        "roofline": {"bound": "hbm", "kernel": "numeric/%s" % dom, "achieved": round(dom_gbs, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "algorithmic_bytes": dom_bytes, "avg_launch_ms": round(num_ms[dom], 4),
+                     "gather_model_gbs": round(dom_gather / (num_ms[dom] * 1e-3) / 1e9, 2)},
+        "phases_ms": phase,
+        "numeric_gflops": round(2 * total_products / (phase["numeric_ms"] * 1e-3) / 1e9, 2),
+        "end_to_end_compulsory_gbs": round(compulsory / (ms_per_step * 1e-3) / 1e9, 2),
+        "numeric_kind_ms": {k: round(float(v), 4) for k, v in num_ms.items() if v > 0},
+    }
+
+
+def overlap_fraction(ts, a="h2d", b="compute"):
+    """Share of the busy time of phase `a` (summed over tiles) during which
+    phase `b` of some tile was running, from the per-tile event instants."""
+    ia = [(t[a + "_begin_ms"], t[a + "_end_ms"]) for t in ts if t[a + "_begin_ms"] >= 0]
+    ib = [(t[b + "_begin_ms"], t[b + "_end_ms"]) for t in ts if t[b + "_begin_ms"] >= 0]
+    busy = sum(e - s for s, e in ia)
+    if busy <= 0:
+        return None
+    both = sum(max(0.0, min(e1, e2) - max(s1, s2)) for s1, e1 in ia for s2, e2 in ib)
+    return round(both / busy, 4)
+
+
+def extras(args):
+    """The other configurations in the same record: cfg2 in core (the
+    bench's step, same timing rules), and cfg5 as the out-of-core call of
+    Algorithm 2 (A and X generated into pinned host memory, a 32 GB device
+    budget, C returned to pinned host memory; whole calls, planning and the
+    host C allocation included)."""
+    import torch
+    import workloads
+    import paper_2507_02006_amd as aires
+    out = {}
+    t0 = time.perf_counter()
+    A, B = workloads.workload(2)
+    gen = time.perf_counter() - t0
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    r = in_core_run(A, B, dA, dB, 10, 3)
+    out["cfg2_in_core"] = {
+        "workload": "cfg2 " + WORKLOAD_NAMES[2], "products": r["products"], "nnz_c": r["nnz_c"],
+        "ms_per_step": round(r["ms_per_step"], 4),
+        "gflops": round(2 * r["products"] / (r["ms_per_step"] * 1e-3) / 1e9, 3),
+        "numeric_gflops": r["numeric_gflops"], "phases_ms": r["phases_ms"],
+        "dominant_kernel": r["roofline"]["kernel"], "dominant_ms": r["roofline"]["avg_launch_ms"],
+        "dominant_frac_hbm": r["roofline"]["frac"], "dominant_gbs": r["roofline"]["achieved"],
+        "steps": 10, "warmup": 3, "generation_s": round(gen, 2)}
+    print("[bench] cfg2 in core: %.3f ms" % r["ms_per_step"], file=sys.stderr, flush=True)
+    del dA, dB, A, B
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    cfg = workloads.CONFIGS[5]
+    n = cfg["n"]
+    hold = []
+
+    def pinned(rp_dtype):
+        def alloc(nnz):
+            rp = torch.empty(n + 1, dtype=rp_dtype, pin_memory=True)
+            col = torch.empty(max(nnz, 1), dtype=torch.int32, pin_memory=True)[:nnz]
+            val = torch.empty(max(nnz, 1), dtype=torch.float32, pin_memory=True)[:nnz]
+            hold.append((rp, col, val))
+            return rp.numpy(), col.numpy(), val.numpy()
+        return alloc
+
+    t0 = time.perf_counter()
+    A = workloads.rmat_sym(n, cfg["deg"], seed=5, rp64=True, out=pinned(torch.int64))
+    B = workloads.features(n, cfg["F"], cfg["rho"], seed=1005, out=pinned(torch.int32))
+    gen = time.perf_counter() - t0
+    print("[bench] cfg5 generated in %.1f s" % gen, file=sys.stderr, flush=True)
+    tA, tB = (A.nrows, A.ncols) + hold[0], (B.nrows, B.ncols) + hold[1]
+    budget = 32 << 30
+    runs = []
+    for it in range(1 + 3):
+        t1 = time.perf_counter()
+        with aires.tile_plan(tA, tB, budget, c_on_host=True, timing=True) as plan:
+            t2 = time.perf_counter()
+            info = aires.plan_info(plan)
+            C = aires.spgemm(plan)
+            torch.cuda.synchronize()
+            t3 = time.perf_counter()
+            st = aires.plan_stats(plan)
+            ts = aires.plan_tile_stats(plan)
+            peak = plan.allocator.peak
+            C.free()
+            del C
+        wall = time.perf_counter() - t1
+        print("[bench] cfg5 streamed call %d: %.1f ms" % (it, 1e3 * wall), file=sys.stderr, flush=True)
+        if it >= 1:
+            runs.append((wall, 1e3 * (t2 - t1), 1e3 * (t3 - t2), st, ts, peak))
+    runs.sort(key=lambda x: x[0])
+    wall, plan_ms, call_ms, st, ts, peak = runs[len(runs) // 2]
+    compute = sum(st[k] for k in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms"))
+    out["cfg5_streamed"] = {
+        "workload": "cfg5 out-of-core aggregation: symmetric R-MAT n=68000000 deg 22 + self-loops (int64 row_ptr), "
+                    "X 68000000x64 10% U(-1,1); A and X in pinned host memory, C to pinned host memory",
+        "budget_gb": 32, "tiles": info.ntiles, "products": st["products"], "nnz_c": st["nnz_c"],
+        "end_to_end_ms": round(1e3 * wall, 2), "plan_ms": round(plan_ms, 2), "call_ms": round(call_ms, 2),
+        "pipeline_ms": round(st["pipeline_ms"], 2), "h2d_ms": round(st["h2d_ms"], 2),
+        "compute_ms": round(compute, 2), "d2h_ms": round(st["d2h_ms"], 2),
+        "parts_in_sequence_ms": round(st["h2d_ms"] + compute + st["d2h_ms"], 2),
+        "h2d_gb": round(st["h2d_bytes"] / 1e9, 3), "d2h_gb": round(st["d2h_bytes"] / 1e9, 3),
+        "h2d_gbs": round(st["h2d_bytes"] / max(st["h2d_ms"], 1e-9) / 1e6, 2),
+        "d2h_gbs": round(st["d2h_bytes"] / max(st["d2h_ms"], 1e-9) / 1e6, 2),
+        "h2d_overlapped_by_compute": overlap_fraction(ts, "h2d", "compute"),
+        "compute_overlapped_by_copies": overlap_fraction(ts, "compute", "h2d"),
+        "gflops_end_to_end": round(2 * st["products"] / wall / 1e9, 3),
+        "device_peak_gb_measured": round(peak / 1e9, 3),
+        "calls": 3, "warmup": 1, "generation_s": round(gen, 2)}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -429,6 +590,8 @@ def main():
                          "min(N, nnz(A_i) max_k nnz(B_k)) (row pointers only)")
     ap.add_argument("--sym-norm", action="store_true",
                     help="--stream: A's values derived on the device from its pattern (Eq. 2) instead of copied")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the extra records of the default run (cfg2 in core, cfg5 streamed)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run one device copy of this many MiB (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -462,52 +625,13 @@ def main():
     if args.dense_h:
         return dense_aggregate(args, A, dA, gen_s)
     torch.cuda.synchronize()
-    P = row_products(A, B)
-    total_products = int(P.sum())
-
-    def step(timing):
-        with aires.tile_plan(dA, dB, 0, timing=timing) as plan:
-            C = aires.spgemm(plan)
-            torch.cuda.synchronize()
-            st = aires.plan_stats(plan) if timing else None
-        return C, st
-
-    for _ in range(args.warmup):
-        C, _ = step(True)
-        del C
-    torch.cuda.synchronize()
-    stats = []
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        C, st = step(True)
-        stats.append(st)
-        last_rp = C.rp  # only the row pointers outlive the step, as for a caller that consumes C
-        del C
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    ms_per_step = 1e3 * elapsed / args.steps
-    assert all(s["products"] == total_products for s in stats)
-    nnz_c = stats[-1]["nnz_c"]
-
-    # dominant kernel: numeric launch of the kind with the largest time
-    num_ms = {k: np.mean([s["kind_ms"]["numeric"][k] for s in stats]) for k in KIND_NAMES}
-    dom = max(num_ms, key=num_ms.get)
-    kinds = row_kinds(P, B.ncols)
-    sel = kinds == KIND_NAMES.index(dom)
-    crow = np.diff(last_rp.cpu().numpy())
-    alen = np.diff(A.rp.astype(np.int64))
-    sA = A.rp.dtype.itemsize
-    dom_bytes = int((sA + 8 * alen[sel] + 8 + 8 * crow[sel]).sum()) + B.nbytes()
-    dom_gbs = dom_bytes / (num_ms[dom] * 1e-3) / 1e9
-    # gather model (no reuse): B.row_ptr per A entry and 8 bytes of B per product
-    sB = B.rp.dtype.itemsize
-    dom_gather = int((sA + 8 * alen[sel] + 2 * sB * alen[sel] + 8 * P[sel] + 8 + 8 * crow[sel]).sum())
-    dom_gather_gbs = dom_gather / (num_ms[dom] * 1e-3) / 1e9
-    del last_rp
-
-    phase = {k: round(float(np.mean([s[k] for s in stats])), 4)
-             for k in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "total_ms")}
-    compulsory = A.nbytes() + B.nbytes() + 8 * (A.nrows + 1) + 8 * nnz_c
+    run = in_core_run(A, B, dA, dB, args.steps, args.warmup)
+    ms_per_step = run["ms_per_step"]
+    P = run["P"]
+    total_products = run["products"]
+    roof = run["roofline"]
+    roof["traffic"] = measured_traffic("cfg%d/numeric/%s" % (args.workload, run["dominant"]),
+                                       roof["algorithmic_bytes"])
     res = {
         "metric": METRIC,
         "value": round(2 * total_products / (ms_per_step * 1e-3) / 1e9, 3),
@@ -523,17 +647,14 @@ def main():
         "data": "synthetic (seeded R-MAT graph and uniform sparse features, generated on the host)",
         "config": {"workload": "cfg%d %s" % (args.workload, WORKLOAD_NAMES[args.workload]),
                    "m": A.nrows, "n": B.ncols, "nnz_a": A.nnz, "nnz_b": B.nnz,
-                   "products": total_products, "nnz_c": nnz_c, "tiles": stats[-1]["ntiles"],
+                   "products": total_products, "nnz_c": run["nnz_c"], "tiles": run["tiles"],
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "numeric/%s" % dom, "achieved": round(dom_gbs, 2),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("cfg%d/numeric/%s" % (args.workload, dom), dom_bytes),
-                     "algorithmic_bytes": dom_bytes, "avg_launch_ms": round(num_ms[dom], 4),
-                     "gather_model_gbs": round(dom_gather_gbs, 2)},
-        "phases_ms": phase,
-        "numeric_gflops": round(2 * total_products / (phase["numeric_ms"] * 1e-3) / 1e9, 2),
-        "end_to_end_compulsory_gbs": round(compulsory / (ms_per_step * 1e-3) / 1e9, 2),
-        "numeric_kind_ms": {k: round(float(v), 4) for k, v in num_ms.items() if v > 0},
+        "roofline": {k: roof[k] for k in ("bound", "kernel", "achieved", "peak", "unit", "frac", "traffic",
+                                          "algorithmic_bytes", "avg_launch_ms", "gather_model_gbs")},
+        "phases_ms": run["phases_ms"],
+        "numeric_gflops": run["numeric_gflops"],
+        "end_to_end_compulsory_gbs": run["end_to_end_compulsory_gbs"],
+        "numeric_kind_ms": run["numeric_kind_ms"],
         "generation_s": round(gen_s, 2),
     }
     if not args.no_cpu:
@@ -543,6 +664,11 @@ def main():
         allc = cpu_baseline(A, B, P, args.cpu_seconds / 2, threads=max(1, min(ncpu, 16)))
         allc["cpu_model"] = model
         res["cpu_baseline_all_cores"] = allc
+    if args.workload == 3 and not args.no_extras:
+        del dA, dB, A, B, P
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        res["extra_workloads"] = extras(args)
     print(json.dumps(res), flush=True)
 
 

@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define AIRES_ABI_VERSION 2
+#define AIRES_ABI_VERSION 3
 
 typedef enum aires_status {
     AIRES_OK = 0,
@@ -232,7 +232,7 @@ typedef struct aires_plan_info {
     int64_t c_bound_entries;    /* sum of u_i, or -1 when not computed     */
     int32_t a_streamed;         /* 1: A moves host->device per tile        */
     int32_t c_on_host;          /* 1: C tiles move device->host            */
-} aires_plan_info;
+} aires_plan_info_t;            /* (the struct tag shares the query's name) */
 
 typedef struct aires_tile {
     int64_t r0, r1;             /* rows [r0, r1)                           */
@@ -242,7 +242,16 @@ typedef struct aires_tile {
     int64_t tile_bytes;         /* planned bytes of one slot of this tile  */
 } aires_tile;
 
-aires_status aires_plan_info_get(const aires_plan *plan, aires_plan_info *info);
+/*
+ * aires_plan_info -- the plan's totals: tile count, sizes, the budget M and
+ * its split (M_B of Eq. 6, the slot left for A tiles as in Eq. 7), planned
+ * peak device bytes and the C bound (Sec. III-A).  aires_plan_info_get is
+ * the same call under its earlier name.  Errors: AIRES_E_INVALID_ARG.
+ */
+aires_status aires_plan_info(const aires_plan *plan, aires_plan_info_t *info);
+aires_status aires_plan_info_get(const aires_plan *plan, aires_plan_info_t *info);
+/* Tile t of the plan (0 <= t < ntiles): a row block of Algorithm 1.
+   Errors: AIRES_E_INVALID_ARG (NULL, t out of range). */
 aires_status aires_plan_tile(const aires_plan *plan, int64_t t, aires_tile *tile);
 
 /*
@@ -263,8 +272,17 @@ aires_status aires_plan_tile(const aires_plan *plan, int64_t t, aires_tile *tile
  * valid when `stream` reaches the end of the enqueued work.  Columns of
  * every row of C are strictly increasing; entries whose value sums to zero
  * are kept (the structure is the union of the column sets).
+ *
+ * Memory (the constraint M of Sec. III-A): every block the call takes from
+ * the allocator, C included, counts against the plan's budget together
+ * with the caller's device-resident inputs; an allocation that would pass
+ * it fails the call with AIRES_E_BUDGET (the kept symbolic bitmaps, a
+ * cache, are dropped first).  Every block is requested and released on
+ * `stream` (the allocator's stream argument), so an allocator that pools
+ * per stream never hands a block still in use by this call to other work.
  * Errors: AIRES_E_INVALID_ARG, AIRES_E_STATE (C not zeroed / plan busy),
- * AIRES_E_BUDGET (exact C does not fit), AIRES_E_OOM, AIRES_E_HIP,
+ * AIRES_E_BUDGET (exact C does not fit), AIRES_E_OOM (the allocator
+ * returned NULL; everything taken so far is released), AIRES_E_HIP,
  * AIRES_E_OVERFLOW.
  */
 aires_status aires_spgemm(aires_plan *plan, void *stream, aires_csr_out *C);
@@ -349,6 +367,34 @@ aires_status aires_spmm(const aires_csr *A, const float *W, int64_t ldw, int64_t
 
 /* Statistics of the last aires_spgemm / aires_stream_tiles on the plan. */
 aires_status aires_plan_stats(const aires_plan *plan, aires_stats *stats);
+
+/*
+ * Per-tile statistics of the last call on the plan: what the paper reports
+ * per method (bytes moved between host and GPU and their latency, Sec. V-B)
+ * broken down by row block.  Counts are always filled; times need
+ * opts->timing (else 0, and the instants -1).  Durations are the busy time
+ * of each phase of this tile on its stream.  The instants are milliseconds
+ * from the start of the call on the compute stream: the tile's host-to-
+ * device copy, its compute (analysis through numeric phase) and its copy of
+ * C back (streamed schedule of Algorithm 2; -1 where the tile has none), so
+ * that the overlap of tile t+1's copy with tile t's products can be read
+ * off directly.
+ */
+typedef struct aires_tile_stats {
+    int64_t r0, r1;             /* rows [r0, r1) of the tile               */
+    int64_t products;           /* sum of P_i over the tile                */
+    int64_t nnz_c;              /* entries of C in the tile                */
+    int64_t h2d_bytes;          /* A bytes copied for the tile             */
+    int64_t d2h_bytes;          /* C bytes (row pointers + entries) copied back */
+    double analyze_ms, bin_ms, symbolic_ms, scan_ms, numeric_ms;
+    double h2d_ms, d2h_ms;
+    double h2d_begin_ms, h2d_end_ms;
+    double compute_begin_ms, compute_end_ms;
+    double d2h_begin_ms, d2h_end_ms;
+} aires_tile_stats;
+
+/* Errors: AIRES_E_INVALID_ARG (NULL, t out of range), AIRES_E_HIP. */
+aires_status aires_plan_tile_stats(const aires_plan *plan, int64_t t, aires_tile_stats *stats);
 
 /* Release C's arrays through the allocator that made them; zeroes *C. */
 void aires_csr_out_free(aires_csr_out *C);

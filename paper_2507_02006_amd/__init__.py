@@ -21,7 +21,7 @@ from dataclasses import dataclass
 from . import _binding as B_
 
 __all__ = ["tile_plan", "spgemm", "spmm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
-           "Plan", "Output", "AiresError", "to_device", "to_pinned"]
+           "plan_tile_stats", "Plan", "Output", "AiresError", "to_device", "to_pinned"]
 
 AiresError = B_.AiresError
 
@@ -66,10 +66,13 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
               window_max_grains: int = 0, window_max_entries: int = 0, count_grains: int = 0,
               keep_bitmap_products: int = 0, split_min_products: int = 0, split_max_rows: int = 0,
               window_pool_bytes: int = 0, a_values: str = "given", torch_allocator: bool = True,
-              device: int = 0) -> Plan:
+              allocator=None, device: int = 0) -> Plan:
     """Plan C = A * B under a device budget (aires_tile_plan).  a_values:
     "given" (A's values) or "sym_norm" (a_ik = 1/sqrt(r_i r_k) of A's
-    pattern, Eq. 2, derived on the device; A's vals may then be None)."""
+    pattern, Eq. 2, derived on the device; A's vals may then be None).
+    ``allocator``: an object with a ctypes ``struct`` (``_binding.Allocator``)
+    such as a ``_binding.TorchAllocator``; by default a TorchAllocator
+    (``torch_allocator``) or the library's own hipMallocAsync."""
     lib = B_.load()
     a = B_.make_csr(*_parts(A))
     b = B_.make_csr(*_parts(B))
@@ -96,9 +99,10 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
     if a_values not in ("given", "sym_norm"):
         raise ValueError("a_values must be 'given' or 'sym_norm'")
     o.a_values = B_.AVALUES_SYM_NORM if a_values == "sym_norm" else B_.AVALUES_GIVEN
-    alloc = None
-    if torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
+    alloc = allocator
+    if alloc is None and torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
         alloc = B_.TorchAllocator(device)
+    if alloc is not None:
         o.allocator = ctypes.pointer(alloc.struct)
     h = ctypes.c_void_p()
     B_.check(lib.aires_tile_plan(ctypes.byref(a), ctypes.byref(b), int(hbm_budget), ctypes.byref(o),
@@ -124,7 +128,7 @@ class Info:
 
 def plan_info(plan: Plan) -> Info:
     i = B_.PlanInfo()
-    B_.check(B_.load().aires_plan_info_get(plan.handle, ctypes.byref(i)), "aires_plan_info_get")
+    B_.check(B_.load().aires_plan_info(plan.handle, ctypes.byref(i)), "aires_plan_info")
     return Info(*(getattr(i, f) for f, _ in B_.PlanInfo._fields_))
 
 
@@ -145,6 +149,16 @@ def plan_stats(plan: Plan) -> dict:
     d["kind_ms"] = {ph: {B_.KIND_NAMES[k]: s.kind_ms[p][k] for k in range(len(B_.KIND_NAMES))}
                     for p, ph in enumerate(("symbolic", "numeric"))}
     return d
+
+
+def plan_tile_stats(plan: Plan, t: int | None = None):
+    """Per-tile counts, phase times and begin/end instants of the last call
+    (aires_plan_tile_stats): one dict, or a list over all tiles."""
+    if t is None:
+        return [plan_tile_stats(plan, i) for i in range(plan_info(plan).ntiles)]
+    x = B_.TileStats()
+    B_.check(B_.load().aires_plan_tile_stats(plan.handle, int(t), ctypes.byref(x)), "aires_plan_tile_stats")
+    return {f: getattr(x, f) for f, _ in B_.TileStats._fields_}
 
 
 class Output:

@@ -76,6 +76,13 @@ class Stats(ctypes.Structure):
                [("numeric_launches", c_i64), ("kind_ms", (c_dbl * 8) * 2), ("pipeline_ms", c_dbl)]
 
 
+class TileStats(ctypes.Structure):
+    _fields_ = [(n, c_i64) for n in ("r0", "r1", "products", "nnz_c", "h2d_bytes", "d2h_bytes")] + \
+               [(n, c_dbl) for n in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "h2d_ms",
+                                     "d2h_ms", "h2d_begin_ms", "h2d_end_ms", "compute_begin_ms",
+                                     "compute_end_ms", "d2h_begin_ms", "d2h_end_ms")]
+
+
 _lib = None
 
 
@@ -100,7 +107,9 @@ def load() -> ctypes.CDLL:
         "aires_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "aires_plan_opts_default": (ctypes.c_int, [P(PlanOpts)]),
         "aires_tile_plan": (ctypes.c_int, [P(Csr), P(Csr), c_u64, P(PlanOpts), P(c_vp)]),
+        "aires_plan_info": (ctypes.c_int, [c_vp, P(PlanInfo)]),
         "aires_plan_info_get": (ctypes.c_int, [c_vp, P(PlanInfo)]),
+        "aires_plan_tile_stats": (ctypes.c_int, [c_vp, c_i64, P(TileStats)]),
         "aires_plan_tile": (ctypes.c_int, [c_vp, c_i64, P(Tile)]),
         "aires_spgemm": (ctypes.c_int, [c_vp, c_vp, P(CsrOut)]),
         "aires_stream_tiles": (ctypes.c_int, [c_vp, c_vp, c_vp, c_vp, P(CsrOut)]),
@@ -182,7 +191,13 @@ def make_csr(nrows: int, ncols: int, rp, col, val) -> Csr:
 class TorchAllocator:
     """Device memory for the library from torch's caching allocator.  Blocks
     are uint8 tensors kept alive in a registry until the library frees them
-    (or Python takes them over as output views)."""
+    (or Python takes them over as output views).
+
+    Each block is allocated with the library's stream (the callback's
+    `stream` argument) as torch's current stream.  torch's cache keeps a
+    freed block for later allocations on that same stream only, so when the
+    library frees a block while its kernels on that stream may still read
+    it, the block cannot be handed to work on any other stream."""
 
     def __init__(self, device: int = 0):
         import torch
@@ -194,10 +209,29 @@ class TorchAllocator:
         self.struct = Allocator(self._alloc, self._free, None)
         self.peak = 0
         self.cur = 0
+        self.calls = 0
+        self._streams: dict[int, object] = {}
+
+    def _stream_of(self, handle):
+        """The torch stream object for a hipStream_t handle."""
+        torch = self.torch
+        h = int(handle or 0)
+        cur = torch.cuda.current_stream(self.device)
+        if cur.cuda_stream == h:
+            return cur
+        if h == 0:
+            return torch.cuda.default_stream(self.device)
+        s = self._streams.get(h)
+        if s is None:
+            s = torch.cuda.ExternalStream(h, device=self.device)
+            self._streams[h] = s
+        return s
 
     def _alloc_cb(self, ctx, nbytes, stream):
+        self.calls += 1
         try:
-            t = self.torch.empty(int(nbytes), dtype=self.torch.uint8, device="cuda:%d" % self.device)
+            with self.torch.cuda.stream(self._stream_of(stream)):
+                t = self.torch.empty(int(nbytes), dtype=self.torch.uint8, device="cuda:%d" % self.device)
         except Exception:  # noqa: BLE001 -- out of memory is reported as NULL
             return None
         p = t.data_ptr()

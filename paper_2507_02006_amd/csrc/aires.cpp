@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -104,17 +105,43 @@ void default_free(void*, void* p, void* stream) {
 
 const aires_allocator kDefaultAllocator = {default_alloc, default_free, nullptr};
 
-// Device allocations of one call, released together (stream-ordered).
+// Device allocations of one call, released together (stream-ordered).  The
+// pool enforces the plan's device budget (Sec. III-A: the memory constraint
+// M): `cap` is what the budget leaves after the borrowed device inputs, and
+// `used` counts every byte the call has taken, including blocks handed to
+// the caller as C, so a call never holds more than the budget.
 struct DevPool {
   aires_allocator a;
   hipStream_t s;
-  std::vector<void*> live;
-  DevPool(const aires_allocator& al, hipStream_t st) : a(al), s(st) {}
+  int64_t cap;      // < 0: no limit
+  int64_t used = 0;
+  struct Block { void* p; int64_t n; };
+  std::vector<Block> live;
+  // Arena mode (the allocation-free entry point): blocks are carved, 256-byte
+  // aligned, from [arena, arena + cap) and nothing is allocated or freed.
+  char* arena = nullptr;
+  DevPool(const aires_allocator& al, hipStream_t st, int64_t cap_bytes = -1) : a(al), s(st), cap(cap_bytes) {}
+  DevPool(void* base, int64_t bytes, hipStream_t st) : a{}, s(st), cap(bytes), arena(static_cast<char*>(base)) {}
   ~DevPool() { release(); }
+  static int64_t round256(int64_t n) { return (n + 255) & ~int64_t(255); }
+  bool fits(int64_t bytes) const { return cap < 0 || used + (arena ? round256(bytes) : bytes) <= cap; }
   aires_status get(size_t bytes, void** out) {
-    void* p = a.alloc(a.ctx, bytes ? bytes : 256, (void*)s);
+    const int64_t n = (int64_t)(bytes ? bytes : 256);
+    if (arena) {
+      if (!fits(n))
+        return fail(AIRES_E_CAPACITY, "the workspace needs more than the %lld-byte fixed scratch array",
+                    (long long)cap);
+      *out = arena + used;
+      used += round256(n);
+      return AIRES_OK;
+    }
+    if (!fits(n))
+      return fail(AIRES_E_BUDGET, "device allocation of %lld bytes exceeds the budget (%lld of %lld bytes in use)",
+                  (long long)n, (long long)used, (long long)cap);
+    void* p = a.alloc(a.ctx, (size_t)n, (void*)s);
     if (!p) return fail(AIRES_E_OOM, "device allocation of %zu bytes failed", bytes);
-    live.push_back(p);
+    live.push_back({p, n});
+    used += n;
     *out = p;
     return AIRES_OK;
   }
@@ -123,11 +150,26 @@ struct DevPool {
     return get((size_t)std::max<int64_t>(n, 1) * sizeof(T), reinterpret_cast<void**>(out));
   }
   void release() {
-    for (void* p : live) a.free(a.ctx, p, (void*)s);
+    for (const Block& b : live) a.free(a.ctx, b.p, (void*)s);
     live.clear();
   }
-  // hand ownership of p to the caller
-  void detach(void* p) { live.erase(std::remove(live.begin(), live.end(), p), live.end()); }
+  int64_t left() const { return cap < 0 ? INT64_MAX : cap - used; }
+  // hand ownership of p to the caller (it still counts against the budget
+  // for the rest of the call)
+  void detach(void* p) {
+    live.erase(std::remove_if(live.begin(), live.end(), [p](const Block& b) { return b.p == p; }), live.end());
+  }
+  // free p now (stream-ordered) and stop counting it
+  void give_back(void* p) {
+    if (arena) return;  // carved blocks stay until the call ends
+    for (size_t i = 0; i < live.size(); ++i)
+      if (live[i].p == p) {
+        a.free(a.ctx, p, (void*)s);
+        used -= live[i].n;
+        live.erase(live.begin() + (long)i);
+        return;
+      }
+  }
 };
 
 struct OutOwner {
@@ -146,7 +188,7 @@ struct aires_plan {
   aires_allocator alloc;
   int64_t budget;
   std::vector<aires_tile> tiles;
-  aires_plan_info info;
+  aires_plan_info_t info;
   aires_stats stats;
   int busy = 0;
   // kernel configuration
@@ -159,10 +201,17 @@ struct aires_plan {
   int split = 0;                   // narrow product with a split-row bin
   int64_t split_cap = 0;           // rows with dense slots for the split bin
   int64_t split_ws = 0;            // bytes of those slots
-  // host copies needed for streaming
+  // per-tile counts of the last call (products, nnz(C), bytes copied)
+  struct TileRun { int64_t products, nnz_c, h2d_bytes, d2h_bytes; };
+  std::vector<TileRun> trun;
+  // per tile, indices into ev of: copy in begin/end, compute begin/end,
+  // copy out begin/end (-1: none); times are taken from ev[ev_base]
+  enum { T_H2D0, T_H2D1, T_C0, T_C1, T_D2H0, T_D2H1, T_NEV };
+  std::vector<std::array<int, T_NEV>> tev;
+  int ev_base = -1;
   // timing events of the last call
   std::vector<hipEvent_t> ev;
-  struct Mark { int kind; int phase; int a, b; };  // elapsed(ev[a], ev[b])
+  struct Mark { int kind; int phase; int a, b; int tile; };  // elapsed(ev[a], ev[b]); tile -1: whole call
   std::vector<Mark> marks;
   ~aires_plan() {
     for (hipEvent_t e : ev) (void)hipEventDestroy(e);
@@ -778,11 +827,13 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   return AIRES_OK;
 }
 
-aires_status aires_plan_info_get(const aires_plan* plan, aires_plan_info* info) {
+aires_status aires_plan_info(const aires_plan* plan, aires_plan_info_t* info) {
   if (!plan || !info) return fail(AIRES_E_INVALID_ARG, "NULL argument");
   *info = plan->info;
   return AIRES_OK;
 }
+
+aires_status aires_plan_info_get(const aires_plan* plan, aires_plan_info_t* info) { return aires_plan_info(plan, info); }
 
 aires_status aires_plan_tile(const aires_plan* plan, int64_t t, aires_tile* tile) {
   if (!plan || !tile) return fail(AIRES_E_INVALID_ARG, "NULL argument");
@@ -803,6 +854,7 @@ struct Timer {
   aires_plan* p;
   hipStream_t s;
   bool on;
+  int tile = -1;  // tile the next marks belong to
   int record() {
     if (!on) return -1;
     hipEvent_t e;
@@ -811,8 +863,16 @@ struct Timer {
     p->ev.push_back(e);
     return (int)p->ev.size() - 1;
   }
+  // event e as moment `which` of the current tile (first setting wins for
+  // a beginning, last for an end)
+  void at(int which, int e) {
+    if (!on || e < 0 || tile < 0 || (size_t)tile >= p->tev.size()) return;
+    int& slot = p->tev[(size_t)tile][(size_t)which];
+    const bool begin = which == aires_plan::T_H2D0 || which == aires_plan::T_C0 || which == aires_plan::T_D2H0;
+    if (!begin || slot < 0) slot = e;
+  }
   void mark(int kind, int phase, int a, int b) {
-    if (on && a >= 0 && b >= 0) p->marks.push_back({kind, phase, a, b});
+    if (on && a >= 0 && b >= 0) p->marks.push_back({kind, phase, a, b, tile});
   }
 };
 
@@ -886,9 +946,17 @@ aires_status alloc_split_ws(aires_plan* p, DevPool& ws, kern::SplitWs& sw) {
   sw = kern::SplitWs{nullptr, nullptr, 0};
   if (!p->split) return AIRES_OK;
   const int64_t N = p->B.ncols;
-  ST_TRY(ws.get_n(p->split_cap * ((N + 31) / 32), &sw.bm));
-  ST_TRY(ws.get_n(p->split_cap * N, &sw.acc));
-  sw.cap = p->split_cap;
+  int64_t cap = p->split_cap;
+  if (ws.arena) {
+    // a fixed workspace gives slots to as many split rows as fit in what is
+    // left of it; the other rows of the bin take a workgroup each
+    const int64_t per = 4 * ((N + 31) / 32) + 4 * N;
+    cap = std::min(cap, (ws.left() - 1024) / per);
+    if (cap < 1) return fail(AIRES_E_CAPACITY, "no room for a split-row slot in the fixed scratch array");
+  }
+  ST_TRY(ws.get_n(cap * ((N + 31) / 32), &sw.bm));
+  ST_TRY(ws.get_n(cap * N, &sw.acc));
+  sw.cap = cap;
   return AIRES_OK;
 }
 
@@ -917,6 +985,7 @@ kern::WindowParams window_params(const aires_plan* p, const TileWs& w) {
 aires_status tile_symbolic(aires_plan* p, const kern::Operands& op, int64_t n, TileWs& w, int64_t* crp,
                            unsigned long long* prod_total, hipStream_t s, Timer& tm) {
   const int e0 = tm.record();
+  tm.at(aires_plan::T_C0, e0);
   HIP_TRY(hipMemsetAsync(w.cntcur, 0, sizeof(int32_t) * (2 * kern::MAX_BINS + 1), s));
   HIP_TRY(kern::analyze(op, n, w.P, prod_total, w.cntcur + 2 * kern::MAX_BINS, w.list, s));
   const int e1 = tm.record();
@@ -978,8 +1047,22 @@ aires_status tile_numeric(aires_plan* p, const kern::Operands& op, int64_t n, co
     tm.mark(kind, 1, ka, tm.record());
     p->stats.numeric_launches++;
   }
-  tm.mark(PH_NUMERIC, 1, e0, tm.record());
+  const int e1 = tm.record();
+  tm.mark(PH_NUMERIC, 1, e0, e1);
+  tm.at(aires_plan::T_C1, e1);
   return AIRES_OK;
+}
+
+// Device bytes of the caller's inputs that the call reads in place; the
+// budget covers them, so the library's own allocations get the rest.
+int64_t borrowed_device_bytes(const aires_plan* p) {
+  int64_t b = 0;
+  if (p->A.mem == AIRES_MEM_DEVICE) {
+    b += (p->A.nrows + 1) * rp_bytes(p->A) + 4 * p->A.nnz;
+    if (p->opts.a_values != AIRES_AVALUES_SYM_NORM) b += 4 * p->A.nnz;
+  }
+  if (p->B.mem == AIRES_MEM_DEVICE) b += csr_bytes(p->B);
+  return b;
 }
 
 aires_status begin_call(aires_plan* p, aires_csr_out* C) {
@@ -989,16 +1072,33 @@ aires_status begin_call(aires_plan* p, aires_csr_out* C) {
     return fail(AIRES_E_STATE, "output descriptor is not zeroed (free it first)");
   std::memset(&p->stats, 0, sizeof p->stats);
   p->stats.ntiles = (int64_t)p->tiles.size();
+  p->trun.assign(p->tiles.size(), aires_plan::TileRun{0, 0, 0, 0});
   reset_timing(p);
+  std::array<int, aires_plan::T_NEV> none;
+  none.fill(-1);
+  p->tev.assign(p->tiles.size(), none);
+  p->ev_base = -1;
   return AIRES_OK;
 }
 
-aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
+// C arrays the caller owns (the allocation-free entry point).
+struct CallerC {
+  int64_t* row_ptr;
+  int32_t* col;
+  float* val;
+  int64_t capacity;
+  int64_t* nnz_out;
+};
+
+// In-core call (device-resident A and B).  Workspace comes from `ws`: the
+// plan's allocator under its budget, or a fixed arena.  C is allocated and
+// handed to *C, or written into the caller's arrays (cc != nullptr).
+aires_status spgemm_device_in(aires_plan* p, hipStream_t s, DevPool& ws, aires_csr_out* C, const CallerC* cc) {
   const int64_t m = p->A.nrows, K = p->B.nrows, N = p->B.ncols;
   const int64_t sA = rp_bytes(p->A);
   Timer tm{p, s, p->opts.timing != 0};
   const int e_total0 = tm.record();
-  DevPool ws(p->alloc, s);
+  p->ev_base = e_total0;
   int64_t max_rows = 1;
   for (const auto& t : p->tiles) max_rows = std::max(max_rows, t.r1 - t.r0);
   const int64_t nt = (int64_t)p->tiles.size();
@@ -1007,16 +1107,16 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   // lists, bin offsets and window bookkeeping persist from the symbolic
   // sweep to the numeric sweep (tile regions of whole-matrix arrays).
   int64_t* crp = nullptr;
-  ST_TRY(ws.get_n(m + 1, &crp));
+  if (cc) crp = cc->row_ptr;
+  else ST_TRY(ws.get_n(m + 1, &crp));
   TileWs shared;
   ST_TRY(alloc_tile_ws(p, ws, max_rows, false, shared));
-  ST_TRY(alloc_split_ws(p, ws, shared.split));
   int32_t *list = nullptr, *binoff = nullptr, *gcnt = nullptr, *bidx = nullptr;
   int64_t* icount = nullptr;
   unsigned long long* prod = nullptr;
   ST_TRY(ws.get_n(m, &list));
   ST_TRY(ws.get_n(nt * (kern::MAX_BINS + 1), &binoff));
-  ST_TRY(ws.get_n(1, &prod));
+  ST_TRY(ws.get_n(nt, &prod));  // intermediate products of each tile
   // A's values: given, or derived from its pattern (Eq. 2) into the workspace
   const float* avals = p->A.vals;
   if (p->opts.a_values == AIRES_AVALUES_SYM_NORM && p->A.nnz > 0) {
@@ -1034,7 +1134,7 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
     ST_TRY(ws.get_n(m * (int64_t)p->nG, &gcnt));
     ST_TRY(ws.get_n(m + nt, &icount));
     ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
-    if (p->keep_bitmap >= 0) {
+    if (p->keep_bitmap >= 0 && !ws.arena) {
       ST_TRY(ws.get_n(m * (int64_t)p->ngg, &bm_off));
       ST_TRY(ws.get_n(1, &bm_top));
       // The kept bitmaps are a cache: they take up to a fifth of the budget
@@ -1050,6 +1150,7 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
       }
     }
   }
+  ST_TRY(alloc_split_ws(p, ws, shared.split));
   auto tile_ws = [&](int64_t t) {
     const aires_tile& T = p->tiles[(size_t)t];
     TileWs w = shared;
@@ -1068,7 +1169,7 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
     return w;
   };
   HIP_TRY(hipMemsetAsync(crp, 0, sizeof(int64_t), s));
-  HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long), s));
+  HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long) * (size_t)std::max<int64_t>(nt, 1), s));
   if (bm_cache) HIP_TRY(hipMemsetAsync(bm_top, 0, sizeof(unsigned long long), s));
   if (p->wide) {
     const int ea = tm.record();
@@ -1084,46 +1185,67 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
     const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
     kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, avals, p->B.row_ptr, p->B.col_idx,
                                       p->B.vals, bidx);
-    ST_TRY(tile_symbolic(p, op, T.r1 - T.r0, w, crp + T.r0, prod, s, tm));
+    tm.tile = (int)t;
+    ST_TRY(tile_symbolic(p, op, T.r1 - T.r0, w, crp + T.r0, prod + t, s, tm));
   }
+  tm.tile = -1;
   // The one host synchronisation: nnz(C) (and the window count of every
-  // tile) decide the allocations.
-  std::vector<int64_t> hostbuf(3 + (size_t)nt);
+  // tile) decide the allocations.  Host buffer: [0, nt) products per tile,
+  // [nt, 2nt) C.row_ptr at each tile's end, [2nt, 3nt) windows per tile.
+  std::vector<int64_t> hostbuf(3 * (size_t)std::max<int64_t>(nt, 1));
   int64_t* hb = hostbuf.data();
-  HIP_TRY(hipMemcpyAsync(hb, crp + m, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipMemcpyAsync(hb + 1, prod, sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
-  if (p->wide)
-    for (int64_t t = 0; t < nt; ++t) {
-      const aires_tile& T = p->tiles[(size_t)t];
-      HIP_TRY(hipMemcpyAsync(hb + 2 + t, icount + T.r0 + t + (T.r1 - T.r0), sizeof(int64_t), hipMemcpyDeviceToHost, s));
-    }
+  int64_t* hb_end = hb + nt;
+  int64_t* hb_win = hb + 2 * nt;
+  if (nt > 0) HIP_TRY(hipMemcpyAsync(hb, prod, sizeof(int64_t) * (size_t)nt, hipMemcpyDeviceToHost, s));
+  for (int64_t t = 0; t < nt; ++t) {
+    const aires_tile& T = p->tiles[(size_t)t];
+    HIP_TRY(hipMemcpyAsync(hb_end + t, crp + T.r1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    if (p->wide)
+      HIP_TRY(hipMemcpyAsync(hb_win + t, icount + T.r0 + t + (T.r1 - T.r0), sizeof(int64_t), hipMemcpyDeviceToHost,
+                             s));
+  }
   HIP_TRY(hipStreamSynchronize(s));
-  const int64_t nnz = hb[0];
+  const int64_t nnz = nt > 0 ? hb_end[nt - 1] : 0;
+  if (cc && cc->nnz_out) *cc->nnz_out = nnz;
   p->stats.host_syncs = 1;
-  p->stats.products = hb[1];
   p->stats.nnz_c = nnz;
-  const int64_t resident = p->info.b_bytes + p->info.a_bytes + 8 * (m + 1);
-  if (resident + 8 * nnz > p->budget)
-    return fail(AIRES_E_BUDGET, "C needs %lld bytes; budget %lld leaves %lld", (long long)(8 * nnz),
-                (long long)p->budget, (long long)(p->budget - resident));
-  if (bm_cache && p->info.peak_bytes + 4 * bm_cap + 8 * nnz > p->budget) {
-    // C and the kept bitmaps do not fit together: drop the bitmaps (the
-    // numeric phase then marks every window from the products)
-    ws.a.free(ws.a.ctx, bm_cache, (void*)s);
-    ws.detach(bm_cache);
+  for (int64_t t = 0; t < nt; ++t) {
+    p->stats.products += hb[t];
+    p->trun[(size_t)t].products = hb[t];
+    p->trun[(size_t)t].nnz_c = hb_end[t] - (t > 0 ? hb_end[t - 1] : 0);
+  }
+  kern::WinItem* items = nullptr;
+  std::vector<int64_t> item_base((size_t)nt + 1, 0);
+  if (p->wide)
+    for (int64_t t = 0; t < nt; ++t) item_base[(size_t)t + 1] = item_base[(size_t)t] + hb_win[t];
+  // C and the window list next to everything the call holds must fit the
+  // budget; the kept bitmaps are a cache and go first if they do not
+  const int64_t need = 8 * std::max<int64_t>(nnz, 1) + (int64_t)sizeof(kern::WinItem) *
+                                                          (p->wide ? std::max<int64_t>(item_base[(size_t)nt], 1) : 0);
+  if (bm_cache && !ws.fits(need)) {
+    // the numeric phase then marks every window from the products
+    ws.give_back(bm_cache);
     bm_cache = nullptr;
     bm_cap = 0;
   }
   int32_t* ccol = nullptr;
   float* cval = nullptr;
-  ST_TRY(ws.get_n(nnz, &ccol));
-  ST_TRY(ws.get_n(nnz, &cval));
-  kern::WinItem* items = nullptr;
-  std::vector<int64_t> item_base((size_t)nt + 1, 0);
-  if (p->wide) {
-    for (int64_t t = 0; t < nt; ++t) item_base[(size_t)t + 1] = item_base[(size_t)t] + hb[2 + t];
-    ST_TRY(ws.get_n(item_base[(size_t)nt], &items));
+  if (cc) {
+    if (nnz > cc->capacity)
+      return fail(AIRES_E_CAPACITY, "C has %lld entries; the caller's arrays hold %lld (C.row_ptr is written)",
+                  (long long)nnz, (long long)cc->capacity);
+    ccol = cc->col;
+    cval = cc->val;
+  } else {
+    if (!ws.fits(need))
+      return fail(AIRES_E_BUDGET,
+                  "C needs %lld bytes (and its window list %lld); the budget of %lld bytes leaves %lld",
+                  (long long)(8 * nnz), (long long)(need - 8 * nnz), (long long)p->budget,
+                  (long long)(ws.cap - ws.used));
+    ST_TRY(ws.get_n(nnz, &ccol));
+    ST_TRY(ws.get_n(nnz, &cval));
   }
+  if (p->wide) ST_TRY(ws.get_n(item_base[(size_t)nt], &items));
 
   // Sweep 2: numeric phase of every tile.
   for (int64_t t = 0; t < nt; ++t) {
@@ -1131,14 +1253,17 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
     TileWs w = tile_ws(t);
     if (p->wide) {
       w.items = items + item_base[(size_t)t];
-      w.nitems = hb[2 + t];
+      w.nitems = hb_win[t];
     }
     const void* arp = static_cast<const char*>(p->A.row_ptr) + T.r0 * sA;
     kern::Operands op = tile_operands(p, arp, 0, p->A.col_idx, avals, p->B.row_ptr, p->B.col_idx,
                                       p->B.vals, bidx);
+    tm.tile = (int)t;
     ST_TRY(tile_numeric(p, op, T.r1 - T.r0, w, crp + T.r0, ccol, cval, 0, s, tm));
   }
+  tm.tile = -1;
   tm.mark(PH_TOTAL, 0, e_total0, tm.record());
+  if (cc) return AIRES_OK;
 
   // hand C to the caller
   ws.detach(crp);
@@ -1156,6 +1281,11 @@ aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
   return AIRES_OK;  // ws releases the workspace stream-ordered on s
 }
 
+aires_status spgemm_device(aires_plan* p, hipStream_t s, aires_csr_out* C) {
+  DevPool ws(p->alloc, s, p->budget - borrowed_device_bytes(p));
+  return spgemm_device_in(p, s, ws, C, nullptr);
+}
+
 // Out-of-core schedule (Algorithm 2): B resident (Phase I), A tiles
 // double-buffered host->device (Phase II), C tiles device->host (Phase III).
 aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStream_t sd, aires_csr_out* C) {
@@ -1169,7 +1299,8 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   if (p->info.c_bound_entries < 0) return fail(AIRES_E_STATE, "plan has no C bound (Algorithm 1 planning mode)");
   Timer tm{p, sc, p->opts.timing != 0};
   const int e_total0 = tm.record();
-  DevPool ws(p->alloc, sc);
+  p->ev_base = e_total0;
+  DevPool ws(p->alloc, sc, p->budget - borrowed_device_bytes(p));
   const int64_t nt = (int64_t)p->tiles.size();
   int64_t max_rows = 1, max_q = 1, max_cb = 1;
   for (const auto& t : p->tiles) {
@@ -1227,7 +1358,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   int32_t* bidx = nullptr;
   unsigned long long* prod = nullptr;
   int64_t* running = nullptr;
-  ST_TRY(ws.get_n(1, &prod));
+  ST_TRY(ws.get_n(nt, &prod));  // intermediate products of each tile
   ST_TRY(ws.get_n(1, &running));
   if (p->wide) ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
   kern::SplitWs split{nullptr, nullptr, 0};
@@ -1247,10 +1378,10 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
       S.ccap = max_cb;
     }
   }
-  int64_t* cnt_host = nullptr;  // pinned per-tile (running nnz, windows)
-  HIP_TRY(hipHostMalloc((void**)&cnt_host, sizeof(int64_t) * 2 * (size_t)std::max<int64_t>(nt, 1), hipHostMallocDefault));
+  int64_t* cnt_host = nullptr;  // pinned per-tile (running nnz, windows, products)
+  HIP_TRY(hipHostMalloc((void**)&cnt_host, sizeof(int64_t) * 3 * (size_t)std::max<int64_t>(nt, 1), hipHostMallocDefault));
   hb.v.push_back(cnt_host);
-  HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long), sc));
+  HIP_TRY(hipMemsetAsync(prod, 0, sizeof(unsigned long long) * (size_t)std::max<int64_t>(nt, 1), sc));
   HIP_TRY(hipMemsetAsync(running, 0, sizeof(int64_t), sc));
 
   std::vector<hipEvent_t> evs;
@@ -1308,7 +1439,9 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     const aires_tile& T = p->tiles[(size_t)t];
     Slot& S = slot[t % 2];
     if (t >= 2) HIP_TRY(hipStreamWaitEvent(sh, ev_done[(size_t)t - 2], 0));
+    th.tile = (int)t;
     const int ea = th.record();
+    th.at(aires_plan::T_H2D0, ea);
     const int64_t k = T.r1 - T.r0, q = T.nnz1 - T.nnz0;
     if (!sym_norm)
       HIP_TRY(hipMemcpyAsync(S.arp, static_cast<const char*>(A.row_ptr) + T.r0 * sA, (size_t)(k + 1) * sA,
@@ -1319,8 +1452,13 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
         HIP_TRY(hipMemcpyAsync(S.aval, A.vals + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
     }
     HIP_TRY(hipEventRecord(ev_in[(size_t)t], sh));
-    th.mark(PH_H2D, 0, ea, th.record());
-    p->stats.h2d_bytes += sym_norm ? 4 * q : (k + 1) * sA + 8 * q;
+    const int eb = th.record();
+    th.mark(PH_H2D, 0, ea, eb);
+    th.at(aires_plan::T_H2D1, eb);
+    th.tile = -1;
+    const int64_t bytes = sym_norm ? 4 * q : (k + 1) * sA + 8 * q;
+    p->stats.h2d_bytes += bytes;
+    p->trun[(size_t)t].h2d_bytes = bytes;
     return AIRES_OK;
   };
 
@@ -1346,39 +1484,44 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     kern::Operands op = tile_operands(p, tile_rp, T.nnz0, S.acol, S.aval, brp, bcol, bval, bidx);
     // running base of C.row_ptr for this tile: crp[0] = total so far
     HIP_TRY(hipMemcpyAsync(S.crp, running, sizeof(int64_t), hipMemcpyDeviceToDevice, sc));
-    ST_TRY(tile_symbolic(p, op, k, S.w, S.crp, prod, sc, tm));
+    tm.tile = (int)t;
+    ST_TRY(tile_symbolic(p, op, k, S.w, S.crp, prod + t, sc, tm));
     HIP_TRY(hipMemcpyAsync(running, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToDevice, sc));
-    HIP_TRY(hipMemcpyAsync(cnt_host + 2 * t, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
+    HIP_TRY(hipMemcpyAsync(cnt_host + 3 * t, S.crp + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
     if (p->wide)
-      HIP_TRY(hipMemcpyAsync(cnt_host + 2 * t + 1, S.w.icount + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
+      HIP_TRY(hipMemcpyAsync(cnt_host + 3 * t + 1, S.w.icount + k, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
+    HIP_TRY(hipMemcpyAsync(cnt_host + 3 * t + 2, prod + t, sizeof(int64_t), hipMemcpyDeviceToHost, sc));
     HIP_TRY(hipEventRecord(ev_cnt[(size_t)t], sc));
     HIP_TRY(hipEventSynchronize(ev_cnt[(size_t)t]));
     p->stats.host_syncs++;
-    const int64_t end = cnt_host[2 * t];
+    const int64_t end = cnt_host[3 * t];
     const int64_t nnz_t = end - base;
+    p->trun[(size_t)t].nnz_c = nnz_t;
+    p->trun[(size_t)t].products = cnt_host[3 * t + 2];
     if (end > cap)
       return fail(AIRES_E_CAPACITY, "C needs more than the planned bound of %lld entries (tile %lld)",
                   (long long)cap, (long long)t);
     if (c_on_host && nnz_t > S.ccap) {
-      // the bound was an estimate (Eq. 5 mode): grow this slot
+      // the bound was an estimate (Eq. 5 mode): grow this slot, within the budget
       HIP_TRY(hipStreamWaitEvent(sc, ev_cfree[t % 2], 0));
-      ws.a.free(ws.a.ctx, S.ccol, (void*)sc);
-      ws.detach(S.ccol);
-      ws.a.free(ws.a.ctx, S.cval, (void*)sc);
-      ws.detach(S.cval);
+      ws.give_back(S.ccol);
+      ws.give_back(S.cval);
+      S.ccol = nullptr;
+      S.cval = nullptr;
       ST_TRY(ws.get_n(nnz_t, &S.ccol));
       ST_TRY(ws.get_n(nnz_t, &S.cval));
       S.ccap = nnz_t;
     }
     if (p->wide) {
-      S.w.nitems = cnt_host[2 * t + 1];
+      S.w.nitems = cnt_host[3 * t + 1];
       if (S.w.nitems > S.icap) {
-        if (S.w.items) {
-          ws.a.free(ws.a.ctx, S.w.items, (void*)sc);
-          ws.detach(S.w.items);
-        }
-        S.icap = std::max<int64_t>(S.w.nitems, 2 * S.icap);
-        ST_TRY(ws.get_n(S.icap, &S.w.items));
+        if (S.w.items) ws.give_back(S.w.items);
+        S.w.items = nullptr;
+        // grow geometrically while the budget allows, else to the exact need
+        const int64_t want = std::max<int64_t>(S.w.nitems, 2 * S.icap);
+        const int64_t grow = ws.fits((int64_t)sizeof(kern::WinItem) * want) ? want : S.w.nitems;
+        ST_TRY(ws.get_n(grow, &S.w.items));
+        S.icap = grow;
       }
     }
     if (c_on_host) {
@@ -1386,19 +1529,26 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     } else {
       ST_TRY(tile_numeric(p, op, k, S.w, S.crp, C_col, C_val, 0, sc, tm));
     }
+    tm.tile = -1;
     HIP_TRY(hipEventRecord(ev_done[(size_t)t], sc));
     // Phase III for this tile
     if (c_on_host) {
       HIP_TRY(hipStreamWaitEvent(sd, ev_done[(size_t)t], 0));
+      td.tile = (int)t;
       const int ea = td.record();
+      td.at(aires_plan::T_D2H0, ea);
       HIP_TRY(hipMemcpyAsync(C_rp + T.r0 + 1, S.crp + 1, sizeof(int64_t) * (size_t)k, hipMemcpyDeviceToHost, sd));
       if (nnz_t > 0) {
         HIP_TRY(hipMemcpyAsync(C_col + base, S.ccol, sizeof(int32_t) * (size_t)nnz_t, hipMemcpyDeviceToHost, sd));
         HIP_TRY(hipMemcpyAsync(C_val + base, S.cval, sizeof(float) * (size_t)nnz_t, hipMemcpyDeviceToHost, sd));
       }
       HIP_TRY(hipEventRecord(ev_cfree[t % 2], sd));
-      td.mark(PH_D2H, 0, ea, td.record());
+      const int eb = td.record();
+      td.mark(PH_D2H, 0, ea, eb);
+      td.at(aires_plan::T_D2H1, eb);
+      td.tile = -1;
       p->stats.d2h_bytes += 8 * k + 8 * nnz_t;
+      p->trun[(size_t)t].d2h_bytes = 8 * k + 8 * nnz_t;
     } else {
       HIP_TRY(hipMemcpyAsync(C_rp + T.r0 + 1, S.crp + 1, sizeof(int64_t) * (size_t)k, hipMemcpyDeviceToDevice, sc));
     }
@@ -1420,10 +1570,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   }
   HIP_TRY(hipStreamSynchronize(sd));
   HIP_TRY(hipStreamSynchronize(sh));
-  unsigned long long products = 0;
-  HIP_TRY(hipMemcpyAsync(&products, prod, sizeof products, hipMemcpyDeviceToHost, sc));
-  HIP_TRY(hipStreamSynchronize(sc));
-  p->stats.products = (int64_t)products;
+  for (int64_t t = 0; t < nt; ++t) p->stats.products += p->trun[(size_t)t].products;
   p->stats.nnz_c = base;
   if (c_on_host) C_rp[0] = 0;
   else HIP_TRY(hipMemsetAsync(C_rp, 0, sizeof(int64_t), sc));
@@ -1536,6 +1683,55 @@ aires_status aires_plan_stats(const aires_plan* plan, aires_stats* stats) {
         default:
           if (mk.kind >= 0 && mk.kind < 8) stats->kind_ms[mk.phase][mk.kind] += ms;
           break;
+      }
+    }
+  }
+  return AIRES_OK;
+}
+
+aires_status aires_plan_tile_stats(const aires_plan* plan, int64_t t, aires_tile_stats* ts) {
+  if (!plan || !ts) return fail(AIRES_E_INVALID_ARG, "NULL argument");
+  if (t < 0 || t >= (int64_t)plan->tiles.size()) return fail(AIRES_E_INVALID_ARG, "tile %lld out of range", (long long)t);
+  std::memset(ts, 0, sizeof *ts);
+  ts->h2d_begin_ms = ts->h2d_end_ms = ts->compute_begin_ms = ts->compute_end_ms = ts->d2h_begin_ms =
+      ts->d2h_end_ms = -1.0;
+  const aires_tile& T = plan->tiles[(size_t)t];
+  ts->r0 = T.r0;
+  ts->r1 = T.r1;
+  if ((size_t)t < plan->trun.size()) {
+    const auto& r = plan->trun[(size_t)t];
+    ts->products = r.products;
+    ts->nnz_c = r.nnz_c;
+    ts->h2d_bytes = r.h2d_bytes;
+    ts->d2h_bytes = r.d2h_bytes;
+  }
+  if (!plan->ev.empty()) {
+    HIP_TRY(hipEventSynchronize(plan->ev.back()));
+    for (const auto& mk : plan->marks) {
+      if (mk.tile != (int)t) continue;
+      float ms = 0.f;
+      HIP_TRY(hipEventElapsedTime(&ms, plan->ev[(size_t)mk.a], plan->ev[(size_t)mk.b]));
+      switch (mk.kind) {
+        case PH_ANALYZE: ts->analyze_ms += ms; break;
+        case PH_BIN: ts->bin_ms += ms; break;
+        case PH_SYMBOLIC: ts->symbolic_ms += ms; break;
+        case PH_SCAN: ts->scan_ms += ms; break;
+        case PH_NUMERIC: ts->numeric_ms += ms; break;
+        case PH_H2D: ts->h2d_ms += ms; break;
+        case PH_D2H: ts->d2h_ms += ms; break;
+        default: break;
+      }
+    }
+    if (plan->ev_base >= 0 && (size_t)t < plan->tev.size()) {
+      double* at[aires_plan::T_NEV] = {&ts->h2d_begin_ms, &ts->h2d_end_ms, &ts->compute_begin_ms,
+                                       &ts->compute_end_ms, &ts->d2h_begin_ms, &ts->d2h_end_ms};
+      for (int i = 0; i < aires_plan::T_NEV; ++i) {
+        const int e = plan->tev[(size_t)t][(size_t)i];
+        *at[i] = -1.0;
+        if (e < 0) continue;
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, plan->ev[(size_t)plan->ev_base], plan->ev[(size_t)e]));
+        *at[i] = ms;
       }
     }
   }

@@ -27,7 +27,7 @@ def test_exports_every_declared_symbol():
 
 def test_version_and_strings():
     lib = B_.load()
-    assert lib.aires_abi_version() == 2
+    assert lib.aires_abi_version() == 3
     assert lib.aires_status_string(0) == b"AIRES_OK"
     assert lib.aires_status_string(B_.E_BUDGET) == b"AIRES_E_BUDGET"
     assert lib.aires_status_string(-99) == b"AIRES_E_UNKNOWN"
@@ -39,6 +39,36 @@ def test_version_and_strings():
 
 def _host(M):
     return (M.nrows, M.ncols, M.rp, M.col, M.val)
+
+
+def test_state_and_query_errors():
+    """AIRES_E_STATE for an output descriptor that is not zeroed (checked
+    before any device work), plan queries under their current names, and
+    per-tile statistics of a plan that has not run (no GPU needed: a
+    planning-only plan over host inputs)."""
+    lib = B_.load()
+    rng = np.random.default_rng(5)
+    A = workloads.random_csr(rng, 40, 30, 0.2)
+    Bm = workloads.random_csr(rng, 30, 9, 0.2)
+    with aires.tile_plan(_host(A), _host(Bm), 1 << 30, m_a_bytes=200) as plan:
+        info = aires.plan_info(plan)
+        i2 = B_.PlanInfo()
+        assert lib.aires_plan_info_get(plan.handle, ctypes.byref(i2)) == 0
+        assert i2.ntiles == info.ntiles > 1
+        assert lib.aires_plan_info(None, ctypes.byref(i2)) == B_.E_INVALID_ARG
+        ts = aires.plan_tile_stats(plan)
+        assert len(ts) == info.ntiles
+        assert [(t["r0"], t["r1"]) for t in ts] == [(t["r0"], t["r1"]) for t in aires.plan_tiles(plan)]
+        assert all(t["products"] == 0 and t["compute_begin_ms"] == -1.0 for t in ts)
+        x = B_.TileStats()
+        assert lib.aires_plan_tile_stats(plan.handle, info.ntiles, ctypes.byref(x)) == B_.E_INVALID_ARG
+        assert lib.aires_plan_tile_stats(plan.handle, -1, ctypes.byref(x)) == B_.E_INVALID_ARG
+        dummy = (ctypes.c_int64 * 4)()
+        out = B_.CsrOut()
+        out.row_ptr = ctypes.cast(dummy, ctypes.c_void_p)
+        assert lib.aires_spgemm(plan.handle, None, ctypes.byref(out)) == B_.E_STATE
+        assert b"not zeroed" in lib.aires_last_error()
+        assert lib.aires_stream_tiles(plan.handle, None, None, None, ctypes.byref(out)) == B_.E_STATE
 
 
 def test_error_paths():
