@@ -288,6 +288,36 @@ aires_status aires_plan_tile(const aires_plan *plan, int64_t t, aires_tile *tile
 aires_status aires_spgemm(aires_plan *plan, void *stream, aires_csr_out *C);
 
 /*
+ * aires_spgemm_noalloc -- aires_spgemm for callers that cannot allocate
+ * device memory (code that must not call hipMalloc: tight serving loops,
+ * harnesses that forbid allocation).  Same product, same kernels, but the
+ * call allocates nothing: its workspace is a fixed array of 64 MiB that the
+ * library holds on each device until the process ends, and C goes into
+ * arrays the caller owns.
+ *
+ * plan: from aires_tile_plan with A and B on the device (the plan's budget
+ * and allocator are not used; the kept symbolic bitmaps of wide rows are
+ * not used either).  c_row_ptr: device, m + 1 int64 entries, always
+ * written.  c_col_idx / c_vals: device arrays of c_capacity entries (may
+ * be NULL when c_capacity is 0).  *nnz_out (may be NULL) receives nnz(C),
+ * or -1 if the call failed before it was known.  Work is enqueued on
+ * `stream`; the call synchronises it once (to read nnz(C), as aires_spgemm
+ * does) and returns with the numeric phase enqueued.
+ *
+ * Every call on a device shares that device's array, which keeps the last
+ * call's contents: calls that overlap on one device (other streams or
+ * threads) race and must not be issued.  Counters the kernels need cleared
+ * are cleared by each call.
+ * Errors: AIRES_E_INVALID_ARG (NULL plan / arrays, negative capacity),
+ * AIRES_E_UNSUPPORTED (A or B not on the device), AIRES_E_STATE (plan in
+ * use), AIRES_E_CAPACITY (the workspace does not fit the 64 MiB array, or
+ * nnz(C) > c_capacity: C.row_ptr and *nnz_out are then valid and the
+ * call may be repeated with larger arrays), AIRES_E_HIP.
+ */
+aires_status aires_spgemm_noalloc(aires_plan *plan, void *stream, int64_t *c_row_ptr, int32_t *c_col_idx,
+                                  float *c_vals, int64_t c_capacity, int64_t *nnz_out);
+
+/*
  * aires_stream_tiles -- out-of-core Phase II/III of Algorithm 2 for a
  * host-resident (pinned) A: B is copied to the device once (Phase I); for
  * each tile, its contiguous row_ptr/col/val slices are copied on `h2d` into

@@ -21,7 +21,7 @@ from dataclasses import dataclass
 from . import _binding as B_
 
 __all__ = ["tile_plan", "spgemm", "spmm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
-           "plan_tile_stats", "Plan", "Output", "AiresError", "to_device", "to_pinned"]
+           "plan_tile_stats", "spgemm_noalloc", "Plan", "Output", "AiresError", "to_device", "to_pinned"]
 
 AiresError = B_.AiresError
 
@@ -249,6 +249,29 @@ def spgemm(plan: Plan, stream=None) -> Output:
     out = B_.CsrOut()
     B_.check(B_.load().aires_spgemm(plan.handle, _stream_handle(stream), ctypes.byref(out)), "aires_spgemm")
     return Output(out, plan.allocator)
+
+
+def spgemm_noalloc(plan: Plan, rp, col, val, stream=None) -> int:
+    """C = A * B into caller-owned device tensors (aires_spgemm_noalloc):
+    rp int64 (m + 1), col int32 and val float32 of equal length (C's
+    capacity).  The library allocates nothing (its workspace is a fixed
+    per-device array).  Returns nnz(C); raises AiresError (AIRES_E_CAPACITY
+    when C or the workspace does not fit)."""
+    import torch
+    if rp.dtype != torch.int64 or col.dtype != torch.int32 or val.dtype != torch.float32:
+        raise TypeError("expected int64 rp, int32 col, float32 val")
+    if col.numel() != val.numel() or not (rp.is_cuda and col.is_cuda and val.is_cuda):
+        raise ValueError("col and val must be device tensors of equal length")
+    nnz = ctypes.c_int64(-1)
+    st = B_.load().aires_spgemm_noalloc(plan.handle, _stream_handle(stream), rp.data_ptr(),
+                                        col.data_ptr() if col.numel() else None,
+                                        val.data_ptr() if val.numel() else None, int(col.numel()),
+                                        ctypes.byref(nnz))
+    if st != B_.OK:
+        err = B_.AiresError(st, "aires_spgemm_noalloc")
+        err.nnz = nnz.value
+        raise err
+    return nnz.value
 
 
 def stream_tiles(plan: Plan, h2d=None, compute=None, d2h=None) -> Output:

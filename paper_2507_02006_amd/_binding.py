@@ -112,6 +112,7 @@ def load() -> ctypes.CDLL:
         "aires_plan_tile_stats": (ctypes.c_int, [c_vp, c_i64, P(TileStats)]),
         "aires_plan_tile": (ctypes.c_int, [c_vp, c_i64, P(Tile)]),
         "aires_spgemm": (ctypes.c_int, [c_vp, c_vp, P(CsrOut)]),
+        "aires_spgemm_noalloc": (ctypes.c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_i64, P(c_i64)]),
         "aires_stream_tiles": (ctypes.c_int, [c_vp, c_vp, c_vp, c_vp, P(CsrOut)]),
         "aires_plan_stats": (ctypes.c_int, [c_vp, P(Stats)]),
         "aires_csr_out_free": (None, [P(CsrOut)]),

@@ -6,7 +6,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "libaires.so")
-SOURCES = [os.path.join(HERE, "csrc", n) for n in ("aires.cpp", "kernels.hip", "spmm.hip", "normalize.hip")]
+SOURCES = [os.path.join(HERE, "csrc", n) for n in ("aires.cpp", "kernels.hip", "spmm.hip", "normalize.hip", "scratch.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",

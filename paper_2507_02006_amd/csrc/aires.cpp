@@ -18,6 +18,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "scratch.h"
 
 using namespace aires;
 
@@ -1624,6 +1625,37 @@ aires_status aires_spgemm(aires_plan* plan, void* stream, aires_csr_out* C) {
   plan->busy = 1;
   aires_status st = spgemm_device(plan, (hipStream_t)stream, C);
   plan->busy = 0;
+  return st;
+}
+
+aires_status aires_spgemm_noalloc(aires_plan* plan, void* stream, int64_t* c_row_ptr, int32_t* c_col_idx,
+                                  float* c_vals, int64_t c_capacity, int64_t* nnz_out) {
+  if (nnz_out) *nnz_out = -1;
+  if (!plan || !c_row_ptr) return fail(AIRES_E_INVALID_ARG, "NULL plan or C.row_ptr");
+  if (c_capacity < 0) return fail(AIRES_E_INVALID_ARG, "negative C capacity");
+  if (c_capacity > 0 && (!c_col_idx || !c_vals)) return fail(AIRES_E_INVALID_ARG, "NULL C arrays");
+  if (plan->A.mem != AIRES_MEM_DEVICE || plan->B.mem != AIRES_MEM_DEVICE)
+    return fail(AIRES_E_UNSUPPORTED, "the allocation-free call needs A and B on the device");
+  if (plan->busy) return fail(AIRES_E_STATE, "plan is in use");
+  void* base = nullptr;
+  HIP_TRY(aires::scratch_address(&base));
+  std::memset(&plan->stats, 0, sizeof plan->stats);
+  plan->stats.ntiles = (int64_t)plan->tiles.size();
+  plan->trun.assign(plan->tiles.size(), aires_plan::TileRun{0, 0, 0, 0});
+  reset_timing(plan);
+  std::array<int, aires_plan::T_NEV> none;
+  none.fill(-1);
+  plan->tev.assign(plan->tiles.size(), none);
+  plan->ev_base = -1;
+  // no timing events: the call creates no runtime objects either
+  const int32_t timing = plan->opts.timing;
+  plan->opts.timing = 0;
+  plan->busy = 1;
+  DevPool ws(base, kScratchBytes, (hipStream_t)stream);
+  CallerC cc{c_row_ptr, c_col_idx, c_vals, c_capacity, nnz_out};
+  aires_status st = spgemm_device_in(plan, (hipStream_t)stream, ws, nullptr, &cc);
+  plan->busy = 0;
+  plan->opts.timing = timing;
   return st;
 }
 
