@@ -952,7 +952,6 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
   const int nwmax = SG * WPG;
   uint32_t* bm = reinterpret_cast<uint32_t*>(smem);
   const size_t bm_bytes = align16((size_t)nwmax * 4);
-  int32_t* gc = reinterpret_cast<int32_t*>(smem + bm_bytes);
   using CH = Chunk<WIN_BLOCK, RB>;
   CH& ch = *reinterpret_cast<CH*>(smem + bm_bytes + align16((size_t)SG * 4));
   Group<WIN_BLOCK, WIN_BLOCK> g;
@@ -979,14 +978,8 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
     for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, row, seg, [&](int j, float) {
       atomicOr(&bma[j >> 5], 1u << (j & 31));
     });
-    // per-grain popcounts: a wavefront per grain, lanes on consecutive words
     const int nw = (g1 - g0) * WPG;
-    for (int gi = wv; gi < g1 - g0; gi += NWV) {
-      uint32_t c = 0;
-      for (int w = gi * WPG + lane; w < (gi + 1) * WPG; w += WAVE) c += __popc(bm[w]);
-      c = wave_sum(c);
-      if (lane == 0) gc[gi] = (int32_t)c;
-    }
+    int64_t off = -1;
     if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
       // heavy row: keep the item's bitmap for the numeric phase, in a slot
       // taken from the workgroup's chunk of the shared cache
@@ -996,22 +989,31 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
           chunk_cur = (int64_t)atomicAdd(wp.bm_top, (unsigned long long)take);
           chunk_end = chunk_cur + take;
         }
-        const int64_t off = chunk_cur + nw <= wp.bm_cap ? chunk_cur : -1;
+        const int64_t o = chunk_cur + nw <= wp.bm_cap ? chunk_cur : -1;
         chunk_cur += nw;
-        s_off = off;
-        wp.bm_off[row * ngg + gg] = off;
+        s_off = o;
+        wp.bm_off[row * ngg + gg] = o;
       }
       __syncthreads();
-      const int64_t off = s_off;
-      if (off >= 0)
-        for (int w = t; w < nw; w += WIN_BLOCK) wp.bm_cache[off + w] = bm[w];  // coalesced
+      off = s_off;
     } else if (wp.bm_cache && t == 0) {
       wp.bm_off[row * ngg + gg] = -1;
     }
-    __syncthreads();  // counts and cache copies have read the bitmap
-    for (int w = t; w < nw; w += WIN_BLOCK) bm[w] = 0u;
-    for (int k = t; k < g1 - g0; k += WIN_BLOCK) wp.gcnt[row * op.nG + g0 + k] = gc[k];
-    __syncthreads();
+    // one pass over the bitmap: per-grain popcounts (a wavefront per grain,
+    // lanes on consecutive words), the copy of a kept bitmap (coalesced)
+    // and the clearing for the next item
+    for (int gi = wv; gi < g1 - g0; gi += NWV) {
+      uint32_t c = 0;
+      for (int w = gi * WPG + lane; w < (gi + 1) * WPG; w += WAVE) {
+        const uint32_t x = bm[w];
+        c += __popc(x);
+        if (off >= 0) wp.bm_cache[off + w] = x;
+        bm[w] = 0u;
+      }
+      c = wave_sum(c);
+      if (lane == 0) wp.gcnt[row * op.nG + g0 + gi] = (int32_t)c;
+    }
+    __syncthreads();  // the bitmap is clear before the next item's terms
   }
 }
 
@@ -1152,7 +1154,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
         const int SG = wp.grains_per_count_item;
         const int64_t o = wp.bm_off[row * ((op.nG + SG - 1) / SG) + g0 / SG];
-        if (o >= 0) cached = o + (int64_t)(g0 % SG) * WPG;  // windows never leave their item
+        if (o >= 0) cached = o + (int64_t)(g0 % SG) * WPG;
       }
       auto load_bits = [&]() {
         __syncthreads();  // the previous window's bitmap is cleared
@@ -1212,19 +1214,34 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
           const int one = wlen > 0 ? wave_seg_map(ch.ex, nk, wlo, wlen, seg_w) : -1;
           int jj[SEG_PER_THREAD];
           float vv[SEG_PER_THREAD];
+          // positions first, then every load, then the products: all of the
+          // window's B loads are in flight together (a product right after
+          // its load would wait for each load in turn)
           auto load_terms = [&](auto rec_of) {
+            int32_t pos[SEG_PER_THREAD];
 #pragma unroll
             for (int i = 0; i < SEG_PER_THREAD; ++i) {
               const int q = lane + i * WAVE;
-              jj[i] = -1;
+              pos[i] = -1;
               vv[i] = 0.f;
               if (q < wlen) {
                 const typename CH::Rec rc = rec_of(q);
-                const int32_t pos = (int32_t)rc.shift + wlo + q;
-                jj[i] = op.bcol[pos];
-                vv[i] = rc.av * op.bval[pos];
+                pos[i] = (int32_t)rc.shift + wlo + q;
+                vv[i] = rc.av;
               }
             }
+            float bv[SEG_PER_THREAD];
+#pragma unroll
+            for (int i = 0; i < SEG_PER_THREAD; ++i) {
+              jj[i] = -1;
+              bv[i] = 0.f;
+              if (pos[i] >= 0) {
+                jj[i] = op.bcol[pos[i]];
+                bv[i] = op.bval[pos[i]];
+              }
+            }
+#pragma unroll
+            for (int i = 0; i < SEG_PER_THREAD; ++i) vv[i] *= bv[i];
           };
           if (one >= 0) {
             const typename CH::Rec r1 = ch.rec[one];
