@@ -316,6 +316,7 @@ def streamed(args):
     n = args.nodes or cfg["n"]
     feats = [int(x) for x in args.features.split(",")] if args.features else [cfg["F"]]
     budgets = [float(x) for x in args.budget_gb.split(",")] if args.budget_gb else [32.0]
+    segs = args.segmentation.split(",")
     hold = []
 
     def pinned(rp_dtype):
@@ -337,7 +338,7 @@ def streamed(args):
         B = workloads.features(n, F, cfg["rho"], seed=1000 + args.workload, out=pinned(torch.int32), verbose=True)
         tB = (B.nrows, B.ncols) + hold[-1]
         gen_s = gen_a + time.perf_counter() - t0
-        for budget in budgets:
+        for budget, seg in [(b, sg) for b in budgets for sg in segs]:
             runs = []
             for it in range(args.warmup + args.steps):
                 t1 = time.perf_counter()
@@ -345,7 +346,7 @@ def streamed(args):
                 with aires.tile_plan(a_in, tB, int(budget * (1 << 30)), c_on_host=not args.c_on_device, timing=True,
                                      max_tile_bytes=args.max_tile_mb << 20,
                                      a_values="sym_norm" if args.sym_norm else "given",
-                                     c_bound=3 if args.c_bound == "rows" else 0) as plan:
+                                     c_bound=3 if args.c_bound == "rows" else 0, segmentation=seg) as plan:
                     t2 = time.perf_counter()
                     info = aires.plan_info(plan)
                     C = aires.spgemm(plan)
@@ -361,8 +362,8 @@ def streamed(args):
                 wall = time.perf_counter() - t1
                 if it >= args.warmup:
                     runs.append((wall, st))
-                print("[stream] F=%d budget=%.1f GB run %d: %.1f ms, %d tiles" % (F, budget, it, 1e3 * wall,
-                                                                               info.ntiles), file=sys.stderr, flush=True)
+                print("[stream] F=%d budget=%.1f GB %s run %d: %.1f ms, %d tiles" %
+                      (F, budget, seg, it, 1e3 * wall, info.ntiles), file=sys.stderr, flush=True)
             walls = sorted(r[0] for r in runs)
             wall = walls[len(walls) // 2]
             st = [r[1] for r in runs if r[0] == wall][0]
@@ -377,7 +378,7 @@ def streamed(args):
                 "data": "synthetic (seeded R-MAT graph and uniform sparse features, in pinned host memory)",
                 "config": {"workload": "cfg%d-shaped streamed aggregation: n=%d, X %d x %d at %g" %
                                        (args.workload, n, n, F, cfg["rho"]),
-                           "budget_gb": budget, "f": F, "nnz_a": A.nnz, "nnz_b": B.nnz,
+                           "budget_gb": budget, "f": F, "nnz_a": A.nnz, "nnz_b": B.nnz, "segmentation": seg,
                            "a_values": "derived on the device (Eq. 2)" if args.sym_norm else "copied",
                            "c_placement": "device" if args.c_on_device else "pinned host",
                            "c_bound": args.c_bound, "c_bound_entries": info.c_bound_entries,
@@ -391,6 +392,8 @@ def streamed(args):
                 "h2d_gb": round(st["h2d_bytes"] / 1e9, 3), "d2h_gb": round(st["d2h_bytes"] / 1e9, 3),
                 "h2d_gbs": round(st["h2d_bytes"] / max(st["h2d_ms"], 1e-9) / 1e6, 2),
                 "d2h_gbs": round(st["d2h_bytes"] / max(st["d2h_ms"], 1e-9) / 1e6, 2),
+                "resent_gb": round(st["resent_bytes"] / 1e9, 4), "merge_ms": round(st["merge_ms"], 2),
+                "host_syncs": st["host_syncs"],
                 "generation_s": round(gen_s, 2),
             }
             print(json.dumps(res), flush=True)
@@ -583,6 +586,10 @@ def main():
     ap.add_argument("--features", default="", help="--stream: comma-separated feature widths (the workload's)")
     ap.add_argument("--nodes", type=int, default=0, help="--stream: graph nodes (the workload's)")
     ap.add_argument("--max-tile-mb", type=int, default=0, help="--stream: cap on a tile's A bytes (0: none)")
+    ap.add_argument("--segmentation", default="robw",
+                    help="--stream: comma-separated segmentations of A: robw (row blocks, Algorithm 1) and/or "
+                         "maxfill (segments filled to the slot, partial rows copied back, packed on the host "
+                         "and sent again)")
     ap.add_argument("--c-on-device", action="store_true",
                     help="--stream: C stays in device memory instead of returning to pinned host memory")
     ap.add_argument("--c-bound", default="products", choices=["products", "rows"],

@@ -137,6 +137,22 @@ typedef enum aires_cbound {
                                    reads no column of A (no gather)       */
 } aires_cbound;
 
+/*
+ * How a streamed A is cut into segments.  ROBW: row blocks of whole rows
+ * (Sec. III-A, Algorithm 1).  MAXFILL: the unaligned scheme the paper
+ * measures against (Sec. I, Sec. III-A and Fig. 3; the MaxMemory baseline
+ * of Sec. V-A): each segment is filled with as many of A's entries as its
+ * slot holds, so it may end inside a row.  Only its complete rows are
+ * multiplied; the entries of the partial last row are copied back to host
+ * memory, packed on the host in front of the next segment's entries in a
+ * pinned staging buffer, and sent again with them.  The product is the
+ * same; the extra copies, host packing and waits are the merging overhead.
+ */
+typedef enum aires_segmentation {
+    AIRES_SEG_ROBW = 0,
+    AIRES_SEG_MAXFILL = 1
+} aires_segmentation;
+
 typedef struct aires_plan_opts {
     uint32_t struct_size;       /* = sizeof(aires_plan_opts)               */
     int32_t validate;           /* 1: canonical-CSR check of host inputs   */
@@ -183,7 +199,9 @@ typedef struct aires_plan_opts {
                                    hold one full grain                     */
     int32_t a_values;           /* aires_avalues: where A's values come
                                    from (AIRES_AVALUES_GIVEN)              */
-    int32_t _reserved0;
+    int32_t segmentation;       /* aires_segmentation, default ROBW;
+                                   MAXFILL needs A in pinned host memory
+                                   and given values                        */
 } aires_plan_opts;
 
 /* Fill *o with defaults (struct_size set, validate 0, C on device). */
@@ -232,6 +250,11 @@ typedef struct aires_plan_info {
     int64_t c_bound_entries;    /* sum of u_i, or -1 when not computed     */
     int32_t a_streamed;         /* 1: A moves host->device per tile        */
     int32_t c_on_host;          /* 1: C tiles move device->host            */
+    int64_t part_budget;        /* slot bytes the tiles were cut under:
+                                   tile_budget, or less when the largest
+                                   row count, entry count and C bound of
+                                   different tiles would not fit one slot
+                                   together                                */
 } aires_plan_info_t;            /* (the struct tag shares the query's name) */
 
 typedef struct aires_tile {
@@ -240,6 +263,9 @@ typedef struct aires_tile {
     int64_t a_bytes;            /* (r1-r0+1)*rp_bytes + 8*(nnz1-nnz0)      */
     int64_t c_bound_entries;    /* sum of u_i over the tile, or -1         */
     int64_t tile_bytes;         /* planned bytes of one slot of this tile  */
+    int64_t sent_nnz1;          /* A entries [nnz0, sent_nnz1) are sent:
+                                   nnz1 for row blocks; beyond nnz1 for a
+                                   max-fill segment ending inside a row    */
 } aires_tile;
 
 /*
@@ -353,6 +379,11 @@ typedef struct aires_stats {
     /* streamed calls: from the first copy of Phase I to the last copy of
        Phase III (the tile pipeline, without the output allocation)       */
     double pipeline_ms;
+    /* max-fill segments: entries of partial rows copied back and sent
+       again (8 bytes each, counted in d2h_bytes and h2d_bytes too), and
+       the host time spent packing segments into the staging buffers      */
+    int64_t resent_bytes;
+    double merge_ms;
 } aires_stats;
 
 /* Activation applied by aires_spmm. */
@@ -421,6 +452,11 @@ typedef struct aires_tile_stats {
     double h2d_begin_ms, h2d_end_ms;
     double compute_begin_ms, compute_end_ms;
     double d2h_begin_ms, d2h_end_ms;
+    int64_t resent_bytes;       /* max-fill: partial-row bytes copied back
+                                   after this segment and sent again with
+                                   the next one (in d2h_bytes here)        */
+    double merge_ms;            /* max-fill: host time packing this
+                                   segment's staging buffer                */
 } aires_tile_stats;
 
 /* Errors: AIRES_E_INVALID_ARG (NULL, t out of range), AIRES_E_HIP. */

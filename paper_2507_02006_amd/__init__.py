@@ -65,11 +65,14 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
               hash_max_products: int = 0, wave_max_products: int = 0, window_grain_cols: int = 0,
               window_max_grains: int = 0, window_max_entries: int = 0, count_grains: int = 0,
               keep_bitmap_products: int = 0, split_min_products: int = 0, split_max_rows: int = 0,
-              window_pool_bytes: int = 0, a_values: str = "given", torch_allocator: bool = True,
-              allocator=None, device: int = 0) -> Plan:
+              window_pool_bytes: int = 0, a_values: str = "given", segmentation: str = "robw",
+              torch_allocator: bool = True, allocator=None, device: int = 0) -> Plan:
     """Plan C = A * B under a device budget (aires_tile_plan).  a_values:
     "given" (A's values) or "sym_norm" (a_ik = 1/sqrt(r_i r_k) of A's
     pattern, Eq. 2, derived on the device; A's vals may then be None).
+    segmentation: "robw" (row blocks, Algorithm 1) or "maxfill" (segments
+    filled to the slot that may end inside a row: the partial row is copied
+    back, packed on the host with the next segment and sent again).
     ``allocator``: an object with a ctypes ``struct`` (``_binding.Allocator``)
     such as a ``_binding.TorchAllocator``; by default a TorchAllocator
     (``torch_allocator``) or the library's own hipMallocAsync."""
@@ -99,6 +102,9 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
     if a_values not in ("given", "sym_norm"):
         raise ValueError("a_values must be 'given' or 'sym_norm'")
     o.a_values = B_.AVALUES_SYM_NORM if a_values == "sym_norm" else B_.AVALUES_GIVEN
+    if segmentation not in ("robw", "maxfill"):
+        raise ValueError("segmentation must be 'robw' or 'maxfill'")
+    o.segmentation = B_.SEG_MAXFILL if segmentation == "maxfill" else B_.SEG_ROBW
     alloc = allocator
     if alloc is None and torch_allocator and (a.mem == B_.MEM_DEVICE or b.mem != B_.MEM_HOST):
         alloc = B_.TorchAllocator(device)
@@ -124,6 +130,7 @@ class Info:
     c_bound_entries: int
     a_streamed: bool
     c_on_host: bool
+    part_budget: int
 
 
 def plan_info(plan: Plan) -> Info:

@@ -56,31 +56,34 @@ class PlanOpts(ctypes.Structure):
                 ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64),
                 ("keep_bitmap_products", c_i64), ("split_min_products", c_i64),
                 ("split_max_rows", c_i64), ("window_pool_bytes", c_i64), ("a_values", c_i32),
-                ("_reserved0", c_i32)]
+                ("segmentation", c_i32)]
 
 
 class PlanInfo(ctypes.Structure):
     _fields_ = [(n, c_i64) for n in ("ntiles", "m", "k", "n", "budget", "b_bytes", "a_bytes", "tile_budget",
                                      "peak_bytes", "c_bound_entries")] + \
-               [("a_streamed", c_i32), ("c_on_host", c_i32)]
+               [("a_streamed", c_i32), ("c_on_host", c_i32), ("part_budget", c_i64)]
 
 
 class Tile(ctypes.Structure):
-    _fields_ = [(n, c_i64) for n in ("r0", "r1", "nnz0", "nnz1", "a_bytes", "c_bound_entries", "tile_bytes")]
+    _fields_ = [(n, c_i64) for n in ("r0", "r1", "nnz0", "nnz1", "a_bytes", "c_bound_entries", "tile_bytes",
+                                     "sent_nnz1")]
 
 
 class Stats(ctypes.Structure):
     _fields_ = [(n, c_i64) for n in ("ntiles", "products", "nnz_c", "h2d_bytes", "d2h_bytes", "host_syncs")] + \
                [(n, c_dbl) for n in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "h2d_ms",
                                      "d2h_ms", "total_ms")] + \
-               [("numeric_launches", c_i64), ("kind_ms", (c_dbl * 8) * 2), ("pipeline_ms", c_dbl)]
+               [("numeric_launches", c_i64), ("kind_ms", (c_dbl * 8) * 2), ("pipeline_ms", c_dbl),
+                ("resent_bytes", c_i64), ("merge_ms", c_dbl)]
 
 
 class TileStats(ctypes.Structure):
     _fields_ = [(n, c_i64) for n in ("r0", "r1", "products", "nnz_c", "h2d_bytes", "d2h_bytes")] + \
                [(n, c_dbl) for n in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "h2d_ms",
                                      "d2h_ms", "h2d_begin_ms", "h2d_end_ms", "compute_begin_ms",
-                                     "compute_end_ms", "d2h_begin_ms", "d2h_end_ms")]
+                                     "compute_end_ms", "d2h_begin_ms", "d2h_end_ms")] + \
+               [("resent_bytes", c_i64), ("merge_ms", c_dbl)]
 
 
 _lib = None
@@ -131,6 +134,7 @@ def load() -> ctypes.CDLL:
 ACT_NONE, ACT_RELU = 0, 1
 SPMM_AUTO, SPMM_ROWS, SPMM_DENSE_TILES = 0, 1, 2
 AVALUES_GIVEN, AVALUES_SYM_NORM = 0, 1
+SEG_ROBW, SEG_MAXFILL = 0, 1
 
 
 class AiresError(RuntimeError):

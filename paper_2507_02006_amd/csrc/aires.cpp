@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <array>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -203,7 +204,7 @@ struct aires_plan {
   int64_t split_cap = 0;           // rows with dense slots for the split bin
   int64_t split_ws = 0;            // bytes of those slots
   // per-tile counts of the last call (products, nnz(C), bytes copied)
-  struct TileRun { int64_t products, nnz_c, h2d_bytes, d2h_bytes; };
+  struct TileRun { int64_t products, nnz_c, h2d_bytes, d2h_bytes, resent_bytes; double merge_ms; };
   std::vector<TileRun> trun;
   // per tile, indices into ev of: copy in begin/end, compute begin/end,
   // copy out begin/end (-1: none); times are taken from ev[ev_base]
@@ -591,6 +592,13 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     return fail(AIRES_E_INVALID_ARG, "opts.c_bound %d invalid", o.c_bound);
   if (o.max_tile_rows < 0 || o.max_tile_bytes < 0 || o.m_a_bytes < 0)
     return fail(AIRES_E_INVALID_ARG, "negative tile cap");
+  if (o.segmentation != AIRES_SEG_ROBW && o.segmentation != AIRES_SEG_MAXFILL)
+    return fail(AIRES_E_INVALID_ARG, "opts.segmentation %d invalid", o.segmentation);
+  if (o.segmentation == AIRES_SEG_MAXFILL &&
+      (A->mem != AIRES_MEM_HOST_PINNED || a_sym_norm || o.m_a_bytes > 0 || o.max_tile_rows > 0))
+    return fail(AIRES_E_UNSUPPORTED,
+                "max-fill segments need A in pinned host memory with given values (and no Algorithm 1 "
+                "planning mode or row cap)");
   if (o.validate) {
     if (A->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*A, "A", !a_sym_norm));
     if (B->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*B, "B"));
@@ -774,20 +782,80 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   int64_t max_tile_bytes = o.max_tile_bytes;
   if (a_streamed && max_tile_bytes == 0 && o.m_a_bytes == 0)
     max_tile_bytes = std::max<int64_t>(p->info.a_bytes / kStreamTiles, kMinStreamTileBytes);
+  int64_t part_budget = tile_budget;  // the budget the partition is cut under
   auto fits = [&](int64_t r0, int64_t r1) -> bool {
     if (o.max_tile_rows > 0 && r1 - r0 > o.max_tile_rows) return false;
     if (max_tile_bytes > 0 && (r1 - r0 + 1) * sA + 8 * (arp[r1] - arp[r0]) > max_tile_bytes)
       return false;
-    return slot_bytes_fast(r0, r1) <= tile_budget;
+    return slot_bytes_fast(r0, r1) <= part_budget;
   };
+  // The two slots of a streamed A are sized by the largest row count, the
+  // largest number of entries sent and the largest C bound over all tiles,
+  // which need not come from one tile: if those maxima together pass the
+  // slot budget, the partition is redone under a budget smaller by the
+  // excess.
   int64_t peak_slot = 0;
+  for (int pass = 0;; ++pass) {
+  p->tiles.clear();
+  peak_slot = 0;
   int64_t r0 = 0;
+  if (o.segmentation == AIRES_SEG_MAXFILL) {
+    // Max-fill segments: from the first row not yet multiplied, as many of
+    // A's entries as the slot holds, wherever that ends.  Entries [E, E + q)
+    // are sent; rows [r0, r1) are complete in them (r1 the last row whose
+    // end is at or before E + q); the head of row r1 goes back and opens
+    // the next segment.  A segment's slot holds its q entries and the rows'
+    // pointers, workspace and C bound, as a row block's does.
+    auto last_row = [&](int64_t e) {  // largest r with arp[r] <= e
+      return (int64_t)(std::upper_bound(arp, arp + m + 1, e) - arp) - 1;
+    };
+    auto seg_fits = [&](int64_t s0, int64_t e, int64_t q) -> bool {
+      const int64_t s1 = std::min(m, last_row(e + q));
+      if (s1 <= s0) return true;  // no complete row yet: the cost so far is below a row's
+      if (max_tile_bytes > 0 && (s1 - s0 + 1) * sA + 8 * q > max_tile_bytes) return false;
+      return slot_bytes_fast(s0, s1) + 8 * (e + q - arp[s1]) <= part_budget;
+    };
+    const int64_t nnzA = arp[m];
+    while (r0 < m) {
+      const int64_t E = arp[r0];
+      const int64_t rest = nnzA - E;
+      int64_t lo = 0, hi = rest + 1;  // seg_fits(lo); the largest q in [0, rest] that fits
+      if (seg_fits(r0, E, rest)) {
+        lo = rest;
+      } else {
+        while (hi - lo > 1) {
+          const int64_t mid = lo + (hi - lo) / 2;
+          if (seg_fits(r0, E, mid)) lo = mid; else hi = mid;
+        }
+      }
+      const int64_t q = lo;
+      const int64_t r1 = q == rest ? m : std::min(m, last_row(E + q));
+      if (r1 <= r0) {
+        const int64_t need = slot_bytes_fast(r0, r0 + 1);
+        delete p;
+        return fail(AIRES_E_BUDGET, "row %lld alone needs %lld bytes; a segment slot has %lld", (long long)r0,
+                    (long long)need, (long long)part_budget);
+      }
+      aires_tile t;
+      t.r0 = r0;
+      t.r1 = r1;
+      t.nnz0 = E;
+      t.nnz1 = arp[r1];
+      t.sent_nnz1 = E + q;
+      t.a_bytes = (r1 - r0 + 1) * sA + 8 * q;
+      t.c_bound_entries = cpre.empty() ? -1 : cpre[(size_t)r1] - cpre[(size_t)r0];
+      t.tile_bytes = slot_bytes_fast(r0, r1) + 8 * (E + q - arp[r1]);
+      peak_slot = std::max(peak_slot, t.tile_bytes);
+      p->tiles.push_back(t);
+      r0 = r1;
+    }
+  }
   while (r0 < m) {
     if (!fits(r0, r0 + 1)) {
       const int64_t need = slot_bytes_fast(r0, r0 + 1);
       delete p;
       return fail(AIRES_E_BUDGET, "row %lld alone needs %lld bytes; a tile slot has %lld", (long long)r0,
-                  (long long)need, (long long)tile_budget);
+                  (long long)need, (long long)part_budget);
     }
     int64_t lo = r0 + 1, step = 1;  // fits(r0, lo)
     int64_t hi = -1;                // first end that does not fit
@@ -817,11 +885,30 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     t.a_bytes = (lo - r0 + 1) * sA + 8 * (t.nnz1 - t.nnz0);
     t.c_bound_entries = cpre.empty() ? -1 : cpre[(size_t)lo] - cpre[(size_t)r0];
     t.tile_bytes = slot_bytes_fast(r0, lo);
+    t.sent_nnz1 = t.nnz1;
     peak_slot = std::max(peak_slot, t.tile_bytes);
     p->tiles.push_back(t);
     r0 = lo;
   }
+  if (!a_streamed || o.m_a_bytes > 0) break;  // one slot sized by its rows alone
+  int64_t mk = 0, mq = 0, mc = 0;
+  for (const aires_tile& t : p->tiles) {
+    mk = std::max(mk, t.r1 - t.r0);
+    mq = std::max(mq, t.sent_nnz1 - t.nnz0);
+    mc = std::max(mc, t.c_bound_entries);
+  }
+  const int64_t need = mk * per_row_ws + (mk + 1) * sA + 8 * mq + (c_on_host ? 8 * mc + 8 * (mk + 1) : 0);
+  peak_slot = std::max(peak_slot, need);
+  if (need <= tile_budget) break;
+  if (pass >= 32 || part_budget <= need - tile_budget) {
+    delete p;
+    return fail(AIRES_E_BUDGET, "tile slots of %lld bytes cannot hold the largest tile parts (%lld bytes)",
+                (long long)tile_budget, (long long)need);
+  }
+  part_budget -= need - tile_budget;
+  }
   p->info.ntiles = (int64_t)p->tiles.size();
+  p->info.part_budget = part_budget;
   p->info.peak_bytes = resident + nslots * peak_slot;
   std::memset(&p->stats, 0, sizeof p->stats);
   *out = p;
@@ -1073,7 +1160,7 @@ aires_status begin_call(aires_plan* p, aires_csr_out* C) {
     return fail(AIRES_E_STATE, "output descriptor is not zeroed (free it first)");
   std::memset(&p->stats, 0, sizeof p->stats);
   p->stats.ntiles = (int64_t)p->tiles.size();
-  p->trun.assign(p->tiles.size(), aires_plan::TileRun{0, 0, 0, 0});
+  p->trun.assign(p->tiles.size(), aires_plan::TileRun{0, 0, 0, 0, 0, 0.0});
   reset_timing(p);
   std::array<int, aires_plan::T_NEV> none;
   none.fill(-1);
@@ -1303,11 +1390,13 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   p->ev_base = e_total0;
   DevPool ws(p->alloc, sc, p->budget - borrowed_device_bytes(p));
   const int64_t nt = (int64_t)p->tiles.size();
-  int64_t max_rows = 1, max_q = 1, max_cb = 1;
+  const bool maxfill = p->opts.segmentation == AIRES_SEG_MAXFILL;
+  int64_t max_rows = 1, max_q = 1, max_cb = 1, max_carry = 1;
   for (const auto& t : p->tiles) {
     max_rows = std::max(max_rows, t.r1 - t.r0);
-    max_q = std::max(max_q, t.nnz1 - t.nnz0);
+    max_q = std::max(max_q, t.sent_nnz1 - t.nnz0);
     max_cb = std::max(max_cb, t.c_bound_entries);
+    max_carry = std::max(max_carry, t.sent_nnz1 - t.nnz1);
   }
   const int64_t cap = p->info.c_bound_entries;
 
@@ -1379,6 +1468,25 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
       S.ccap = max_cb;
     }
   }
+  // max-fill segments: two pinned staging buffers a segment is packed into
+  // (the head of the partial row returned by the previous segment, then
+  // the new entries) and the pinned buffer the partial row returns to
+  int32_t* stage_col[2] = {nullptr, nullptr};
+  float* stage_val[2] = {nullptr, nullptr};
+  int32_t* carry_col = nullptr;
+  float* carry_val = nullptr;
+  if (maxfill) {
+    for (int b = 0; b < 2; ++b) {
+      HIP_TRY(hipHostMalloc((void**)&stage_col[b], sizeof(int32_t) * (size_t)max_q, hipHostMallocDefault));
+      hb.v.push_back(stage_col[b]);
+      HIP_TRY(hipHostMalloc((void**)&stage_val[b], sizeof(float) * (size_t)max_q, hipHostMallocDefault));
+      hb.v.push_back(stage_val[b]);
+    }
+    HIP_TRY(hipHostMalloc((void**)&carry_col, sizeof(int32_t) * (size_t)max_carry, hipHostMallocDefault));
+    hb.v.push_back(carry_col);
+    HIP_TRY(hipHostMalloc((void**)&carry_val, sizeof(float) * (size_t)max_carry, hipHostMallocDefault));
+    hb.v.push_back(carry_val);
+  }
   int64_t* cnt_host = nullptr;  // pinned per-tile (running nnz, windows, products)
   HIP_TRY(hipHostMalloc((void**)&cnt_host, sizeof(int64_t) * 3 * (size_t)std::max<int64_t>(nt, 1), hipHostMallocDefault));
   hb.v.push_back(cnt_host);
@@ -1395,12 +1503,13 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     evs.push_back(*e);
     return AIRES_OK;
   };
-  std::vector<hipEvent_t> ev_in(nt), ev_cnt(nt), ev_done(nt);
+  std::vector<hipEvent_t> ev_in(nt), ev_cnt(nt), ev_done(nt), ev_carry(maxfill ? nt : 0);
   hipEvent_t ev_cfree[2] = {nullptr, nullptr};
   for (int64_t t = 0; t < nt; ++t) {
     ST_TRY(mkev(&ev_in[(size_t)t]));
     ST_TRY(mkev(&ev_cnt[(size_t)t]));
     ST_TRY(mkev(&ev_done[(size_t)t]));
+    if (maxfill) ST_TRY(mkev(&ev_carry[(size_t)t]));
   }
   ST_TRY(mkev(&ev_cfree[0]));
   ST_TRY(mkev(&ev_cfree[1]));
@@ -1436,30 +1545,78 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     p->stats.h2d_bytes += (m + 1) * sA;
   }
 
+  // Max-fill: pack segment t into its staging buffer on the host: the head
+  // of the partial row segment t-1 returned (waited for here), then A's
+  // new entries.  The buffer's previous copy (segment t-2) must be done.
+  auto pack_segment = [&](int64_t t) -> aires_status {
+    const aires_tile& T = p->tiles[(size_t)t];
+    const int b = (int)(t % 2);
+    if (t >= 2) HIP_TRY(hipEventSynchronize(ev_in[(size_t)t - 2]));
+    int64_t c = 0;
+    if (t >= 1) {
+      const aires_tile& Tp = p->tiles[(size_t)t - 1];
+      c = Tp.sent_nnz1 - Tp.nnz1;  // == T.nnz0 .. Tp.sent_nnz1
+      if (c > 0) {
+        HIP_TRY(hipEventSynchronize(ev_carry[(size_t)t - 1]));
+        p->stats.host_syncs++;
+      }
+    }
+    const auto t0 = std::chrono::steady_clock::now();
+    const int64_t q = T.sent_nnz1 - T.nnz0;
+    if (c > 0) {
+      std::memcpy(stage_col[b], carry_col, sizeof(int32_t) * (size_t)c);
+      std::memcpy(stage_val[b], carry_val, sizeof(float) * (size_t)c);
+    }
+    parallel_ranges(q - c, [&](int64_t lo, int64_t hi, int) {
+      std::memcpy(stage_col[b] + c + lo, A.col_idx + T.nnz0 + c + lo, sizeof(int32_t) * (size_t)(hi - lo));
+      std::memcpy(stage_val[b] + c + lo, A.vals + T.nnz0 + c + lo, sizeof(float) * (size_t)(hi - lo));
+    });
+    const double ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    p->stats.merge_ms += ms;
+    p->trun[(size_t)t].merge_ms = ms;
+    return AIRES_OK;
+  };
+
   auto issue_h2d = [&](int64_t t) -> aires_status {
     const aires_tile& T = p->tiles[(size_t)t];
     Slot& S = slot[t % 2];
+    if (maxfill) ST_TRY(pack_segment(t));
     if (t >= 2) HIP_TRY(hipStreamWaitEvent(sh, ev_done[(size_t)t - 2], 0));
     th.tile = (int)t;
     const int ea = th.record();
     th.at(aires_plan::T_H2D0, ea);
-    const int64_t k = T.r1 - T.r0, q = T.nnz1 - T.nnz0;
+    const int64_t k = T.r1 - T.r0, q = T.sent_nnz1 - T.nnz0;
+    const int32_t* src_col = maxfill ? stage_col[t % 2] : A.col_idx + T.nnz0;
+    const float* src_val = maxfill ? stage_val[t % 2] : A.vals + T.nnz0;
     if (!sym_norm)
       HIP_TRY(hipMemcpyAsync(S.arp, static_cast<const char*>(A.row_ptr) + T.r0 * sA, (size_t)(k + 1) * sA,
                              hipMemcpyHostToDevice, sh));
     if (q > 0) {
-      HIP_TRY(hipMemcpyAsync(S.acol, A.col_idx + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
-      if (!sym_norm)
-        HIP_TRY(hipMemcpyAsync(S.aval, A.vals + T.nnz0, (size_t)q * 4, hipMemcpyHostToDevice, sh));
+      HIP_TRY(hipMemcpyAsync(S.acol, src_col, (size_t)q * 4, hipMemcpyHostToDevice, sh));
+      if (!sym_norm) HIP_TRY(hipMemcpyAsync(S.aval, src_val, (size_t)q * 4, hipMemcpyHostToDevice, sh));
     }
     HIP_TRY(hipEventRecord(ev_in[(size_t)t], sh));
     const int eb = th.record();
     th.mark(PH_H2D, 0, ea, eb);
     th.at(aires_plan::T_H2D1, eb);
-    th.tile = -1;
     const int64_t bytes = sym_norm ? 4 * q : (k + 1) * sA + 8 * q;
     p->stats.h2d_bytes += bytes;
     p->trun[(size_t)t].h2d_bytes = bytes;
+    if (maxfill && T.sent_nnz1 > T.nnz1) {
+      // the partial last row goes back to host memory (it is sent again,
+      // packed in front of the next segment)
+      const int64_t c = T.sent_nnz1 - T.nnz1, off = T.nnz1 - T.nnz0;
+      const int ec = th.record();
+      HIP_TRY(hipMemcpyAsync(carry_col, S.acol + off, (size_t)c * 4, hipMemcpyDeviceToHost, sh));
+      HIP_TRY(hipMemcpyAsync(carry_val, S.aval + off, (size_t)c * 4, hipMemcpyDeviceToHost, sh));
+      HIP_TRY(hipEventRecord(ev_carry[(size_t)t], sh));
+      th.mark(PH_D2H, 0, ec, th.record());
+      p->stats.d2h_bytes += 8 * c;
+      p->stats.resent_bytes += 8 * c;
+      p->trun[(size_t)t].d2h_bytes += 8 * c;
+      p->trun[(size_t)t].resent_bytes = 8 * c;
+    }
+    th.tile = -1;
     return AIRES_OK;
   };
 
@@ -1549,7 +1706,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
       td.at(aires_plan::T_D2H1, eb);
       td.tile = -1;
       p->stats.d2h_bytes += 8 * k + 8 * nnz_t;
-      p->trun[(size_t)t].d2h_bytes = 8 * k + 8 * nnz_t;
+      p->trun[(size_t)t].d2h_bytes += 8 * k + 8 * nnz_t;
     } else {
       HIP_TRY(hipMemcpyAsync(C_rp + T.r0 + 1, S.crp + 1, sizeof(int64_t) * (size_t)k, hipMemcpyDeviceToDevice, sc));
     }
@@ -1641,7 +1798,7 @@ aires_status aires_spgemm_noalloc(aires_plan* plan, void* stream, int64_t* c_row
   HIP_TRY(aires::scratch_address(&base));
   std::memset(&plan->stats, 0, sizeof plan->stats);
   plan->stats.ntiles = (int64_t)plan->tiles.size();
-  plan->trun.assign(plan->tiles.size(), aires_plan::TileRun{0, 0, 0, 0});
+  plan->trun.assign(plan->tiles.size(), aires_plan::TileRun{0, 0, 0, 0, 0, 0.0});
   reset_timing(plan);
   std::array<int, aires_plan::T_NEV> none;
   none.fill(-1);
@@ -1736,6 +1893,8 @@ aires_status aires_plan_tile_stats(const aires_plan* plan, int64_t t, aires_tile
     ts->nnz_c = r.nnz_c;
     ts->h2d_bytes = r.h2d_bytes;
     ts->d2h_bytes = r.d2h_bytes;
+    ts->resent_bytes = r.resent_bytes;
+    ts->merge_ms = r.merge_ms;
   }
   if (!plan->ev.empty()) {
     HIP_TRY(hipEventSynchronize(plan->ev.back()));

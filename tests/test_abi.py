@@ -172,10 +172,17 @@ def test_streamed_plan_invariants(seed):
         assert t0["r1"] == t1["r0"]
     for t in tiles:
         sb = _slot_bytes(A, P, Bm.ncols, t["r0"], t["r1"], 4)
-        assert t["tile_bytes"] == sb and sb <= info.tile_budget
+        assert t["tile_bytes"] == sb and sb <= info.part_budget <= info.tile_budget
         assert t["c_bound_entries"] == int(np.minimum(P[t["r0"]:t["r1"]], Bm.ncols).sum())
     for t in tiles[:-1]:
-        assert _slot_bytes(A, P, Bm.ncols, t["r0"], t["r1"] + 1, 4) > info.tile_budget
+        assert _slot_bytes(A, P, Bm.ncols, t["r0"], t["r1"] + 1, 4) > info.part_budget
+    # the two slots hold the largest row count, entry count and C bound of
+    # any tiles together (row pointers 4 B, 12 B of row workspace, 8 B of C
+    # row pointer per row, 8 B per entry and per C bound entry)
+    mk = max(t["r1"] - t["r0"] for t in tiles)
+    mq = max(t["nnz1"] - t["nnz0"] for t in tiles)
+    mc = max(t["c_bound_entries"] for t in tiles)
+    assert mk * 12 + (mk + 1) * 4 + 8 * mq + 8 * mc + 8 * (mk + 1) <= info.tile_budget
     assert len(tiles) > 1
 
 
@@ -290,3 +297,84 @@ def test_streamed_rows_bound(N):
     with aires.tile_plan(_host(A), _host(Bm), 1 << 40, c_bound=B_.CBOUND_ROWS) as p:
         assert aires.plan_info(p).c_bound_entries == int(want.sum())
         assert all(t["c_bound_entries"] == -1 for t in aires.plan_tiles(p))
+
+
+def _pinned_desc(M):
+    """A descriptor labelled pinned host memory over numpy arrays: planning
+    reads host arrays only, so no device is needed to plan a streamed A."""
+    d = B_.make_csr(M.nrows, M.ncols, M.rp, M.col, M.val)
+    d.mem = B_.MEM_HOST_PINNED
+    return d
+
+
+def _plan_tiles(A, Bm, budget, **opts):
+    lib = B_.load()
+    o = B_.PlanOpts()
+    lib.aires_plan_opts_default(ctypes.byref(o))
+    for k, v in opts.items():
+        setattr(o, k, v)
+    a, b = _pinned_desc(A), _pinned_desc(Bm)
+    h = ctypes.c_void_p()
+    st = lib.aires_tile_plan(ctypes.byref(a), ctypes.byref(b), int(budget), ctypes.byref(o), ctypes.byref(h))
+    if st != 0:
+        raise aires.AiresError(st, "aires_tile_plan")
+    info = B_.PlanInfo()
+    lib.aires_plan_info(h, ctypes.byref(info))
+    tiles = []
+    for t in range(info.ntiles):
+        x = B_.Tile()
+        lib.aires_plan_tile(h, t, ctypes.byref(x))
+        tiles.append({f: getattr(x, f) for f, _ in B_.Tile._fields_})
+    lib.aires_plan_destroy(h)
+    return info, tiles
+
+
+def test_maxfill_segments_hand_example(golden_dir):
+    """Max-fill segments of the 4x4 hand example (row lengths 2, 0, 2, 2;
+    int32 row pointers) under a 40-byte cap on a segment's A bytes,
+    (k + 1) * 4 + 8 q: entries [0, 3) (rows 0-1 complete, one entry of
+    row 2 sent ahead), then [2, 5) (row 2 again, one entry of row 3 ahead),
+    then [4, 6).  Row blocks under the same cap cut the same rows."""
+    g = json.load(open(os.path.join(golden_dir, "hand_4x4.json")))
+    mk = lambda d: workloads.CSR(d["nrows"], d["ncols"], np.array(d["rp"], np.int32), np.array(d["col"], np.int32),
+                                 np.array(d["val"], np.float32))
+    A, Bm = mk(g["A"]), mk(g["B"])
+    _, seg = _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=40, segmentation=B_.SEG_MAXFILL)
+    assert [(t["r0"], t["r1"], t["nnz0"], t["nnz1"], t["sent_nnz1"]) for t in seg] == \
+        [(0, 2, 0, 2, 3), (2, 3, 2, 4, 5), (3, 4, 4, 6, 6)]
+    _, rb = _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=40)
+    assert [(t["r0"], t["r1"], t["nnz1"], t["sent_nnz1"]) for t in rb] == [(0, 2, 2, 2), (2, 3, 4, 4), (3, 4, 6, 6)]
+    with pytest.raises(aires.AiresError) as e:
+        _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=23, segmentation=B_.SEG_MAXFILL)
+    assert e.value.status == B_.E_BUDGET
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_maxfill_segments_fill_and_cover(seed):
+    """On random row lengths (empty rows included): segments start where
+    the previous one's complete rows end, cover every row once, send every
+    entry at least once (the partial rows twice), end inside the next row
+    unless they end the matrix, and are full: one more entry would pass
+    the cap."""
+    rng = np.random.default_rng(seed)
+    m = 400
+    lens = rng.integers(0, 30, m)
+    lens[rng.random(m) < 0.2] = 0
+    rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    col = np.concatenate([np.sort(rng.choice(50, int(L), replace=False)) for L in lens]).astype(np.int32)
+    A = workloads.CSR(m, 50, rp, col, np.ones(len(col), np.float32))
+    Bm = workloads.random_csr(rng, 50, 20, 0.2)
+    cap = 600
+    _, seg = _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=cap, segmentation=B_.SEG_MAXFILL)
+    assert seg[0]["r0"] == 0 and seg[-1]["r1"] == m and seg[-1]["sent_nnz1"] == rp[-1]
+    for a, b in zip(seg, seg[1:]):
+        assert b["r0"] == a["r1"] and b["nnz0"] == a["nnz1"] == rp[a["r1"]]
+    for t in seg:
+        r0, r1, q = t["r0"], t["r1"], t["sent_nnz1"] - t["nnz0"]
+        assert r1 > r0 and t["nnz0"] == rp[r0] and t["nnz1"] == rp[r1]
+        assert (r1 - r0 + 1) * 4 + 8 * q <= cap
+        if t is not seg[-1]:
+            assert rp[r1] <= t["sent_nnz1"] < rp[r1 + 1]  # ends inside row r1
+            # one more entry: either past the cap, or it would complete more rows
+            r1x = int(np.searchsorted(rp, t["sent_nnz1"] + 1, side="right")) - 1
+            assert (r1x - r0 + 1) * 4 + 8 * (q + 1) > cap

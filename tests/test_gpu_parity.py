@@ -585,3 +585,59 @@ def test_streamed_rows_bound(torch_gpu):
         C = aires.spgemm(plan)
         assert_match(C.rp, C.col, C.val, ref)
         C.free()
+
+
+# ------------------------------------- max-fill segments (the unaligned baseline)
+
+@pytest.mark.parametrize("c_on_host", [True, False])
+def test_maxfill_streamed(torch_gpu, c_on_host):
+    """Segments filled to their slot that end inside rows (Sec. III-A's
+    unaligned scheme): the same C as the oracle and as row blocks; every
+    partial row is copied back and sent again, which the byte counts show
+    exactly."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(5, n=60000)
+    ref = oracle.spgemm(A, B)
+    pA, pB = aires.to_pinned(A), aires.to_pinned(B)
+    budget = 1 << 32
+    say("max-fill streamed cfg5 n=60000 c_on_host=%s" % c_on_host)
+    out = {}
+    for seg in ("maxfill", "robw"):
+        with aires.tile_plan(pA, pB, budget, c_on_host=c_on_host, timing=True, max_tile_bytes=300_000,
+                             segmentation=seg) as plan:
+            tiles = aires.plan_tiles(plan)
+            C = aires.spgemm(plan)
+            torch_gpu.cuda.synchronize()
+            st = aires.plan_stats(plan)
+            ts = aires.plan_tile_stats(plan)
+            if c_on_host:
+                got = (C.rp.copy(), C.col.copy(), C.val.copy())
+                C.free()
+            else:
+                got = (C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy())
+        assert_match(*got, ref)
+        out[seg] = (tiles, st, ts)
+    tiles, st, ts = out["maxfill"]
+    nt = len(tiles)
+    carried = sum(t["sent_nnz1"] - t["nnz1"] for t in tiles)
+    assert nt >= 10 and carried > 0
+    assert st["resent_bytes"] == 8 * carried
+    assert st["h2d_bytes"] == A.nbytes() + B.nbytes() + 8 * (nt - 1) + 8 * carried
+    assert sum(t["resent_bytes"] for t in ts) == 8 * carried
+    assert st["merge_ms"] > 0 and all(t["merge_ms"] >= 0 for t in ts)
+    assert st["host_syncs"] == nt + sum(1 for t in tiles[:-1] if t["sent_nnz1"] > t["nnz1"])
+    assert out["robw"][1]["resent_bytes"] == 0 and out["robw"][1]["merge_ms"] == 0
+
+
+def test_maxfill_streamed_wide(torch_gpu):
+    """Max-fill segments of a wide product (column windows), C to host."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(3, n=20000)
+    ref = oracle.spgemm(A, B)
+    say("max-fill streamed wide cfg3 n=20000")
+    with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 34, c_on_host=True, max_tile_bytes=120_000,
+                         dense_max_cols=4096, window_grain_cols=4096, segmentation="maxfill") as plan:
+        assert aires.plan_info(plan).ntiles >= 5
+        C = aires.spgemm(plan)
+        assert_match(C.rp, C.col, C.val, ref)
+        C.free()
