@@ -599,6 +599,9 @@ def main():
                     help="--stream: A's values derived on the device from its pattern (Eq. 2) instead of copied")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the extra records of the default run (cfg2 in core, cfg5 streamed)")
+    ap.add_argument("--gather-probe-mib", type=int, default=0,
+                    help="first run a random 4-byte gather from an array of this many MiB (sub-line reads of "
+                         "known footprint for reading rocprofv3 FETCH_SIZE)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run one device copy of this many MiB (a known-size kernel for "
                          "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -623,6 +626,23 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.gather_probe_mib:
+        # a gather of known footprint: n random 4-byte reads from an array
+        # of gather_probe_mib MiB (index_select), for reading the counters
+        # of sub-line reads against the lines they touch
+        n_src = args.gather_probe_mib << 18
+        g = torch.Generator(device="cuda").manual_seed(23)
+        src = torch.ones(n_src, dtype=torch.float32, device="cuda")
+        idx = torch.randint(0, n_src, (n_src // 64,), generator=g, device="cuda")
+        out = torch.index_select(src, 0, idx)
+        torch.cuda.synchronize()
+        ix = idx.cpu().numpy()
+        print(json.dumps({"gather_probe": {"src_mib": args.gather_probe_mib, "reads": int(ix.size),
+                                           "distinct_64B_lines": int(np.unique(ix // 16).size),
+                                           "distinct_128B_lines": int(np.unique(ix // 32).size),
+                                           "index_bytes": int(ix.size * 8), "out_bytes": int(ix.size * 4)}}),
+              file=sys.stderr, flush=True)
+        del src, idx, out
     t0 = time.perf_counter()
     A, B = workloads.workload(args.workload)
     gen_s = time.perf_counter() - t0
