@@ -351,7 +351,10 @@ aires_status aires_spgemm_noalloc(aires_plan *plan, void *stream, int64_t *c_row
  * each finished C tile is copied on `d2h` into pinned host memory at the
  * running offset (opts->c_placement == AIRES_MEM_HOST_PINNED) or kept on
  * the device.  The host waits only for each tile's nnz, one tile behind.
- * Host C arrays are sized by the plan's C bound.  On return all work has
+ * C's arrays are sized by the plan's C bound; where that bound was only an
+ * estimate (AIRES_CBOUND_PAPER_EQ5) and C outgrows it, they are replaced by
+ * larger ones (by half again at least) and the entries so far moved over,
+ * within the budget when C is on the device.  On return all work has
  * completed and C is valid.
  * Errors: as aires_spgemm, plus AIRES_E_UNSUPPORTED if A is not pinned.
  */

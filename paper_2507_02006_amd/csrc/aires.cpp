@@ -1398,7 +1398,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     max_cb = std::max(max_cb, t.c_bound_entries);
     max_carry = std::max(max_carry, t.sent_nnz1 - t.nnz1);
   }
-  const int64_t cap = p->info.c_bound_entries;
+  int64_t cap = p->info.c_bound_entries;  // grows when the bound was only an estimate (Eq. 5)
 
   // output arrays
   int64_t* C_rp = nullptr;
@@ -1656,9 +1656,42 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     const int64_t nnz_t = end - base;
     p->trun[(size_t)t].nnz_c = nnz_t;
     p->trun[(size_t)t].products = cnt_host[3 * t + 2];
-    if (end > cap)
-      return fail(AIRES_E_CAPACITY, "C needs more than the planned bound of %lld entries (tile %lld)",
-                  (long long)cap, (long long)t);
+    if (end > cap) {
+      // The C bound was an estimate (Eq. 5 mode) and C's arrays are full:
+      // move the entries so far into larger ones (by half again at least).
+      const int64_t ncap = std::max<int64_t>(end, cap + cap / 2);
+      if (c_on_host) {
+        HIP_TRY(hipStreamSynchronize(sd));  // earlier tiles' copies into C have landed
+        int32_t* nc = nullptr;
+        float* nv = nullptr;
+        HIP_TRY(hipHostMalloc((void**)&nc, sizeof(int32_t) * (size_t)ncap, hipHostMallocDefault));
+        hb.v.push_back(nc);
+        HIP_TRY(hipHostMalloc((void**)&nv, sizeof(float) * (size_t)ncap, hipHostMallocDefault));
+        hb.v.push_back(nv);
+        std::memcpy(nc, C_col, sizeof(int32_t) * (size_t)base);
+        std::memcpy(nv, C_val, sizeof(float) * (size_t)base);
+        for (void* old : {(void*)C_col, (void*)C_val}) {
+          hb.v.erase(std::remove(hb.v.begin(), hb.v.end(), old), hb.v.end());
+          (void)hipHostFree(old);
+        }
+        C_col = nc;
+        C_val = nv;
+      } else {
+        int32_t* nc = nullptr;
+        float* nv = nullptr;
+        ST_TRY(ws.get_n(ncap, &nc));
+        ST_TRY(ws.get_n(ncap, &nv));
+        if (base > 0) {  // after the earlier tiles' numeric kernels on sc
+          HIP_TRY(hipMemcpyAsync(nc, C_col, sizeof(int32_t) * (size_t)base, hipMemcpyDeviceToDevice, sc));
+          HIP_TRY(hipMemcpyAsync(nv, C_val, sizeof(float) * (size_t)base, hipMemcpyDeviceToDevice, sc));
+        }
+        ws.give_back(C_col);
+        ws.give_back(C_val);
+        C_col = nc;
+        C_val = nv;
+      }
+      cap = ncap;
+    }
     if (c_on_host && nnz_t > S.ccap) {
       // the bound was an estimate (Eq. 5 mode): grow this slot, within the budget
       HIP_TRY(hipStreamWaitEvent(sc, ev_cfree[t % 2], 0));

@@ -641,3 +641,27 @@ def test_maxfill_streamed_wide(torch_gpu):
         C = aires.spgemm(plan)
         assert_match(C.rp, C.col, C.val, ref)
         C.free()
+
+
+@pytest.mark.parametrize("c_on_host", [True, False])
+def test_streamed_eq5_bound_grows(torch_gpu, c_on_host):
+    """The paper's Eq. 5 estimate as the C bound undershoots the square
+    product's C many times over: C's arrays grow as tiles complete and the
+    result still equals the oracle's."""
+    import paper_2507_02006_amd as aires
+    from paper_2507_02006_amd import _binding as B_
+    A, B = workloads.workload(3, n=20000)
+    ref = oracle.spgemm(A, B)
+    say("streamed Eq. 5 bound, square n=20000, c_on_host=%s" % c_on_host)
+    with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 34, c_on_host=c_on_host, timing=True,
+                         c_bound=B_.CBOUND_PAPER_EQ5, max_tile_bytes=100_000, dense_max_cols=4096,
+                         window_grain_cols=4096) as plan:
+        info = aires.plan_info(plan)
+        assert info.ntiles >= 4 and info.c_bound_entries * 4 < ref.nnz
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        if c_on_host:
+            assert_match(C.rp, C.col, C.val, ref)
+            C.free()
+        else:
+            assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
