@@ -333,6 +333,15 @@ def streamed(args):
                            out=pinned(torch.int64 if cfg["rp64"] else torch.int32), verbose=True)
     tA = (A.nrows, A.ncols) + hold[-1]
     gen_a = time.perf_counter() - t0
+    meta = None
+    if args.storage:
+        # A on storage: its arrays written once into a file, then each call
+        # reads every tile from it (direct I/O) before sending it
+        t1 = time.perf_counter()
+        meta = workloads.write_csr_file(os.path.join(args.storage, "aires_a_cfg%d.csr" % args.workload), A)
+        os.sync()
+        print("[stream] A written to %s in %.1f s" % (meta["path"], time.perf_counter() - t1), file=sys.stderr,
+              flush=True)
     for F in feats:
         t0 = time.perf_counter()
         B = workloads.features(n, F, cfg["rho"], seed=1000 + args.workload, out=pinned(torch.int32), verbose=True)
@@ -343,10 +352,16 @@ def streamed(args):
             for it in range(args.warmup + args.steps):
                 t1 = time.perf_counter()
                 a_in = tA[:4] + (None,) if args.sym_norm else tA
-                with aires.tile_plan(a_in, tB, int(budget * (1 << 30)), c_on_host=not args.c_on_device, timing=True,
-                                     max_tile_bytes=args.max_tile_mb << 20,
-                                     a_values="sym_norm" if args.sym_norm else "given",
-                                     c_bound=3 if args.c_bound == "rows" else 0, segmentation=seg) as plan:
+                if meta is not None:
+                    plan_cm = aires.tile_plan_file(meta, tB, int(budget * (1 << 30)), c_on_host=not args.c_on_device,
+                                                   timing=True, max_tile_bytes=args.max_tile_mb << 20,
+                                                   a_values="sym_norm" if args.sym_norm else "given")
+                else:
+                    plan_cm = aires.tile_plan(a_in, tB, int(budget * (1 << 30)), c_on_host=not args.c_on_device,
+                                              timing=True, max_tile_bytes=args.max_tile_mb << 20,
+                                              a_values="sym_norm" if args.sym_norm else "given",
+                                              c_bound=3 if args.c_bound == "rows" else 0, segmentation=seg)
+                with plan_cm as plan:
                     t2 = time.perf_counter()
                     info = aires.plan_info(plan)
                     C = aires.spgemm(plan)
@@ -381,7 +396,9 @@ def streamed(args):
                            "budget_gb": budget, "f": F, "nnz_a": A.nnz, "nnz_b": B.nnz, "segmentation": seg,
                            "a_values": "derived on the device (Eq. 2)" if args.sym_norm else "copied",
                            "c_placement": "device" if args.c_on_device else "pinned host",
-                           "c_bound": args.c_bound, "c_bound_entries": info.c_bound_entries,
+                           "c_bound": "rows" if meta is not None else args.c_bound,
+                           "c_bound_entries": info.c_bound_entries,
+                           "a_source": "file (direct I/O)" if meta is not None else "pinned host memory",
                            "products": st["products"], "nnz_c": st["nnz_c"], "tiles": info.ntiles,
                            "peak_device_gb": round(info.peak_bytes / 1e9, 2), "parallelism": "single GPU"},
                 "plan_ms": round(st["_plan_ms"], 2), "call_ms": round(st["_call_ms"], 2),
@@ -393,12 +410,16 @@ def streamed(args):
                 "h2d_gbs": round(st["h2d_bytes"] / max(st["h2d_ms"], 1e-9) / 1e6, 2),
                 "d2h_gbs": round(st["d2h_bytes"] / max(st["d2h_ms"], 1e-9) / 1e6, 2),
                 "resent_gb": round(st["resent_bytes"] / 1e9, 4), "merge_ms": round(st["merge_ms"], 2),
+                "storage_gb": round(st["storage_bytes"] / 1e9, 3), "storage_read_ms": round(st["storage_ms"], 2),
+                "storage_gbs": round(st["storage_bytes"] / max(st["storage_ms"], 1e-9) / 1e6, 2),
                 "host_syncs": st["host_syncs"],
                 "generation_s": round(gen_s, 2),
             }
             print(json.dumps(res), flush=True)
         del B, tB
         hold.pop()
+    if meta is not None:
+        os.unlink(meta["path"])
 
 
 def in_core_run(A, B, dA, dB, steps, warmup):
@@ -586,6 +607,9 @@ def main():
     ap.add_argument("--features", default="", help="--stream: comma-separated feature widths (the workload's)")
     ap.add_argument("--nodes", type=int, default=0, help="--stream: graph nodes (the workload's)")
     ap.add_argument("--max-tile-mb", type=int, default=0, help="--stream: cap on a tile's A bytes (0: none)")
+    ap.add_argument("--storage", default="",
+                    help="--stream: a directory; A's arrays are written to a file there and every call reads "
+                         "its tiles from that file (direct I/O) instead of pinned memory (c_bound rows)")
     ap.add_argument("--segmentation", default="robw",
                     help="--stream: comma-separated segmentations of A: robw (row blocks, Algorithm 1) and/or "
                          "maxfill (segments filled to the slot, partial rows copied back, packed on the host "

@@ -204,6 +204,23 @@ typedef struct aires_plan_opts {
                                    and given values                        */
 } aires_plan_opts;
 
+/*
+ * A held in a file (the storage tier of Sec. III-B: A on the SSD, brought
+ * to the host, then to the GPU).  The three CSR arrays are raw arrays in
+ * the file at the given byte offsets: row pointers (nrows + 1 of rp_type),
+ * column indices (nnz int32), values (nnz fp32; not read when A's values
+ * are derived, AIRES_AVALUES_SYM_NORM).  direct_io = 1 asks for reads that
+ * bypass the page cache (O_DIRECT, in whole 4 KiB blocks), falling back
+ * to ordinary reads where the filesystem refuses.
+ */
+typedef struct aires_file_csr {
+    int64_t nrows, ncols, nnz;
+    int32_t rp_type;            /* aires_idx                               */
+    int32_t direct_io;
+    const char *path;
+    int64_t row_ptr_offset, col_idx_offset, vals_offset;
+} aires_file_csr;
+
 /* Fill *o with defaults (struct_size set, validate 0, C on device). */
 aires_status aires_plan_opts_default(aires_plan_opts *o);
 
@@ -239,6 +256,24 @@ typedef struct aires_plan aires_plan;
 aires_status aires_tile_plan(const aires_csr *A, const aires_csr *B, uint64_t hbm_budget,
                              const aires_plan_opts *opts, aires_plan **out);
 
+/*
+ * aires_tile_plan_file -- the same plan for an A that stays in a file.  The
+ * planner reads A's row pointers (into pinned host memory the plan keeps)
+ * and nothing else, so the C bound must come from row pointers:
+ * opts->c_bound = AIRES_CBOUND_ROWS, DENSE or PAPER_EQ5, row blocks, no
+ * validation.  The plan is streamed (aires_spgemm / aires_stream_tiles):
+ * each tile's column indices and values are read from the file into one of
+ * two pinned staging buffers while earlier tiles copy and compute, then sent
+ * to the device as for a pinned-host A (Algorithm 2 with the first stage on
+ * storage).  The file stays open until aires_plan_destroy.
+ * Errors: AIRES_E_INVALID_ARG (NULL, bad offsets, file cannot be opened or
+ * is too short), AIRES_E_INVALID_CSR (row pointers do not run from 0 to
+ * nnz), AIRES_E_UNSUPPORTED (a C bound that needs A's columns, max-fill
+ * segments, validation), and the errors of aires_tile_plan.
+ */
+aires_status aires_tile_plan_file(const aires_file_csr *A, const aires_csr *B, uint64_t hbm_budget,
+                                  const aires_plan_opts *opts, aires_plan **out);
+
 typedef struct aires_plan_info {
     int64_t ntiles;
     int64_t m, k, n;            /* A is m x k, B is k x n                  */
@@ -255,6 +290,8 @@ typedef struct aires_plan_info {
                                    row count, entry count and C bound of
                                    different tiles would not fit one slot
                                    together                                */
+    int32_t a_in_file;          /* 1: A's entries are read from a file     */
+    int32_t _pad1;
 } aires_plan_info_t;            /* (the struct tag shares the query's name) */
 
 typedef struct aires_tile {
@@ -387,6 +424,10 @@ typedef struct aires_stats {
        the host time spent packing segments into the staging buffers      */
     int64_t resent_bytes;
     double merge_ms;
+    /* A in a file: bytes read from it for the tiles and the host time the
+       reads took (they run one tile ahead of the copies to the device)    */
+    int64_t storage_bytes;
+    double storage_ms;
 } aires_stats;
 
 /* Activation applied by aires_spmm. */
@@ -460,6 +501,8 @@ typedef struct aires_tile_stats {
                                    the next one (in d2h_bytes here)        */
     double merge_ms;            /* max-fill: host time packing this
                                    segment's staging buffer                */
+    double storage_ms;          /* A in a file: host time reading this
+                                   tile's entries                          */
 } aires_tile_stats;
 
 /* Errors: AIRES_E_INVALID_ARG (NULL, t out of range), AIRES_E_HIP. */

@@ -20,7 +20,7 @@ from dataclasses import dataclass
 
 from . import _binding as B_
 
-__all__ = ["tile_plan", "spgemm", "spmm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
+__all__ = ["tile_plan", "tile_plan_file", "spgemm", "spmm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
            "plan_tile_stats", "spgemm_noalloc", "Plan", "Output", "AiresError", "to_device", "to_pinned"]
 
 AiresError = B_.AiresError
@@ -57,6 +57,42 @@ class Plan:
 
     def __exit__(self, *a):
         self.close()
+
+
+def _opts(lib, **kw):
+    o = B_.PlanOpts()
+    B_.check(lib.aires_plan_opts_default(ctypes.byref(o)), "aires_plan_opts_default")
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def tile_plan_file(A, B, hbm_budget: int = 0, *, c_on_host: bool = True, c_bound: int = B_.CBOUND_ROWS,
+                   timing: bool = False, max_tile_bytes: int = 0, a_values: str = "given", direct_io: bool = True,
+                   torch_allocator: bool = True, device: int = 0) -> Plan:
+    """Plan C = A * B with A's arrays in a file (aires_tile_plan_file).  A is
+    a dict with nrows, ncols, nnz, rp_dtype ("int32"/"int64"), path and the
+    byte offsets row_ptr_offset, col_idx_offset, vals_offset (as written by
+    ``workloads.write_csr_file``); B as for tile_plan.  The plan streams:
+    each tile is read from the file into pinned staging, then sent."""
+    lib = B_.load()
+    path = A["path"].encode()
+    fa = B_.FileCsr(int(A["nrows"]), int(A["ncols"]), int(A["nnz"]),
+                    B_.IDX_I64 if A["rp_dtype"] == "int64" else B_.IDX_I32, int(bool(direct_io)), path,
+                    int(A["row_ptr_offset"]), int(A["col_idx_offset"]), int(A["vals_offset"]))
+    b = B_.make_csr(*_parts(B))
+    if a_values not in ("given", "sym_norm"):
+        raise ValueError("a_values must be 'given' or 'sym_norm'")
+    o = _opts(lib, c_placement=B_.MEM_HOST_PINNED if c_on_host else B_.MEM_DEVICE, c_bound=c_bound,
+              timing=int(timing), max_tile_bytes=max_tile_bytes,
+              a_values=B_.AVALUES_SYM_NORM if a_values == "sym_norm" else B_.AVALUES_GIVEN)
+    alloc = B_.TorchAllocator(device) if torch_allocator else None
+    if alloc is not None:
+        o.allocator = ctypes.pointer(alloc.struct)
+    h = ctypes.c_void_p()
+    B_.check(lib.aires_tile_plan_file(ctypes.byref(fa), ctypes.byref(b), int(hbm_budget), ctypes.byref(o),
+                                      ctypes.byref(h)), "aires_tile_plan_file")
+    return Plan(h.value, (fa, path), B, alloc, o)
 
 
 def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: bool = False,
@@ -131,6 +167,8 @@ class Info:
     a_streamed: bool
     c_on_host: bool
     part_budget: int
+    a_in_file: bool
+    _pad1: int = 0
 
 
 def plan_info(plan: Plan) -> Info:

@@ -62,7 +62,8 @@ class PlanOpts(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [(n, c_i64) for n in ("ntiles", "m", "k", "n", "budget", "b_bytes", "a_bytes", "tile_budget",
                                      "peak_bytes", "c_bound_entries")] + \
-               [("a_streamed", c_i32), ("c_on_host", c_i32), ("part_budget", c_i64)]
+               [("a_streamed", c_i32), ("c_on_host", c_i32), ("part_budget", c_i64), ("a_in_file", c_i32),
+                ("_pad1", c_i32)]
 
 
 class Tile(ctypes.Structure):
@@ -75,7 +76,7 @@ class Stats(ctypes.Structure):
                [(n, c_dbl) for n in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "h2d_ms",
                                      "d2h_ms", "total_ms")] + \
                [("numeric_launches", c_i64), ("kind_ms", (c_dbl * 8) * 2), ("pipeline_ms", c_dbl),
-                ("resent_bytes", c_i64), ("merge_ms", c_dbl)]
+                ("resent_bytes", c_i64), ("merge_ms", c_dbl), ("storage_bytes", c_i64), ("storage_ms", c_dbl)]
 
 
 class TileStats(ctypes.Structure):
@@ -83,7 +84,13 @@ class TileStats(ctypes.Structure):
                [(n, c_dbl) for n in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "h2d_ms",
                                      "d2h_ms", "h2d_begin_ms", "h2d_end_ms", "compute_begin_ms",
                                      "compute_end_ms", "d2h_begin_ms", "d2h_end_ms")] + \
-               [("resent_bytes", c_i64), ("merge_ms", c_dbl)]
+               [("resent_bytes", c_i64), ("merge_ms", c_dbl), ("storage_ms", c_dbl)]
+
+
+class FileCsr(ctypes.Structure):
+    _fields_ = [("nrows", c_i64), ("ncols", c_i64), ("nnz", c_i64), ("rp_type", c_i32), ("direct_io", c_i32),
+                ("path", ctypes.c_char_p), ("row_ptr_offset", c_i64), ("col_idx_offset", c_i64),
+                ("vals_offset", c_i64)]
 
 
 _lib = None
@@ -110,6 +117,7 @@ def load() -> ctypes.CDLL:
         "aires_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "aires_plan_opts_default": (ctypes.c_int, [P(PlanOpts)]),
         "aires_tile_plan": (ctypes.c_int, [P(Csr), P(Csr), c_u64, P(PlanOpts), P(c_vp)]),
+        "aires_tile_plan_file": (ctypes.c_int, [P(FileCsr), P(Csr), c_u64, P(PlanOpts), P(c_vp)]),
         "aires_plan_info": (ctypes.c_int, [c_vp, P(PlanInfo)]),
         "aires_plan_info_get": (ctypes.c_int, [c_vp, P(PlanInfo)]),
         "aires_plan_tile_stats": (ctypes.c_int, [c_vp, c_i64, P(TileStats)]),

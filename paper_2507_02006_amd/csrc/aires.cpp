@@ -18,6 +18,9 @@
 #include <thread>
 #include <vector>
 
+#include <fcntl.h>
+#include <unistd.h>
+
 #include "kernels.h"
 #include "scratch.h"
 
@@ -184,6 +187,100 @@ struct OutOwner {
 
 // ------------------------------------------------------------------- plan
 
+namespace {
+
+// A's column and value arrays in a file (the storage tier): read per tile
+// into pinned staging buffers.  With direct I/O the reads bypass the page
+// cache, cover whole 4 KiB blocks around the range and land in a bounce
+// buffer of ordinary memory (the runtime's pinned pages cannot be handed to
+// the block layer), from which the same threads copy them out.
+struct FileSrc {
+  int fd = -1;
+  bool direct = false;
+  int64_t col_off = 0, val_off = 0;
+  void* rp_host = nullptr;  // A's row pointers, read at planning (pinned when possible)
+  bool rp_pinned = false;
+  char* bounce = nullptr;
+  size_t bounce_cap = 0;
+  ~FileSrc() {
+    if (fd >= 0) close(fd);
+    if (rp_host) {
+      if (rp_pinned) (void)hipHostFree(rp_host);
+      else std::free(rp_host);
+    }
+    std::free(bounce);
+  }
+};
+
+constexpr int64_t kIoAlign = 4096;
+
+// Reads file bytes [off, off + len) into dst; *shift receives where they
+// start in dst (always 0 now; kept for the callers' buffer layout).
+// Ranges of 8 MiB or more are read by several host threads.
+aires_status file_read(FileSrc& f, int64_t off, int64_t len, char* dst, int64_t* shift) {
+  const int64_t a0 = f.direct ? off & ~(kIoAlign - 1) : off;
+  const int64_t a1 = f.direct ? (off + len + kIoAlign - 1) & ~(kIoAlign - 1) : off + len;
+  *shift = 0;
+  if (len <= 0) return AIRES_OK;
+  const int64_t total = a1 - a0;
+  char* buf = dst;
+  if (f.direct) {
+    if ((size_t)total > f.bounce_cap) {
+      std::free(f.bounce);
+      f.bounce_cap = (size_t)total;
+      f.bounce = static_cast<char*>(std::aligned_alloc((size_t)kIoAlign, f.bounce_cap));
+      if (!f.bounce) {
+        f.bounce_cap = 0;
+        return fail(AIRES_E_OOM, "host allocation of %lld bytes failed", (long long)total);
+      }
+    }
+    buf = f.bounce;
+  }
+  const int nt = total >= (int64_t(8) << 20) ? 8 : 1;
+  std::vector<int> err(nt, 0);
+  std::vector<int64_t> got(nt, 0);
+  auto part = [&](int i) {
+    int64_t lo = total * i / nt, hi = total * (i + 1) / nt;
+    if (f.direct) {
+      lo &= ~(kIoAlign - 1);
+      if (i + 1 < nt) hi &= ~(kIoAlign - 1);
+    }
+    for (int64_t p = lo; p < hi;) {
+      const ssize_t r = pread(f.fd, buf + p, (size_t)(hi - p), (off_t)(a0 + p));
+      if (r < 0) { err[i] = errno; return; }
+      if (r == 0) break;  // end of file
+      p += r;
+      got[i] = p - lo;
+    }
+    if (f.direct) {  // this thread's share of the wanted bytes, out of the bounce buffer
+      const int64_t w0 = std::max(lo, off - a0), w1 = std::min(lo + got[i], off - a0 + len);
+      if (w1 > w0) std::memcpy(dst + (w0 - (off - a0)), buf + w0, (size_t)(w1 - w0));
+    }
+  };
+  if (nt == 1) {
+    part(0);
+  } else {
+    std::vector<std::thread> th;
+    for (int i = 0; i < nt; ++i) th.emplace_back(part, i);
+    for (auto& x : th) x.join();
+  }
+  for (int i = 0; i < nt; ++i)
+    if (err[i]) return fail(AIRES_E_INVALID_ARG, "reading A's file failed: %s", strerror(err[i]));
+  // the bytes asked for must all be there (a direct read may stop at the
+  // end of the file inside the last block)
+  int64_t have = 0;
+  for (int i = 0; i < nt; ++i) {
+    int64_t lo = total * i / nt;
+    if (f.direct) lo &= ~(kIoAlign - 1);
+    have = std::max(have, lo + got[i]);
+  }
+  if (have < (off - a0) + len)
+    return fail(AIRES_E_INVALID_ARG, "A's file ends before byte %lld", (long long)(off + len));
+  return AIRES_OK;
+}
+
+}  // namespace
+
 struct aires_plan {
   aires_csr A, B;
   aires_plan_opts opts;
@@ -193,6 +290,7 @@ struct aires_plan {
   aires_plan_info_t info;
   aires_stats stats;
   int busy = 0;
+  std::unique_ptr<FileSrc> file;   // A's entries in a file (aires_tile_plan_file)
   // kernel configuration
   kern::BinThresholds th;
   int wide = 0;
@@ -204,7 +302,7 @@ struct aires_plan {
   int64_t split_cap = 0;           // rows with dense slots for the split bin
   int64_t split_ws = 0;            // bytes of those slots
   // per-tile counts of the last call (products, nnz(C), bytes copied)
-  struct TileRun { int64_t products, nnz_c, h2d_bytes, d2h_bytes, resent_bytes; double merge_ms; };
+  struct TileRun { int64_t products, nnz_c, h2d_bytes, d2h_bytes, resent_bytes; double merge_ms, storage_ms; };
   std::vector<TileRun> trun;
   // per tile, indices into ev of: copy in begin/end, compute begin/end,
   // copy out begin/end (-1: none); times are taken from ev[ev_base]
@@ -563,13 +661,25 @@ aires_status aires_plan_opts_default(aires_plan_opts* o) {
   return AIRES_OK;
 }
 
-aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hbm_budget,
-                             const aires_plan_opts* opts, aires_plan** out) {
+}  // extern "C"
+
+namespace {
+
+// The planner.  file != nullptr: A's entries are in that file (A->col_idx
+// and A->vals are NULL; its row pointers are in host memory); the plan
+// takes the file over when it succeeds.
+aires_status plan_impl(const aires_csr* A, const aires_csr* B, uint64_t hbm_budget, const aires_plan_opts* opts,
+                       aires_plan** out, std::unique_ptr<FileSrc>* file) {
   if (!out) return fail(AIRES_E_INVALID_ARG, "out is NULL");
   if (opts && opts->struct_size != sizeof(aires_plan_opts))
     return fail(AIRES_E_INVALID_ARG, "opts.struct_size %u != %zu", opts->struct_size, sizeof(aires_plan_opts));
   const bool a_sym_norm = opts && opts->a_values == AIRES_AVALUES_SYM_NORM;
-  ST_TRY(check_csr_desc(A, "A", !a_sym_norm));
+  if (file) {
+    if (!A || !A->row_ptr || A->nrows < 0 || A->ncols < 0 || A->nnz < 0)
+      return fail(AIRES_E_INVALID_ARG, "A's descriptor is incomplete");
+  } else {
+    ST_TRY(check_csr_desc(A, "A", !a_sym_norm));
+  }
   ST_TRY(check_csr_desc(B, "B"));
   if (opts && opts->a_values != AIRES_AVALUES_GIVEN && opts->a_values != AIRES_AVALUES_SYM_NORM)
     return fail(AIRES_E_INVALID_ARG, "opts.a_values %d invalid", opts->a_values);
@@ -599,6 +709,11 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
     return fail(AIRES_E_UNSUPPORTED,
                 "max-fill segments need A in pinned host memory with given values (and no Algorithm 1 "
                 "planning mode or row cap)");
+  if (file && (o.segmentation != AIRES_SEG_ROBW || o.c_bound == AIRES_CBOUND_PRODUCTS || o.validate ||
+               o.m_a_bytes > 0))
+    return fail(AIRES_E_UNSUPPORTED,
+                "a file-backed A is planned from its row pointers alone: row blocks with c_bound ROWS, DENSE "
+                "or PAPER_EQ5, no validation, no Algorithm 1 planning mode");
   if (o.validate) {
     if (A->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*A, "A", !a_sym_norm));
     if (B->mem != AIRES_MEM_DEVICE) ST_TRY(validate_host(*B, "B"));
@@ -910,9 +1025,70 @@ aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hb
   p->info.ntiles = (int64_t)p->tiles.size();
   p->info.part_budget = part_budget;
   p->info.peak_bytes = resident + nslots * peak_slot;
+  if (file) {
+    p->file = std::move(*file);
+    p->info.a_in_file = 1;
+  }
   std::memset(&p->stats, 0, sizeof p->stats);
   *out = p;
   return AIRES_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+aires_status aires_tile_plan(const aires_csr* A, const aires_csr* B, uint64_t hbm_budget,
+                             const aires_plan_opts* opts, aires_plan** out) {
+  return plan_impl(A, B, hbm_budget, opts, out, nullptr);
+}
+
+aires_status aires_tile_plan_file(const aires_file_csr* A, const aires_csr* B, uint64_t hbm_budget,
+                                  const aires_plan_opts* opts, aires_plan** out) {
+  if (!A || !A->path || !out) return fail(AIRES_E_INVALID_ARG, "NULL argument");
+  if (A->nrows < 0 || A->ncols < 0 || A->nnz < 0) return fail(AIRES_E_DIM, "A has a negative size");
+  if (A->rp_type != AIRES_IDX_I32 && A->rp_type != AIRES_IDX_I64)
+    return fail(AIRES_E_INVALID_ARG, "A.rp_type %d invalid", A->rp_type);
+  if (A->rp_type == AIRES_IDX_I32 && A->nnz > INT32_MAX)
+    return fail(AIRES_E_OVERFLOW, "A.nnz needs int64 row pointers");
+  if (A->ncols > INT32_MAX) return fail(AIRES_E_OVERFLOW, "A.ncols exceeds int32 column indices");
+  if (A->row_ptr_offset < 0 || A->col_idx_offset < 0 || A->vals_offset < 0)
+    return fail(AIRES_E_INVALID_ARG, "negative file offset");
+  auto f = std::make_unique<FileSrc>();
+  f->fd = open(A->path, O_RDONLY | (A->direct_io ? O_DIRECT : 0));
+  if (f->fd >= 0 && A->direct_io) f->direct = true;
+  if (f->fd < 0 && A->direct_io) f->fd = open(A->path, O_RDONLY);  // no direct I/O on this filesystem
+  if (f->fd < 0) return fail(AIRES_E_INVALID_ARG, "cannot open %s: %s", A->path, strerror(errno));
+  f->col_off = A->col_idx_offset;
+  f->val_off = A->vals_offset;
+  // A's row pointers to host memory (pinned where a device is present:
+  // each tile copies its slice from them)
+  const int64_t s = A->rp_type == AIRES_IDX_I64 ? 8 : 4;
+  const int64_t rp_len = (A->nrows + 1) * s;
+  const size_t cap = (size_t)(rp_len + 2 * kIoAlign);
+  if (hipHostMalloc(&f->rp_host, cap, hipHostMallocDefault) == hipSuccess) {
+    f->rp_pinned = true;
+  } else {
+    (void)hipGetLastError();
+    f->rp_host = std::aligned_alloc((size_t)kIoAlign, (cap + kIoAlign - 1) / kIoAlign * kIoAlign);
+    if (!f->rp_host) return fail(AIRES_E_OOM, "host allocation of %zu bytes failed", cap);
+  }
+  int64_t shift = 0;
+  ST_TRY(file_read(*f, A->row_ptr_offset, rp_len, static_cast<char*>(f->rp_host), &shift));
+  if (shift) std::memmove(f->rp_host, static_cast<char*>(f->rp_host) + shift, (size_t)rp_len);
+  aires_csr a{};
+  a.nrows = A->nrows;
+  a.ncols = A->ncols;
+  a.nnz = A->nnz;
+  a.rp_type = A->rp_type;
+  a.mem = AIRES_MEM_HOST_PINNED;
+  a.row_ptr = f->rp_host;
+  const int64_t last = s == 8 ? static_cast<const int64_t*>(f->rp_host)[A->nrows]
+                              : (int64_t) static_cast<const int32_t*>(f->rp_host)[A->nrows];
+  const int64_t first = s == 8 ? static_cast<const int64_t*>(f->rp_host)[0]
+                               : (int64_t) static_cast<const int32_t*>(f->rp_host)[0];
+  if (first != 0 || last != A->nnz) return fail(AIRES_E_INVALID_CSR, "A's row pointers in the file do not end at nnz");
+  return plan_impl(&a, B, hbm_budget, opts, out, &f);
 }
 
 aires_status aires_plan_info(const aires_plan* plan, aires_plan_info_t* info) {
@@ -1160,7 +1336,7 @@ aires_status begin_call(aires_plan* p, aires_csr_out* C) {
     return fail(AIRES_E_STATE, "output descriptor is not zeroed (free it first)");
   std::memset(&p->stats, 0, sizeof p->stats);
   p->stats.ntiles = (int64_t)p->tiles.size();
-  p->trun.assign(p->tiles.size(), aires_plan::TileRun{0, 0, 0, 0, 0, 0.0});
+  p->trun.assign(p->tiles.size(), aires_plan::TileRun{0, 0, 0, 0, 0, 0.0, 0.0});
   reset_timing(p);
   std::array<int, aires_plan::T_NEV> none;
   none.fill(-1);
@@ -1391,6 +1567,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   DevPool ws(p->alloc, sc, p->budget - borrowed_device_bytes(p));
   const int64_t nt = (int64_t)p->tiles.size();
   const bool maxfill = p->opts.segmentation == AIRES_SEG_MAXFILL;
+  FileSrc* file = p->file.get();
   int64_t max_rows = 1, max_q = 1, max_cb = 1, max_carry = 1;
   for (const auto& t : p->tiles) {
     max_rows = std::max(max_rows, t.r1 - t.r0);
@@ -1475,13 +1652,19 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   float* stage_val[2] = {nullptr, nullptr};
   int32_t* carry_col = nullptr;
   float* carry_val = nullptr;
-  if (maxfill) {
+  // (A in a file: the staging buffers take each tile's entries as read,
+  // with room for the whole 4 KiB blocks of direct reads)
+  int64_t shift_col[2] = {0, 0}, shift_val[2] = {0, 0};
+  if (maxfill || file) {
+    const size_t sb = sizeof(int32_t) * (size_t)max_q + (file ? 2 * kIoAlign : 0);
     for (int b = 0; b < 2; ++b) {
-      HIP_TRY(hipHostMalloc((void**)&stage_col[b], sizeof(int32_t) * (size_t)max_q, hipHostMallocDefault));
+      HIP_TRY(hipHostMalloc((void**)&stage_col[b], sb, hipHostMallocDefault));
       hb.v.push_back(stage_col[b]);
-      HIP_TRY(hipHostMalloc((void**)&stage_val[b], sizeof(float) * (size_t)max_q, hipHostMallocDefault));
+      HIP_TRY(hipHostMalloc((void**)&stage_val[b], sb, hipHostMallocDefault));
       hb.v.push_back(stage_val[b]);
     }
+  }
+  if (maxfill) {
     HIP_TRY(hipHostMalloc((void**)&carry_col, sizeof(int32_t) * (size_t)max_carry, hipHostMallocDefault));
     hb.v.push_back(carry_col);
     HIP_TRY(hipHostMalloc((void**)&carry_val, sizeof(float) * (size_t)max_carry, hipHostMallocDefault));
@@ -1577,10 +1760,32 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     return AIRES_OK;
   };
 
+  // A in a file: read tile t's entries into its staging buffer (the
+  // buffer's previous copy, tile t-2's, must be done)
+  auto read_tile = [&](int64_t t) -> aires_status {
+    const aires_tile& T = p->tiles[(size_t)t];
+    const int b = (int)(t % 2);
+    if (t >= 2) HIP_TRY(hipEventSynchronize(ev_in[(size_t)t - 2]));
+    const auto t0 = std::chrono::steady_clock::now();
+    const int64_t q = T.nnz1 - T.nnz0;
+    ST_TRY(file_read(*file, file->col_off + 4 * T.nnz0, 4 * q, reinterpret_cast<char*>(stage_col[b]), &shift_col[b]));
+    p->stats.storage_bytes += 4 * q;
+    if (!sym_norm) {
+      ST_TRY(file_read(*file, file->val_off + 4 * T.nnz0, 4 * q, reinterpret_cast<char*>(stage_val[b]),
+                       &shift_val[b]));
+      p->stats.storage_bytes += 4 * q;
+    }
+    const double ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    p->stats.storage_ms += ms;
+    p->trun[(size_t)t].storage_ms = ms;
+    return AIRES_OK;
+  };
+
   auto issue_h2d = [&](int64_t t) -> aires_status {
     const aires_tile& T = p->tiles[(size_t)t];
     Slot& S = slot[t % 2];
     if (maxfill) ST_TRY(pack_segment(t));
+    if (file) ST_TRY(read_tile(t));
     if (t >= 2) HIP_TRY(hipStreamWaitEvent(sh, ev_done[(size_t)t - 2], 0));
     th.tile = (int)t;
     const int ea = th.record();
@@ -1588,6 +1793,10 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
     const int64_t k = T.r1 - T.r0, q = T.sent_nnz1 - T.nnz0;
     const int32_t* src_col = maxfill ? stage_col[t % 2] : A.col_idx + T.nnz0;
     const float* src_val = maxfill ? stage_val[t % 2] : A.vals + T.nnz0;
+    if (file) {
+      src_col = reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(stage_col[t % 2]) + shift_col[t % 2]);
+      src_val = reinterpret_cast<const float*>(reinterpret_cast<const char*>(stage_val[t % 2]) + shift_val[t % 2]);
+    }
     if (!sym_norm)
       HIP_TRY(hipMemcpyAsync(S.arp, static_cast<const char*>(A.row_ptr) + T.r0 * sA, (size_t)(k + 1) * sA,
                              hipMemcpyHostToDevice, sh));
@@ -1831,7 +2040,7 @@ aires_status aires_spgemm_noalloc(aires_plan* plan, void* stream, int64_t* c_row
   HIP_TRY(aires::scratch_address(&base));
   std::memset(&plan->stats, 0, sizeof plan->stats);
   plan->stats.ntiles = (int64_t)plan->tiles.size();
-  plan->trun.assign(plan->tiles.size(), aires_plan::TileRun{0, 0, 0, 0, 0, 0.0});
+  plan->trun.assign(plan->tiles.size(), aires_plan::TileRun{0, 0, 0, 0, 0, 0.0, 0.0});
   reset_timing(plan);
   std::array<int, aires_plan::T_NEV> none;
   none.fill(-1);
@@ -1928,6 +2137,7 @@ aires_status aires_plan_tile_stats(const aires_plan* plan, int64_t t, aires_tile
     ts->d2h_bytes = r.d2h_bytes;
     ts->resent_bytes = r.resent_bytes;
     ts->merge_ms = r.merge_ms;
+    ts->storage_ms = r.storage_ms;
   }
   if (!plan->ev.empty()) {
     HIP_TRY(hipEventSynchronize(plan->ev.back()));

@@ -378,3 +378,71 @@ def test_maxfill_segments_fill_and_cover(seed):
             # one more entry: either past the cap, or it would complete more rows
             r1x = int(np.searchsorted(rp, t["sent_nnz1"] + 1, side="right")) - 1
             assert (r1x - r0 + 1) * 4 + 8 * (q + 1) > cap
+
+
+def _plan_file(meta, Bm, budget, **opts):
+    lib = B_.load()
+    o = B_.PlanOpts()
+    lib.aires_plan_opts_default(ctypes.byref(o))
+    for k, v in opts.items():
+        setattr(o, k, v)
+    fa = B_.FileCsr(meta["nrows"], meta["ncols"], meta["nnz"], B_.IDX_I64 if meta["rp_dtype"] == "int64" else
+                    B_.IDX_I32, int(meta.get("direct_io", 0)), meta["path"].encode(), meta["row_ptr_offset"],
+                    meta["col_idx_offset"], meta["vals_offset"])
+    b = _pinned_desc(Bm)
+    h = ctypes.c_void_p()
+    st = lib.aires_tile_plan_file(ctypes.byref(fa), ctypes.byref(b), int(budget), ctypes.byref(o), ctypes.byref(h))
+    if st != 0:
+        raise aires.AiresError(st, "aires_tile_plan_file")
+    info = B_.PlanInfo()
+    lib.aires_plan_info(h, ctypes.byref(info))
+    tiles = []
+    for t in range(info.ntiles):
+        x = B_.Tile()
+        lib.aires_plan_tile(h, t, ctypes.byref(x))
+        tiles.append({f: getattr(x, f) for f, _ in B_.Tile._fields_})
+    lib.aires_plan_destroy(h)
+    return info, tiles
+
+
+@pytest.mark.parametrize("rp64", [False, True])
+def test_file_plan_equals_memory_plan(tmp_path, rp64):
+    """A's arrays in a file (aligned raw arrays): the planner reads its row
+    pointers and cuts the same row blocks, with the same C bound, as for
+    the same A in host memory; direct I/O or not."""
+    A, Bm = workloads.workload(5, n=6000)
+    if not rp64:
+        A = workloads.CSR(A.nrows, A.ncols, A.rp.astype(np.int32), A.col, A.val)
+    meta = workloads.write_csr_file(str(tmp_path / "a.csr"), A)
+    kw = dict(c_placement=B_.MEM_HOST_PINNED, c_bound=B_.CBOUND_ROWS, max_tile_bytes=40_000)
+    budget = Bm.nbytes() + (16 << 20)
+    info_m, tiles_m = _plan_tiles(A, Bm, budget, **kw)
+    for direct in (0, 1):
+        info_f, tiles_f = _plan_file(dict(meta, direct_io=direct), Bm, budget, **kw)
+        assert tiles_f == tiles_m and len(tiles_f) > 5
+        assert info_f.a_in_file == 1 and info_m.a_in_file == 0
+        assert info_f.c_bound_entries == info_m.c_bound_entries and info_f.peak_bytes == info_m.peak_bytes
+
+
+def test_file_plan_errors(tmp_path):
+    A, Bm = workloads.workload(5, n=3000)
+    meta = workloads.write_csr_file(str(tmp_path / "a.csr"), A)
+    budget = Bm.nbytes() + (16 << 20)
+    rows = dict(c_placement=B_.MEM_HOST_PINNED, c_bound=B_.CBOUND_ROWS)
+    with pytest.raises(aires.AiresError) as e:  # the exact bound needs A's columns
+        _plan_file(meta, Bm, budget, c_placement=B_.MEM_HOST_PINNED)
+    assert e.value.status == B_.E_UNSUPPORTED
+    with pytest.raises(aires.AiresError) as e:
+        _plan_file(dict(meta, path=str(tmp_path / "missing")), Bm, budget, **rows)
+    assert e.value.status == B_.E_INVALID_ARG
+    with pytest.raises(aires.AiresError) as e:  # row pointers that do not end at nnz
+        _plan_file(dict(meta, nnz=meta["nnz"] + 1), Bm, budget, **rows)
+    assert e.value.status == B_.E_INVALID_CSR
+    short = tmp_path / "short.csr"
+    short.write_bytes((tmp_path / "a.csr").read_bytes()[:meta["row_ptr_offset"] + 100])
+    with pytest.raises(aires.AiresError) as e:
+        _plan_file(dict(meta, path=str(short)), Bm, budget, **rows)
+    assert e.value.status == B_.E_INVALID_ARG and "ends before" in str(e.value)
+    with pytest.raises(aires.AiresError) as e:
+        _plan_file(meta, Bm, budget, segmentation=B_.SEG_MAXFILL, **rows)
+    assert e.value.status == B_.E_UNSUPPORTED

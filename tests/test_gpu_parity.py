@@ -665,3 +665,37 @@ def test_streamed_eq5_bound_grows(torch_gpu, c_on_host):
             C.free()
         else:
             assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
+
+
+# ------------------------------------------------------- A on storage (a file)
+
+@pytest.mark.parametrize("direct,c_on_host,values", [(1, True, "given"), (0, False, "given"), (1, True, "sym_norm")])
+def test_storage_tier_streamed(torch_gpu, tmp_path, direct, c_on_host, values):
+    """A's arrays in a file: each tile is read into pinned staging (direct
+    I/O or the page cache), then streamed as from pinned memory; the same C
+    as the oracle, and every byte of A read exactly once."""
+    import paper_2507_02006_amd as aires
+    from paper_2507_02006_amd import _binding as B_
+    A, B = workloads.workload(5, n=60000)
+    ref = oracle.spgemm(A, B)
+    meta = workloads.write_csr_file(str(tmp_path / "a.csr"), A)
+    budget = B.nbytes() + (24 << 20) + 8 * (A.nrows + 1) + 2 * 3_000_000
+    say("storage tier cfg5 n=60000 direct=%d c_on_host=%s values=%s" % (direct, c_on_host, values))
+    with aires.tile_plan_file(meta, aires.to_pinned(B), budget if c_on_host else 1 << 32, c_on_host=c_on_host,
+                              timing=True, direct_io=bool(direct), max_tile_bytes=200_000, a_values=values) as plan:
+        info = aires.plan_info(plan)
+        assert info.a_in_file and info.ntiles >= 5
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        st = aires.plan_stats(plan)
+        ts = aires.plan_tile_stats(plan)
+        if c_on_host:
+            assert_match(C.rp, C.col, C.val, ref)
+            C.free()
+        else:
+            assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
+    per_entry = 8 if values == "given" else 4
+    assert st["storage_bytes"] == per_entry * A.nnz
+    assert st["storage_ms"] > 0 and sum(t["storage_ms"] for t in ts) == pytest.approx(st["storage_ms"])
+    if values == "given":
+        assert st["h2d_bytes"] == A.nbytes() + B.nbytes() + 8 * (info.ntiles - 1)

@@ -181,3 +181,23 @@ def random_csr(rng: np.random.Generator, m: int, n: int, density: float,
     np.add.at(rp, rows + 1, 1)
     rp = np.cumsum(rp)
     return CSR(m, n, rp if rp64 else rp.astype(np.int32), cols.astype(np.int32), v)
+
+
+def write_csr_file(path: str, M: CSR, align: int = 4096) -> dict:
+    """Write M's three CSR arrays as raw arrays into one file, each starting
+    at a multiple of `align` bytes; returns the descriptor fields of
+    aires_file_csr (path, sizes, row-pointer width, byte offsets)."""
+    offs = {}
+    pos = 0
+    with open(path, "wb") as f:
+        for name, arr in (("row_ptr_offset", M.rp), ("col_idx_offset", M.col), ("vals_offset", M.val)):
+            pad = (-pos) % align
+            if pad:
+                f.write(b"\0" * pad)
+                pos += pad
+            offs[name] = pos
+            a = np.ascontiguousarray(arr)
+            f.write(memoryview(a).cast("B"))
+            pos += a.nbytes
+    return dict(path=path, nrows=M.nrows, ncols=M.ncols, nnz=M.nnz, rp_dtype=str(M.rp.dtype), **offs)
+
