@@ -202,6 +202,11 @@ typedef struct aires_plan_opts {
     int32_t segmentation;       /* aires_segmentation, default ROBW;
                                    MAXFILL needs A in pinned host memory
                                    and given values                        */
+    int64_t bitmap_cache_bytes; /* 0: default (a fifth of what the plan
+                                   leaves of the budget, at most 32 GiB);
+                                   > 0: at most this many bytes of kept
+                                   symbolic bitmaps (items that do not fit
+                                   are marked again in the numeric phase) */
 } aires_plan_opts;
 
 /*

@@ -56,7 +56,7 @@ class PlanOpts(ctypes.Structure):
                 ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64),
                 ("keep_bitmap_products", c_i64), ("split_min_products", c_i64),
                 ("split_max_rows", c_i64), ("window_pool_bytes", c_i64), ("a_values", c_i32),
-                ("segmentation", c_i32)]
+                ("segmentation", c_i32), ("bitmap_cache_bytes", c_i64)]
 
 
 class PlanInfo(ctypes.Structure):

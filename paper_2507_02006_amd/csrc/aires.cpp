@@ -700,8 +700,8 @@ aires_status plan_impl(const aires_csr* A, const aires_csr* B, uint64_t hbm_budg
     return fail(AIRES_E_INVALID_ARG, "opts.c_placement %d invalid", o.c_placement);
   if (o.c_bound < AIRES_CBOUND_PRODUCTS || o.c_bound > AIRES_CBOUND_ROWS)
     return fail(AIRES_E_INVALID_ARG, "opts.c_bound %d invalid", o.c_bound);
-  if (o.max_tile_rows < 0 || o.max_tile_bytes < 0 || o.m_a_bytes < 0)
-    return fail(AIRES_E_INVALID_ARG, "negative tile cap");
+  if (o.max_tile_rows < 0 || o.max_tile_bytes < 0 || o.m_a_bytes < 0 || o.bitmap_cache_bytes < 0)
+    return fail(AIRES_E_INVALID_ARG, "negative tile or cache cap");
   if (o.segmentation != AIRES_SEG_ROBW && o.segmentation != AIRES_SEG_MAXFILL)
     return fail(AIRES_E_INVALID_ARG, "opts.segmentation %d invalid", o.segmentation);
   if (o.segmentation == AIRES_SEG_MAXFILL &&
@@ -1405,7 +1405,8 @@ aires_status spgemm_device_in(aires_plan* p, hipStream_t s, DevPool& ws, aires_c
       // the plan leaves free; items that do not fit are marked again by the
       // numeric phase, and the cache is dropped if C then does not fit.
       const int64_t spare = p->budget - p->info.peak_bytes;
-      bm_cap = spare > 0 ? std::min<int64_t>(spare / 5, kBitmapCacheBytes) / (int64_t)sizeof(uint32_t) : 0;
+      const int64_t cache_max = p->opts.bitmap_cache_bytes > 0 ? p->opts.bitmap_cache_bytes : kBitmapCacheBytes;
+      bm_cap = spare > 0 ? std::min<int64_t>(spare / 5, cache_max) / (int64_t)sizeof(uint32_t) : 0;
       const int64_t words_all = m * (int64_t)p->nG * (p->G / 32);  // every row's bitmaps
       if (words_all / std::max<int64_t>(m, 1) == (int64_t)p->nG * (p->G / 32)) bm_cap = std::min(bm_cap, words_all);
       if (bm_cap > 0 && ws.get_n(bm_cap, &bm_cache) != AIRES_OK) {

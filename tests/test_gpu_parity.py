@@ -154,6 +154,18 @@ def test_cfg3_scaled_kept_bitmaps(torch_gpu, keep):
           window_grain_cols=4096, window_max_grains=8, window_max_entries=16384, count_grains=4)
 
 
+@pytest.mark.parametrize("cache_bytes", [256 << 10, 4 << 20])
+def test_cfg3_scaled_partial_bitmap_cache(torch_gpu, cache_bytes):
+    """Kept bitmaps for every wide row, but a cache far too small for them
+    (items of 4 grains of 4096 columns: 2 KB each, about 2 * 10^4 of them):
+    the first items to claim cache chunks keep their bitmaps, the rest are
+    marked again from their terms in the numeric phase, in the same launch."""
+    A, B = workloads.workload(3, n=40000)
+    check(torch_gpu, A, B, "cfg3 n=40000 bitmap cache %d bytes" % cache_bytes, keep_bitmap_products=1,
+          bitmap_cache_bytes=cache_bytes, window_grain_cols=4096, window_max_grains=8, window_max_entries=16384,
+          count_grains=4)
+
+
 def test_cfg3_scaled_small_windows(torch_gpu):
     """Many windows per row: 1024-column grains, windows of <= 4 grains and
     <= 1024 entries, 8 grains per symbolic item (64-word grains: wave sums)."""
