@@ -194,7 +194,7 @@ typedef struct aires_plan_opts {
                                    slots for splitting; further rows of the
                                    split bin take one workgroup each       */
     int64_t window_pool_bytes;  /* 0: default (38912).  LDS a window's
-                                   bitmap (8 bytes per 32 columns) and
+                                   bitmap (8 bytes per 48 columns) and
                                    values (4 bytes per entry) share; must
                                    hold one full grain                     */
     int32_t a_values;           /* aires_avalues: where A's values come

@@ -755,7 +755,7 @@ aires_status plan_impl(const aires_csr* A, const aires_csr* B, uint64_t hbm_budg
     if (p->G < 32 || p->G % 32 || p->G > (1 << 20) || p->win_entries < p->G || p->win_entries > 65535 ||
         p->win_grains < 1 || p->count_grains < 1 ||
         kern::window_numeric_lds(p->win_pool_words) > kern::kMaxLds ||
-        2 * (int64_t)(p->G / 32) + p->G > p->win_pool_words ||  // one full grain fits the pool
+        2 * kern::win_words(p->G) + p->G > p->win_pool_words ||  // one full grain fits the pool
         kern::grain_count_lds(p->count_grains, p->G) > kern::kMaxLds || p->nG > 65535 ||
         (int64_t)p->count_grains * p->G * kern::group_size(kern::KIND_WINDOWS) >= (int64_t(1) << 31)) {
       aires_status st = fail(AIRES_E_INVALID_ARG,

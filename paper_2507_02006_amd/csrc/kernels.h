@@ -135,6 +135,11 @@ size_t lds_bytes(int kind, int phase, int32_t W);
 size_t grain_count_lds(int sg, int G);
 size_t window_numeric_lds(int pool_words);
 constexpr size_t kMaxLds = 160 * 1024;  // LDS of one gfx950 workgroup
+// A window's bitmap in LDS: 8-byte words, each with WIN_WORD_BITS presence
+// bits (low) and the 16-bit rank of its first set bit (high), so a window
+// holds fewer than 65536 entries.
+constexpr int WIN_WORD_BITS = 48;
+__host__ __device__ constexpr int64_t win_words(int64_t cols) { return (cols + WIN_WORD_BITS - 1) / WIN_WORD_BITS; }
 int group_size(int kind);
 
 }  // namespace kern

@@ -1021,17 +1021,17 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
 // entries, never across a symbolic item boundary, a multiple of sg grains);
 // empty windows are skipped.  Calls f(g0, g1, n, roff).
 template <typename F>
-__device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, const WindowParams& wp, int wpg, F&& f) {
+__device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, const WindowParams& wp, int gcols, F&& f) {
   const int sg = wp.grains_per_count_item;
   int64_t roff = 0;
   int g0 = 0;
   while (g0 < nG) {
     int n = gc[g0];
     int g1 = g0 + 1;
-    // the window's bitmap (two words per bitmap word: bits and rank) and its
-    // values share the LDS pool
+    // the window's bitmap (8 bytes per WIN_WORD_BITS columns: bits and rank)
+    // and its values share the LDS pool
     while (g1 < nG && g1 - g0 < wp.max_grains && g1 % sg != 0 && n + gc[g1] <= wp.max_entries &&
-           2 * (g1 + 1 - g0) * wpg + n + gc[g1] <= wp.pool_words)
+           2 * win_words((g1 + 1 - g0) * gcols) + n + gc[g1] <= wp.pool_words)
       n += gc[g1++];
     if (n > 0) f(g0, g1, n, roff);
     roff += n;
@@ -1040,25 +1040,25 @@ __device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, const
   return roff;
 }
 
-__global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, int32_t wpg, const WindowParams wp,
+__global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, int32_t gcols, const WindowParams wp,
                                                   int64_t* counts) {
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t nwin = 0;
-    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp, wpg, [&](int, int, int, int64_t) { ++nwin; });
+    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp, gcols, [&](int, int, int, int64_t) { ++nwin; });
     wp.item_count[1 + d] = nwin;
   }
 }
 
-__global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, int32_t wpg, const WindowParams wp) {
+__global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, int32_t gcols, const WindowParams wp) {
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t o = wp.item_count[d];  // scanned: windows of the rows before d
-    plan_windows(wp.gcnt + row * nG, nG, wp, wpg, [&](int g0, int g1, int n, int64_t roff) {
+    plan_windows(wp.gcnt + row * nG, nG, wp, gcols, [&](int g0, int g1, int n, int64_t roff) {
                    WinItem w;
                    w.row = (int32_t)row;
                    w.g0 = (uint16_t)g0;
@@ -1070,10 +1070,11 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
   }
 }
 
-// A window's LDS: a pool holding, per bitmap word, its presence bits and
-// the rank of its first set bit side by side (a term's rank is one 8-byte
-// read), followed by the window's fp32 values (a wide window with few
-// entries and a narrow one with many use the same pool); then the chunk.
+// A window's LDS: a pool holding the bitmap as 8-byte words of
+// WIN_WORD_BITS presence bits with the rank of the word's first set bit in
+// the top 16 bits (a term's rank is one 8-byte read), followed by the
+// window's fp32 values (a wide window with few entries and a narrow one with
+// many use the same pool); then the chunk.
 
 template <typename S>
 __host__ __device__ constexpr size_t window_lds_bytes(int pool_words) {
@@ -1095,8 +1096,9 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                                                            const WindowParams wp, const Outputs out) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t s_row;
-  const int WPG = op.G / 32;
-  uint2* bw = reinterpret_cast<uint2*>(smem);  // (presence bits, rank of the word's first bit)
+  const int WPG = op.G / 32;  // 32-bit words per grain of a kept symbolic bitmap
+  constexpr uint64_t BITS = (uint64_t(1) << WIN_WORD_BITS) - 1u;
+  uint64_t* bw = reinterpret_cast<uint64_t*>(smem);  // presence bits | rank of the word's first bit << 48
   using CH = Chunk<WIN_BLOCK, RB>;
   CH& ch = *reinterpret_cast<CH*>(smem + align16((size_t)wp.pool_words * 4));
   Group<WIN_BLOCK, WIN_BLOCK> g;
@@ -1142,13 +1144,15 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       }
       const int g0 = I.g0, g1 = I.g1, n = I.n;
       const int c0 = g0 * op.G;
-      const int nw = (g1 - g0) * WPG;
+      const int nw32 = (g1 - g0) * WPG;
+      const int nw = (int)win_words((int64_t)(g1 - g0) * op.G);
       float* vals = reinterpret_cast<float*>(bw + nw);  // the values follow this window's bitmap
       const int64_t base = rbase + I.roff;
-      // terms carry absolute columns: bwa is the bitmap seen from column 0
-      // (c0 is a multiple of 32, so a column's bit index is the same)
-      uint2* bwa = bw - (c0 >> 5);
-      auto set_bit = [&](int j) { atomicOr(&bwa[j >> 5].x, 1u << (j & 31)); };
+      auto set_bit = [&](int j) {
+        const uint32_t dj = (uint32_t)(j - c0);
+        const uint32_t w = dj / WIN_WORD_BITS;
+        atomicOr(reinterpret_cast<unsigned long long*>(&bw[w]), 1ull << (dj - w * WIN_WORD_BITS));
+      };
       // Heavy rows: the symbolic phase kept the window's bitmap.
       int64_t cached = -1;
       if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
@@ -1156,14 +1160,23 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         const int64_t o = wp.bm_off[row * ((op.nG + SG - 1) / SG) + g0 / SG];
         if (o >= 0) cached = o + (int64_t)(g0 % SG) * WPG;
       }
+      // the kept bitmap has 32 columns per word from c0 on: a window word is
+      // the 48 bits from column 48 w, i.e. of kept words 3w/2 and 3w/2 + 1
       auto load_bits = [&]() {
         __syncthreads();  // the previous window's bitmap is cleared
-        for (int w = t; w < nw; w += WIN_BLOCK) bw[w].x = wp.bm_cache[cached + w];
+        for (int w = t; w < nw; w += WIN_BLOCK) {
+          const int q = (w * WIN_WORD_BITS) >> 5;
+          const uint64_t lo = wp.bm_cache[cached + q];
+          const uint64_t hi = q + 1 < nw32 ? wp.bm_cache[cached + q + 1] : 0u;
+          bw[w] = ((hi << 32 | lo) >> ((w * WIN_WORD_BITS) & 31)) & BITS;
+        }
         __syncthreads();
       };
       auto add_at_rank = [&](int j, float v) {
-        const uint2 e = bwa[j >> 5];
-        const int rk = (int)e.y + __popc(e.x & ((1u << (j & 31)) - 1u));
+        const uint32_t dj = (uint32_t)(j - c0);
+        const uint32_t w = dj / WIN_WORD_BITS;
+        const uint64_t e = bw[w];
+        const int rk = (int)(e >> WIN_WORD_BITS) + __popcll(e & ((1ull << (dj - w * WIN_WORD_BITS)) - 1u));
         if (rk < n) lds_add<false>(&vals[rk], v);
       };
       // exclusive popcount prefix over the window's words: each wavefront
@@ -1175,7 +1188,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         const int cw = (nw + NWV * WAVE - 1) / (NWV * WAVE) * WAVE;
         const int a0 = wv * cw, a1 = min(nw, a0 + cw);
         uint32_t sw = 0;
-        for (int w = a0 + lane; w < a1; w += WAVE) sw += __popc(bw[w].x);
+        for (int w = a0 + lane; w < a1; w += WAVE) sw += __popcll(bw[w]);
         sw = wave_sum(sw);
         if (lane == 0) g.red[wv] = sw;
         __syncthreads();
@@ -1183,9 +1196,11 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         for (int i = 0; i < wv; ++i) carry += (uint32_t)g.red[i];
         for (int b = a0; b < a1; b += WAVE) {
           const int w = b + lane;
-          const uint32_t c = w < a1 ? __popc(bw[w].x) : 0u;
+          const uint64_t x = w < a1 ? bw[w] : 0u;
+          const uint32_t c = __popcll(x);
           const uint32_t incl = wave_incl_scan(c);
-          if (c) bw[w].y = carry + incl - c;  // only set bits are ranked: empty words stay all zero
+          // only set bits are ranked: empty words stay all zero
+          if (c) bw[w] = x | (uint64_t)(carry + incl - c) << WIN_WORD_BITS;
           carry += wave_last(incl);
         }
         __syncthreads();
@@ -1341,17 +1356,17 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       __syncthreads();
       int32_t* cid = reinterpret_cast<int32_t*>(vals);
       for (int w = t; w < nw; w += WIN_BLOCK) {
-        const uint2 e = bw[w];
-        uint32_t b = e.x;
+        const uint64_t e = bw[w];
+        uint64_t b = e & BITS;
         if (!b) continue;  // an empty word holds no rank either
-        int r = (int)e.y;
-        const int cw = c0 + (w << 5);
+        int r = (int)(e >> WIN_WORD_BITS);
+        const int cw = c0 + w * WIN_WORD_BITS;
         do {
-          if (r < n) cid[r] = cw + __builtin_ctz(b);
+          if (r < n) cid[r] = cw + __builtin_ctzll(b);
           ++r;
           b &= b - 1u;
         } while (b);
-        bw[w] = make_uint2(0u, 0u);  // ranks too: the next window's values may lie here
+        bw[w] = 0u;  // ranks too: the next window's values may lie here
       }
       __syncthreads();
       for (int kk = t; kk < n; kk += WIN_BLOCK) {
@@ -1585,7 +1600,7 @@ hipError_t win_symbolic_t(const Operands& op, const BinView& bv, const WindowPar
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WIN_BLOCK), lds, s, op, bv, wp);
   int64_t pg = (ub_rows + 255) / 256;
   if (pg > 8192) pg = 8192;
-  hipLaunchKernelGGL(k_win_plan, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, op.G / 32, wp, out.counts);
+  hipLaunchKernelGGL(k_win_plan, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, op.G, wp, out.counts);
   return hipGetLastError();
 }
 
@@ -1594,7 +1609,7 @@ hipError_t win_numeric_t(const Operands& op, const BinView& bv, const WindowPara
                          const Outputs& out, int64_t ub_rows, int64_t nitems, hipStream_t s) {
   int64_t pg = (ub_rows + 255) / 256;
   if (pg > 8192) pg = 8192;
-  hipLaunchKernelGGL(k_win_fill, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, op.G / 32, wp);
+  hipLaunchKernelGGL(k_win_fill, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, op.G, wp);
   if (nitems <= 0) return hipGetLastError();
   hipError_t ez = hipMemsetAsync(wp.row_counter, 0, sizeof(int32_t), s);
   if (ez != hipSuccess) return ez;
