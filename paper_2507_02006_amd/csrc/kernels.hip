@@ -1180,29 +1180,35 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         if (rk < n) lds_add<false>(&vals[rk], v);
       };
       // exclusive popcount prefix over the window's words: each wavefront
-      // takes a contiguous share, its lanes consecutive words, with one
-      // wavefront scan per 64 words and the shares' totals carried in
+      // takes a contiguous share [wa0, wa1), its lanes consecutive words,
+      // with one wavefront scan per 64 words and the shares' totals carried
+      // in; the share's set bits have the ranks [wr0, wr1)
+      constexpr int NWV = WIN_BLOCK / WAVE;
+      const int wcw = (nw + NWV * WAVE - 1) / (NWV * WAVE) * WAVE;
+      // wavefront-uniform: kept in scalar registers
+      const int wa0 = __builtin_amdgcn_readfirstlane(min(nw, (t / WAVE) * wcw));
+      const int wa1 = min(nw, wa0 + wcw);
+      uint32_t wr0 = 0, wr1 = 0;
       auto word_ranks = [&]() {
-        constexpr int NWV = WIN_BLOCK / WAVE;
         const int lane = lane_id(), wv = t / WAVE;
-        const int cw = (nw + NWV * WAVE - 1) / (NWV * WAVE) * WAVE;
-        const int a0 = wv * cw, a1 = min(nw, a0 + cw);
         uint32_t sw = 0;
-        for (int w = a0 + lane; w < a1; w += WAVE) sw += __popcll(bw[w]);
+        for (int w = wa0 + lane; w < wa1; w += WAVE) sw += __popcll(bw[w]);
         sw = wave_sum(sw);
         if (lane == 0) g.red[wv] = sw;
         __syncthreads();
         uint32_t carry = 0;
         for (int i = 0; i < wv; ++i) carry += (uint32_t)g.red[i];
-        for (int b = a0; b < a1; b += WAVE) {
+        wr0 = __builtin_amdgcn_readfirstlane(carry);
+        for (int b = wa0; b < wa1; b += WAVE) {
           const int w = b + lane;
-          const uint64_t x = w < a1 ? bw[w] : 0u;
+          const uint64_t x = w < wa1 ? bw[w] : 0u;
           const uint32_t c = __popcll(x);
           const uint32_t incl = wave_incl_scan(c);
           // only set bits are ranked: empty words stay all zero
           if (c) bw[w] = x | (uint64_t)(carry + incl - c) << WIN_WORD_BITS;
           carry += wave_last(incl);
         }
+        wr1 = __builtin_amdgcn_readfirstlane(carry);
         __syncthreads();
       };
       if (short_row) {
@@ -1348,30 +1354,37 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                                                             [&](int j, float v) { add_at_rank(j, v); });
       }
       __syncthreads();
-      // values out (coalesced); then the value slots take the column ids,
-      // written at their ranks from the bitmap words (a thread per word),
-      // and go out coalesced too: C's column array is written in whole
-      // lines rather than an entry at a time from the add loops
-      for (int kk = t; kk < n; kk += WIN_BLOCK) store_stream(&out.cval[base + kk], vals[kk]);
-      __syncthreads();
-      int32_t* cid = reinterpret_cast<int32_t*>(vals);
-      for (int w = t; w < nw; w += WIN_BLOCK) {
-        const uint64_t e = bw[w];
-        uint64_t b = e & BITS;
-        if (!b) continue;  // an empty word holds no rank either
-        int r = (int)(e >> WIN_WORD_BITS);
-        const int cw = c0 + w * WIN_WORD_BITS;
-        do {
-          if (r < n) cid[r] = cw + __builtin_ctzll(b);
-          ++r;
-          b &= b - 1u;
-        } while (b);
-        bw[w] = 0u;  // ranks too: the next window's values may lie here
-      }
-      __syncthreads();
-      for (int kk = t; kk < n; kk += WIN_BLOCK) {
-        store_stream(&out.ccol[base + kk], cid[kk]);
-        cid[kk] = 0;  // the bits of +0.0f: the slots are clear for the next window
+      // Output, each wavefront on its own share of the bitmap words and so on
+      // its own range of ranks (no workgroup barrier): the values out
+      // (coalesced); then those value slots take the column ids, written at
+      // their ranks from the words (a lane per word), and go out coalesced
+      // too, so that C's column array is written in whole lines rather than
+      // an entry at a time from the add loops.  A wavefront's LDS operations
+      // complete in order, so the slots are read before they are rewritten.
+      {
+        const int lane = lane_id();
+        const int r0 = min((int)wr0, n), r1 = min((int)wr1, n);
+        for (int kk = r0 + lane; kk < r1; kk += WAVE) store_stream(&out.cval[base + kk], vals[kk]);
+        wave_sync();
+        int32_t* cid = reinterpret_cast<int32_t*>(vals);
+        for (int w = wa0 + lane; w < wa1; w += WAVE) {
+          const uint64_t e = bw[w];
+          uint64_t b = e & BITS;
+          if (!b) continue;  // an empty word holds no rank either
+          int r = (int)(e >> WIN_WORD_BITS);
+          const int cw = c0 + w * WIN_WORD_BITS;
+          do {
+            if (r < n) cid[r] = cw + __builtin_ctzll(b);
+            ++r;
+            b &= b - 1u;
+          } while (b);
+          bw[w] = 0u;  // ranks too: the next window's values may lie here
+        }
+        wave_sync();
+        for (int kk = r0 + lane; kk < r1; kk += WAVE) {
+          store_stream(&out.ccol[base + kk], cid[kk]);
+          cid[kk] = 0;  // the bits of +0.0f: the slots are clear for the next window
+        }
       }
     }
   }

@@ -246,6 +246,31 @@ def test_streamed_tiles_host_c(torch_gpu):
         C.free()
 
 
+@pytest.mark.parametrize("F", [16, 32, 256])
+def test_streamed_feature_sizes(torch_gpu, F):
+    """The streamed schedule across feature widths (the feature-size study
+    runs F = 16 ... 256): out-of-core-shaped graph, features of width F at
+    the same density, A in pinned host memory, C tiles to pinned host
+    memory, a budget that forces several tiles; every entry against the
+    oracle."""
+    import paper_2507_02006_amd as aires
+    A, _ = workloads.workload(5, n=60000)
+    B = workloads.features(60000, F, 0.10, seed=1000 + F)
+    ref = oracle.spgemm(A, B)
+    pA, pB = aires.to_pinned(A), aires.to_pinned(B)
+    budget = B.nbytes() + (4 << 20) + 2 * 1_500_000 + 8 * int(np.minimum(oracle.products(A, B), F).sum()) // 3
+    say("streamed cfg5-shaped n=60000 F=%d budget=%d" % (F, budget))
+    with aires.tile_plan(pA, pB, budget, c_on_host=True, timing=True) as plan:
+        info = aires.plan_info(plan)
+        assert info.ntiles >= 3
+        C = aires.spgemm(plan)
+        assert C.on_host
+        assert_match(C.rp, C.col, C.val, ref)
+        st = aires.plan_stats(plan)
+        assert st["products"] == ref.products and st["nnz_c"] == ref.nnz
+        C.free()
+
+
 def test_streamed_tiles_device_c(torch_gpu):
     import paper_2507_02006_amd as aires
     A, B = workloads.workload(4, n=40000)
