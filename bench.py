@@ -683,6 +683,10 @@ def main():
     roof = run["roofline"]
     roof["traffic"] = measured_traffic("cfg%d/numeric/%s" % (args.workload, run["dominant"]),
                                        roof["algorithmic_bytes"])
+    # the counter bytes as a rate over this run's launch time, beside the
+    # algorithmic (achieved) and gather-model rates
+    roof["traffic_gbs"] = (round(roof["traffic"] / (roof["avg_launch_ms"] * 1e-3) / 1e9, 2)
+                           if roof["traffic"] else None)
     res = {
         "metric": METRIC,
         "value": round(2 * total_products / (ms_per_step * 1e-3) / 1e9, 3),
@@ -701,7 +705,8 @@ def main():
                    "products": total_products, "nnz_c": run["nnz_c"], "tiles": run["tiles"],
                    "parallelism": "single GPU"},
         "roofline": {k: roof[k] for k in ("bound", "kernel", "achieved", "peak", "unit", "frac", "traffic",
-                                          "algorithmic_bytes", "avg_launch_ms", "gather_model_gbs")},
+                                          "algorithmic_bytes", "avg_launch_ms", "gather_model_gbs",
+                                          "traffic_gbs")},
         "phases_ms": run["phases_ms"],
         "numeric_gflops": run["numeric_gflops"],
         "end_to_end_compulsory_gbs": run["end_to_end_compulsory_gbs"],
