@@ -1395,7 +1395,9 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
 // bidx[k*(nwin+1) + g] = first position p of B_k with bcol[p] >= g*W (or
 // the row end), for grains g in [0, nwin]; W is the grain width.  A B row's
 // entries are contiguous, so the lookups of one k for successive windows
-// share cache lines.  One wavefront per B row.
+// share cache lines.  One wavefront per B row, a lane per grain, each a
+// binary search over the row's sorted columns: the row's index entries are
+// written by consecutive lanes.
 template <typename RB>
 __global__ __launch_bounds__(256) void k_window_index(const void* brp, const int32_t* bcol,
                                                       int64_t K, int32_t W, int32_t nwin,
@@ -1403,14 +1405,17 @@ __global__ __launch_bounds__(256) void k_window_index(const void* brp, const int
   const int64_t nw = (int64_t)gridDim.x * (blockDim.x / WAVE);
   for (int64_t k = (int64_t)blockIdx.x * (blockDim.x / WAVE) + threadIdx.x / WAVE; k < K; k += nw) {
     const int64_t s = ld_rp<RB>(brp, k), e = ld_rp<RB>(brp, k + 1);
-    for (int64_t p = s + lane_id(); p < e; p += WAVE) {
-      const int wc = bcol[p] / W;
-      const int wp = (p == s) ? -1 : bcol[p - 1] / W;
-      for (int w = wp + 1; w <= wc; ++w) bidx[k * (nwin + 1) + w] = (int32_t)p;
-    }
-    if (lane_id() == 0) {
-      const int wl = (e > s) ? bcol[e - 1] / W : -1;
-      for (int w = wl + 1; w <= nwin; ++w) bidx[k * (nwin + 1) + w] = (int32_t)e;
+    for (int w = lane_id(); w <= nwin; w += WAVE) {
+      const int64_t c = (int64_t)w * W;  // the grain's first column
+      int64_t lo = s, hi = e;
+      while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (bcol[mid] < c)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      bidx[k * (nwin + 1) + w] = (int32_t)lo;
     }
   }
 }
