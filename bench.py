@@ -43,7 +43,8 @@ WORKLOAD_NAMES = {
     4: "large GCN aggregation: symmetric R-MAT n=8388608 deg 24 + self-loops; X 8388608x128 10% U(-1,1)",
 }
 
-KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split"]
+KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split",
+              "hash_4096"]
 
 
 def row_kinds(P: np.ndarray, N: int) -> np.ndarray:
@@ -56,7 +57,8 @@ def row_kinds(P: np.ndarray, N: int) -> np.ndarray:
     else:
         k[(P > 0) & (P <= 64)] = 3
         k[(P > 64) & (P <= 512)] = 4
-        k[(P > 512) & (P <= 4096)] = 5
+        k[(P > 512) & (P <= 2048)] = 8
+        k[(P > 2048) & (P <= 4096)] = 5
         k[P > 4096] = 6 if N > 16384 else 2
     return k
 

@@ -42,7 +42,10 @@
 extern "C" {
 #endif
 
-#define AIRES_ABI_VERSION 3
+#define AIRES_ABI_VERSION 4
+
+/* slots of aires_stats.kind_ms per phase (row kinds in use: 0 ... 8) */
+#define AIRES_NUM_KINDS 16
 
 typedef enum aires_status {
     AIRES_OK = 0,
@@ -418,9 +421,9 @@ typedef struct aires_stats {
     int64_t numeric_launches;   /* numeric-phase kernel launches           */
     /* milliseconds per kernel kind (index = kind id of the row bins:
        0 empty, 1 dense-wave, 2 dense-block, 3 hash-128, 4 hash-1024,
-       5 hash-8192, 6 column windows, 7 split rows); [0] symbolic, [1]
-       numeric phase                                                        */
-    double kind_ms[2][8];
+       5 hash-8192, 6 column windows, 7 split rows, 8 hash-4096; the
+       other slots stay 0); [0] symbolic, [1] numeric phase                */
+    double kind_ms[2][AIRES_NUM_KINDS];
     /* streamed calls: from the first copy of Phase I to the last copy of
        Phase III (the tile pipeline, without the output allocation)       */
     double pipeline_ms;

@@ -27,7 +27,9 @@ OK, E_INVALID_ARG, E_INVALID_CSR, E_DIM, E_BUDGET, E_OVERFLOW, E_OOM, E_HIP, E_S
 IDX_I32, IDX_I64 = 0, 1
 MEM_DEVICE, MEM_HOST_PINNED, MEM_HOST = 0, 1, 2
 CBOUND_PRODUCTS, CBOUND_DENSE, CBOUND_PAPER_EQ5, CBOUND_ROWS = 0, 1, 2, 3
-KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split"]
+KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split",
+              "hash_4096"]
+NUM_KINDS = 16  # kind_ms slots per phase
 
 
 class Csr(ctypes.Structure):
@@ -75,7 +77,7 @@ class Stats(ctypes.Structure):
     _fields_ = [(n, c_i64) for n in ("ntiles", "products", "nnz_c", "h2d_bytes", "d2h_bytes", "host_syncs")] + \
                [(n, c_dbl) for n in ("analyze_ms", "bin_ms", "symbolic_ms", "scan_ms", "numeric_ms", "h2d_ms",
                                      "d2h_ms", "total_ms")] + \
-               [("numeric_launches", c_i64), ("kind_ms", (c_dbl * 8) * 2), ("pipeline_ms", c_dbl),
+               [("numeric_launches", c_i64), ("kind_ms", (c_dbl * NUM_KINDS) * 2), ("pipeline_ms", c_dbl),
                 ("resent_bytes", c_i64), ("merge_ms", c_dbl), ("storage_bytes", c_i64), ("storage_ms", c_dbl)]
 
 

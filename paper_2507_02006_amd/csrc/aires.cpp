@@ -352,7 +352,8 @@ void bin_plan(aires_plan* p) {
     // light rows hash in LDS (load factor <= 1/2: nnz(C_i) <= P_i <= slots/2)
     if (hash_max > 0) add(kern::KIND_HASH_128, std::min<int64_t>(hash_max, 64));
     if (hash_max > 64) add(kern::KIND_HASH_1024, std::min<int64_t>(hash_max, 512));
-    if (hash_max > 512) add(kern::KIND_HASH_8192, hash_max);
+    if (hash_max > 512) add(kern::KIND_HASH_4096, std::min<int64_t>(hash_max, 2048));
+    if (hash_max > 2048) add(kern::KIND_HASH_8192, hash_max);
     if (N <= dense_max) {
       add(kern::KIND_DENSE_BLOCK, INT64_MAX);
     } else {
@@ -2113,7 +2114,7 @@ aires_status aires_plan_stats(const aires_plan* plan, aires_stats* stats) {
         case PH_TOTAL: stats->total_ms += ms; break;
         case PH_PIPELINE: stats->pipeline_ms += ms; break;
         default:
-          if (mk.kind >= 0 && mk.kind < 8) stats->kind_ms[mk.phase][mk.kind] += ms;
+          if (mk.kind >= 0 && mk.kind < AIRES_NUM_KINDS) stats->kind_ms[mk.phase][mk.kind] += ms;
           break;
       }
     }

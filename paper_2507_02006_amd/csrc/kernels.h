@@ -21,8 +21,9 @@ enum Kind : int {
   KIND_HASH_8192 = 5,   // one workgroup per row, LDS hash of 8192 slots
   KIND_WINDOWS = 6,     // wide rows: per-grain counts, then bitmap-rank column windows
   KIND_DENSE_SPLIT = 7, // heavy rows of a narrow product: runs of A entries per workgroup
+  KIND_HASH_4096 = 8,   // one 256-thread workgroup per row, LDS hash of 4096 slots
 };
-constexpr int NUM_KINDS = 8;
+constexpr int NUM_KINDS = 9;
 
 struct BinThresholds {
   int32_t nb;                    // number of bins

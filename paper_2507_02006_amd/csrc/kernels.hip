@@ -1554,6 +1554,8 @@ hipError_t run_bin_t(int kind, const Operands& op, const BinView& bv, const Outp
       return launch_hash<RA, RB, 128, 64, 256, NUM>(op, bv, out, ub_rows, s);
     case KIND_HASH_1024:
       return launch_hash<RA, RB, 1024, 64, 256, NUM>(op, bv, out, ub_rows, s);
+    case KIND_HASH_4096:
+      return launch_hash<RA, RB, 4096, 256, 256, NUM>(op, bv, out, ub_rows, s);
     case KIND_HASH_8192:
       return launch_hash<RA, RB, 8192, 512, 512, NUM>(op, bv, out, ub_rows, s);
     default:
@@ -1740,6 +1742,7 @@ size_t lds_bytes(int kind, int phase, int32_t W) {
       return phase ? dense_group_bytes<512, true, int64_t>(W) : dense_group_bytes<512, false, int64_t>(W);
     case KIND_HASH_128: return 4 * sizeof(HashLds<128, 64, true, int64_t>);
     case KIND_HASH_1024: return 4 * sizeof(HashLds<1024, 64, true, int64_t>);
+    case KIND_HASH_4096: return sizeof(HashLds<4096, 256, true, int64_t>);
     case KIND_HASH_8192: return sizeof(HashLds<8192, 512, true, int64_t>);
     default: return 0;
   }
@@ -1754,6 +1757,7 @@ int group_size(int kind) {
   switch (kind) {
     case KIND_DENSE_BLOCK: return 512;
     case KIND_DENSE_SPLIT: return SPLIT_BLOCK;
+    case KIND_HASH_4096: return 256;
     case KIND_HASH_8192: return 512;
     case KIND_WINDOWS: return WIN_BLOCK;
     default: return 64;

@@ -27,7 +27,7 @@ def test_exports_every_declared_symbol():
 
 def test_version_and_strings():
     lib = B_.load()
-    assert lib.aires_abi_version() == 3
+    assert lib.aires_abi_version() == 4
     assert lib.aires_status_string(0) == b"AIRES_OK"
     assert lib.aires_status_string(B_.E_BUDGET) == b"AIRES_E_BUDGET"
     assert lib.aires_status_string(-99) == b"AIRES_E_UNKNOWN"

@@ -97,6 +97,8 @@ PATHS = {
                                   window_max_grains=1, window_max_entries=128, count_grains=1),
     "hash8192_then_windows": dict(dense_max_cols=160, hash_max_products=4096, window_grain_cols=96,
                                   window_max_grains=4, window_max_entries=200, count_grains=5),
+    "hash4096_then_windows": dict(dense_max_cols=160, hash_max_products=2048, window_grain_cols=96,
+                                  window_max_grains=4, window_max_entries=200, count_grains=5),
     # windows cut by the shared LDS pool (bitmap words + values), not by the
     # grain or entry caps: a wide sparse window or a narrow dense one
     "windows_pool": dict(dense_max_cols=64, hash_max_products=-1, window_grain_cols=64,
