@@ -73,7 +73,7 @@ struct WindowParams {
   int32_t pool_words;      // LDS words a window's bitmap (2 per bitmap word) and values (1 per entry) share
   int64_t* item_count;     // [1 + d]: windows of the d-th row of the bins; scanned into offsets
   WinItem* items;          // filled in the numeric sweep
-  int32_t* row_counter;    // zeroed before the numeric launch (dynamic row scheduling)
+  int32_t* row_counter;    // zeroed before each window launch, symbolic and numeric (dynamic row scheduling)
   // Presence bitmaps kept by the symbolic phase for heavy rows (nullptr:
   // none): the words of symbolic item (row, run of grains) start at
   // bm_off[row * items_per_row + item] (-1: not kept), so the numeric phase

@@ -374,6 +374,14 @@ struct FullRows {
     len = ld_rp<RB>(brp, k + 1) - lo;
   }
 };
+// ... or a range each thread already holds for its own k (one chunk) ...
+struct HeldRange {
+  int64_t lo, len;
+  __device__ __forceinline__ void operator()(int64_t, int64_t& l, int64_t& n) const {
+    l = lo;
+    n = len;
+  }
+};
 // ... or the part of it in a run of column grains (two slabs of the index).
 struct GrainRange {
   const int32_t* bidx;  // the grain index, nG + 1 entries per B row
@@ -943,7 +951,7 @@ template <typename RA, typename RB>
 __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op, const BinView bv,
                                                            const WindowParams wp) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int64_t s_off;
+  __shared__ int64_t s_off, s_row;
   constexpr int64_t CACHE_CHUNK = 65536;  // cache words a workgroup takes from the shared buffer at once
   constexpr int NWV = WIN_BLOCK / WAVE;
   int64_t chunk_cur = 0, chunk_end = 0;   // thread 0: the workgroup's current chunk
@@ -964,56 +972,85 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
   const int64_t ngg = (op.nG + SG - 1) / SG;
-  for (int64_t it = blockIdx.x; it < cnt * ngg; it += gridDim.x) {
-    const int64_t gg = it / cnt;  // grain-group major: one column slab of B at a time
-    const int64_t row = list[it - gg * cnt];
-    const int g0 = (int)(gg * SG);
-    const int g1 = min((int)op.nG, g0 + SG);
-    const int c0 = g0 * op.G;
-    const GrainRange seg{op.bidx, op.nG + 1, g0, g1};
-    // terms carry absolute columns: bma is the bitmap seen from column 0
-    // (c0 is a multiple of 32, so a column's bit index is the same)
-    uint32_t* bma = bm - (c0 >> 5);
-    // eight B loads in flight per thread: the symbolic loop reads columns only
-    for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, row, seg, [&](int j, float) {
-      atomicOr(&bma[j >> 5], 1u << (j & 31));
-    });
-    const int nw = (g1 - g0) * WPG;
-    int64_t off = -1;
-    if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
-      // heavy row: keep the item's bitmap for the numeric phase, in a slot
-      // taken from the workgroup's chunk of the shared cache
-      if (t == 0) {
-        if (chunk_cur + nw > chunk_end) {
-          const int64_t take = max<int64_t>(CACHE_CHUNK, nw);
-          chunk_cur = (int64_t)atomicAdd(wp.bm_top, (unsigned long long)take);
-          chunk_end = chunk_cur + take;
+  // Workgroups take rows from a shared counter (the heaviest bin first) and
+  // walk a row's items in column order.  A row with at most WIN_BLOCK
+  // entries keeps one k per thread in a register with the B position where
+  // its segment for the current item starts; consecutive items share a
+  // grain boundary, so an item needs one index lookup per k (its end),
+  // issued while the previous item is counted.
+  for (;;) {
+    __syncthreads();
+    if (t == 0) s_row = atomicAdd(wp.row_counter, 1);
+    __syncthreads();
+    const int64_t dd = s_row;
+    if (dd >= cnt) break;
+    const int64_t row = list[cnt - 1 - dd];
+    const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
+    const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
+    const bool short_row = (p1 - p0) <= WIN_BLOCK;
+    int32_t k = -1;
+    if (short_row && p0 + t < p1) k = op.acol[p0 + t];
+    const int32_t* kr = op.bidx + (int64_t)(k >= 0 ? k : 0) * (op.nG + 1);
+    int32_t lo = 0, hi_next = 0;
+    if (k >= 0) {
+      lo = kr[0];
+      hi_next = kr[min((int)op.nG, SG)];
+    }
+    for (int64_t gg = 0; gg < ngg; ++gg) {
+      const int g0 = (int)(gg * SG);
+      const int g1 = min((int)op.nG, g0 + SG);
+      const int c0 = g0 * op.G;
+      const int32_t hi = hi_next;
+      if (k >= 0 && gg + 1 < ngg) hi_next = kr[min((int)op.nG, g1 + SG)];  // the next item's segment end
+      // terms carry absolute columns: bma is the bitmap seen from column 0
+      // (c0 is a multiple of 32, so a column's bit index is the same)
+      uint32_t* bma = bm - (c0 >> 5);
+      auto mark = [&](int j, float) { atomicOr(&bma[j >> 5], 1u << (j & 31)); };
+      // eight B loads in flight per thread: the symbolic loop reads columns only
+      if (short_row)
+        for_each_term_in<WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, p0, p1, HeldRange{lo, (int64_t)hi - lo},
+                                                               mark);
+      else
+        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, row,
+                                                                GrainRange{op.bidx, op.nG + 1, g0, g1}, mark);
+      lo = hi;
+      const int nw = (g1 - g0) * WPG;
+      int64_t off = -1;
+      if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
+        // heavy row: keep the item's bitmap for the numeric phase, in a slot
+        // taken from the workgroup's chunk of the shared cache
+        if (t == 0) {
+          if (chunk_cur + nw > chunk_end) {
+            const int64_t take = max<int64_t>(CACHE_CHUNK, nw);
+            chunk_cur = (int64_t)atomicAdd(wp.bm_top, (unsigned long long)take);
+            chunk_end = chunk_cur + take;
+          }
+          const int64_t o = chunk_cur + nw <= wp.bm_cap ? chunk_cur : -1;
+          chunk_cur += nw;
+          s_off = o;
+          wp.bm_off[row * ngg + gg] = o;
         }
-        const int64_t o = chunk_cur + nw <= wp.bm_cap ? chunk_cur : -1;
-        chunk_cur += nw;
-        s_off = o;
-        wp.bm_off[row * ngg + gg] = o;
+        __syncthreads();
+        off = s_off;
+      } else if (wp.bm_cache && t == 0) {
+        wp.bm_off[row * ngg + gg] = -1;
       }
-      __syncthreads();
-      off = s_off;
-    } else if (wp.bm_cache && t == 0) {
-      wp.bm_off[row * ngg + gg] = -1;
-    }
-    // one pass over the bitmap: per-grain popcounts (a wavefront per grain,
-    // lanes on consecutive words), the copy of a kept bitmap (coalesced)
-    // and the clearing for the next item
-    for (int gi = wv; gi < g1 - g0; gi += NWV) {
-      uint32_t c = 0;
-      for (int w = gi * WPG + lane; w < (gi + 1) * WPG; w += WAVE) {
-        const uint32_t x = bm[w];
-        c += __popc(x);
-        if (off >= 0) wp.bm_cache[off + w] = x;
-        bm[w] = 0u;
+      // one pass over the bitmap: per-grain popcounts (a wavefront per grain,
+      // lanes on consecutive words), the copy of a kept bitmap (coalesced)
+      // and the clearing for the next item
+      for (int gi = wv; gi < g1 - g0; gi += NWV) {
+        uint32_t c = 0;
+        for (int w = gi * WPG + lane; w < (gi + 1) * WPG; w += WAVE) {
+          const uint32_t x = bm[w];
+          c += __popc(x);
+          if (off >= 0) wp.bm_cache[off + w] = x;
+          bm[w] = 0u;
+        }
+        c = wave_sum(c);
+        if (lane == 0) wp.gcnt[row * op.nG + g0 + gi] = (int32_t)c;
       }
-      c = wave_sum(c);
-      if (lane == 0) wp.gcnt[row * op.nG + g0 + gi] = (int32_t)c;
+      __syncthreads();  // the bitmap is clear before the next item's terms
     }
-    __syncthreads();  // the bitmap is clear before the next item's terms
   }
 }
 
@@ -1615,8 +1652,9 @@ hipError_t win_symbolic_t(const Operands& op, const BinView& bv, const WindowPar
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  const int64_t ngg = (op.nG + wp.grains_per_count_item - 1) / wp.grains_per_count_item;
-  const int64_t grid = grid_for(kern, WIN_BLOCK, lds, 1, ub_rows * ngg);
+  hipError_t ez = hipMemsetAsync(wp.row_counter, 0, sizeof(int32_t), s);
+  if (ez != hipSuccess) return ez;
+  const int64_t grid = grid_for(kern, WIN_BLOCK, lds, 1, ub_rows);
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WIN_BLOCK), lds, s, op, bv, wp);
   int64_t pg = (ub_rows + 255) / 256;
   if (pg > 8192) pg = 8192;
