@@ -30,6 +30,7 @@ CBOUND_PRODUCTS, CBOUND_DENSE, CBOUND_PAPER_EQ5, CBOUND_ROWS = 0, 1, 2, 3
 KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split",
               "hash_4096"]
 NUM_KINDS = 16  # kind_ms slots per phase
+ABI_VERSION = 4  # AIRES_ABI_VERSION of the header these structures mirror
 
 
 class Csr(ctypes.Structure):
@@ -137,6 +138,10 @@ def load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.restype = res
         f.argtypes = args
+    # the structures above follow one version of include/aires.h
+    if lib.aires_abi_version() != ABI_VERSION:
+        raise RuntimeError("libaires.so has ABI version %d, this binding expects %d (rebuild it)"
+                           % (lib.aires_abi_version(), ABI_VERSION))
     _lib = lib
     return lib
 
