@@ -1,6 +1,7 @@
 """C-ABI checks that need no GPU: the library loads, exports every symbol
 its header declares, reports errors, and plans RoBW tiles (host inputs)."""
 import ctypes
+import re
 import json
 import os
 import subprocess
@@ -28,6 +29,10 @@ def test_exports_every_declared_symbol():
 def test_version_and_strings():
     lib = B_.load()
     assert lib.aires_abi_version() == 4
+    # the binding's structures, the header and the library agree on the version
+    hdr = open(B_.HEADER).read()
+    assert int(re.search(r"#define AIRES_ABI_VERSION (\d+)", hdr).group(1)) == B_.ABI_VERSION == 4
+    assert int(re.search(r"#define AIRES_NUM_KINDS (\d+)", hdr).group(1)) == B_.NUM_KINDS
     assert lib.aires_status_string(0) == b"AIRES_OK"
     assert lib.aires_status_string(B_.E_BUDGET) == b"AIRES_E_BUDGET"
     assert lib.aires_status_string(-99) == b"AIRES_E_UNKNOWN"
