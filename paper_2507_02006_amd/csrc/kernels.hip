@@ -558,6 +558,33 @@ __device__ __forceinline__ void for_each_term(const Operands& op, const Group<GR
   for_each_term_in<GROUP, BLOCK, NUM, P32, UR>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
 }
 
+// A row with a single A entry is a_ik times B_k: its columns are B_k's
+// (sorted, distinct) and each value is the one product added to +0, as the
+// accumulation of every other row starts.  Counts (!NUM) or writes (NUM)
+// such a row with the group's threads and returns true; false for any other
+// row.  The test is the same for every thread of the group.
+template <typename RA, typename RB, int GROUP, bool NUM>
+__device__ __forceinline__ bool single_entry_row(const Operands& op, const Outputs& out, int64_t row, int t) {
+  const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
+  const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
+  if (p1 - p0 != 1) return false;
+  const int64_t k = op.acol[p0];
+  const int64_t lo = ld_rp<RB>(op.brp, k);
+  const int64_t len = ld_rp<RB>(op.brp, k + 1) - lo;
+  if constexpr (!NUM) {
+    if (t == 0) out.counts[row] = len;
+  } else {
+    const float a = op.aval[p0];
+    const int64_t o0 = out.crp[row];
+    for (int64_t j = t; j < len; j += GROUP) {
+      const float prod = a * op.bval[lo + j];
+      store_stream(&out.ccol[o0 + j], op.bcol[lo + j]);
+      store_stream(&out.cval[o0 + j], 0.f + prod);
+    }
+  }
+  return true;
+}
+
 // -------------------------------------------------- dense path (narrow N)
 
 // LDS layout of one group: [bitmap N/32 words][acc N floats if NUM][Chunk][red]
@@ -599,6 +626,7 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
   const FullRows<RB> seg{op.brp};
   for (int64_t it = (int64_t)blockIdx.x * NG + gi + bv.skip; it < cnt; it += (int64_t)gridDim.x * NG) {
     const int64_t row = list[it];
+    if (single_entry_row<RA, RB, GROUP, NUM>(op, out, row, t)) continue;
     for_each_term<RA, GROUP, BLOCK, NUM>(op, g, ch, row, seg, [&](int j, float v) {
       atomicOr(&bm[j >> 5], 1u << (j & 31));
       if constexpr (NUM) lds_add<true>(&acc[j], v);
@@ -801,6 +829,7 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
   const FullRows<RB> seg{op.brp};
   for (int64_t it = (int64_t)blockIdx.x * NG + gi; it < cnt; it += (int64_t)gridDim.x * NG) {
     const int64_t row = list[it];
+    if (single_entry_row<RA, RB, GROUP, NUM>(op, out, row, t)) continue;
     int64_t mine = 0;
     for_each_term<RA, GROUP, BLOCK, NUM>(op, g, L.ch, row, seg, [&](int j, float v) {
       uint32_t h = hslot<TABLE>(j);
