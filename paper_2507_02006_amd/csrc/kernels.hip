@@ -976,6 +976,12 @@ __host__ __device__ constexpr size_t count_lds_bytes(int sg, int G) {
          16;  // + the static list offset
 }
 
+// Rows whose symbolic bitmaps are kept for the numeric phase (one copy per
+// symbolic item, as far as the cache holds them).
+__device__ __forceinline__ bool keeps_bitmaps(const WindowParams& wp, int64_t row) {
+  return wp.bm_cache && wp.P[row] > wp.bm_min_products;
+}
+
 template <typename RA, typename RB>
 __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op, const BinView bv,
                                                            const WindowParams wp) {
@@ -1045,7 +1051,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
       lo = hi;
       const int nw = (g1 - g0) * WPG;
       int64_t off = -1;
-      if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
+      if (keeps_bitmaps(wp, row)) {
         // heavy row: keep the item's bitmap for the numeric phase, in a slot
         // taken from the workgroup's chunk of the shared cache
         if (t == 0) {
@@ -1084,11 +1090,14 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
 }
 
 // Greedy windows of whole grains (at most max_grains grains and max_entries
-// entries, never across a symbolic item boundary, a multiple of sg grains);
-// empty windows are skipped.  Calls f(g0, g1, n, roff).
+// entries; for a row whose symbolic bitmaps are kept, never across a
+// symbolic item boundary, a multiple of sg grains, as a window loads its
+// bits from one item's copy); empty windows are skipped.  Calls
+// f(g0, g1, n, roff).
 template <typename F>
-__device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, const WindowParams& wp, int gcols, F&& f) {
-  const int sg = wp.grains_per_count_item;
+__device__ __forceinline__ int64_t plan_windows(const int32_t* gc, int nG, const WindowParams& wp, int gcols,
+                                                bool kept, F&& f) {
+  const int sg = kept ? wp.grains_per_count_item : nG + 1;
   int64_t roff = 0;
   int g0 = 0;
   while (g0 < nG) {
@@ -1113,7 +1122,8 @@ __global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, 
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t nwin = 0;
-    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp, gcols, [&](int, int, int, int64_t) { ++nwin; });
+    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp, gcols, keeps_bitmaps(wp, row),
+                               [&](int, int, int, int64_t) { ++nwin; });
     wp.item_count[1 + d] = nwin;
   }
 }
@@ -1124,7 +1134,7 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t o = wp.item_count[d];  // scanned: windows of the rows before d
-    plan_windows(wp.gcnt + row * nG, nG, wp, gcols, [&](int g0, int g1, int n, int64_t roff) {
+    plan_windows(wp.gcnt + row * nG, nG, wp, gcols, keeps_bitmaps(wp, row), [&](int g0, int g1, int n, int64_t roff) {
                    WinItem w;
                    w.row = (int32_t)row;
                    w.g0 = (uint16_t)g0;
@@ -1221,7 +1231,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       };
       // Heavy rows: the symbolic phase kept the window's bitmap.
       int64_t cached = -1;
-      if (wp.bm_cache && wp.P[row] > wp.bm_min_products) {
+      if (keeps_bitmaps(wp, row)) {
         const int SG = wp.grains_per_count_item;
         const int64_t o = wp.bm_off[row * ((op.nG + SG - 1) / SG) + g0 / SG];
         if (o >= 0) cached = o + (int64_t)(g0 % SG) * WPG;
