@@ -350,6 +350,21 @@ def test_edge_stored_zeros_kept(torch_gpu):
     assert val.tolist() == [0.0, 5.0, 0.0, 0.0]
 
 
+@pytest.mark.parametrize("N", [4, 20000])
+def test_edge_single_entry_rows_signed_zeros(torch_gpu, N):
+    """Rows with a single A entry are written as a_ik times B_k: each value
+    is still one product added to +0, so a product that is -0 comes out +0
+    as in the oracle (bit patterns compared), in the dense (N = 4) and the
+    hash (N = 20000) kernels."""
+    A = _csr(3, 2, [[(0, -1.0)], [(1, 2.0)], [(0, 1.0), (1, 1.0)]])
+    B = _csr(2, N, [[(0, 0.0), (3, 4.0)], [(0, -0.0), (2, 1.5)]])
+    ref = oracle.spgemm(A, B)
+    rp, col, val, _, _ = run(torch_gpu, A, B)
+    assert rp.tolist() == ref.rp.tolist() and col.tolist() == ref.col.tolist()
+    assert np.array_equal(val.view(np.uint32), ref.val.view(np.uint32)), (val, ref.val)
+    assert not np.signbit(val[0]) and not np.signbit(val[2])
+
+
 def test_determinism_of_structure(torch_gpu):
     A, B = workloads.workload(3, n=20000)
     r1 = run(torch_gpu, A, B)
