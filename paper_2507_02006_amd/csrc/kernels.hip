@@ -955,17 +955,18 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 // ------------------------------------------------- wide rows: column windows
 //
 // Wide products (N above the densest LDS row) split the columns into grains
-// of G columns.  Symbolic: a workgroup sets a presence bitmap for a run of
-// grains of one row (a symbolic item), writes each grain's popcount, and
-// for heavy rows keeps the bitmap in global memory.  A plan kernel then cuts
-// every row into windows of whole grains whose bitmap and values fit one
-// LDS pool (and at most max_entries entries and max_grains grains), never
-// leaving a symbolic item.  Numeric, per window: the presence bitmap is set
-// from the terms (or loaded from the kept one), wavefront scans turn word
-// popcounts into ranks, and each term is added into a compact fp32 array at
-// the rank of its column; the values are written out, then the column ids,
-// staged at their ranks from the bitmap.  LDS grows with the window's
-// entries, not its width.
+// of G columns.  Symbolic: a workgroup takes a row and, for each run of
+// grains (a symbolic item) in column order, sets a presence bitmap, writes
+// each grain's popcount and, for heavy rows, keeps the bitmap in global
+// memory.  A plan kernel then cuts every row into windows of whole grains
+// whose bitmap and values fit one LDS pool (and at most max_entries entries
+// and max_grains grains), within one symbolic item where the row's bitmaps
+// are kept.  Numeric, per window: the presence bitmap is set from the terms
+// (or loaded from the kept one), wavefront scans turn word popcounts into
+// ranks, and each term is added into a compact fp32 array at the rank of
+// its column; the values are written out, then the column ids, staged at
+// their ranks from the bitmap.  LDS grows with the window's entries, not
+// its width.
 
 constexpr int WIN_BLOCK = 512;
 constexpr int WIN_UNROLL = 2;  // the numeric window kernel keeps fewer loads in flight (registers)
