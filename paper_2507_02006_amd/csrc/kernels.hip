@@ -468,7 +468,10 @@ __device__ __forceinline__ int wave_share(int rn, int nw) {
 // into equal contiguous parts, one per wavefront, whose lane l takes terms
 // l, l + WAVE, ..., so consecutive lanes read consecutive entries of a B row.
 // P32: B positions fit 32 bits (wide products, nnz(B) < 2^31).
-template <int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, typename CH, typename SEG, typename F>
+// SMALL_SCAN: a chunk of at most WAVE entries is scanned by the first
+// wavefront alone (two workgroup barriers less).
+template <int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, bool SMALL_SCAN = false, typename CH,
+          typename SEG, typename F>
 __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group<GROUP, BLOCK>& g,
                                                  CH& ch, int64_t p0, int64_t p1, const SEG& seg, F&& f) {
   using S = typename CH::shift_t;
@@ -489,14 +492,33 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
       seg(k, lo, len);
     }
     int32_t total;  // a chunk holds fewer than 2^31 terms
-    const int32_t incl = g.incl_scan32((int32_t)len, &total);
-    const int32_t excl = incl - (int32_t)len;
-    ch.rec[t].shift = (S)(lo - excl);
-    ch.rec[t].av = av;
-    ch.ex[t] = excl;
-    if (t == 0) ch.ex[GROUP] = total;
-    g.sync();
     const int nk = (int)((p1 - cb) < GROUP ? (p1 - cb) : GROUP);
+    if (SMALL_SCAN && GROUP > WAVE && nk <= WAVE) {
+      // every A entry of the chunk sits in the first wavefront: its scan
+      // alone gives the segment starts (entries past nk are never read; the
+      // lanes from nk on write ex[nk] = total)
+      if (t < WAVE) {
+        const int32_t incl = wave_incl_scan((int32_t)len);
+        const int32_t excl = incl - (int32_t)len;
+        ch.rec[t].shift = (S)(lo - excl);
+        ch.rec[t].av = av;
+        ch.ex[t] = excl;
+        if (t == WAVE - 1) {
+          ch.ex[WAVE] = incl;
+          ch.ex[GROUP] = incl;
+        }
+      }
+      g.sync();
+      total = ch.ex[GROUP];
+    } else {
+      const int32_t incl = g.incl_scan32((int32_t)len, &total);
+      const int32_t excl = incl - (int32_t)len;
+      ch.rec[t].shift = (S)(lo - excl);
+      ch.rec[t].av = av;
+      ch.ex[t] = excl;
+      if (t == 0) ch.ex[GROUP] = total;
+      g.sync();
+    }
     for (int32_t r0 = 0; r0 < total; r0 += RUN) {
       const int rn = (int)((total - r0) < RUN ? (total - r0) : RUN);
       const int per = wave_share(rn, GROUP / WAVE);
@@ -1044,7 +1066,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op,
       auto mark = [&](int j, float) { atomicOr(&bma[j >> 5], 1u << (j & 31)); };
       // eight B loads in flight per thread: the symbolic loop reads columns only
       if (short_row)
-        for_each_term_in<WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, p0, p1, HeldRange{lo, (int64_t)hi - lo},
+        for_each_term_in<WIN_BLOCK, WIN_BLOCK, false, true, 8, true>(op, g, ch, p0, p1, HeldRange{lo, (int64_t)hi - lo},
                                                                mark);
       else
         for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, row,
