@@ -647,7 +647,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU; --gpus %d is not supported "
-              "(the path would shard by row blocks, see DESIGN.md)" % args.gpus, file=sys.stderr)
+              "(the path would shard by row blocks of A and C)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import torch
