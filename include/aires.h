@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define AIRES_ABI_VERSION 4
+#define AIRES_ABI_VERSION 5
 
 /* slots of aires_stats.kind_ms per phase (row kinds in use: 0 ... 8) */
 #define AIRES_NUM_KINDS 16
@@ -210,6 +210,12 @@ typedef struct aires_plan_opts {
                                    > 0: at most this many bytes of kept
                                    symbolic bitmaps (items that do not fit
                                    are marked again in the numeric phase) */
+    int64_t slab_min_products;  /* 0: default (262144), < 0: never.  Rows of
+                                   a wide product with more products have
+                                   their windows spread over column slabs
+                                   in the numeric phase (one per XCD, so
+                                   each XCD's L2 caches one slab of B);
+                                   the result does not depend on it        */
 } aires_plan_opts;
 
 /*

@@ -101,8 +101,8 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
               hash_max_products: int = 0, wave_max_products: int = 0, window_grain_cols: int = 0,
               window_max_grains: int = 0, window_max_entries: int = 0, count_grains: int = 0,
               keep_bitmap_products: int = 0, split_min_products: int = 0, split_max_rows: int = 0,
-              window_pool_bytes: int = 0, bitmap_cache_bytes: int = 0, a_values: str = "given",
-              segmentation: str = "robw",
+              window_pool_bytes: int = 0, bitmap_cache_bytes: int = 0, slab_min_products: int = 0,
+              a_values: str = "given", segmentation: str = "robw",
               torch_allocator: bool = True, allocator=None, device: int = 0) -> Plan:
     """Plan C = A * B under a device budget (aires_tile_plan).  a_values:
     "given" (A's values) or "sym_norm" (a_ik = 1/sqrt(r_i r_k) of A's
@@ -133,6 +133,7 @@ def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: b
     o.window_max_entries = window_max_entries
     o.count_grains = count_grains
     o.keep_bitmap_products = keep_bitmap_products
+    o.slab_min_products = slab_min_products
     o.split_min_products = split_min_products
     o.split_max_rows = split_max_rows
     o.window_pool_bytes = window_pool_bytes

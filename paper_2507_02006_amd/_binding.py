@@ -30,7 +30,7 @@ CBOUND_PRODUCTS, CBOUND_DENSE, CBOUND_PAPER_EQ5, CBOUND_ROWS = 0, 1, 2, 3
 KIND_NAMES = ["empty", "dense_wave", "dense_block", "hash_128", "hash_1024", "hash_8192", "windows", "split",
               "hash_4096"]
 NUM_KINDS = 16  # kind_ms slots per phase
-ABI_VERSION = 4  # AIRES_ABI_VERSION of the header these structures mirror
+ABI_VERSION = 5  # AIRES_ABI_VERSION of the header these structures mirror
 
 
 class Csr(ctypes.Structure):
@@ -59,7 +59,8 @@ class PlanOpts(ctypes.Structure):
                 ("window_max_grains", c_i64), ("window_max_entries", c_i64), ("count_grains", c_i64),
                 ("keep_bitmap_products", c_i64), ("split_min_products", c_i64),
                 ("split_max_rows", c_i64), ("window_pool_bytes", c_i64), ("a_values", c_i32),
-                ("segmentation", c_i32), ("bitmap_cache_bytes", c_i64)]
+                ("segmentation", c_i32), ("bitmap_cache_bytes", c_i64),
+                ("slab_min_products", c_i64)]
 
 
 class PlanInfo(ctypes.Structure):

@@ -70,6 +70,7 @@ constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps ke
 constexpr int64_t kStreamTiles = 16;                       // default tile count of a streamed A
 constexpr int64_t kMinStreamTileBytes = int64_t(32) << 20;  // ... with at least this much of A per tile
 constexpr int64_t kKeepBitmapProducts = 65536;           // rows above this many products keep them
+constexpr int64_t kSlabMinProducts = 262144;             // rows above this many products: column slabs
 constexpr int64_t kWaveMaxProducts = 8192;   // rows up to this go to one wavefront
 constexpr int64_t kSplitMinProducts = 65536; // narrow rows above this are split over workgroups
 constexpr int64_t kSplitWsBytes = int64_t(256) << 20;  // their dense slots
@@ -298,6 +299,7 @@ struct aires_plan {
   int32_t win_grains = 0, win_entries = 0, count_grains = 0, win_pool_words = 0;
   int32_t ngg = 0;                 // symbolic items per wide row (runs of count_grains grains)
   int64_t keep_bitmap = 0;         // rows with more products keep their symbolic bitmaps (-1: none)
+  int32_t slab_bin = -1;           // first window bin whose rows are split over column slabs (-1: none)
   int split = 0;                   // narrow product with a split-row bin
   int64_t split_cap = 0;           // rows with dense slots for the split bin
   int64_t split_ws = 0;            // bytes of those slots
@@ -357,9 +359,23 @@ void bin_plan(aires_plan* p) {
     if (N <= dense_max) {
       add(kern::KIND_DENSE_BLOCK, INT64_MAX);
     } else {
-      // two window bins, the heavy rows last in the list (processed first)
-      add(kern::KIND_WINDOWS, std::max<int64_t>(hash_max, 1) << 8);
+      // window bins, the heavy rows last in the list (processed first): cut
+      // where rows start keeping their symbolic bitmaps and where their
+      // windows start being spread over column slabs (the bins from there on)
+      const int64_t w_lo = std::max<int64_t>(hash_max, 1);
+      const int64_t keep = o.keep_bitmap_products == 0 ? kKeepBitmapProducts : o.keep_bitmap_products;
+      const int64_t slab_min = o.slab_min_products == 0 ? kSlabMinProducts : o.slab_min_products;
+      const int64_t heavy = slab_min > 0 ? slab_min : w_lo << 8;
+      int64_t cuts[2] = {keep, heavy};
+      if (cuts[0] > cuts[1]) std::swap(cuts[0], cuts[1]);
+      const int first_window_bin = nb;
+      for (int64_t c : cuts)
+        if (c > w_lo && th.max_p[nb - 1] != c) {
+          add(kern::KIND_WINDOWS, c);
+          if (c == slab_min) p->slab_bin = nb;
+        }
       add(kern::KIND_WINDOWS, INT64_MAX);
+      if (slab_min > 0 && slab_min <= w_lo) p->slab_bin = first_window_bin;
       p->wide = 1;
       p->G = (int32_t)(o.window_grain_cols > 0 ? o.window_grain_cols : kGrainCols);
       p->nG = (int32_t)((N + p->G - 1) / p->G);
@@ -369,7 +385,7 @@ void bin_plan(aires_plan* p) {
       p->count_grains = (int32_t)(o.count_grains > 0 ? o.count_grains : kCountGrains);
       p->win_pool_words = (int32_t)((o.window_pool_bytes > 0 ? o.window_pool_bytes : kWindowPoolBytes) / 4);
       p->ngg = (p->nG + p->count_grains - 1) / p->count_grains;
-      p->keep_bitmap = o.keep_bitmap_products == 0 ? kKeepBitmapProducts : o.keep_bitmap_products;
+      p->keep_bitmap = keep;
     }
   }
   th.nb = nb;
@@ -1182,7 +1198,7 @@ struct TileWs {
   int64_t* icount = nullptr;     // [n + 1] windows per bin row, scanned  (wide)
   kern::WinItem* items = nullptr;
   int64_t nitems = 0;            // host copy of icount[n]
-  int32_t* wcounter = nullptr;   // row counter of the window kernel
+  int32_t* wcounter = nullptr;   // row counters of the window kernels (shared, then one per column slab)
   void* scan_ws = nullptr;
   kern::SplitWs split{nullptr, nullptr, 0};  // dense slots of split rows (shared by all tiles)
   int64_t* bm_off = nullptr;     // [n * ngg] kept bitmaps of the symbolic items (wide, in-core)
@@ -1202,7 +1218,7 @@ aires_status alloc_tile_ws(aires_plan* p, DevPool& ws, int64_t n, bool with_list
     ST_TRY(ws.get_n(kern::MAX_BINS + 1, &w.binoff));
   }
   ST_TRY(ws.get_n(2 * kern::MAX_BINS + 1, &w.cntcur));
-  ST_TRY(ws.get_n(1, &w.wcounter));
+  ST_TRY(ws.get_n(1 + kern::WIN_MAX_SLABS, &w.wcounter));
   ST_TRY(ws.get(kern::scan_workspace_bytes(n), &w.scan_ws));
   return AIRES_OK;
 }
@@ -1241,6 +1257,8 @@ kern::WindowParams window_params(const aires_plan* p, const TileWs& w) {
   wp.bm_off = w.bm_off;
   wp.P = w.P;
   wp.bm_min_products = p->keep_bitmap;
+  wp.slab_bin = p->slab_bin;
+  wp.nslab = 1;  // set at the numeric launch from its grid
   return wp;
 }
 

@@ -58,6 +58,10 @@ struct Outputs {
 
 // One column window of one wide row: grains [g0, g1), n entries of C,
 // written at C position crp[row] + roff.
+// Column slabs of the numeric window kernel: one per XCD of the MI355X,
+// whose L2 caches are separate.
+constexpr int WIN_MAX_SLABS = 8;
+
 struct WinItem {
   int32_t row;
   uint16_t g0, g1;
@@ -73,7 +77,11 @@ struct WindowParams {
   int32_t pool_words;      // LDS words a window's bitmap (2 per bitmap word) and values (1 per entry) share
   int64_t* item_count;     // [1 + d]: windows of the d-th row of the bins; scanned into offsets
   WinItem* items;          // filled in the numeric sweep
-  int32_t* row_counter;    // zeroed before each window launch, symbolic and numeric (dynamic row scheduling)
+  // zeroed before each window launch (dynamic row scheduling): [0] shared by
+  // all workgroups, [1 + x] the rows of the slab bins for column slab x
+  int32_t* row_counter;
+  int32_t slab_bin;        // first bin whose rows' windows are spread over column slabs (-1: none)
+  int32_t nslab;           // column slabs of the numeric launch (1..WIN_MAX_SLABS)
   // Presence bitmaps kept by the symbolic phase for heavy rows (nullptr:
   // none): the words of symbolic item (row, run of grains) start at
   // bm_off[row * items_per_row + item] (-1: not kept), so the numeric phase

@@ -1199,6 +1199,11 @@ __host__ __device__ constexpr size_t window_lds_bytes(int pool_words) {
 
 // Numeric phase of wide rows.  Workgroups take rows from a shared counter
 // (the heaviest bin first) and walk each row's windows in column order.
+// The rows of the slab bins (the heaviest) are taken once per column slab:
+// workgroup b serves slab b mod nslab through that slab's counter and does
+// the row's windows whose middle grain lies in the slab, then joins the
+// shared counter.  The hardware places workgroup b on XCD b mod 8, so each
+// XCD's L2 holds the B segments of one slab of columns rather than of all.
 // For a row with at most WIN_BLOCK entries each thread keeps one (k, a_ik)
 // of the row in registers with the position where B_k's segment for the
 // current window starts; consecutive windows share a grain boundary, so a
@@ -1212,6 +1217,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                                                            const WindowParams wp, const Outputs out) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t s_row;
+  __shared__ int s_shared;  // this workgroup's slab rows are done
   const int WPG = op.G / 32;  // 32-bit words per grain of a kept symbolic bitmap
   constexpr uint64_t BITS = (uint64_t(1) << WIN_WORD_BITS) - 1u;
   uint64_t* bw = reinterpret_cast<uint64_t*>(smem);  // presence bits | rank of the word's first bit << 48
@@ -1224,16 +1230,45 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
   constexpr int RUN = WIN_BLOCK * SEG_PER_THREAD;
   const int32_t* list = bv.list + bv.binoff[bv.bin];
   const int64_t cnt = bv.binoff[bv.last() + 1] - bv.binoff[bv.bin];
+  // the slab bins are the last of the view: their rows end the list
+  const int64_t nslab_rows = wp.slab_bin >= 0 ? bv.binoff[bv.last() + 1] - bv.binoff[wp.slab_bin] : 0;
+  const int slab = (int)(blockIdx.x % (unsigned)wp.nslab);
+  if (t == 0) s_shared = nslab_rows > 0 ? 0 : 1;
 
   for (;;) {
     __syncthreads();
-    if (t == 0) s_row = atomicAdd(wp.row_counter, 1);
+    if (t == 0) {
+      int64_t v = 0;
+      if (!s_shared) {
+        v = atomicAdd(wp.row_counter + 1 + slab, 1);
+        if (v >= nslab_rows) s_shared = 1;
+      }
+      if (s_shared) v = nslab_rows + atomicAdd(wp.row_counter, 1);
+      s_row = v;
+    }
     __syncthreads();
     const int64_t dd = s_row;
     if (dd >= cnt) break;
     const int64_t d = cnt - 1 - dd;  // the heavy bin sits at the end of the list
     const int64_t row = list[d];
-    const int64_t i0 = wp.item_count[d], i1 = wp.item_count[d + 1];
+    int64_t i0 = wp.item_count[d], i1 = wp.item_count[d + 1];
+    if (dd < nslab_rows) {
+      // this slab's windows: a run of the row's (column-ordered) windows,
+      // counted by each wavefront from their headers, 64 at a time
+      int64_t j0 = i0, j1 = i0;
+      for (int64_t c = i0; c < i1; c += WAVE) {
+        const int64_t q = c + lane_id();
+        int sl = wp.nslab;
+        if (q < i1) {
+          const WinItem w = wp.items[q];
+          sl = (int)(((int64_t)w.g0 + w.g1) * wp.nslab / (2 * (int64_t)op.nG));
+        }
+        j0 += __popcll(__ballot(sl < slab));
+        j1 += __popcll(__ballot(sl <= slab));
+      }
+      i0 = j0;
+      i1 = j1;
+    }
     const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
     const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
     const int64_t rbase = out.crp[row];
@@ -1748,7 +1783,7 @@ hipError_t win_numeric_t(const Operands& op, const BinView& bv, const WindowPara
   if (pg > 8192) pg = 8192;
   hipLaunchKernelGGL(k_win_fill, dim3((unsigned)pg), dim3(256), 0, s, bv, op.nG, op.G, wp);
   if (nitems <= 0) return hipGetLastError();
-  hipError_t ez = hipMemsetAsync(wp.row_counter, 0, sizeof(int32_t), s);
+  hipError_t ez = hipMemsetAsync(wp.row_counter, 0, sizeof(int32_t) * (1 + WIN_MAX_SLABS), s);
   if (ez != hipSuccess) return ez;
   auto kern = k_win_rows<RA, RB>;
   const size_t lds = window_lds_bytes<RB>(wp.pool_words);
@@ -1757,7 +1792,9 @@ hipError_t win_numeric_t(const Operands& op, const BinView& bv, const WindowPara
     if (e != hipSuccess) return e;
   }
   const int64_t grid = grid_for(kern, WIN_BLOCK, lds, 1, ub_rows);
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WIN_BLOCK), lds, s, op, bv, wp, out);
+  WindowParams wq = wp;
+  wq.nslab = (int32_t)(grid < WIN_MAX_SLABS ? grid : WIN_MAX_SLABS);  // every slab has a workgroup
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WIN_BLOCK), lds, s, op, bv, wq, out);
   return hipGetLastError();
 }
 

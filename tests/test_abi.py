@@ -28,10 +28,10 @@ def test_exports_every_declared_symbol():
 
 def test_version_and_strings():
     lib = B_.load()
-    assert lib.aires_abi_version() == 4
+    assert lib.aires_abi_version() == 5
     # the binding's structures, the header and the library agree on the version
     hdr = open(B_.HEADER).read()
-    assert int(re.search(r"#define AIRES_ABI_VERSION (\d+)", hdr).group(1)) == B_.ABI_VERSION == 4
+    assert int(re.search(r"#define AIRES_ABI_VERSION (\d+)", hdr).group(1)) == B_.ABI_VERSION == 5
     assert int(re.search(r"#define AIRES_NUM_KINDS (\d+)", hdr).group(1)) == B_.NUM_KINDS
     assert lib.aires_status_string(0) == b"AIRES_OK"
     assert lib.aires_status_string(B_.E_BUDGET) == b"AIRES_E_BUDGET"

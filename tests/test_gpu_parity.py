@@ -104,6 +104,15 @@ PATHS = {
     "windows_pool": dict(dense_max_cols=64, hash_max_products=-1, window_grain_cols=64,
                          window_max_grains=16, window_max_entries=1000, count_grains=8,
                          window_pool_bytes=4 * 100),
+    # the numeric kernel's column slabs: every window row's windows spread
+    # over the slabs (one per XCD; several slabs get none of a row's
+    # windows), then only rows above 50 products, the rest from the shared
+    # counter, with every window row keeping its symbolic bitmaps
+    "windows_slabs": dict(dense_max_cols=64, hash_max_products=-1, window_grain_cols=64,
+                          window_max_grains=2, window_max_entries=64, count_grains=3, slab_min_products=1),
+    "windows_slabs_kept": dict(dense_max_cols=64, hash_max_products=-1, window_grain_cols=64,
+                               window_max_grains=2, window_max_entries=64, count_grains=3,
+                               keep_bitmap_products=1, slab_min_products=50),
     # 2048 < N <= 16384 handled as narrow: hash bins then workgroup dense rows
     "narrow_block_hash": dict(dense_max_cols=200, hash_max_products=512),
     # narrow rows split over workgroups (dense slots in global memory); then
@@ -166,6 +175,18 @@ def test_cfg3_scaled_partial_bitmap_cache(torch_gpu, cache_bytes):
     check(torch_gpu, A, B, "cfg3 n=40000 bitmap cache %d bytes" % cache_bytes, keep_bitmap_products=1,
           bitmap_cache_bytes=cache_bytes, window_grain_cols=4096, window_max_grains=8, window_max_entries=16384,
           count_grains=4)
+
+
+@pytest.mark.parametrize("slab,keep", [(1, 0), (20000, 1), (-1, 0)])
+def test_cfg3_scaled_column_slabs(torch_gpu, slab, keep):
+    """Windows of the rows above `slab` products spread over the numeric
+    kernel's column slabs (1: every window row; -1: none), with 1024-column
+    grains so that a row has windows in every slab; kept bitmaps from the
+    default threshold or for every row."""
+    A, B = workloads.workload(3, n=40000)
+    check(torch_gpu, A, B, "cfg3 n=40000 slabs above %d products, keep %d" % (slab, keep),
+          slab_min_products=slab, keep_bitmap_products=keep, window_grain_cols=1024, window_max_grains=3,
+          window_max_entries=1024, count_grains=5)
 
 
 def test_cfg3_scaled_small_windows(torch_gpu):
@@ -296,11 +317,12 @@ def test_streamed_wide(torch_gpu):
     A, B = workloads.workload(3, n=20000)
     ref = oracle.spgemm(A, B)
     say("streamed wide cfg3 n=20000")
-    with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 34, c_on_host=True, max_tile_rows=5000,
-                         dense_max_cols=4096, window_grain_cols=4096) as plan:
-        C = aires.spgemm(plan)
-        assert_match(C.rp, C.col, C.val, ref)
-        C.free()
+    for slab in (0, 1):
+        with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 34, c_on_host=True, max_tile_rows=5000,
+                             dense_max_cols=4096, window_grain_cols=4096, slab_min_products=slab) as plan:
+            C = aires.spgemm(plan)
+            assert_match(C.rp, C.col, C.val, ref)
+            C.free()
 
 
 # ------------------------------------------------------------- edge cases
@@ -340,6 +362,8 @@ def test_edge_hub_row(torch_gpu):
     check(torch_gpu, A, B2, "hub row wide")
     check(torch_gpu, A, B2, "hub row wide, kept bitmaps", keep_bitmap_products=1)
     check(torch_gpu, A, B2, "hub row wide, no kept bitmaps", keep_bitmap_products=-1)
+    # three rows: a numeric grid of three workgroups, so three column slabs
+    check(torch_gpu, A, B2, "hub row wide, column slabs", slab_min_products=1)
 
 
 def test_edge_stored_zeros_kept(torch_gpu):
