@@ -288,6 +288,35 @@ aires_status aires_tile_plan(const aires_csr *A, const aires_csr *B, uint64_t hb
 aires_status aires_tile_plan_file(const aires_file_csr *A, const aires_csr *B, uint64_t hbm_budget,
                                   const aires_plan_opts *opts, aires_plan **out);
 
+/*
+ * aires_csr_read_file -- a CSR held in a file (laid out as for
+ * aires_tile_plan_file) brought whole into device memory (mem =
+ * AIRES_MEM_DEVICE) or pinned host memory (AIRES_MEM_HOST_PINNED): the way
+ * the storage tier of Sec. III-B moves B from the SSD to the GPU before the
+ * tiles stream, here through host memory, as this platform has no GPU file
+ * API.  For device memory the column indices and values are read in chunks
+ * of chunk_bytes (0: 64 MiB; rounded up to 4 KiB) into two pinned staging
+ * buffers, and each chunk is sent with hipMemcpyAsync on `stream` (a
+ * hipStream_t; NULL: the null stream) while the next one is read.  Row
+ * pointers are checked (0 to nnz, non-decreasing) and widened to int64.
+ * On success *out holds the matrix, owned by the caller until
+ * aires_csr_out_free; device arrays come from `alloc` (NULL: hipMallocAsync)
+ * on `stream`.  Returns once every copy is complete.  With st non-NULL it
+ * receives the bytes read from the file and the times taken.
+ * Errors: AIRES_E_INVALID_ARG (NULL, mem, negative offsets or chunk size,
+ * file cannot be opened or is too short), AIRES_E_DIM, AIRES_E_OVERFLOW,
+ * AIRES_E_INVALID_CSR (row pointers), AIRES_E_OOM, AIRES_E_HIP; *out is
+ * untouched on error.
+ */
+typedef struct aires_read_stats {
+    int64_t bytes_read;         /* bytes of the three arrays read           */
+    double read_ms;             /* time in file reads                      */
+    double total_ms;            /* the whole call                          */
+} aires_read_stats;
+
+aires_status aires_csr_read_file(const aires_file_csr *M, int32_t mem, const aires_allocator *alloc, void *stream,
+                                 int64_t chunk_bytes, aires_csr_out *out, aires_read_stats *st);
+
 typedef struct aires_plan_info {
     int64_t ntiles;
     int64_t m, k, n;            /* A is m x k, B is k x n                  */

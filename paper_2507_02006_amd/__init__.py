@@ -20,8 +20,9 @@ from dataclasses import dataclass
 
 from . import _binding as B_
 
-__all__ = ["tile_plan", "tile_plan_file", "spgemm", "spmm", "stream_tiles", "plan_info", "plan_tile", "plan_stats",
-           "plan_tile_stats", "spgemm_noalloc", "Plan", "Output", "AiresError", "to_device", "to_pinned"]
+__all__ = ["tile_plan", "tile_plan_file", "read_csr_file", "spgemm", "spmm", "stream_tiles", "plan_info",
+           "plan_tile", "plan_stats", "plan_tile_stats", "spgemm_noalloc", "Plan", "Output", "AiresError",
+           "to_device", "to_pinned"]
 
 AiresError = B_.AiresError
 
@@ -93,6 +94,29 @@ def tile_plan_file(A, B, hbm_budget: int = 0, *, c_on_host: bool = True, c_bound
     B_.check(lib.aires_tile_plan_file(ctypes.byref(fa), ctypes.byref(b), int(hbm_budget), ctypes.byref(o),
                                       ctypes.byref(h)), "aires_tile_plan_file")
     return Plan(h.value, (fa, path), B, alloc, o)
+
+
+def _file_csr(F) -> B_.FileCsr:
+    return B_.FileCsr(int(F["nrows"]), int(F["ncols"]), int(F["nnz"]),
+                      B_.IDX_I64 if F["rp_dtype"] == "int64" else B_.IDX_I32, int(bool(F.get("direct_io", True))),
+                      F["path"].encode(), int(F["row_ptr_offset"]), int(F["col_idx_offset"]), int(F["vals_offset"]))
+
+
+def read_csr_file(F, mem: str = "device", chunk_bytes: int = 0, stream=None, device: int = 0):
+    """A CSR held in a file (a dict as for ``tile_plan_file``, optionally
+    with ``direct_io``) read whole into device memory (torch tensors from
+    torch's allocator) or pinned host memory (numpy views owned by the
+    library) through aires_csr_read_file.  Returns (Output, stats dict)."""
+    if mem not in ("device", "pinned"):
+        raise ValueError("mem must be 'device' or 'pinned'")
+    lib = B_.load()
+    fc = _file_csr(F)
+    out, st = B_.CsrOut(), B_.ReadStats()
+    alloc = B_.TorchAllocator(device) if mem == "device" else None
+    B_.check(lib.aires_csr_read_file(ctypes.byref(fc), B_.MEM_DEVICE if mem == "device" else B_.MEM_HOST_PINNED,
+                                     ctypes.byref(alloc.struct) if alloc else None, _stream_handle(stream),
+                                     int(chunk_bytes), ctypes.byref(out), ctypes.byref(st)), "aires_csr_read_file")
+    return Output(out, alloc), {"bytes_read": st.bytes_read, "read_ms": st.read_ms, "total_ms": st.total_ms}
 
 
 def tile_plan(A, B, hbm_budget: int = 0, *, validate: bool = False, c_on_host: bool = False,

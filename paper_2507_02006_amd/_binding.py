@@ -97,6 +97,10 @@ class FileCsr(ctypes.Structure):
                 ("vals_offset", c_i64)]
 
 
+class ReadStats(ctypes.Structure):
+    _fields_ = [("bytes_read", c_i64), ("read_ms", c_dbl), ("total_ms", c_dbl)]
+
+
 _lib = None
 
 
@@ -122,6 +126,7 @@ def load() -> ctypes.CDLL:
         "aires_plan_opts_default": (ctypes.c_int, [P(PlanOpts)]),
         "aires_tile_plan": (ctypes.c_int, [P(Csr), P(Csr), c_u64, P(PlanOpts), P(c_vp)]),
         "aires_tile_plan_file": (ctypes.c_int, [P(FileCsr), P(Csr), c_u64, P(PlanOpts), P(c_vp)]),
+        "aires_csr_read_file": (ctypes.c_int, [P(FileCsr), c_i32, c_vp, c_vp, c_i64, P(CsrOut), P(ReadStats)]),
         "aires_plan_info": (ctypes.c_int, [c_vp, P(PlanInfo)]),
         "aires_plan_info_get": (ctypes.c_int, [c_vp, P(PlanInfo)]),
         "aires_plan_tile_stats": (ctypes.c_int, [c_vp, c_i64, P(TileStats)]),

@@ -215,6 +215,16 @@ struct FileSrc {
 
 constexpr int64_t kIoAlign = 4096;
 
+// Opens a file for reading, with direct I/O when asked for and the
+// filesystem allows it (else buffered reads).
+aires_status open_file_src(const char* path, int direct_io, FileSrc& f) {
+  f.fd = open(path, O_RDONLY | (direct_io ? O_DIRECT : 0));
+  if (f.fd >= 0 && direct_io) f.direct = true;
+  if (f.fd < 0 && direct_io) f.fd = open(path, O_RDONLY);  // no direct I/O on this filesystem
+  if (f.fd < 0) return fail(AIRES_E_INVALID_ARG, "cannot open %s: %s", path, strerror(errno));
+  return AIRES_OK;
+}
+
 // Reads file bytes [off, off + len) into dst; *shift receives where they
 // start in dst (always 0 now; kept for the callers' buffer layout).
 // Ranges of 8 MiB or more are read by several host threads.
@@ -1072,10 +1082,7 @@ aires_status aires_tile_plan_file(const aires_file_csr* A, const aires_csr* B, u
   if (A->row_ptr_offset < 0 || A->col_idx_offset < 0 || A->vals_offset < 0)
     return fail(AIRES_E_INVALID_ARG, "negative file offset");
   auto f = std::make_unique<FileSrc>();
-  f->fd = open(A->path, O_RDONLY | (A->direct_io ? O_DIRECT : 0));
-  if (f->fd >= 0 && A->direct_io) f->direct = true;
-  if (f->fd < 0 && A->direct_io) f->fd = open(A->path, O_RDONLY);  // no direct I/O on this filesystem
-  if (f->fd < 0) return fail(AIRES_E_INVALID_ARG, "cannot open %s: %s", A->path, strerror(errno));
+  ST_TRY(open_file_src(A->path, A->direct_io, *f));
   f->col_off = A->col_idx_offset;
   f->val_off = A->vals_offset;
   // A's row pointers to host memory (pinned where a device is present:
@@ -1124,6 +1131,154 @@ aires_status aires_plan_tile(const aires_plan* plan, int64_t t, aires_tile* tile
 }
 
 void aires_plan_destroy(aires_plan* plan) { delete plan; }
+
+aires_status aires_csr_read_file(const aires_file_csr* M, int32_t mem, const aires_allocator* alloc, void* stream,
+                                 int64_t chunk_bytes, aires_csr_out* out, aires_read_stats* st) {
+  if (!M || !M->path || !out) return fail(AIRES_E_INVALID_ARG, "NULL argument");
+  if (mem != AIRES_MEM_DEVICE && mem != AIRES_MEM_HOST_PINNED)
+    return fail(AIRES_E_INVALID_ARG, "mem %d: AIRES_MEM_DEVICE or AIRES_MEM_HOST_PINNED", mem);
+  if (M->nrows < 0 || M->ncols < 0 || M->nnz < 0) return fail(AIRES_E_DIM, "the matrix has a negative size");
+  if (M->rp_type != AIRES_IDX_I32 && M->rp_type != AIRES_IDX_I64)
+    return fail(AIRES_E_INVALID_ARG, "rp_type %d invalid", M->rp_type);
+  if (M->rp_type == AIRES_IDX_I32 && M->nnz > INT32_MAX) return fail(AIRES_E_OVERFLOW, "nnz needs int64 row pointers");
+  if (M->ncols > INT32_MAX) return fail(AIRES_E_OVERFLOW, "ncols exceeds int32 column indices");
+  if (M->row_ptr_offset < 0 || M->col_idx_offset < 0 || M->vals_offset < 0)
+    return fail(AIRES_E_INVALID_ARG, "negative file offset");
+  if (chunk_bytes < 0) return fail(AIRES_E_INVALID_ARG, "negative chunk size");
+  const int64_t chunk = chunk_bytes > 0 ? (chunk_bytes + kIoAlign - 1) / kIoAlign * kIoAlign : int64_t(64) << 20;
+  const auto t0 = std::chrono::steady_clock::now();
+  double read_ms = 0;
+  FileSrc f;
+  ST_TRY(open_file_src(M->path, M->direct_io, f));
+  auto timed_read = [&](int64_t off, int64_t len, char* dst) {
+    const auto r0 = std::chrono::steady_clock::now();
+    int64_t shift = 0;
+    const aires_status s = file_read(f, off, len, dst, &shift);
+    read_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - r0).count();
+    return s;
+  };
+  // row pointers: read, checked (0 .. nnz, non-decreasing) and widened to int64
+  const int64_t n = M->nrows, nnz = M->nnz, s = M->rp_type == AIRES_IDX_I64 ? 8 : 4;
+  std::vector<char> rpf((size_t)((n + 1) * s));
+  ST_TRY(timed_read(M->row_ptr_offset, (n + 1) * s, rpf.data()));
+  std::vector<int64_t> rp((size_t)n + 1);
+  std::vector<int64_t> first_drop(17, INT64_MAX);  // per host thread: the first row whose pointer decreases
+  parallel_ranges(n + 1, [&](int64_t lo, int64_t hi, int t) {
+    for (int64_t i = lo; i < hi; ++i)
+      rp[(size_t)i] = s == 8 ? reinterpret_cast<const int64_t*>(rpf.data())[i]
+                             : (int64_t) reinterpret_cast<const int32_t*>(rpf.data())[i];
+    const int64_t prev = lo > 0 ? (s == 8 ? reinterpret_cast<const int64_t*>(rpf.data())[lo - 1]
+                                          : (int64_t) reinterpret_cast<const int32_t*>(rpf.data())[lo - 1])
+                                : INT64_MIN;
+    for (int64_t i = lo; i < hi; ++i)
+      if (rp[(size_t)i] < (i > lo ? rp[(size_t)i - 1] : prev)) {
+        first_drop[(size_t)t] = i - 1;
+        break;
+      }
+  });
+  if (rp[0] != 0 || rp[(size_t)n] != nnz) return fail(AIRES_E_INVALID_CSR, "row pointers do not run from 0 to nnz");
+  const int64_t drop = *std::min_element(first_drop.begin(), first_drop.end());
+  if (drop != INT64_MAX) return fail(AIRES_E_INVALID_CSR, "row pointers decrease at row %lld", (long long)drop);
+  const hipStream_t hs = (hipStream_t)stream;
+  const aires_allocator a = alloc ? *alloc : kDefaultAllocator;
+  const bool host = mem == AIRES_MEM_HOST_PINNED;
+  int64_t* d_rp = nullptr;
+  int32_t* d_col = nullptr;
+  float* d_val = nullptr;
+  char* stage[2] = {nullptr, nullptr};
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  auto release = [&](bool keep_out) {
+    for (int i = 0; i < 2; ++i) {
+      if (stage[i]) (void)hipHostFree(stage[i]);
+      if (ev[i]) (void)hipEventDestroy(ev[i]);
+    }
+    if (keep_out) return;
+    void* arr[3] = {d_rp, d_col, d_val};
+    for (void* q : arr) {
+      if (!q) continue;
+      if (host) (void)hipHostFree(q);
+      else a.free(a.ctx, q, (void*)hs);
+    }
+  };
+  auto get = [&](int64_t bytes, void** q) {
+    if (bytes <= 0) return AIRES_OK;
+    if (host) {
+      if (hipHostMalloc(q, (size_t)bytes, hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        *q = nullptr;
+      }
+    } else {
+      *q = a.alloc(a.ctx, (size_t)bytes, (void*)hs);
+    }
+    return *q ? AIRES_OK : fail(AIRES_E_OOM, "allocation of %lld bytes failed", (long long)bytes);
+  };
+  aires_status rc = get(8 * (n + 1), reinterpret_cast<void**>(&d_rp));
+  if (rc == AIRES_OK) rc = get(4 * nnz, reinterpret_cast<void**>(&d_col));
+  if (rc == AIRES_OK) rc = get(4 * nnz, reinterpret_cast<void**>(&d_val));
+  if (rc != AIRES_OK) {
+    release(false);
+    return rc;
+  }
+  int64_t bytes = (n + 1) * s;
+  if (host) {
+    // straight into the caller's pinned arrays
+    std::memcpy(d_rp, rp.data(), (size_t)(8 * (n + 1)));
+    if (nnz > 0) rc = timed_read(M->col_idx_offset, 4 * nnz, reinterpret_cast<char*>(d_col));
+    if (rc == AIRES_OK && nnz > 0) rc = timed_read(M->vals_offset, 4 * nnz, reinterpret_cast<char*>(d_val));
+    bytes += 8 * nnz;
+  } else {
+    // two pinned staging buffers: chunk c + 1 is read from the file while
+    // chunk c is copied to the device
+    auto hip_ok = [&](hipError_t e, const char* what) {
+      if (e == hipSuccess) return AIRES_OK;
+      (void)hipGetLastError();
+      return fail(AIRES_E_HIP, "%s: %s", what, hipGetErrorString(e));
+    };
+    for (int i = 0; i < 2 && rc == AIRES_OK; ++i) {
+      rc = hip_ok(hipHostMalloc(reinterpret_cast<void**>(&stage[i]), (size_t)chunk, hipHostMallocDefault), "hipHostMalloc");
+      if (rc == AIRES_OK) rc = hip_ok(hipEventCreateWithFlags(&ev[i], hipEventDisableTiming), "hipEventCreate");
+    }
+    int64_t c = 0;
+    auto send = [&](const char* src_host, int64_t len, char* dst_dev, int64_t file_off) {
+      for (int64_t o = 0; o < len && rc == AIRES_OK; o += chunk, ++c) {
+        const int64_t l = std::min(chunk, len - o);
+        char* buf = stage[c & 1];
+        if (c >= 2) rc = hip_ok(hipEventSynchronize(ev[c & 1]), "hipEventSynchronize");  // its last copy is done
+        if (rc != AIRES_OK) break;
+        if (src_host) std::memcpy(buf, src_host + o, (size_t)l);
+        else rc = timed_read(file_off + o, l, buf);
+        if (rc == AIRES_OK) rc = hip_ok(hipMemcpyAsync(dst_dev + o, buf, (size_t)l, hipMemcpyHostToDevice, hs), "hipMemcpyAsync");
+        if (rc == AIRES_OK) rc = hip_ok(hipEventRecord(ev[c & 1], hs), "hipEventRecord");
+      }
+    };
+    if (rc == AIRES_OK) send(reinterpret_cast<const char*>(rp.data()), 8 * (n + 1), reinterpret_cast<char*>(d_rp), 0);
+    if (rc == AIRES_OK) send(nullptr, 4 * nnz, reinterpret_cast<char*>(d_col), M->col_idx_offset);
+    if (rc == AIRES_OK) send(nullptr, 4 * nnz, reinterpret_cast<char*>(d_val), M->vals_offset);
+    const aires_status sync = hip_ok(hipStreamSynchronize(hs), "hipStreamSynchronize");  // staging is freed next
+    if (rc == AIRES_OK) rc = sync;
+    bytes += 8 * nnz;
+  }
+  if (rc != AIRES_OK) {
+    release(false);
+    return rc;
+  }
+  release(true);
+  std::memset(out, 0, sizeof *out);
+  out->nrows = n;
+  out->ncols = M->ncols;
+  out->nnz = nnz;
+  out->row_ptr = d_rp;
+  out->col_idx = d_col;
+  out->vals = d_val;
+  out->mem = mem;
+  out->_owner = new OutOwner{a, hs, host ? 1 : 0};
+  if (st) {
+    st->bytes_read = bytes;
+    st->read_ms = read_ms;
+    st->total_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  }
+  return AIRES_OK;
+}
 
 }  // extern "C"
 

@@ -451,3 +451,38 @@ def test_file_plan_errors(tmp_path):
     with pytest.raises(aires.AiresError) as e:
         _plan_file(meta, Bm, budget, segmentation=B_.SEG_MAXFILL, **rows)
     assert e.value.status == B_.E_UNSUPPORTED
+
+
+def test_read_csr_file_errors(tmp_path):
+    """aires_csr_read_file's argument and file checks, all taken before any
+    device work; *out is left as it was."""
+    lib = B_.load()
+    A, _ = workloads.workload(5, n=3000)
+    meta = workloads.write_csr_file(str(tmp_path / "a.csr"), A)
+
+    def call(m=meta, mem=B_.MEM_DEVICE, chunk=0, null=False):
+        out = B_.CsrOut()
+        out.nnz = -7
+        fc = None if null else aires._file_csr(m)
+        st = lib.aires_csr_read_file(ctypes.byref(fc) if fc is not None else None, mem, None, None, chunk,
+                                     ctypes.byref(out), None)
+        assert out.nnz == -7 and not out.row_ptr
+        return st, lib.aires_last_error()
+
+    assert call(null=True)[0] == B_.E_INVALID_ARG
+    assert call(mem=B_.MEM_HOST)[0] == B_.E_INVALID_ARG            # pageable host memory is not offered
+    assert call(chunk=-1)[0] == B_.E_INVALID_ARG
+    assert call(dict(meta, nrows=-1))[0] == B_.E_DIM
+    assert call(dict(meta, path=str(tmp_path / "missing")))[0] == B_.E_INVALID_ARG
+    st, msg = call(dict(meta, nnz=meta["nnz"] + 1))                # row pointers that do not end at nnz
+    assert st == B_.E_INVALID_CSR and b"0 to nnz" in msg
+    short = tmp_path / "short.csr"
+    short.write_bytes((tmp_path / "a.csr").read_bytes()[:meta["row_ptr_offset"] + 100])
+    st, msg = call(dict(meta, path=str(short)))
+    assert st == B_.E_INVALID_ARG and b"ends before" in msg
+    # row pointers 0, 3, 2, 4: a decreasing step
+    bad = workloads.CSR(3, 5, np.array([0, 3, 2, 4], np.int32), np.array([0, 1, 2, 3], np.int32),
+                        np.ones(4, np.float32))
+    mb = workloads.write_csr_file(str(tmp_path / "bad.csr"), bad)
+    st, msg = call(mb)
+    assert st == B_.E_INVALID_CSR and b"decrease" in msg

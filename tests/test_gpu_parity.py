@@ -777,3 +777,57 @@ def test_storage_tier_streamed(torch_gpu, tmp_path, direct, c_on_host, values):
     assert st["storage_ms"] > 0 and sum(t["storage_ms"] for t in ts) == pytest.approx(st["storage_ms"])
     if values == "given":
         assert st["h2d_bytes"] == A.nbytes() + B.nbytes() + 8 * (info.ntiles - 1)
+
+
+# ----------------------------------------------- B on storage (a file) too
+
+@pytest.mark.parametrize("which,mem,direct,chunk", [("features", "device", 1, 1 << 20), ("features", "device", 0, 0),
+                                                     ("graph", "device", 1, 4096), ("features", "pinned", 1, 0),
+                                                     ("graph", "pinned", 0, 0)])
+def test_read_csr_file(torch_gpu, tmp_path, which, mem, direct, chunk):
+    """A CSR read whole from a file (aires_csr_read_file) into device or
+    pinned memory, in chunks through two pinned staging buffers (1 MiB:
+    several chunks and a ragged last one; 4 KiB: many): row pointers widened
+    to int64, every array equal to what was written, bitwise."""
+    import paper_2507_02006_amd as aires
+    A, X = workloads.workload(5, n=60000)
+    M = X if which == "features" else workloads.workload(1)[0]
+    meta = workloads.write_csr_file(str(tmp_path / "m.csr"), M)
+    meta["direct_io"] = bool(direct)
+    say("read_csr_file %s mem=%s direct=%d chunk=%d nnz=%d" % (which, mem, direct, chunk, M.nnz))
+    out, st = aires.read_csr_file(meta, mem=mem, chunk_bytes=chunk)
+    if mem == "device":
+        torch_gpu.cuda.synchronize()
+        rp, col, val = out.rp.cpu().numpy(), out.col.cpu().numpy(), out.val.cpu().numpy()
+    else:
+        rp, col, val = out.rp.copy(), out.col.copy(), out.val.copy()
+        out.free()
+    assert rp.dtype == np.int64 and np.array_equal(rp, M.rp.astype(np.int64))
+    assert np.array_equal(col, M.col) and np.array_equal(val.view(np.int32), M.val.view(np.int32))
+    assert st["bytes_read"] == M.rp.nbytes + 8 * M.nnz and st["total_ms"] >= st["read_ms"] > 0
+
+
+@pytest.mark.parametrize("c_on_host", [True, False])
+def test_storage_tier_both_ways(torch_gpu, tmp_path, c_on_host):
+    """A and B both in files: B read once into device memory before the
+    tiles (aires_csr_read_file), A's tiles read from their file and streamed
+    (aires_tile_plan_file); the same C as the oracle."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(5, n=60000)
+    ref = oracle.spgemm(A, B)
+    ma = workloads.write_csr_file(str(tmp_path / "a.csr"), A)
+    mb = workloads.write_csr_file(str(tmp_path / "b.csr"), B)
+    say("storage tier, A and B in files, cfg5 n=60000 c_on_host=%s" % c_on_host)
+    Bd, st = aires.read_csr_file(mb, mem="device", chunk_bytes=1 << 20)
+    dB = (B.nrows, B.ncols, Bd.rp, Bd.col, Bd.val)
+    budget = B.nbytes() + 8 * (B.nrows + 1) + (24 << 20) + 8 * (A.nrows + 1) + 2 * 3_000_000
+    with aires.tile_plan_file(ma, dB, budget if c_on_host else 1 << 32, c_on_host=c_on_host,
+                              max_tile_bytes=200_000) as plan:
+        assert aires.plan_info(plan).ntiles >= 5
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        if c_on_host:
+            assert_match(C.rp, C.col, C.val, ref)
+            C.free()
+        else:
+            assert_match(C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy(), ref)
