@@ -1201,7 +1201,7 @@ aires_status aires_csr_read_file(const aires_file_csr* M, int32_t mem, const air
     }
   };
   auto get = [&](int64_t bytes, void** q) {
-    if (bytes <= 0) return AIRES_OK;
+    bytes = std::max<int64_t>(bytes, 4);  // an empty array is still a block of its own
     if (host) {
       if (hipHostMalloc(q, (size_t)bytes, hipHostMallocDefault) != hipSuccess) {
         (void)hipGetLastError();
