@@ -824,9 +824,11 @@ aires_status plan_impl(const aires_csr* A, const aires_csr* B, uint64_t hbm_budg
   // derived values of a streamed A need all of A's row pointers on the device
   if (a_streamed && a_sym_norm) resident += (m + 1) * sA;
   if (!a_streamed) {
-    // A and C.row_ptr resident; bin lists and window bookkeeping for all rows
-    resident += p->info.a_bytes + 8 * (m + 1) + (4 + (p->wide ? 4 * nG + 8 + 8 * p->ngg : 0)) * m;
-    per_row_ws = 8;
+    // A and C.row_ptr resident; products, bin lists and window bookkeeping
+    // for all rows (the numeric sweep of a tile reads its rows' products
+    // after the symbolic sweep of every tile)
+    resident += p->info.a_bytes + 8 * (m + 1) + (8 + 4 + (p->wide ? 4 * nG + 8 + 8 * p->ngg : 0)) * m;
+    per_row_ws = 0;
   } else if (o.m_a_bytes == 0) {
     // C bound per row for the C slots (or for a device-resident C)
     if (o.c_bound == AIRES_CBOUND_PRODUCTS) {
@@ -1360,11 +1362,14 @@ struct TileWs {
   uint32_t* bm_cache = nullptr;  // shared bitmap cache (nullptr: none)
   int64_t bm_cap = 0;
   unsigned long long* bm_top = nullptr;
+  bool item_cut = false;          // the call started with a bitmap cache (window cuts of kept rows)
 };
 
+// with_list_gcnt: the per-row arrays (products, bin list, grain and window
+// counts) for n rows; without, the caller points them into arrays of its own
 aires_status alloc_tile_ws(aires_plan* p, DevPool& ws, int64_t n, bool with_list_gcnt, TileWs& w) {
-  ST_TRY(ws.get_n(n, &w.P));
   if (with_list_gcnt) {
+    ST_TRY(ws.get_n(n, &w.P));
     ST_TRY(ws.get_n(n, &w.list));
     if (p->wide) {
       ST_TRY(ws.get_n(n * (int64_t)p->nG, &w.gcnt));
@@ -1412,6 +1417,7 @@ kern::WindowParams window_params(const aires_plan* p, const TileWs& w) {
   wp.bm_off = w.bm_off;
   wp.P = w.P;
   wp.bm_min_products = p->keep_bitmap;
+  wp.item_cut = w.item_cut ? 1 : 0;
   wp.slab_bin = p->slab_bin;
   wp.nslab = 1;  // set at the numeric launch from its grid
   return wp;
@@ -1553,6 +1559,11 @@ aires_status spgemm_device_in(aires_plan* p, hipStream_t s, DevPool& ws, aires_c
   int64_t* icount = nullptr;
   unsigned long long* prod = nullptr;
   ST_TRY(ws.get_n(m, &list));
+  // products per row for all rows: the numeric sweep of tile t reads the
+  // values its symbolic sweep wrote (which rows keep their bitmaps), after
+  // the symbolic sweeps of the later tiles
+  int64_t* P_all = nullptr;
+  ST_TRY(ws.get_n(m, &P_all));
   ST_TRY(ws.get_n(nt * (kern::MAX_BINS + 1), &binoff));
   ST_TRY(ws.get_n(nt, &prod));  // intermediate products of each tile
   // A's values: given, or derived from its pattern (Eq. 2) into the workspace
@@ -1589,10 +1600,13 @@ aires_status spgemm_device_in(aires_plan* p, hipStream_t s, DevPool& ws, aires_c
       }
     }
   }
+  const bool item_cut = bm_cache != nullptr;  // kept for the call, even if the cache is released later
   ST_TRY(alloc_split_ws(p, ws, shared.split));
   auto tile_ws = [&](int64_t t) {
     const aires_tile& T = p->tiles[(size_t)t];
     TileWs w = shared;
+    w.P = P_all + T.r0;
+    w.item_cut = item_cut;
     w.list = list + T.r0;
     w.binoff = binoff + t * (kern::MAX_BINS + 1);
     if (p->wide) {

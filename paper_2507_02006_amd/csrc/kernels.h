@@ -92,6 +92,10 @@ struct WindowParams {
   int64_t* bm_off;                   // [row * items_per_row + item] per tile
   const int64_t* P;                  // intermediate products per tile row
   int64_t bm_min_products;           // rows with more products keep their bitmaps
+  // 1: the windows of those rows are cut at symbolic items, as the symbolic
+  // phase planned them; fixed for the call even if the cache is released
+  // before the numeric phase (its windows then mark their bits again)
+  int32_t item_cut;
 };
 
 // P_i per tile row and their total; rows longer than `long_row` entries are

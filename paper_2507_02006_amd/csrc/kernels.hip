@@ -1005,6 +1005,13 @@ __device__ __forceinline__ bool keeps_bitmaps(const WindowParams& wp, int64_t ro
   return wp.bm_cache && wp.P[row] > wp.bm_min_products;
 }
 
+// Rows whose windows never straddle a symbolic item: the rows that keep
+// their bitmaps when the cache is there.  The window plan (symbolic phase)
+// and its fill (numeric phase) must cut a row alike.
+__device__ __forceinline__ bool cuts_at_items(const WindowParams& wp, int64_t row) {
+  return wp.item_cut && wp.P[row] > wp.bm_min_products;
+}
+
 template <typename RA, typename RB>
 __global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op, const BinView bv,
                                                            const WindowParams wp) {
@@ -1162,7 +1169,7 @@ __global__ __launch_bounds__(256) void k_win_plan(const BinView bv, int32_t nG, 
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t nwin = 0;
-    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp, gcols, keeps_bitmaps(wp, row),
+    counts[row] = plan_windows(wp.gcnt + row * nG, nG, wp, gcols, cuts_at_items(wp, row),
                                [&](int, int, int, int64_t) { ++nwin; });
     wp.item_count[1 + d] = nwin;
   }
@@ -1174,7 +1181,7 @@ __global__ __launch_bounds__(256) void k_win_fill(const BinView bv, int32_t nG, 
   for (int64_t d = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; d < cnt; d += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = list[d];
     int64_t o = wp.item_count[d];  // scanned: windows of the rows before d
-    plan_windows(wp.gcnt + row * nG, nG, wp, gcols, keeps_bitmaps(wp, row), [&](int g0, int g1, int n, int64_t roff) {
+    plan_windows(wp.gcnt + row * nG, nG, wp, gcols, cuts_at_items(wp, row), [&](int g0, int g1, int n, int64_t roff) {
                    WinItem w;
                    w.row = (int32_t)row;
                    w.g0 = (uint16_t)g0;

@@ -1,0 +1,112 @@
+"""GPU parity over seeded random cases: random shapes with heavy-tailed row
+lengths (hub rows in A, long rows in B), random row-pointer widths, and a
+random valid combination of the plan options that pick the kernel paths
+(dense rows, split rows, the four hash tiers, column windows with their
+grain, pool, entry and item sizes, kept symbolic bitmaps and a too-small
+bitmap cache, column slabs, tiling).  Each case is compared with the oracle:
+structure bit-exact, values bit-exact for integer inputs (every product and
+partial sum is exact in fp32) and within 1e-5 * (1 + |ref|) otherwise."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from workloads import CSR
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+CASES = 48
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    return torch
+
+
+def heavy_tailed_csr(rng, m, n, mean_len, ints, rp64):
+    """Rows of Pareto-distributed lengths (capped at n) with distinct random
+    columns; a few rows are hubs."""
+    lens = np.minimum(n, (rng.pareto(1.3, size=m) * mean_len).astype(np.int64))
+    hubs = rng.random(m) < 0.01
+    lens[hubs] = np.minimum(n, rng.integers(n // 4 + 1, n + 1, size=int(hubs.sum())))
+    cols = [np.sort(rng.choice(n, size=int(k), replace=False)) if k else np.zeros(0, np.int64) for k in lens]
+    col = np.concatenate(cols).astype(np.int32) if m else np.zeros(0, np.int32)
+    rp = np.zeros(m + 1, np.int64)
+    rp[1:] = np.cumsum(lens)
+    nnz = int(rp[-1])
+    val = (rng.integers(-4, 5, size=nnz) if ints else rng.uniform(-1, 1, size=nnz)).astype(np.float32)
+    return CSR(m, n, rp if rp64 else rp.astype(np.int32), col, val)
+
+
+def draw_options(rng, N):
+    o = {}
+    if rng.random() < 0.3:
+        o["dense_max_cols"] = int(rng.choice([32, 96, 512, 2048]))
+    if rng.random() < 0.5:
+        o["hash_max_products"] = int(rng.choice([-1, 64, 512, 2048, 4096]))
+    if rng.random() < 0.4:
+        o["wave_max_products"] = int(rng.choice([1, 16, 256]))
+    if rng.random() < 0.3:
+        o["split_min_products"] = int(rng.choice([-1, 1, 500]))
+        if rng.random() < 0.5:
+            o["split_max_rows"] = int(rng.integers(1, 8))
+    # column windows: a grain of 32..2048 columns, windows of 1..6 grains and
+    # G..4G entries, symbolic items of 1..8 grains, sometimes a small pool
+    G = int(rng.choice([32, 64, 96, 256, 1024, 2048]))
+    o["window_grain_cols"] = G
+    o["window_max_grains"] = int(rng.integers(1, 7))
+    o["window_max_entries"] = int(min(65535, G * rng.integers(1, 5)))
+    o["count_grains"] = int(rng.integers(1, 9))
+    if rng.random() < 0.3:
+        words = 2 * ((G + 47) // 48) + G  # one full grain
+        o["window_pool_bytes"] = int(4 * (words + rng.integers(0, 2 * words)))
+    o["keep_bitmap_products"] = int(rng.choice([0, 1, -1, 100]))
+    if o["keep_bitmap_products"] != -1 and rng.random() < 0.3:
+        o["bitmap_cache_bytes"] = int(rng.choice([4096, 65536]))
+    o["slab_min_products"] = int(rng.choice([0, 1, -1, 50, 2000]))
+    return o
+
+
+def case(seed):
+    rng = np.random.default_rng(1_000_003 * seed + 17)
+    m = int(rng.integers(1, 2500))
+    K = int(rng.integers(1, 1500))
+    N = int(rng.choice([1, 17, 100, 333, 700, 2049, 5000, 40000]))
+    ints = bool(rng.random() < 0.5)
+    A = heavy_tailed_csr(rng, m, K, float(rng.uniform(0.5, 12)), ints, bool(rng.random() < 0.3))
+    B = heavy_tailed_csr(rng, K, N, float(rng.uniform(0.5, 20)), ints, bool(rng.random() < 0.3))
+    opts = draw_options(rng, N)
+    tiles = int(rng.choice([0, 0, max(1, m // 3)]))
+    return A, B, ints, opts, tiles
+
+
+@pytest.mark.parametrize("seed", range(CASES))
+def test_random_case(torch_gpu, seed):
+    import paper_2507_02006_amd as aires
+    A, B, ints, opts, tiles = case(seed)
+    print("[gpu-case] fuzz seed=%d m=%d K=%d N=%d nnzA=%d nnzB=%d ints=%s tiles=%d opts=%s" %
+          (seed, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, ints, tiles, opts), flush=True)
+    sys.stdout.flush()
+    ref = oracle.spgemm(A, B)
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    with aires.tile_plan(dA, dB, 0, max_tile_rows=tiles, **opts) as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        st = aires.plan_stats(plan)
+    rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    assert st["products"] == ref.products and st["nnz_c"] == ref.nnz
+    if ints:
+        assert np.array_equal(val, ref.val), "integer values differ"
+    else:
+        err = np.abs(val.astype(np.float64) - ref.val.astype(np.float64))
+        bad = err > TOL * (1 + np.abs(ref.val.astype(np.float64)))
+        assert not bad.any(), "values differ at %d entries, max err %g" % (bad.sum(), err.max())

@@ -246,6 +246,40 @@ def test_tiled_wide(torch_gpu):
     check(torch_gpu, A, B, "cfg3 tiled wide", max_tile_rows=4099)
 
 
+@pytest.mark.parametrize("keep", [1, 0])
+def test_tiled_wide_kept_bitmaps(torch_gpu, keep):
+    """In-core tiles with kept symbolic bitmaps: every tile's symbolic phase
+    runs before any numeric phase, and a tile's numeric phase must decide
+    which rows keep their bitmaps (and so where their windows are cut) from
+    its own rows' products, not from the tile symbolised last.  Items of 2
+    grains of 1024 columns and windows of up to 6 grains make the two cuts
+    differ."""
+    A, B = workloads.workload(3, n=30000)
+    check(torch_gpu, A, B, "cfg3 tiled wide, kept bitmaps above %d products" % keep, max_tile_rows=7001,
+          keep_bitmap_products=keep, window_grain_cols=1024, window_max_grains=6, window_max_entries=4096,
+          count_grains=2)
+
+
+def test_kept_bitmaps_cache_released(torch_gpu):
+    """A budget whose slack, after the plan's peak, is 1.1 times C: the
+    kept-bitmap cache (a fifth of the slack) is released after the symbolic
+    phase so that C fits, and the numeric phase marks every window again,
+    cut where the symbolic phase planned the cuts."""
+    import paper_2507_02006_amd as aires
+    A, B = workloads.workload(3, n=30000)
+    ref = oracle.spgemm(A, B)
+    kw = dict(keep_bitmap_products=1, window_grain_cols=1024, window_max_grains=6, window_max_entries=4096,
+              count_grains=2)
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    with aires.tile_plan(dA, dB, 1 << 36, **kw) as plan:
+        peak = aires.plan_info(plan).peak_bytes
+    for slack in (1.1, 1.25):
+        budget = peak + int(slack * 8 * ref.nnz) + (1 << 20)
+        say("cache released: budget %d = peak %d + %.2f x C" % (budget, peak, slack))
+        rp, col, val, st, _ = run(torch_gpu, A, B, budget, **kw)
+        assert_match(rp, col, val, ref)
+
+
 def test_streamed_tiles_host_c(torch_gpu):
     """A in pinned host memory, double-buffered tiles, C tiles copied to
     pinned host memory at the running offset (Algorithm 2, Phases I-III)."""
