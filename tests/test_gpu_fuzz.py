@@ -18,7 +18,7 @@ from workloads import CSR
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-5
-CASES = 48
+CASES = 160
 
 
 @pytest.fixture(scope="module")
@@ -110,3 +110,80 @@ def test_random_case(torch_gpu, seed):
         err = np.abs(val.astype(np.float64) - ref.val.astype(np.float64))
         bad = err > TOL * (1 + np.abs(ref.val.astype(np.float64)))
         assert not bad.any(), "values differ at %d entries, max err %g" % (bad.sum(), err.max())
+
+
+STREAMED = 64
+NOALLOC = 32
+
+
+def check_values(val, ref, ints):
+    if ints:
+        assert np.array_equal(val, ref.val), "integer values differ"
+    else:
+        err = np.abs(val.astype(np.float64) - ref.val.astype(np.float64))
+        bad = err > TOL * (1 + np.abs(ref.val.astype(np.float64)))
+        assert not bad.any(), "values differ at %d entries, max err %g" % (bad.sum(), err.max())
+
+
+@pytest.mark.parametrize("seed", range(STREAMED))
+def test_random_streamed_case(torch_gpu, seed):
+    """A in pinned host memory, streamed in 2..5 row blocks with double-
+    buffered copies; B on the device or in pinned memory; C returned in
+    pinned host or device memory; C bound from the products or from the row
+    pointers; random path options as above."""
+    import paper_2507_02006_amd as aires
+    from paper_2507_02006_amd import _binding as B_
+    A, B, ints, opts, _ = case(1000 + seed)
+    rng = np.random.default_rng(7_000 + seed)
+    c_on_host = bool(rng.random() < 0.5)
+    c_bound = B_.CBOUND_ROWS if rng.random() < 0.5 else B_.CBOUND_PRODUCTS
+    b_pinned = bool(rng.random() < 0.5)
+    tiles = max(1, A.nrows // int(rng.integers(2, 6)))
+    print("[gpu-case] fuzz streamed seed=%d m=%d K=%d N=%d nnzA=%d nnzB=%d ints=%s tiles=%d c_on_host=%s "
+          "c_bound=%d b_pinned=%s opts=%s" % (seed, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, ints, tiles, c_on_host,
+                                              c_bound, b_pinned, opts), flush=True)
+    ref = oracle.spgemm(A, B)
+    dB = aires.to_pinned(B) if b_pinned else aires.to_device(B)
+    with aires.tile_plan(aires.to_pinned(A), dB, 1 << 34, c_on_host=c_on_host, c_bound=c_bound,
+                         max_tile_rows=tiles, **opts) as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        if c_on_host:
+            rp, col, val = C.rp.copy(), C.col.copy(), C.val.copy()
+            C.free()
+        else:
+            rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    check_values(val, ref, ints)
+
+
+@pytest.mark.parametrize("seed", range(NOALLOC))
+def test_random_noalloc_case(torch_gpu, seed):
+    """The allocation-free entry point on random cases (C arrays with room
+    to spare; nothing is written past nnz(C))."""
+    import paper_2507_02006_amd as aires
+    A, B, ints, opts, tiles = case(2000 + seed)
+    print("[gpu-case] fuzz noalloc seed=%d m=%d K=%d N=%d nnzA=%d nnzB=%d ints=%s tiles=%d opts=%s" %
+          (seed, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, ints, tiles, opts), flush=True)
+    ref = oracle.spgemm(A, B)
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    with aires.tile_plan(dA, dB, 0, max_tile_rows=tiles, **opts) as plan:
+        rp = torch_gpu.full((A.nrows + 1,), -1, dtype=torch_gpu.int64, device="cuda")
+        cap = ref.nnz + 17
+        col = torch_gpu.full((cap,), -1, dtype=torch_gpu.int32, device="cuda")
+        val = torch_gpu.zeros((cap,), dtype=torch_gpu.float32, device="cuda")
+        try:
+            nnz = aires.spgemm_noalloc(plan, rp, col, val)
+        except aires.AiresError as e:
+            from paper_2507_02006_amd import _binding as B_
+            if e.status == B_.E_CAPACITY and "workspace" in str(e):
+                pytest.skip("workspace beyond the fixed array: %s" % e)
+            raise
+        torch_gpu.cuda.synchronize()
+    assert nnz == ref.nnz
+    assert np.all(col[nnz:].cpu().numpy() == -1)
+    rpn = rp.cpu().numpy()
+    assert np.array_equal(rpn - rpn[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col[:nnz].cpu().numpy(), ref.col), "col_idx differs"
+    check_values(val[:nnz].cpu().numpy(), ref, ints)
