@@ -166,7 +166,8 @@ typedef struct aires_plan_opts {
     int64_t max_tile_rows;      /* 0: no cap                               */
     int64_t max_tile_bytes;     /* cap on a tile's A bytes; 0: none, or for
                                    a streamed A max(A bytes / 16, 32 MB),
-                                   so that copies overlap the products    */
+                                   so that copies overlap the products; a
+                                   row above it is a tile of its own     */
     int64_t m_a_bytes;          /* > 0: plan exactly as Algorithm 1 with
                                    calcMem(k,q) = (k+1)*rp_bytes + 8q <=
                                    m_a_bytes, ignoring the budget split    */

@@ -927,9 +927,11 @@ aires_status plan_impl(const aires_csr* A, const aires_csr* B, uint64_t hbm_budg
   if (a_streamed && max_tile_bytes == 0 && o.m_a_bytes == 0)
     max_tile_bytes = std::max<int64_t>(p->info.a_bytes / kStreamTiles, kMinStreamTileBytes);
   int64_t part_budget = tile_budget;  // the budget the partition is cut under
+  // (the tile-bytes cap sets the pipeline's grain: a row above it, which
+  // cannot be divided, is a tile of its own)
   auto fits = [&](int64_t r0, int64_t r1) -> bool {
     if (o.max_tile_rows > 0 && r1 - r0 > o.max_tile_rows) return false;
-    if (max_tile_bytes > 0 && (r1 - r0 + 1) * sA + 8 * (arp[r1] - arp[r0]) > max_tile_bytes)
+    if (max_tile_bytes > 0 && r1 - r0 > 1 && (r1 - r0 + 1) * sA + 8 * (arp[r1] - arp[r0]) > max_tile_bytes)
       return false;
     return slot_bytes_fast(r0, r1) <= part_budget;
   };
@@ -972,13 +974,19 @@ aires_status plan_impl(const aires_csr* A, const aires_csr* B, uint64_t hbm_budg
           if (seg_fits(r0, E, mid)) lo = mid; else hi = mid;
         }
       }
-      const int64_t q = lo;
-      const int64_t r1 = q == rest ? m : std::min(m, last_row(E + q));
+      int64_t q = lo;
+      int64_t r1 = q == rest ? m : std::min(m, last_row(E + q));
       if (r1 <= r0) {
+        // not one whole row under the tile-bytes cap: the segment is row r0
+        // alone if its slot fits the budget (a row is never divided)
         const int64_t need = slot_bytes_fast(r0, r0 + 1);
-        delete p;
-        return fail(AIRES_E_BUDGET, "row %lld alone needs %lld bytes; a segment slot has %lld", (long long)r0,
-                    (long long)need, (long long)part_budget);
+        if (need > part_budget) {
+          delete p;
+          return fail(AIRES_E_BUDGET, "row %lld alone needs %lld bytes; a segment slot has %lld", (long long)r0,
+                      (long long)need, (long long)part_budget);
+        }
+        q = arp[r0 + 1] - E;
+        r1 = r0 + 1;
       }
       aires_tile t;
       t.r0 = r0;

@@ -339,7 +339,8 @@ def test_maxfill_segments_hand_example(golden_dir):
     int32 row pointers) under a 40-byte cap on a segment's A bytes,
     (k + 1) * 4 + 8 q: entries [0, 3) (rows 0-1 complete, one entry of
     row 2 sent ahead), then [2, 5) (row 2 again, one entry of row 3 ahead),
-    then [4, 6).  Row blocks under the same cap cut the same rows."""
+    then [4, 6).  Row blocks under the same cap cut the same rows.  Under a
+    cap below one row, every such row is a segment (a tile) of its own."""
     g = json.load(open(os.path.join(golden_dir, "hand_4x4.json")))
     mk = lambda d: workloads.CSR(d["nrows"], d["ncols"], np.array(d["rp"], np.int32), np.array(d["col"], np.int32),
                                  np.array(d["val"], np.float32))
@@ -349,9 +350,14 @@ def test_maxfill_segments_hand_example(golden_dir):
         [(0, 2, 0, 2, 3), (2, 3, 2, 4, 5), (3, 4, 4, 6, 6)]
     _, rb = _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=40)
     assert [(t["r0"], t["r1"], t["nnz1"], t["sent_nnz1"]) for t in rb] == [(0, 2, 2, 2), (2, 3, 4, 4), (3, 4, 6, 6)]
-    with pytest.raises(aires.AiresError) as e:
-        _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=23, segmentation=B_.SEG_MAXFILL)
-    assert e.value.status == B_.E_BUDGET
+    # a 23-byte cap is below every non-empty row (2 * 4 + 8 * 2 = 24 bytes):
+    # such a row is a segment of its own, never divided; the empty row 1
+    # goes with the head of row 2, which is sent again with the rest of it
+    _, seg = _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=23, segmentation=B_.SEG_MAXFILL)
+    assert [(t["r0"], t["r1"], t["nnz0"], t["nnz1"], t["sent_nnz1"]) for t in seg] == \
+        [(0, 1, 0, 2, 2), (1, 2, 2, 2, 3), (2, 3, 2, 4, 4), (3, 4, 4, 6, 6)]
+    _, rb = _plan_tiles(A, Bm, 1 << 30, max_tile_bytes=23)
+    assert [(t["r0"], t["r1"]) for t in rb] == [(0, 1), (1, 2), (2, 3), (3, 4)]  # rows 1-2: 12 + 16 > 23
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2])

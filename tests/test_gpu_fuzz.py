@@ -187,3 +187,70 @@ def test_random_noalloc_case(torch_gpu, seed):
     assert np.array_equal(rpn - rpn[0], ref.rp), "row_ptr differs"
     assert np.array_equal(col[:nnz].cpu().numpy(), ref.col), "col_idx differs"
     check_values(val[:nnz].cpu().numpy(), ref, ints)
+
+
+MAXFILL = 32
+FILES = 16
+
+
+@pytest.mark.parametrize("seed", range(MAXFILL))
+def test_random_maxfill_case(torch_gpu, seed):
+    """Max-fill segments (ending inside rows; the partial row is copied back
+    and sent again with the next segment) of a pinned A, in slots of a
+    random size, C on the host or the device."""
+    import paper_2507_02006_amd as aires
+    A, B, ints, opts, _ = case(3000 + seed)
+    rng = np.random.default_rng(9_000 + seed)
+    c_on_host = bool(rng.random() < 0.5)
+    slot = max(4096, int(A.nbytes() // int(rng.integers(2, 9))))
+    print("[gpu-case] fuzz maxfill seed=%d m=%d K=%d N=%d nnzA=%d nnzB=%d ints=%s slot=%d c_on_host=%s opts=%s" %
+          (seed, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, ints, slot, c_on_host, opts), flush=True)
+    ref = oracle.spgemm(A, B)
+    with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 34, c_on_host=c_on_host, max_tile_bytes=slot,
+                         segmentation="maxfill", **opts) as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        if c_on_host:
+            rp, col, val = C.rp.copy(), C.col.copy(), C.val.copy()
+            C.free()
+        else:
+            rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    check_values(val, ref, ints)
+
+
+@pytest.mark.parametrize("seed", range(FILES))
+def test_random_file_case(torch_gpu, tmp_path, seed):
+    """A (and, for half the cases, B) in files: A's tiles read per tile with
+    direct or buffered I/O, B read whole into HBM first; row-pointer C bound."""
+    import paper_2507_02006_amd as aires
+    A, B, ints, opts, _ = case(4000 + seed)
+    rng = np.random.default_rng(11_000 + seed)
+    c_on_host = bool(rng.random() < 0.5)
+    direct = bool(rng.random() < 0.5)
+    b_file = bool(rng.random() < 0.5)
+    slot = max(4096, int(A.nbytes() // int(rng.integers(2, 6))))
+    print("[gpu-case] fuzz file seed=%d m=%d K=%d N=%d nnzA=%d nnzB=%d ints=%s slot=%d c_on_host=%s direct=%s "
+          "b_file=%s opts=%s" % (seed, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, ints, slot, c_on_host, direct,
+                                 b_file, opts), flush=True)
+    ref = oracle.spgemm(A, B)
+    ma = workloads.write_csr_file(str(tmp_path / "a.csr"), A)
+    if b_file:
+        mb = workloads.write_csr_file(str(tmp_path / "b.csr"), B)
+        mb["direct_io"] = direct
+        Bd, _ = aires.read_csr_file(mb, mem="device", chunk_bytes=int(rng.choice([4096, 1 << 20])))
+        dB = (B.nrows, B.ncols, Bd.rp, Bd.col, Bd.val)
+    else:
+        dB = aires.to_pinned(B)
+    with aires.tile_plan_file(ma, dB, 1 << 34, c_on_host=c_on_host, direct_io=direct, max_tile_bytes=slot) as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        if c_on_host:
+            rp, col, val = C.rp.copy(), C.col.copy(), C.val.copy()
+            C.free()
+        else:
+            rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    check_values(val, ref, ints)
