@@ -254,3 +254,27 @@ def test_random_file_case(torch_gpu, tmp_path, seed):
     assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
     assert np.array_equal(col, ref.col), "col_idx differs"
     check_values(val, ref, ints)
+
+
+SPMM = 48
+
+
+@pytest.mark.parametrize("seed", range(SPMM))
+def test_random_spmm_case(torch_gpu, seed):
+    """The combination step Y = act(A * W) (aires_spmm) on random shapes
+    with heavy-tailed rows, a random feature width, kernel family, ReLU,
+    row strides, offsets and row-pointer width, held to the fp32 summation
+    bound (bit-exact for integer inputs) by the spmm tests' own checker."""
+    from test_gpu_spmm import check as spmm_check
+    rng = np.random.default_rng(13_000 + seed)
+    m = int(rng.integers(1, 3000))
+    K = int(rng.integers(1, 2000))
+    ints = bool(rng.random() < 0.4)
+    rp64 = bool(rng.random() < 0.3)
+    A = heavy_tailed_csr(rng, m, K, float(rng.uniform(0.5, 30)), ints, False)
+    F = int(rng.choice([1, 3, 16, 63, 64, 65, 128, 200, 256, 511, 700]))
+    W = (rng.integers(-4, 5, size=(K, F)) if ints else rng.uniform(-1, 1, size=(K, F))).astype(np.float32)
+    spmm_check(torch_gpu, A, W, relu=bool(rng.random() < 0.5), rp64=rp64, ldw_pad=int(rng.choice([0, 0, 3, 64])),
+               ldy_pad=int(rng.choice([0, 0, 5])), w_offset=int(rng.choice([0, 0, 1, 3])), exact=ints,
+               name="fuzz spmm seed=%d" % seed, algo=str(rng.choice(["auto", "rows", "dense_tiles"])),
+               a_offset=int(rng.choice([0, 0, 1, 2])))
