@@ -278,3 +278,61 @@ def test_random_spmm_case(torch_gpu, seed):
                ldy_pad=int(rng.choice([0, 0, 5])), w_offset=int(rng.choice([0, 0, 1, 3])), exact=ints,
                name="fuzz spmm seed=%d" % seed, algo=str(rng.choice(["auto", "rows", "dense_tiles"])),
                a_offset=int(rng.choice([0, 0, 1, 2])))
+
+
+WIDE = 32
+
+
+def sparse_wide_csr(rng, m, n, mean_len, ints, rp64):
+    """Like heavy_tailed_csr for a very wide n: columns drawn with
+    replacement and made distinct (rows a little shorter than drawn)."""
+    lens = np.minimum(n, (rng.pareto(1.3, size=m) * mean_len).astype(np.int64))
+    hubs = rng.random(m) < 0.01
+    lens[hubs] = np.minimum(n, rng.integers(1000, 20000, size=int(hubs.sum())))
+    cols = [np.unique(rng.integers(0, n, size=int(k))) for k in lens]
+    lens = np.array([len(c) for c in cols], np.int64)
+    col = np.concatenate(cols).astype(np.int32) if m else np.zeros(0, np.int32)
+    rp = np.zeros(m + 1, np.int64)
+    rp[1:] = np.cumsum(lens)
+    nnz = int(rp[-1])
+    val = (rng.integers(-4, 5, size=nnz) if ints else rng.uniform(-1, 1, size=nnz)).astype(np.float32)
+    return CSR(m, n, rp if rp64 else rp.astype(np.int32), col, val)
+
+
+def case_wide(seed):
+    rng = np.random.default_rng(5_000_011 * seed + 3)
+    m = int(rng.integers(1, 2000))
+    K = int(rng.integers(1, 3000))
+    N = int(rng.choice([131072, 1048576]))
+    ints = bool(rng.random() < 0.5)
+    A = heavy_tailed_csr(rng, m, K, float(rng.uniform(1, 30)), ints, bool(rng.random() < 0.3))
+    B = sparse_wide_csr(rng, K, N, float(rng.uniform(5, 200)), ints, bool(rng.random() < 0.3))
+    o = {"window_grain_cols": int(rng.choice([4096, 8192])), "count_grains": int(rng.choice([16, 32])),
+         "keep_bitmap_products": int(rng.choice([0, 1, -1, 20000])),
+         "slab_min_products": int(rng.choice([0, 1, -1, 20000]))}
+    if rng.random() < 0.5:
+        o["hash_max_products"] = int(rng.choice([-1, 512, 2048, 4096]))
+    tiles = int(rng.choice([0, 0, max(1, m // 3)]))
+    return A, B, ints, o, tiles
+
+
+@pytest.mark.parametrize("seed", range(WIDE))
+def test_random_wide_case(torch_gpu, seed):
+    """Products of 2^17 or 2^20 columns with default-like windows (grains of
+    4096 or 8192 columns, items of 16 or 32 grains), kept bitmaps, column
+    slabs and tiles drawn at random; hub rows in A and long rows in B."""
+    import paper_2507_02006_amd as aires
+    A, B, ints, opts, tiles = case_wide(seed)
+    print("[gpu-case] fuzz wide seed=%d m=%d K=%d N=%d nnzA=%d nnzB=%d ints=%s tiles=%d opts=%s" %
+          (seed, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, ints, tiles, opts), flush=True)
+    ref = oracle.spgemm(A, B)
+    dA, dB = aires.to_device(A), aires.to_device(B)
+    with aires.tile_plan(dA, dB, 0, max_tile_rows=tiles, **opts) as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        st = aires.plan_stats(plan)
+    rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    assert st["products"] == ref.products and st["nnz_c"] == ref.nnz
+    check_values(val, ref, ints)
