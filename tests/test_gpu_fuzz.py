@@ -336,3 +336,60 @@ def test_random_wide_case(torch_gpu, seed):
     assert np.array_equal(col, ref.col), "col_idx differs"
     assert st["products"] == ref.products and st["nnz_c"] == ref.nnz
     check_values(val, ref, ints)
+
+
+BUDGET = 40
+
+
+@pytest.mark.parametrize("seed", range(BUDGET))
+def test_random_budget_case(torch_gpu, seed):
+    """A device budget of the caller's device inputs (which the budget
+    covers), the planner's 4 MiB of fixed slack, and 0 to 1.5 times what a
+    first call measured at the allocator, in core or with A streamed from
+    pinned memory: the call either returns the oracle's C with the
+    allocator's peak within the budget, or fails with AIRES_E_BUDGET (at
+    planning or after the symbolic phase) leaving nothing allocated."""
+    import paper_2507_02006_amd as aires
+    from paper_2507_02006_amd import _binding as B_
+    A, B, ints, opts, tiles = case(5000 + seed)
+    rng = np.random.default_rng(17_000 + seed)
+    streamed = bool(rng.random() < 0.5)
+    c_on_host = streamed and bool(rng.random() < 0.5)
+    f = float(rng.uniform(0.0, 1.5))
+    ref = oracle.spgemm(A, B)
+    dA = aires.to_pinned(A) if streamed else aires.to_device(A)
+    dB = aires.to_device(B)
+    inputs = B.nbytes() + (0 if streamed else A.nbytes())
+    kw = dict(opts, max_tile_rows=tiles, c_on_host=c_on_host)
+    probe = B_.TorchAllocator(0)
+    with aires.tile_plan(dA, dB, 1 << 36, allocator=probe, **kw) as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        if c_on_host:
+            C.free()
+        del C
+    need = probe.peak
+    budget = inputs + (4 << 20) + int(f * need)
+    print("[gpu-case] fuzz budget seed=%d m=%d K=%d N=%d streamed=%s c_on_host=%s need=%d budget=%d (%.2f x) opts=%s" %
+          (seed, A.nrows, A.ncols, B.ncols, streamed, c_on_host, need, budget, f, kw), flush=True)
+    alloc = B_.TorchAllocator(0)
+    try:
+        with aires.tile_plan(dA, dB, budget, allocator=alloc, **kw) as plan:
+            C = aires.spgemm(plan)
+            torch_gpu.cuda.synchronize()
+            if c_on_host:
+                rp, col, val = C.rp.copy(), C.col.copy(), C.val.copy()
+                C.free()
+            else:
+                rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    except aires.AiresError as e:
+        torch_gpu.cuda.synchronize()
+        assert e.status == B_.E_BUDGET, str(e)
+        assert alloc.cur == 0 and not alloc.live, "blocks left after %s" % e
+        print("[gpu-case] refused: %s" % e, flush=True)
+        return
+    print("[gpu-case] ran: allocator peak %d of %d" % (alloc.peak, budget - inputs), flush=True)
+    assert alloc.peak <= budget - inputs, "allocator peak %d over the budget's %d" % (alloc.peak, budget - inputs)
+    assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    check_values(val, ref, ints)
