@@ -185,7 +185,7 @@ typedef struct aires_plan_opts {
     int64_t window_max_grains;  /* grains one window may span (64)         */
     int64_t window_max_entries; /* C entries one window may hold, in
                                    [grain, 65535] (16384)                  */
-    int64_t count_grains;       /* grains one symbolic item covers (32)    */
+    int64_t count_grains;       /* grains one symbolic item covers (24)    */
     int64_t keep_bitmap_products; /* 0: default (65536), < 0: never.  The
                                    symbolic phase keeps the presence bitmaps
                                    of rows with more products than this for

@@ -65,7 +65,7 @@ constexpr int64_t kGrainCols = 8192;         // column grain of wide products
 constexpr int64_t kWindowMaxGrains = 64;     // grains one window may span
 constexpr int64_t kWindowMaxEntries = 16384; // C entries one window may hold
 constexpr int64_t kWindowPoolBytes = 38912;  // LDS shared by a window's bitmap and values
-constexpr int64_t kCountGrains = 32;         // grains one symbolic item covers
+constexpr int64_t kCountGrains = 24;         // grains one symbolic item covers (four counting workgroups per CU)
 constexpr int64_t kBitmapCacheBytes = int64_t(32) << 30;  // symbolic bitmaps kept for heavy rows
 constexpr int64_t kStreamTiles = 16;                       // default tile count of a streamed A
 constexpr int64_t kMinStreamTileBytes = int64_t(32) << 20;  // ... with at least this much of A per tile

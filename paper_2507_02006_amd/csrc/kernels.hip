@@ -1013,7 +1013,7 @@ __device__ __forceinline__ bool cuts_at_items(const WindowParams& wp, int64_t ro
 }
 
 template <typename RA, typename RB>
-__global__ __launch_bounds__(WIN_BLOCK, 4) void k_grain_count(const Operands op, const BinView bv,
+__global__ __launch_bounds__(WIN_BLOCK, 8) void k_grain_count(const Operands op, const BinView bv,
                                                            const WindowParams wp) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t s_off, s_row;
