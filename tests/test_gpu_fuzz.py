@@ -393,3 +393,33 @@ def test_random_budget_case(torch_gpu, seed):
     assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
     assert np.array_equal(col, ref.col), "col_idx differs"
     check_values(val, ref, ints)
+
+
+WIDE_STREAMED = 16
+
+
+@pytest.mark.parametrize("seed", range(WIDE_STREAMED))
+def test_random_wide_streamed_case(torch_gpu, seed):
+    """The wide cases above with A streamed from pinned host memory in 2..5
+    row blocks (windows and column slabs per tile), C on the host or the
+    device."""
+    import paper_2507_02006_amd as aires
+    A, B, ints, opts, _ = case_wide(100 + seed)
+    rng = np.random.default_rng(19_000 + seed)
+    c_on_host = bool(rng.random() < 0.5)
+    tiles = max(1, A.nrows // int(rng.integers(2, 6)))
+    print("[gpu-case] fuzz wide streamed seed=%d m=%d K=%d N=%d nnzA=%d nnzB=%d ints=%s tiles=%d c_on_host=%s opts=%s" %
+          (seed, A.nrows, A.ncols, B.ncols, A.nnz, B.nnz, ints, tiles, c_on_host, opts), flush=True)
+    ref = oracle.spgemm(A, B)
+    with aires.tile_plan(aires.to_pinned(A), aires.to_device(B), 1 << 36, c_on_host=c_on_host, max_tile_rows=tiles,
+                         **opts) as plan:
+        C = aires.spgemm(plan)
+        torch_gpu.cuda.synchronize()
+        if c_on_host:
+            rp, col, val = C.rp.copy(), C.col.copy(), C.val.copy()
+            C.free()
+        else:
+            rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
+    assert np.array_equal(rp - rp[0], ref.rp), "row_ptr differs"
+    assert np.array_equal(col, ref.col), "col_idx differs"
+    check_values(val, ref, ints)
