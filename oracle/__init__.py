@@ -28,7 +28,7 @@ CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-shared", "-fPIC"]
 def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC])
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -61,6 +61,8 @@ def _load():
         lib.oracle_validate.argtypes = [i64, i64, i64, vp, vp]
         lib.oracle_spmm.restype = None
         lib.oracle_spmm.argtypes = [i64, vp, vp, vp, vp, i64, i64, ctypes.c_int, vp, vp]
+        lib.oracle_sym_norm.restype = None
+        lib.oracle_sym_norm.argtypes = [i64, vp, vp, vp]
         _lib = lib
     return _lib
 
@@ -138,6 +140,19 @@ def spmm(A, W: np.ndarray, relu: bool = False) -> tuple[np.ndarray, np.ndarray]:
         lib.oracle_spmm(int(m), arp.ctypes.data, acol.ctypes.data, aval.ctypes.data, W.ctypes.data, int(F), int(F),
                         1 if relu else 0, Y.ctypes.data, Ya.ctypes.data)
     return Y, Ya
+
+
+def sym_norm(rp: np.ndarray, col: np.ndarray) -> np.ndarray:
+    """The values of the normalised adjacency (Sec. II-A, Eq. 2) of a square
+    pattern whose self-loops are stored: a_ij = 1/sqrt(r_i r_j), r_i the
+    stored entries of row i, in double, rounded once to float32."""
+    lib = _load()
+    rp64, c = _rp64(rp), _c(col, np.int32)
+    m = len(rp64) - 1
+    out = np.empty(len(c), dtype=np.float32)
+    if len(c):
+        lib.oracle_sym_norm(int(m), rp64.ctypes.data, c.ctypes.data, out.ctypes.data)
+    return out
 
 
 def products(A, B, r0: int = 0, r1: int | None = None) -> np.ndarray:

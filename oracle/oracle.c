@@ -38,9 +38,15 @@
  *    from its definition: y_ij = act(sum over stored k of A_i of
  *    a_ik * w_kj), accumulated in double in ascending k, together with the
  *    sum of |a_ik * w_kj| for the standard summation error bound.
+ * 6. oracle_sym_norm: the values of the normalised adjacency of Sec. II-A
+ *    (Eq. 2) from a square pattern alone, D^-1/2 (A + I) D^-1/2 with the
+ *    self-loops already in the pattern: a_ij = 1 / sqrt(r_i r_j), r_i the
+ *    stored entries of row i, evaluated in double and rounded once to
+ *    binary32.
  *
  * Row pointers are passed as int64 (the Python side widens int32 arrays).
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -253,5 +259,18 @@ void oracle_spmm(int64_t m, const int64_t *arp, const int32_t *acol, const float
         }
         if (relu)
             for (int64_t j = 0; j < F; ++j) if (y[j] < 0.0) y[j] = 0.0;
+    }
+}
+
+/* out[p] = 1 / sqrt(r_i r_j) for the stored entry p = (i, j) of the pattern */
+void oracle_sym_norm(int64_t m, const int64_t *rp, const int32_t *col, float *out)
+{
+    for (int64_t i = 0; i < m; ++i) {
+        const double ri = (double)(rp[i + 1] - rp[i]);
+        for (int64_t p = rp[i]; p < rp[i + 1]; ++p) {
+            const int64_t j = col[p];
+            const double rj = (double)(rp[j + 1] - rp[j]);
+            out[p] = (float)(1.0 / sqrt(ri * rj));
+        }
     }
 }

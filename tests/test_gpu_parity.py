@@ -561,20 +561,12 @@ def _identity(n):
     return CSR(n, n, np.arange(n + 1, dtype=np.int32), np.arange(n, dtype=np.int32), np.ones(n, np.float32))
 
 
-def _eq2(rp, col):
-    """Eq. 2 evaluated here from the pattern alone, in double, rounded once:
-    a_ij = 1/sqrt(r_i r_j) with r the stored entries per row."""
-    lens = np.diff(rp.astype(np.int64))
-    rows = np.repeat(np.arange(len(lens)), lens)
-    return (1.0 / np.sqrt(lens[rows].astype(np.float64) * lens[col].astype(np.float64))).astype(np.float32)
-
-
 @pytest.mark.parametrize("n", [20000, 1048576])
 def test_sym_norm_values_bitwise(torch_gpu, n):
     """a_values='sym_norm': C = A_norm * I gives 1/sqrt(r_i r_j) bit for bit
     (double arithmetic, one rounding to fp32) with A's own values not passed
-    at all, against Eq. 2 evaluated on the host from the pattern, on the
-    square workload's graph scaled and at full size."""
+    at all, against the oracle's Eq. 2 (oracle.sym_norm) on the square
+    workload's graph scaled and at full size."""
     import paper_2507_02006_amd as aires
     A, _ = workloads.workload(3, n=n)
     dA = aires.to_device(A)
@@ -585,13 +577,13 @@ def test_sym_norm_values_bitwise(torch_gpu, n):
         rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
     assert np.array_equal(rp, A.rp.astype(np.int64))
     assert np.array_equal(col, A.col)
-    assert np.array_equal(val.view(np.uint32), _eq2(A.rp, A.col).view(np.uint32))
+    assert np.array_equal(val.view(np.uint32), oracle.sym_norm(A.rp, A.col).view(np.uint32))
 
 
 def test_sym_norm_values_sparse_rows(torch_gpu):
     """Derived values when runs of empty rows make a 2048-entry chunk span
     more rows than the kernel stages in LDS (its global-search branch):
-    C = A_norm * I against Eq. 2 evaluated in double on the host."""
+    C = A_norm * I against the oracle's Eq. 2."""
     import paper_2507_02006_amd as aires
     rng = np.random.default_rng(31)
     m = 200000
@@ -602,8 +594,7 @@ def test_sym_norm_values_sparse_rows(torch_gpu):
     rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     col = np.concatenate(cols).astype(np.int32)
     A = CSR(m, m, rp, col, np.zeros(len(col), np.float32))
-    rows = np.repeat(np.arange(m), lens)
-    want = (1.0 / np.sqrt(lens[rows].astype(np.float64) * lens[col].astype(np.float64))).astype(np.float32)
+    want = oracle.sym_norm(rp, col)
     dA = aires.to_device(A)
     say("sym_norm sparse rows m=%d nnz=%d" % (m, len(col)))
     with aires.tile_plan(dA[:4] + (None,), aires.to_device(_identity(m)), 0, a_values="sym_norm") as plan:

@@ -450,3 +450,26 @@ def test_spmm_gcn_layer_composes():
     Da = np.zeros((40, 40)); Da[pattern_dense(A)] = A.val
     H2 = np.maximum(Da @ (Dx @ W.astype(np.float64)), 0)
     assert np.allclose(H1, H2, rtol=1e-5, atol=1e-6)
+
+
+def test_sym_norm_closed_forms():
+    """Eq. 2 from a pattern with its self-loops (oracle.sym_norm), against
+    values worked by hand: the complete graph on 8 vertices gives 1/8
+    everywhere (exact); a 6-cycle, three entries per row, gives fl32(1/3) =
+    0.333333343...; a star with 3 leaves gives 1/4 at the centre's loop,
+    1/sqrt(8) = 0.353553385... on its edges and 1/2 at the leaves' loops; an
+    isolated vertex (its loop alone) gives 1.  Then the generator's own
+    values for the tiny workload's graph, computed there independently."""
+    n = 8
+    v = oracle.sym_norm(np.arange(0, n * n + 1, n), np.tile(np.arange(n), n))
+    assert np.all(v == np.float32(0.125))
+    cyc = [sorted({(i - 1) % 6, i, (i + 1) % 6}) for i in range(6)]
+    v = oracle.sym_norm(np.arange(0, 19, 3), np.array(sum(cyc, []), np.int32))
+    assert np.all(v.view(np.uint32) == np.uint32(0x3EAAAAAB))
+    star_rp = np.array([0, 4, 6, 8, 10, 11])
+    star_col = np.array([0, 1, 2, 3, 0, 1, 0, 2, 0, 3, 4], np.int32)
+    e = np.float32(0.35355338)
+    want = np.array([0.25, e, e, e, e, 0.5, e, 0.5, e, 0.5, 1.0], np.float32)
+    assert np.array_equal(oracle.sym_norm(star_rp, star_col), want)
+    A, _ = workloads.workload(1)
+    assert np.array_equal(oracle.sym_norm(A.rp, A.col).view(np.uint32), A.val.view(np.uint32))
