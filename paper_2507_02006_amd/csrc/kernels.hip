@@ -470,8 +470,11 @@ __device__ __forceinline__ int wave_share(int rn, int nw) {
 // P32: B positions fit 32 bits (wide products, nnz(B) < 2^31).
 // SMALL_SCAN: a chunk of at most WAVE entries is scanned by the first
 // wavefront alone (two workgroup barriers less).
-template <int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, bool SMALL_SCAN = false, typename CH,
-          typename SEG, typename F>
+// BATCH: f(j[UR], v[UR], ok[UR]) takes a lane's UR terms at once, with no
+// branch per term: a term past the wavefront's share (ok false) repeats the
+// lane's first term of the step, so that every read stays in range.
+template <int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, bool SMALL_SCAN = false,
+          bool BATCH = false, typename CH, typename SEG, typename F>
 __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group<GROUP, BLOCK>& g,
                                                  CH& ch, int64_t p0, int64_t p1, const SEG& seg, F&& f) {
   using S = typename CH::shift_t;
@@ -529,33 +532,56 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
       // the wavefront's terms, each with the record of its segment
       auto terms = [&](auto rec_of) {
         for (int q0 = lane; q0 < wlen; q0 += WAVE * UR) {
-          PI pos[UR];
-          float am[UR];
+          if constexpr (BATCH) {
+            PI pos[UR];
+            float am[UR];
+            bool ok[UR];
 #pragma unroll
-          for (int u = 0; u < UR; ++u) {
-            const int q = q0 + u * WAVE;
-            pos[u] = -1;
-            am[u] = 0.f;
-            if (q < wlen) {
-              const typename CH::Rec rc = rec_of(q);
-              pos[u] = (PI)rc.shift + base + q;
+            for (int u = 0; u < UR; ++u) {
+              const int q = q0 + u * WAVE;
+              ok[u] = q < wlen;
+              const int qc = ok[u] ? q : q0;
+              const typename CH::Rec rc = rec_of(qc);
+              pos[u] = (PI)rc.shift + base + qc;
               am[u] = rc.av;
             }
-          }
-          int j[UR];
-          float bv[UR];
+            int j[UR];
+            float v[UR];
 #pragma unroll
-          for (int u = 0; u < UR; ++u) {
-            j[u] = 0;
-            bv[u] = 0.f;
-            if (pos[u] >= 0) {
+            for (int u = 0; u < UR; ++u) {
               j[u] = op.bcol[pos[u]];
-              if constexpr (NUM) bv[u] = op.bval[pos[u]];
+              v[u] = NUM ? am[u] * op.bval[pos[u]] : 0.f;
             }
-          }
+            f(j, v, ok);
+          } else {
+            PI pos[UR];
+            float am[UR];
 #pragma unroll
-          for (int u = 0; u < UR; ++u)
-            if (pos[u] >= 0) f(j[u], am[u] * bv[u]);
+            for (int u = 0; u < UR; ++u) {
+              const int q = q0 + u * WAVE;
+              pos[u] = -1;
+              am[u] = 0.f;
+              if (q < wlen) {
+                const typename CH::Rec rc = rec_of(q);
+                pos[u] = (PI)rc.shift + base + q;
+                am[u] = rc.av;
+              }
+            }
+            int j[UR];
+            float bv[UR];
+#pragma unroll
+            for (int u = 0; u < UR; ++u) {
+              j[u] = 0;
+              bv[u] = 0.f;
+              if (pos[u] >= 0) {
+                j[u] = op.bcol[pos[u]];
+                if constexpr (NUM) bv[u] = op.bval[pos[u]];
+              }
+            }
+#pragma unroll
+            for (int u = 0; u < UR; ++u)
+              if (pos[u] >= 0) f(j[u], am[u] * bv[u]);
+          }
         }
       };
       const int one = wave_seg_map(ch.ex, nk, base, wlen, seg_w);
@@ -571,13 +597,13 @@ __device__ __forceinline__ void for_each_term_in(const Operands& op, const Group
 }
 
 // ... over the terms of A entries [p0, p1); the whole row:
-template <typename RA, int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, typename CH, typename SEG,
-          typename F>
+template <typename RA, int GROUP, int BLOCK, bool NUM, bool P32 = false, int UR = UNROLL, bool BATCH = false,
+          typename CH, typename SEG, typename F>
 __device__ __forceinline__ void for_each_term(const Operands& op, const Group<GROUP, BLOCK>& g,
                                               CH& ch, int64_t row, const SEG& seg, F&& f) {
   const int64_t p0 = ld_rp<RA>(op.arp, row) - op.a_base;
   const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
-  for_each_term_in<GROUP, BLOCK, NUM, P32, UR>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
+  for_each_term_in<GROUP, BLOCK, NUM, P32, UR, false, BATCH>(op, g, ch, p0, p1, seg, static_cast<F&&>(f));
 }
 
 // A row with a single A entry is a_ik times B_k: its columns are B_k's
@@ -1070,14 +1096,19 @@ __global__ __launch_bounds__(WIN_BLOCK, 8) void k_grain_count(const Operands op,
       // terms carry absolute columns: bma is the bitmap seen from column 0
       // (c0 is a multiple of 32, so a column's bit index is the same)
       uint32_t* bma = bm - (c0 >> 5);
-      auto mark = [&](int j, float) { atomicOr(&bma[j >> 5], 1u << (j & 31)); };
+      // a lane's eight terms at once, with no branch per term (a missing
+      // term ORs in nothing): all eight B loads in flight, then the ORs
+      auto mark = [&](const int (&j)[8], const float (&)[8], const bool (&ok)[8]) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) atomicOr(&bma[j[u] >> 5], ok[u] ? 1u << (j[u] & 31) : 0u);
+      };
       // eight B loads in flight per thread: the symbolic loop reads columns only
       if (short_row)
-        for_each_term_in<WIN_BLOCK, WIN_BLOCK, false, true, 8, true>(op, g, ch, p0, p1, HeldRange{lo, (int64_t)hi - lo},
-                                                               mark);
+        for_each_term_in<WIN_BLOCK, WIN_BLOCK, false, true, 8, true, true>(
+            op, g, ch, p0, p1, HeldRange{lo, (int64_t)hi - lo}, mark);
       else
-        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, 8>(op, g, ch, row,
-                                                                GrainRange{op.bidx, op.nG + 1, g0, g1}, mark);
+        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, 8, true>(op, g, ch, row,
+                                                                      GrainRange{op.bidx, op.nG + 1, g0, g1}, mark);
       lo = hi;
       const int nw = (g1 - g0) * WPG;
       int64_t off = -1;
