@@ -1342,6 +1342,13 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         const uint32_t w = dj / WIN_WORD_BITS;
         atomicOr(reinterpret_cast<unsigned long long*>(&bw[w]), 1ull << (dj - w * WIN_WORD_BITS));
       };
+      // the same with no branch for a term that may be missing (ok false):
+      // j is then any column of the window, and nothing is ORed in
+      auto set_bit_if = [&](int j, bool ok) {
+        const uint32_t dj = (uint32_t)(j - c0);
+        const uint32_t w = dj / WIN_WORD_BITS;
+        atomicOr(reinterpret_cast<unsigned long long*>(&bw[w]), ok ? 1ull << (dj - w * WIN_WORD_BITS) : 0ull);
+      };
       // Heavy rows: the symbolic phase kept the window's bitmap.
       int64_t cached = -1;
       if (keeps_bitmaps(wp, row)) {
@@ -1484,6 +1491,25 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
               const int base = (int)r0 + wlo;
               auto terms = [&](auto rec_of) {
                 for (int q0 = lane; q0 < wlen; q0 += WAVE * WIN_UNROLL) {
+                  if (!pass) {
+                    // presence bits, with no branch per term: a term past the
+                    // share repeats the lane's first one and sets nothing
+                    int32_t pp[WIN_UNROLL];
+                    bool ok[WIN_UNROLL];
+#pragma unroll
+                    for (int u = 0; u < WIN_UNROLL; ++u) {
+                      const int q = q0 + u * WAVE;
+                      ok[u] = q < wlen;
+                      const int qc = ok[u] ? q : q0;
+                      pp[u] = (int32_t)rec_of(qc).shift + base + qc;
+                    }
+                    int jb[WIN_UNROLL];
+#pragma unroll
+                    for (int u = 0; u < WIN_UNROLL; ++u) jb[u] = op.bcol[pp[u]];
+#pragma unroll
+                    for (int u = 0; u < WIN_UNROLL; ++u) set_bit_if(jb[u], ok[u]);
+                    continue;
+                  }
                   int32_t pos[WIN_UNROLL];
                   float am[WIN_UNROLL];
 #pragma unroll
@@ -1536,8 +1562,12 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         if (cached >= 0)
           load_bits();
         else
-          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, WIN_UNROLL>(op, g, ch, row, seg,
-                                                               [&](int j, float) { set_bit(j); });
+          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, false, true, WIN_UNROLL, true>(
+              op, g, ch, row, seg,
+              [&](const int (&j)[WIN_UNROLL], const float (&)[WIN_UNROLL], const bool (&ok)[WIN_UNROLL]) {
+#pragma unroll
+                for (int u = 0; u < WIN_UNROLL; ++u) set_bit_if(j[u], ok[u]);
+              });
         word_ranks();
         for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true, WIN_UNROLL>(op, g, ch, row, seg,
                                                             [&](int j, float v) { add_at_rank(j, v); });
