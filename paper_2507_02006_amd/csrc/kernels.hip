@@ -675,10 +675,19 @@ __global__ __launch_bounds__(BLOCK) void k_dense(const Operands op, const BinVie
   for (int64_t it = (int64_t)blockIdx.x * NG + gi + bv.skip; it < cnt; it += (int64_t)gridDim.x * NG) {
     const int64_t row = list[it];
     if (single_entry_row<RA, RB, GROUP, NUM>(op, out, row, t)) continue;
-    for_each_term<RA, GROUP, BLOCK, NUM>(op, g, ch, row, seg, [&](int j, float v) {
-      atomicOr(&bm[j >> 5], 1u << (j & 31));
-      if constexpr (NUM) lds_add<true>(&acc[j], v);
-    });
+    if constexpr (!NUM) {
+      // presence marks are fire-and-forget ORs: a lane's terms go out with
+      // no branch per term (a missing term ORs in nothing)
+      for_each_term<RA, GROUP, BLOCK, false, false, UNROLL, true>(
+          op, g, ch, row, seg, [&](const int (&j)[UNROLL], const float (&)[UNROLL], const bool (&ok)[UNROLL]) {
+            for (int u = 0; u < UNROLL; ++u) atomicOr(&bm[j[u] >> 5], ok[u] ? 1u << (j[u] & 31) : 0u);
+          });
+    } else {
+      for_each_term<RA, GROUP, BLOCK, true>(op, g, ch, row, seg, [&](int j, float v) {
+        atomicOr(&bm[j >> 5], 1u << (j & 31));
+        lds_add<true>(&acc[j], v);
+      });
+    }
     if constexpr (!NUM) {
       int64_t c = 0;
       for (int i = t; i < nwd; i += GROUP) {
@@ -755,11 +764,19 @@ __global__ __launch_bounds__(SPLIT_BLOCK) void k_split_parts(const Operands op, 
     const int64_t p1 = ld_rp<RA>(op.arp, row + 1) - op.a_base;
     const int64_t len = (p1 - p0 + SPLIT_PARTS - 1) / SPLIT_PARTS;
     const int64_t q0 = min(p1, p0 + part * len), q1 = min(p1, q0 + len);
-    if (q0 < q1)
-      for_each_term_in<SPLIT_BLOCK, SPLIT_BLOCK, NUM>(op, g, ch, q0, q1, seg, [&](int j, float v) {
-        atomicOr(&bm[j >> 5], 1u << (j & 31));
-        if constexpr (NUM) lds_add<true>(&acc[j], v);
-      });
+    if (q0 < q1) {
+      if constexpr (!NUM) {
+        for_each_term_in<SPLIT_BLOCK, SPLIT_BLOCK, false, false, UNROLL, false, true>(
+            op, g, ch, q0, q1, seg, [&](const int (&j)[UNROLL], const float (&)[UNROLL], const bool (&ok)[UNROLL]) {
+              for (int u = 0; u < UNROLL; ++u) atomicOr(&bm[j[u] >> 5], ok[u] ? 1u << (j[u] & 31) : 0u);
+            });
+      } else {
+        for_each_term_in<SPLIT_BLOCK, SPLIT_BLOCK, true>(op, g, ch, q0, q1, seg, [&](int j, float v) {
+          atomicOr(&bm[j >> 5], 1u << (j & 31));
+          lds_add<true>(&acc[j], v);
+        });
+      }
+    }
     if constexpr (NUM) {
       for (int j = t; j < N; j += SPLIT_BLOCK)
         if ((bm[j >> 5] >> (j & 31)) & 1u) {
