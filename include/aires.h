@@ -380,6 +380,15 @@ aires_status aires_plan_tile(const aires_plan *plan, int64_t t, aires_tile *tile
  * every row of C are strictly increasing; entries whose value sums to zero
  * are kept (the structure is the union of the column sets).
  *
+ * Values (Eq. 1, c_ij = sum_k a_ik b_kj): fp32 products summed in fp32 in an
+ * unspecified order, except in rows of wide products (N above the densest
+ * row the device holds in LDS) handled by column windows whose bound
+ * S_i = sum_k |a_ik| max_j |b_kj| allows 32-bit fixed point: there the
+ * products are scaled by 2^f (S_i < 2^(30-f)), rounded to integers and
+ * summed exactly, so an entry's error is at most |A_i| 2^-(f+1) <= 1e-6
+ * plus its final rounding to fp32, and its value does not depend on the
+ * order of the products.
+ *
  * Memory (the constraint M of Sec. III-A): every block the call takes from
  * the allocator, C included, counts against the plan's budget together
  * with the caller's device-resident inputs; an allocation that would pass

@@ -798,7 +798,7 @@ aires_status plan_impl(const aires_csr* A, const aires_csr* B, uint64_t hbm_budg
     }
   }
   const int64_t nG = p->wide ? p->nG : 0;
-  const int64_t index_bytes = p->wide ? 4 * (nG + 1) * K : 0;
+  const int64_t index_bytes = p->wide ? 4 * (nG + 2) * K : 0;  // grain index and max |b| per B row
 
   // A's row pointers on the host as int64 (in place when they already are)
   std::vector<int64_t> arp_own;
@@ -1328,6 +1328,14 @@ void reset_timing(aires_plan* p) {
   p->marks.clear();
 }
 
+// 32-bit words of B's grain index, bidx[k * (nG + 1) + g], followed by
+// max_j |b_kj| per B row (fp32), both built once per call for wide products.
+int64_t index_words(const aires_plan* p) { return ((int64_t)p->nG + 2) * p->B.nrows; }
+
+float* index_bmax(const aires_plan* p, int32_t* bidx) {
+  return reinterpret_cast<float*>(bidx + ((int64_t)p->nG + 1) * p->B.nrows);
+}
+
 kern::Operands tile_operands(const aires_plan* p, const void* arp, int64_t a_base, const int32_t* acol,
                              const float* aval, const void* brp, const int32_t* bcol, const float* bval,
                              const int32_t* bidx) {
@@ -1346,6 +1354,8 @@ kern::Operands tile_operands(const aires_plan* p, const void* arp, int64_t a_bas
   op.bidx = p->wide ? bidx : nullptr;
   op.G = p->G;
   op.nG = p->nG;
+  // max |b| per B row, stored after the grain index (index_words)
+  op.bmax = p->wide && bidx ? reinterpret_cast<const float*>(bidx + ((int64_t)p->nG + 1) * p->B.nrows) : nullptr;
   return op;
 }
 
@@ -1590,7 +1600,7 @@ aires_status spgemm_device_in(aires_plan* p, hipStream_t s, DevPool& ws, aires_c
   if (p->wide) {
     ST_TRY(ws.get_n(m * (int64_t)p->nG, &gcnt));
     ST_TRY(ws.get_n(m + nt, &icount));
-    ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
+    ST_TRY(ws.get_n(index_words(p), &bidx));
     if (p->keep_bitmap >= 0 && !ws.arena) {
       ST_TRY(ws.get_n(m * (int64_t)p->ngg, &bm_off));
       ST_TRY(ws.get_n(1, &bm_top));
@@ -1634,8 +1644,8 @@ aires_status spgemm_device_in(aires_plan* p, hipStream_t s, DevPool& ws, aires_c
   if (bm_cache) HIP_TRY(hipMemsetAsync(bm_top, 0, sizeof(unsigned long long), s));
   if (p->wide) {
     const int ea = tm.record();
-    HIP_TRY(kern::build_window_index(p->B.row_ptr, p->B.rp_type == AIRES_IDX_I64, p->B.col_idx, K, p->G, p->nG,
-                                     bidx, s));
+    HIP_TRY(kern::build_window_index(p->B.row_ptr, p->B.rp_type == AIRES_IDX_I64, p->B.col_idx, p->B.vals, K, p->G,
+                                     p->nG, bidx, index_bmax(p, bidx), s));
     tm.mark(PH_INDEX, 0, ea, tm.record());
   }
 
@@ -1824,7 +1834,7 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   int64_t* running = nullptr;
   ST_TRY(ws.get_n(nt, &prod));  // intermediate products of each tile
   ST_TRY(ws.get_n(1, &running));
-  if (p->wide) ST_TRY(ws.get_n(((int64_t)p->nG + 1) * K, &bidx));
+  if (p->wide) ST_TRY(ws.get_n(index_words(p), &bidx));
   kern::SplitWs split{nullptr, nullptr, 0};
   ST_TRY(alloc_split_ws(p, ws, split));
   for (int s = 0; s < 2; ++s) {
@@ -2030,7 +2040,8 @@ aires_status stream_impl(aires_plan* p, hipStream_t sh, hipStream_t sc, hipStrea
   if (nt > 1) ST_TRY(issue_h2d(1));
   if (p->wide && nt > 0) {
     HIP_TRY(hipStreamWaitEvent(sc, ev_in[0], 0));  // B is resident once tile 0 arrived
-    HIP_TRY(kern::build_window_index(brp, B.rp_type == AIRES_IDX_I64, bcol, K, p->G, p->nG, bidx, sc));
+    HIP_TRY(kern::build_window_index(brp, B.rp_type == AIRES_IDX_I64, bcol, bval, K, p->G, p->nG, bidx,
+                                     index_bmax(p, bidx), sc));
   }
   int64_t base = 0;
   for (int64_t t = 0; t < nt; ++t) {

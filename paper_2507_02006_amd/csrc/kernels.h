@@ -38,6 +38,9 @@ struct Operands {
   // Column grains of a wide product: bidx[k*(nG+1) + g] = first position of
   // B_k with column >= g*G, for g in [0, nG]; nullptr when N is narrow.
   const int32_t* bidx; int32_t G; int32_t nG;
+  // bmax[k] = max_j |b_kj| for wide products (the bound that lets a window
+  // row accumulate in fixed point); nullptr: fp32 accumulation everywhere.
+  const float* bmax;
 };
 
 struct BinView {
@@ -124,8 +127,9 @@ hipError_t windows_symbolic(const Operands& op, const BinView& bv, const WindowP
 // wide rows: fill the window list (item_count scanned into offsets), then numeric
 hipError_t windows_numeric(const Operands& op, const BinView& bv, const WindowParams& wp,
                            const Outputs& out, int64_t ub_rows, int64_t nitems, hipStream_t s);
-hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, int64_t K,
-                              int32_t G, int32_t nG, int32_t* bidx, hipStream_t s);
+// The grain index of B and bmax[k] = max_j |b_kj| (NaN if the row holds one).
+hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, const float* bval, int64_t K,
+                              int32_t G, int32_t nG, int32_t* bidx, float* bmax, hipStream_t s);
 // In-place inclusive scan of x[0..n) plus x[-1] (the base): x[i] = x[-1] + sum_{j<=i} x[j].
 size_t scan_workspace_bytes(int64_t n);
 hipError_t scan_inplace(int64_t* x, int64_t n, void* ws, hipStream_t s);

@@ -108,6 +108,13 @@ __device__ __forceinline__ T wave_sum(T v) {
   return wave_last(wave_incl_scan(v));
 }
 
+// fp32 sum over the wavefront, in every lane (butterfly over lane pairs).
+__device__ __forceinline__ float wave_sum_f32(float v) {
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
 // A cooperating group: one wavefront (GROUP == 64) or the whole block.
 template <int GROUP, int BLOCK>
 struct Group {
@@ -1035,6 +1042,9 @@ __global__ __launch_bounds__(BLOCK) void k_hash(const Operands op, const BinView
 
 constexpr int WIN_BLOCK = 512;
 constexpr int WIN_UNROLL = 2;  // the numeric window kernel keeps fewer loads in flight (registers)
+// Largest rounding error (absolute, per entry of C) that a row's fixed-point
+// accumulation may carry; rows whose bound exceeds it add in fp32.
+constexpr float FIXED_ERR = 1e-6f;
 
 template <typename S>
 __host__ __device__ constexpr size_t count_lds_bytes(int sg, int G) {
@@ -1273,6 +1283,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t s_row;
   __shared__ int s_shared;  // this workgroup's slab rows are done
+  __shared__ float s_fsum[WIN_BLOCK / WAVE];  // per-wavefront parts of a row's bound
   const int WPG = op.G / 32;  // 32-bit words per grain of a kept symbolic bitmap
   constexpr uint64_t BITS = (uint64_t(1) << WIN_WORD_BITS) - 1u;
   uint64_t* bw = reinterpret_cast<uint64_t*>(smem);  // presence bits | rank of the word's first bit << 48
@@ -1334,6 +1345,45 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       k = op.acol[p0 + t];
       a = op.aval[p0 + t];
     }
+    // The row's accumulation (uniform over the workgroup, in scalar
+    // registers): fixed point where a bound allows, else fp32.
+    // S = sum_k |a_ik| max_j |b_kj| bounds every |a_ik b_kj| of the row and
+    // every |c_ij|.  With S < 2^e and f = 30 - e, each product scaled by 2^f
+    // and rounded to an integer is below 2^30 in magnitude, and so is the sum
+    // of an entry's scaled products plus their roundings (at most |A_i| / 2),
+    // so adding them in 32-bit two's complement gives that integer sum
+    // exactly, whatever the order; the entry's only errors are the roundings
+    // of its products, at most 2^-(f+1) each for at most |A_i| products, and
+    // the final conversion to fp32.  (S itself is an fp32 sum; with
+    // |A_i| < 2^20 its rounding leaves the scaled sums below 2^31.)  Where
+    // |A_i| 2^-(f+1) <= FIXED_ERR the
+    // adds are plain integer adds (one LDS operation with no return, no
+    // retry); otherwise, and for NaN or infinite values, fp32
+    // compare-and-swap adds.
+    float fx_scale = 0.f, fx_inv = 0.f;  // 0: fp32 adds
+    if (op.bmax && i0 < i1) {
+      float sv = 0.f;
+      if (short_row) {
+        if (k >= 0) sv = fabsf(a) * op.bmax[k];
+      } else {
+        for (int64_t p = p0 + t; p < p1; p += WIN_BLOCK) sv += fabsf(op.aval[p]) * op.bmax[op.acol[p]];
+      }
+      sv = wave_sum_f32(sv);
+      if (lane_id() == 0) s_fsum[t / WAVE] = sv;
+      __syncthreads();
+      float S = 0.f;
+#pragma unroll
+      for (int i = 0; i < WIN_BLOCK / WAVE; ++i) S += s_fsum[i];
+      int e = 0;
+      frexpf(S, &e);
+      const int f = min(30 - e, 120);
+      if (S <= 1e30f && p1 - p0 < (1 << 20) && (float)(p1 - p0) * ldexpf(1.f, -(f + 1)) <= FIXED_ERR) {
+        fx_scale = ldexpf(1.f, f);
+        fx_inv = ldexpf(1.f, -f);
+      }
+      fx_scale = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(fx_scale)));
+      fx_inv = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(fx_inv)));
+    }
     int32_t cur = 0, nxt_hi = 0;
     int prev_g1 = -1;
     WinItem nextI{};
@@ -1390,7 +1440,12 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         const uint32_t w = dj / WIN_WORD_BITS;
         const uint64_t e = bw[w];
         const int rk = (int)(e >> WIN_WORD_BITS) + __popcll(e & ((1ull << (dj - w * WIN_WORD_BITS)) - 1u));
-        if (rk < n) lds_add<false>(&vals[rk], v);
+        if (rk < n) {
+          if (fx_scale != 0.f)
+            atomicAdd(reinterpret_cast<int32_t*>(&vals[rk]), (int32_t)rintf(v * fx_scale));
+          else
+            lds_add<false>(&vals[rk], v);
+        }
       };
       // exclusive popcount prefix over the window's words: each wavefront
       // takes a contiguous share [wa0, wa1), its lanes consecutive words,
@@ -1600,7 +1655,12 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
       {
         const int lane = lane_id();
         const int r0 = min((int)wr0, n), r1 = min((int)wr1, n);
-        for (int kk = r0 + lane; kk < r1; kk += WAVE) store_stream(&out.cval[base + kk], vals[kk]);
+        if (fx_inv != 0.f) {
+          const int32_t* iv = reinterpret_cast<const int32_t*>(vals);
+          for (int kk = r0 + lane; kk < r1; kk += WAVE) store_stream(&out.cval[base + kk], (float)iv[kk] * fx_inv);
+        } else {
+          for (int kk = r0 + lane; kk < r1; kk += WAVE) store_stream(&out.cval[base + kk], vals[kk]);
+        }
         wave_sync();
         int32_t* cid = reinterpret_cast<int32_t*>(vals);
         for (int w = wa0 + lane; w < wa1; w += WAVE) {
@@ -1619,7 +1679,7 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
         wave_sync();
         for (int kk = r0 + lane; kk < r1; kk += WAVE) {
           store_stream(&out.ccol[base + kk], cid[kk]);
-          cid[kk] = 0;  // the bits of +0.0f: the slots are clear for the next window
+          cid[kk] = 0;  // +0.0f and integer 0 alike: the slots are clear for the next window
         }
       }
     }
@@ -1635,12 +1695,18 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
 // binary search over the row's sorted columns: the row's index entries are
 // written by consecutive lanes.
 template <typename RB>
-__global__ __launch_bounds__(256) void k_window_index(const void* brp, const int32_t* bcol,
+__global__ __launch_bounds__(256) void k_window_index(const void* brp, const int32_t* bcol, const float* bval,
                                                       int64_t K, int32_t W, int32_t nwin,
-                                                      int32_t* bidx) {
+                                                      int32_t* bidx, float* bmax) {
   const int64_t nw = (int64_t)gridDim.x * (blockDim.x / WAVE);
   for (int64_t k = (int64_t)blockIdx.x * (blockDim.x / WAVE) + threadIdx.x / WAVE; k < K; k += nw) {
     const int64_t s = ld_rp<RB>(brp, k), e = ld_rp<RB>(brp, k + 1);
+    // max_j |b_kj|: the bits of non-negative floats order as their values,
+    // and a NaN's above all of them, so a NaN in the row gives a NaN
+    uint32_t mx = 0u;
+    for (int64_t q = s + lane_id(); q < e; q += WAVE) mx = max(mx, __float_as_uint(fabsf(bval[q])));
+    mx = wave_last(wave_scan_op<false>(mx));
+    if (lane_id() == 0) bmax[k] = __uint_as_float(mx);
     for (int w = lane_id(); w <= nwin; w += WAVE) {
       const int64_t c = (int64_t)w * W;  // the grain's first column
       int64_t lo = s, hi = e;
@@ -1945,15 +2011,17 @@ hipError_t windows_numeric(const Operands& op, const BinView& bv, const WindowPa
   return AIRES_DISPATCH_RP(op, win_numeric_t, op, bv, wp, out, ub_rows, nitems, s);
 }
 
-hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, int64_t K, int32_t G,
-                              int32_t nG, int32_t* bidx, hipStream_t s) {
+hipError_t build_window_index(const void* brp, int rpb64, const int32_t* bcol, const float* bval, int64_t K,
+                              int32_t G, int32_t nG, int32_t* bidx, float* bmax, hipStream_t s) {
   if (K <= 0) return hipSuccess;
   int64_t grid = (K + 3) / 4;
   if (grid > 65536) grid = 65536;
   if (rpb64)
-    hipLaunchKernelGGL((k_window_index<int64_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, K, G, nG, bidx);
+    hipLaunchKernelGGL((k_window_index<int64_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, bval, K, G, nG,
+                       bidx, bmax);
   else
-    hipLaunchKernelGGL((k_window_index<int32_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, K, G, nG, bidx);
+    hipLaunchKernelGGL((k_window_index<int32_t>), dim3((unsigned)grid), dim3(256), 0, s, brp, bcol, bval, K, G, nG,
+                       bidx, bmax);
   return hipGetLastError();
 }
 

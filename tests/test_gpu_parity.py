@@ -136,6 +136,76 @@ def test_each_path_integer_values_exact(torch_gpu, path):
     assert np.array_equal(val, ref.val)
 
 
+WINDOW_PATHS = ["windows_only", "windows_pool", "windows_slabs_kept"]
+
+
+def ones_and_tiny(rng, m, K, N, a_per_row, a_val, tiny):
+    """A: m rows of a_per_row distinct columns of K, every value a_val.
+    B: K rows of about N/2 random columns of N, each value 1.0 with
+    probability 1/4, else `tiny`; every row holds at least one 1.0."""
+    arp = np.arange(m + 1, dtype=np.int32) * a_per_row
+    acol = np.concatenate([np.sort(rng.choice(K, a_per_row, replace=False)) for _ in range(m)]).astype(np.int32)
+    A = CSR(m, K, arp, acol, np.full(m * a_per_row, a_val, np.float32))
+    rows, vals = [], []
+    for _ in range(K):
+        c = np.sort(rng.choice(N, N // 2, replace=False)).astype(np.int32)
+        v = np.where(rng.random(len(c)) < 0.25, 1.0, tiny).astype(np.float32)
+        v[rng.integers(len(c))] = 1.0
+        rows.append(c)
+        vals.append(v)
+    brp = np.zeros(K + 1, np.int32)
+    brp[1:] = np.cumsum([len(c) for c in rows])
+    return A, CSR(K, N, brp, np.concatenate(rows), np.concatenate(vals))
+
+
+# (A rows, K, entries per A row, their value, B's small value): short rows,
+# and rows longer than a numeric workgroup (512 entries)
+FIXED_SHAPES = {"short": (300, 96, 24, 1.0, 2.0 ** -24), "long": (40, 1024, 600, 2.0 ** -10, 2.0 ** -20)}
+
+
+@pytest.mark.parametrize("shape", list(FIXED_SHAPES))
+@pytest.mark.parametrize("path", WINDOW_PATHS)
+def test_window_rows_fixed_point_exact(torch_gpu, path, shape):
+    """Window rows whose bound allows it accumulate in fixed point.  Short:
+    24 entries of 1 per A row, B values 1 or 2^-24; the row's bound is
+    S = 24 < 2^5, so products are scaled by 2^25 (rounding error bound
+    24 * 2^-26 < 1e-6).  Long: 600 entries of 2^-10, B values 1 or 2^-20;
+    S = 600 * 2^-10 < 2^0, scale 2^30 (error bound 600 * 2^-31).  Every
+    product is then an exact multiple of the scale's unit, the integer sum
+    is exact and its one rounding to fp32 equals the oracle's fp64 sum
+    (exact for these products too) rounded once: values bit-exact.  Summed
+    in fp32 instead, a small term added to a partial sum many times larger
+    is lost."""
+    m, K, per, a_val, tiny = FIXED_SHAPES[shape]
+    rng = np.random.default_rng(zlib.crc32((path + shape).encode()) + 1)
+    A, B = ones_and_tiny(rng, m, K, 333, per, a_val, tiny)
+    say("fixed-point exact %s %s" % (path, shape))
+    ref = oracle.spgemm(A, B, f64=True)
+    exact = ref.val64.astype(np.float32)  # the exact sums rounded once to fp32
+    rp, col, val, st, _ = run(torch_gpu, A, B, **PATHS[path])
+    assert np.array_equal(rp - rp[0], ref.rp) and np.array_equal(col, ref.col)
+    assert np.array_equal(val, exact), "fixed-point sums differ from the exactly rounded ones at %d entries" % (
+        (val != exact).sum())
+
+
+@pytest.mark.parametrize("path", WINDOW_PATHS)
+def test_window_rows_fp32_where_bound_fails(torch_gpu, path):
+    """Rows whose bound leaves too few fractional bits stay in fp32: an A row
+    with one entry of 2^20 has S > 2^20, so a fixed-point scale would be at
+    most 2^9 and would flush entries made only of 2^-24 products to zero.
+    All values are positive (no cancellation), so fp32 sums in any order
+    are within 24 * 2^-24 of the exact ones relative to each entry."""
+    rng = np.random.default_rng(zlib.crc32(path.encode()) + 2)
+    A, B = ones_and_tiny(rng, 300, 96, 333, 24, 1.0, 2.0 ** -24)
+    A.val[A.rp[:-1]] = 2.0 ** 20  # each row's first entry
+    say("fp32 fallback %s" % path)
+    ref = oracle.spgemm(A, B, f64=True)
+    rp, col, val, st, _ = run(torch_gpu, A, B, **PATHS[path])
+    assert np.array_equal(rp - rp[0], ref.rp) and np.array_equal(col, ref.col)
+    rel = np.abs(val.astype(np.float64) - ref.val64) / np.abs(ref.val64)
+    assert rel.max() <= 2e-6, "relative error %g" % rel.max()
+
+
 @pytest.mark.parametrize("path", list(PATHS))
 def test_each_path_cfg1(torch_gpu, path):
     A, B = workloads.workload(1)
