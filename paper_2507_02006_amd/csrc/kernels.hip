@@ -1447,6 +1447,17 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
             lds_add<false>(&vals[rk], v);
         }
       };
+      // fixed point with no branch per term: a missing term (ok false, j any
+      // column of the window) or a rank past the window's entries adds 0 to
+      // slot 0, which changes nothing
+      auto add_fixed_if = [&](int j, float v, bool ok) {
+        const uint32_t dj = (uint32_t)(j - c0);
+        const uint32_t w = dj / WIN_WORD_BITS;
+        const uint64_t e = bw[w];
+        const int rk = (int)(e >> WIN_WORD_BITS) + __popcll(e & ((1ull << (dj - w * WIN_WORD_BITS)) - 1u));
+        const bool in = ok && rk < n;
+        atomicAdd(reinterpret_cast<int32_t*>(vals) + (in ? rk : 0), in ? (int32_t)rintf(v * fx_scale) : 0);
+      };
       // exclusive popcount prefix over the window's words: each wavefront
       // takes a contiguous share [wa0, wa1), its lanes consecutive words,
       // with one wavefront scan per 64 words and the shares' totals carried
@@ -1582,6 +1593,31 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                     for (int u = 0; u < WIN_UNROLL; ++u) set_bit_if(jb[u], ok[u]);
                     continue;
                   }
+                  if (fx_scale != 0.f) {
+                    // fixed-point adds, with no branch per term either
+                    int32_t pp[WIN_UNROLL];
+                    float am[WIN_UNROLL];
+                    bool ok[WIN_UNROLL];
+#pragma unroll
+                    for (int u = 0; u < WIN_UNROLL; ++u) {
+                      const int q = q0 + u * WAVE;
+                      ok[u] = q < wlen;
+                      const int qc = ok[u] ? q : q0;
+                      const typename CH::Rec rc = rec_of(qc);
+                      pp[u] = (int32_t)rc.shift + base + qc;
+                      am[u] = rc.av;
+                    }
+                    int jb[WIN_UNROLL];
+                    float bb[WIN_UNROLL];
+#pragma unroll
+                    for (int u = 0; u < WIN_UNROLL; ++u) {
+                      jb[u] = op.bcol[pp[u]];
+                      bb[u] = op.bval[pp[u]];
+                    }
+#pragma unroll
+                    for (int u = 0; u < WIN_UNROLL; ++u) add_fixed_if(jb[u], am[u] * bb[u], ok[u]);
+                    continue;
+                  }
                   int32_t pos[WIN_UNROLL];
                   float am[WIN_UNROLL];
 #pragma unroll
@@ -1641,8 +1677,16 @@ __global__ __launch_bounds__(WIN_BLOCK, 6) void k_win_rows(const Operands op, co
                 for (int u = 0; u < WIN_UNROLL; ++u) set_bit_if(j[u], ok[u]);
               });
         word_ranks();
-        for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true, WIN_UNROLL>(op, g, ch, row, seg,
-                                                            [&](int j, float v) { add_at_rank(j, v); });
+        if (fx_scale != 0.f)
+          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true, WIN_UNROLL, true>(
+              op, g, ch, row, seg,
+              [&](const int (&j)[WIN_UNROLL], const float (&v)[WIN_UNROLL], const bool (&ok)[WIN_UNROLL]) {
+#pragma unroll
+                for (int u = 0; u < WIN_UNROLL; ++u) add_fixed_if(j[u], v[u], ok[u]);
+              });
+        else
+          for_each_term<RA, WIN_BLOCK, WIN_BLOCK, true, true, WIN_UNROLL>(op, g, ch, row, seg,
+                                                              [&](int j, float v) { add_at_rank(j, v); });
       }
       __syncthreads();
       // Output, each wavefront on its own share of the bitmap words and so on
