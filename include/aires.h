@@ -387,7 +387,9 @@ aires_status aires_plan_tile(const aires_plan *plan, int64_t t, aires_tile *tile
  * products are scaled by 2^f (S_i < 2^(30-f)), rounded to integers and
  * summed exactly, so an entry's error is at most |A_i| 2^-(f+1) <= 1e-6
  * plus its final rounding to fp32, and its value does not depend on the
- * order of the products.
+ * order of the products.  An entry made of a single product is therefore
+ * exact in fp32 rows but rounded to a multiple of 2^-f in fixed-point rows
+ * (so C = A * I reproduces A only within that bound there).
  *
  * Memory (the constraint M of Sec. III-A): every block the call takes from
  * the allocator, C included, counts against the plan's budget together

@@ -136,7 +136,9 @@ def test_each_path_integer_values_exact(torch_gpu, path):
     assert np.array_equal(val, ref.val)
 
 
-WINDOW_PATHS = ["windows_only", "windows_pool", "windows_slabs_kept"]
+# wide products whose rows all go to column windows (plain, cut by the LDS
+# pool, and over column slabs with kept bitmaps)
+FIXED_PATHS = ["windows_only", "windows_pool", "windows_slabs_kept"]
 
 
 def ones_and_tiny(rng, m, K, N, a_per_row, a_val, tiny):
@@ -160,16 +162,18 @@ def ones_and_tiny(rng, m, K, N, a_per_row, a_val, tiny):
 
 # (A rows, K, entries per A row, their value, B's small value): short rows,
 # and rows longer than a numeric workgroup (512 entries)
-FIXED_SHAPES = {"short": (300, 96, 24, 1.0, 2.0 ** -24), "long": (40, 1024, 600, 2.0 ** -10, 2.0 ** -20)}
+FIXED_SHAPES = {"short": (300, 96, 24, 1.0, 2.0 ** -24), "short12": (300, 96, 12, 1.0, 2.0 ** -24),
+                "long": (40, 1024, 600, 2.0 ** -10, 2.0 ** -20)}
 
 
 @pytest.mark.parametrize("shape", list(FIXED_SHAPES))
-@pytest.mark.parametrize("path", WINDOW_PATHS)
+@pytest.mark.parametrize("path", FIXED_PATHS)
 def test_window_rows_fixed_point_exact(torch_gpu, path, shape):
     """Window rows whose bound allows it accumulate in fixed point.  Short:
     24 entries of 1 per A row, B values 1 or 2^-24; the row's bound is
     S = 24 < 2^5, so products are scaled by 2^25 (rounding error bound
-    24 * 2^-26 < 1e-6).  Long: 600 entries of 2^-10, B values 1 or 2^-20;
+    24 * 2^-26 < 1e-6); with 12 entries, S = 12 and scale 2^26.  Long: 600
+    entries of 2^-10, B values 1 or 2^-20;
     S = 600 * 2^-10 < 2^0, scale 2^30 (error bound 600 * 2^-31).  Every
     product is then an exact multiple of the scale's unit, the integer sum
     is exact and its one rounding to fp32 equals the oracle's fp64 sum
@@ -188,7 +192,7 @@ def test_window_rows_fixed_point_exact(torch_gpu, path, shape):
         (val != exact).sum())
 
 
-@pytest.mark.parametrize("path", WINDOW_PATHS)
+@pytest.mark.parametrize("path", FIXED_PATHS)
 def test_window_rows_fp32_where_bound_fails(torch_gpu, path):
     """Rows whose bound leaves too few fractional bits stay in fp32: an A row
     with one entry of 2^20 has S > 2^20, so a fixed-point scale would be at
@@ -627,33 +631,41 @@ def test_cfg5_full_streamed(torch_gpu):
 
 # ------------------------------------------- values derived from the pattern (Eq. 2)
 
-def _identity(n):
-    return CSR(n, n, np.arange(n + 1, dtype=np.int32), np.arange(n, dtype=np.int32), np.ones(n, np.float32))
+def _identity(n, scale=1.0):
+    return CSR(n, n, np.arange(n + 1, dtype=np.int32), np.arange(n, dtype=np.int32), np.full(n, scale, np.float32))
+
+
+# C = A * (2^64 I): the rows' bound (>= 2^44 here) leaves fixed point no
+# fractional bits, so the product runs in fp32, where an entry made of one
+# product is exact; the power-of-two scale is exact too.
+CARRIER = 2.0 ** 64
 
 
 @pytest.mark.parametrize("n", [20000, 1048576])
 def test_sym_norm_values_bitwise(torch_gpu, n):
-    """a_values='sym_norm': C = A_norm * I gives 1/sqrt(r_i r_j) bit for bit
-    (double arithmetic, one rounding to fp32) with A's own values not passed
-    at all, against the oracle's Eq. 2 (oracle.sym_norm) on the square
-    workload's graph scaled and at full size."""
+    """a_values='sym_norm': C = A_norm * (2^64 I) gives 2^64 / sqrt(r_i r_j)
+    bit for bit (double arithmetic, one rounding to fp32) with A's own values
+    not passed at all, against the oracle's Eq. 2 (oracle.sym_norm) on the
+    square workload's graph scaled and at full size."""
     import paper_2507_02006_amd as aires
     A, _ = workloads.workload(3, n=n)
     dA = aires.to_device(A)
     say("sym_norm values n=%d nnz=%d" % (n, A.nnz))
-    with aires.tile_plan(dA[:4] + (None,), aires.to_device(_identity(A.ncols)), 0, a_values="sym_norm") as plan:
+    with aires.tile_plan(dA[:4] + (None,), aires.to_device(_identity(A.ncols, CARRIER)), 0,
+                         a_values="sym_norm") as plan:
         C = aires.spgemm(plan)
         torch_gpu.cuda.synchronize()
         rp, col, val = C.rp.cpu().numpy(), C.col.cpu().numpy(), C.val.cpu().numpy()
     assert np.array_equal(rp, A.rp.astype(np.int64))
     assert np.array_equal(col, A.col)
-    assert np.array_equal(val.view(np.uint32), oracle.sym_norm(A.rp, A.col).view(np.uint32))
+    want = oracle.sym_norm(A.rp, A.col) * np.float32(CARRIER)
+    assert np.array_equal(val.view(np.uint32), want.view(np.uint32))
 
 
 def test_sym_norm_values_sparse_rows(torch_gpu):
     """Derived values when runs of empty rows make a 2048-entry chunk span
     more rows than the kernel stages in LDS (its global-search branch):
-    C = A_norm * I against the oracle's Eq. 2."""
+    C = A_norm * (2^64 I) against the oracle's Eq. 2 scaled alike."""
     import paper_2507_02006_amd as aires
     rng = np.random.default_rng(31)
     m = 200000
@@ -664,10 +676,11 @@ def test_sym_norm_values_sparse_rows(torch_gpu):
     rp = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     col = np.concatenate(cols).astype(np.int32)
     A = CSR(m, m, rp, col, np.zeros(len(col), np.float32))
-    want = oracle.sym_norm(rp, col)
+    want = oracle.sym_norm(rp, col) * np.float32(CARRIER)
     dA = aires.to_device(A)
     say("sym_norm sparse rows m=%d nnz=%d" % (m, len(col)))
-    with aires.tile_plan(dA[:4] + (None,), aires.to_device(_identity(m)), 0, a_values="sym_norm") as plan:
+    with aires.tile_plan(dA[:4] + (None,), aires.to_device(_identity(m, CARRIER)), 0,
+                         a_values="sym_norm") as plan:
         C = aires.spgemm(plan)
         torch_gpu.cuda.synchronize()
         c_col, c_val = C.col.cpu().numpy(), C.val.cpu().numpy()
