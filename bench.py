@@ -736,6 +736,8 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "accumulation": "fp32 products; sums in 32-bit fixed point (at most 1e-6 rounding per entry) in "
+                        "window rows whose bound allows it, fp32 elsewhere",
         "data": "synthetic (seeded R-MAT graph and uniform sparse features, generated on the host)",
         "config": {"workload": "cfg%d %s" % (args.workload, WORKLOAD_NAMES[args.workload]),
                    "m": A.nrows, "n": B.ncols, "nnz_a": A.nnz, "nnz_b": B.nnz,
