@@ -141,13 +141,16 @@ def test_each_path_integer_values_exact(torch_gpu, path):
 FIXED_PATHS = ["windows_only", "windows_pool", "windows_slabs_kept"]
 
 
-def ones_and_tiny(rng, m, K, N, a_per_row, a_val, tiny):
+def ones_and_tiny(rng, m, K, N, a_per_row, a_val, tiny, signed=False):
     """A: m rows of a_per_row distinct columns of K, every value a_val.
     B: K rows of about N/2 random columns of N, each value 1.0 with
-    probability 1/4, else `tiny`; every row holds at least one 1.0."""
+    probability 1/4, else `tiny`; every row holds at least one 1.0.
+    signed: every value of A and B takes a random sign."""
     arp = np.arange(m + 1, dtype=np.int32) * a_per_row
     acol = np.concatenate([np.sort(rng.choice(K, a_per_row, replace=False)) for _ in range(m)]).astype(np.int32)
     A = CSR(m, K, arp, acol, np.full(m * a_per_row, a_val, np.float32))
+    if signed:
+        A.val[rng.random(len(A.val)) < 0.5] *= -1
     rows, vals = [], []
     for _ in range(K):
         c = np.sort(rng.choice(N, N // 2, replace=False)).astype(np.int32)
@@ -157,13 +160,16 @@ def ones_and_tiny(rng, m, K, N, a_per_row, a_val, tiny):
         vals.append(v)
     brp = np.zeros(K + 1, np.int32)
     brp[1:] = np.cumsum([len(c) for c in rows])
-    return A, CSR(K, N, brp, np.concatenate(rows), np.concatenate(vals))
+    bval = np.concatenate(vals)
+    if signed:
+        bval[rng.random(len(bval)) < 0.5] *= -1
+    return A, CSR(K, N, brp, np.concatenate(rows), bval)
 
 
 # (A rows, K, entries per A row, their value, B's small value): short rows,
 # and rows longer than a numeric workgroup (512 entries)
 FIXED_SHAPES = {"short": (300, 96, 24, 1.0, 2.0 ** -24), "short12": (300, 96, 12, 1.0, 2.0 ** -24),
-                "long": (40, 1024, 600, 2.0 ** -10, 2.0 ** -20)}
+                "long": (40, 1024, 600, 2.0 ** -10, 2.0 ** -20), "signed": (300, 96, 24, 1.0, 2.0 ** -24)}
 
 
 @pytest.mark.parametrize("shape", list(FIXED_SHAPES))
@@ -173,8 +179,9 @@ def test_window_rows_fixed_point_exact(torch_gpu, path, shape):
     24 entries of 1 per A row, B values 1 or 2^-24; the row's bound is
     S = 24 < 2^5, so products are scaled by 2^25 (rounding error bound
     24 * 2^-26 < 1e-6); with 12 entries, S = 12 and scale 2^26.  Long: 600
-    entries of 2^-10, B values 1 or 2^-20;
-    S = 600 * 2^-10 < 2^0, scale 2^30 (error bound 600 * 2^-31).  Every
+    entries of 2^-10, B values 1 or 2^-20; S = 600 * 2^-10 < 2^0, scale
+    2^30 (error bound 600 * 2^-31).  Signed: the short shape with random
+    signs (negative products, sums that cancel to zero).  Every
     product is then an exact multiple of the scale's unit, the integer sum
     is exact and its one rounding to fp32 equals the oracle's fp64 sum
     (exact for these products too) rounded once: values bit-exact.  Summed
@@ -182,7 +189,7 @@ def test_window_rows_fixed_point_exact(torch_gpu, path, shape):
     is lost."""
     m, K, per, a_val, tiny = FIXED_SHAPES[shape]
     rng = np.random.default_rng(zlib.crc32((path + shape).encode()) + 1)
-    A, B = ones_and_tiny(rng, m, K, 333, per, a_val, tiny)
+    A, B = ones_and_tiny(rng, m, K, 333, per, a_val, tiny, signed=shape == "signed")
     say("fixed-point exact %s %s" % (path, shape))
     ref = oracle.spgemm(A, B, f64=True)
     exact = ref.val64.astype(np.float32)  # the exact sums rounded once to fp32
